@@ -1,0 +1,224 @@
+#!/usr/bin/env python3
+"""Throughput of the ACP-SGD compressor + decompressor on one MI355X.
+
+One step = every bucket of the workload compressed (acp_compress), its factor buffer passed
+on unchanged (the all-reduce of one worker) and decompressed (acp_decompress) into a separate
+output buffer; steps alternate P-steps and Q-steps.  Inputs are two resident gradient sets
+used in turn (2.7 GB for BERT-large, more than the 256 MB last-level cache).
+
+value = algorithmic bytes per step / measured step time, where the algorithmic bytes are
+16 B per gradient element (read M, read E, write E, write M_hat; pack + unpack for raw
+vectors) plus the factor traffic 10 r (n + m) B per matrix (average of a P-step and a Q-step).
+
+Also reported: the roofline entry of the dominant kernel (its own bytes per launch over its
+event-timed average launch duration) and the CPU oracle's throughput on a bounded sample of
+the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+HBM_PEAK_GBS = 8000.0
+
+
+def algorithmic_bytes(wl, rank):
+    """(bytes per average step, bytes of P-step compress, of Q-step compress, of decompress)."""
+    nc = n1 = fac = 0
+    fac_p = fac_q = 0
+    for p in wl.params:
+        s = p.shape
+        if len(s) >= 2:
+            n, m = s[0], p.numel // s[0]
+            if rank < min(n, m):
+                nc += p.numel
+                fac += 10 * rank * (n + m)
+                fac_p += 4 * rank * (m + n)       # read Q, write P
+                fac_q += 4 * rank * (n + m)       # read P, write Q
+                continue
+        n1 += p.numel
+    step = 16 * nc + 16 * n1 + fac
+    comp = 12 * nc + 8 * n1
+    return step, comp + fac_p, comp + fac_q, 4 * nc + 8 * n1, nc, n1
+
+
+def cpu_baseline(wl, seconds: float = 12.0):
+    """The fp64 oracle on a bounded sample: whole buckets, one P-step and one Q-step each."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    import synthgrad as sg
+    from oracle.acp import AcpOracle
+    from oracle.layout import plan
+
+    shapes = [p.shape for p in wl.params]
+    lay = plan(shapes, wl.rank, wl.cap_bytes)
+    done_bytes = 0.0
+    buckets = []
+    elapsed = 0.0
+    for b in range(1, len(lay.buckets)):
+        tids = lay.buckets[b].tids
+        orc = AcpOracle(shapes, wl.rank, seed=wl.seed, cap_bytes=wl.cap_bytes, tensor_ids=tids)
+        grads = {t: sg.gradient(wl, t, 1) for t in tids}
+        sub = type(wl)(wl.name, [wl.params[t] for t in tids], wl.rank, 2, wl.sigma)
+        step_bytes = algorithmic_bytes(sub, wl.rank)[0]
+        tb = time.perf_counter()
+        for t in (1, 2):
+            buf = orc.compress_bucket(t, b, grads)
+            orc.decompress_bucket(t, b, buf)
+        elapsed += time.perf_counter() - tb
+        done_bytes += 2 * step_bytes
+        buckets.append(b)
+        if elapsed > seconds:
+            break
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": round(done_bytes / elapsed / 1e9, 4), "unit": "GB/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{wl.name}: buckets {buckets[0]}..{buckets[-1]} ({len(buckets)} of {len(lay.buckets)}), "
+                      f"steps 1-2 (one P-step, one Q-step), fp64 NumPy, {elapsed:.1f} s of oracle work"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="bert_large_r4")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kernel-steps", type=int, default=20,
+                    help="steps of the per-launch event pass that times the dominant kernel")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
+              "(the compressor is data-parallel: each rank runs this same step on its own GPU).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import synthgrad as sg
+    from paper_2306_08881_amd.acp import Acp
+
+    wl = sg.WORKLOADS[args.workload]
+    shapes = [p.shape for p in wl.params]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t_setup = time.time()
+    acp = Acp(shapes, wl.rank, seed=wl.seed, cap_bytes=wl.cap_bytes, device=dev)
+    nb = acp.num_buckets()
+    info = [acp.bucket_info(b) for b in range(nb)]
+    lay = [acp.layout(b) for b in range(nb)]
+    gsets = []
+    for key in (1, 2):
+        grads = sg.gradient_set(wl, key, threads=16)
+        bufs = []
+        for b in range(nb):
+            host = np.empty(info[b][1], np.float32)
+            tids, go = lay[b][0], lay[b][1]
+            for k, tid in enumerate(tids):
+                g = grads[int(tid)].reshape(-1)
+                host[go[k]:go[k] + g.size] = g
+            bufs.append(torch.from_numpy(host).to(dev))
+        gsets.append(bufs)
+        del grads
+    fbuf = [torch.zeros(max(i[2], i[3], 4), dtype=torch.float32, device=dev) for i in info]
+    out = [torch.zeros(i[1], dtype=torch.float32, device=dev) for i in info]
+    torch.cuda.synchronize()
+    print(f"# setup {time.time() - t_setup:.1f}s: {wl.name}, {nb} buckets, {wl.numel} parameters",
+          file=sys.stderr, flush=True)
+
+    step_no = [0]
+
+    def one_step(events=None):
+        step_no[0] += 1
+        t = step_no[0]
+        g = gsets[t % 2]
+        for b in range(nb):
+            if events is not None:
+                events.append(("c", t, b, torch.cuda.Event(enable_timing=True)))
+                events[-1][3].record()
+            acp.compress(t, b, g[b], fbuf[b])
+            if events is not None:
+                events.append(("d", t, b, torch.cuda.Event(enable_timing=True)))
+                events[-1][3].record()
+            acp.decompress(t, b, fbuf[b], out[b])
+        if events is not None:
+            events.append(("e", t, -1, torch.cuda.Event(enable_timing=True)))
+            events[-1][3].record()
+
+    for _ in range(args.warmup):
+        one_step()
+    if args.warmup % 2:  # start the timed region on a P-step
+        one_step()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        one_step()
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / args.steps
+
+    # per-launch pass: the P-step compress launch is the dominant kernel (12 B per element of
+    # the 16 B step); time each compress call with events on the stream the kernels run on
+    ev = []
+    for _ in range(args.kernel_steps + (args.kernel_steps % 2)):
+        one_step(ev)
+    torch.cuda.synchronize()
+    comp_p, comp_q, dec = [], [], []
+    for i, (kind, t, b, e) in enumerate(ev[:-1]):
+        nxt = ev[i + 1][3]
+        dt = e.elapsed_time(nxt) * 1e-3
+        if kind == "c":
+            (comp_p if t % 2 == 1 else comp_q).append((b, dt))
+        elif kind == "d":
+            dec.append((b, dt))
+    step_bytes, bp, bq, bd, nc, n1 = algorithmic_bytes(wl, wl.rank)
+    t_p = sum(dt for _, dt in comp_p) / (len(comp_p) / nb)   # seconds of P-step compress per step
+    t_q = sum(dt for _, dt in comp_q) / (len(comp_q) / nb)
+    t_d = sum(dt for _, dt in dec) / (len(dec) / nb)
+    launches = len(comp_p) / (len(comp_p) / nb) if comp_p else 1
+    kern = {"name": "acp_compress P-step (orth apply + fused P-step kernels)",
+            "avg_launch_us": t_p / nb * 1e6, "bytes_per_launch": bp / nb}
+    achieved = bp / t_p / 1e9
+
+    gbs = step_bytes / (ms * 1e-3) / 1e9
+    res = {
+        "metric": "ACP-SGD compress+decompress gradient GB/s and % HBM peak, BERT-large r=4",
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded N(0, 0.02^2) gradients of the workload's shapes)",
+        "config": {"workload": f"{wl.name}: BERT-large-shaped gradients, {len(shapes)} tensors, "
+                               f"{wl.numel} parameters, rank {wl.rank}, 25 MiB buckets ({nb})",
+                   "rank": wl.rank, "buckets": nb, "parameters": wl.numel,
+                   "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+                   "gradient_elements_per_s": round(wl.numel / (ms * 1e-3), 1),
+                   "algorithmic_bytes_per_step": step_bytes,
+                   "ms_p_compress": round(t_p * 1e3, 4), "ms_q_compress": round(t_q * 1e3, 4),
+                   "ms_decompress": round(t_d * 1e3, 4)},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": kern["name"], "avg_launch_us": round(kern["avg_launch_us"], 3),
+                     "bytes_per_launch": kern["bytes_per_launch"]},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(wl)
+    res["cpu_baseline_host"] = {"cpu": platform.processor() or platform.machine(),
+                                "affinity_cores": len(os.sched_getaffinity(0))}
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,182 @@
+/*
+ * acp.h - C ABI of the ACP-SGD gradient compressor for AMD Instinct MI355X (gfx950).
+ *
+ * ACP-SGD ("alternate compressed Power-SGD", arXiv 2306.08881, Section IV-A,
+ * Algorithms 1 and 2) compresses every gradient matrix M_t (n x m) of a model
+ * to one rank-r factor per step, alternating by the parity of the step t:
+ *
+ *   odd t  (P-step): Q_t = orth(Q_{t-1});  P_t = (M_t + E_{t-1}) Q_t;
+ *   even t (Q-step): P_t = orth(P_{t-1});  Q_t = (M_t + E_{t-1})^T P_t;
+ *   both:            E_t = M_t + E_{t-1} - P_t Q_t^T   (local factor, before the all-reduce)
+ *                    the new factor (P_t or Q_t) is all-reduced (summed over p workers)
+ *                    and the step returns M_hat_t = P_t Q_t^T / p with the aggregated factor.
+ *
+ * orth() is the Gram-Schmidt factor: thin QR with a positive diagonal R; a
+ * column whose residual norm is at most 1e-4 of its norm (or zero) is set to
+ * zero.  E_0 = 0 and P_0, Q_0 are i.i.d. standard normal (Section IV-A,
+ * "Error-feedback"), drawn by a counter-based generator (see acp_init).
+ *
+ * Gradients are fused into buckets (Section IV-B, "Tensor Fusion", "Buffer
+ * Size"): tensors in reverse registration order, a bucket closes once its
+ * byte size reaches the cap (25 MiB by default).  Vector-shaped gradients,
+ * and matrices with r >= min(n, m), are not compressed (Section IV-C): they
+ * travel raw in the factor buffer.  A tensor of shape (d0, d1, ...) is the
+ * matrix n = d0, m = d1 * d2 * ... .
+ *
+ * Buffers (all fp32, row-major, packed, no padding):
+ *   gradient bucket b : grad_elems(b) floats; tensor k of the bucket at grad_off[k].
+ *   factor buffer b   : on odd steps factor_elems_p(b) floats (P_t, n x r, per compressed
+ *                       tensor at fac_off_p[k]; raw vector at fac_off_p[k]); on even steps
+ *                       factor_elems_q(b) floats (Q_t, m x r, at fac_off_q[k]).
+ *   output bucket b   : like the gradient bucket; receives M_hat_t (and raw vectors / p).
+ *
+ * Ownership: the caller owns every device buffer and stream.  The library
+ * needs one device block for its state (the error E, the factors, small
+ * workspaces and its launch tables); the caller allocates it (acp_state_bytes)
+ * and hands it over with acp_bind_state.  The library itself never allocates
+ * device memory.  Device pointers must be 16-byte aligned.
+ *
+ * Sequencing: per bucket, steps run 1, 2, 3, ... and compress(t) must precede
+ * decompress(t); anything else returns ACP_E_STEP and changes nothing.
+ * Buckets are independent and may be processed on different streams; calls
+ * on one bucket must be ordered on the caller's side.  A context is not
+ * thread-safe.  All argument, state and sequencing checks run on the host
+ * before anything is enqueued.  Kernel launch failures return ACP_E_DEVICE;
+ * asynchronous device faults surface at a later HIP call.
+ */
+#ifndef ACP_H
+#define ACP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct acp_ctx acp_ctx;
+
+typedef enum {
+  ACP_OK = 0,
+  ACP_E_INVALID = -1,     /* bad argument (null, out of range, misaligned, bad shape) */
+  ACP_E_STEP = -2,        /* call out of step order */
+  ACP_E_STATE = -3,       /* state not bound / wrong size / corrupt checkpoint */
+  ACP_E_DEVICE = -4,      /* a HIP call failed */
+  ACP_E_UNSUPPORTED = -5  /* valid request this build does not implement */
+} acp_status;
+
+/* flags of acp_init */
+#define ACP_FLAG_EF 1u            /* error feedback (Algorithm 2); off = Algorithm 1's ACP branch */
+#define ACP_FLAG_REUSE 2u         /* reuse the previous factor (always on in this build) */
+#define ACP_FLAGS_DEFAULT 3u
+
+/* which factor for acp_factor / acp_init_factor */
+#define ACP_FACTOR_P 0
+#define ACP_FACTOR_Q 1
+
+/*
+ * acp_init - plan the layout and draw P_0, Q_0 on the host.  No device work.
+ *   num_tensors      number of parameters, in registration (forward) order.
+ *   ndims[i]         rank of parameter i (>= 1); dims holds all dims flattened.
+ *   rank             r: 1, 2, 4, 8, 16 or 32.
+ *   seed             key of the initial-factor draw: element i (row-major) of P_0 (f = 0) or
+ *                    Q_0 (f = 1) of tensor k is z = sqrt(-2 ln u1) cos(2 pi u2) rounded to fp32,
+ *                    with s = mix(seed ^ mix(2k + f)), u1 = ((mix(s + (2i+1)g) >> 11) + 1) 2^-53,
+ *                    u2 = (mix(s + (2i+2)g) >> 11) 2^-53, mix the SplitMix64 finaliser and
+ *                    g = 0x9E3779B97F4A7C15.
+ *   bucket_cap_bytes fusion cap (> 0); 26214400 is PyTorch-DDP's 25 MiB default.
+ *   world_size       p >= 1; decompress divides the aggregated sum by p.
+ *   flags            ACP_FLAG_* ; clearing ACP_FLAG_REUSE returns ACP_E_UNSUPPORTED.
+ * On success *out owns host memory only; free it with acp_destroy.
+ */
+acp_status acp_init(acp_ctx **out, int32_t num_tensors, const int32_t *ndims, const int64_t *dims,
+                    int32_t rank, uint64_t seed, int64_t bucket_cap_bytes, int32_t world_size,
+                    uint32_t flags);
+
+/* Size in bytes of the device state block the caller must allocate (256-byte aligned). */
+acp_status acp_state_bytes(const acp_ctx *ctx, int64_t *bytes);
+
+/*
+ * acp_bind_state - adopt the caller's device block (>= acp_state_bytes, 256-byte aligned) on
+ * the current HIP device.  Uploads P_0, Q_0 and the launch tables, zeroes E and the workspace
+ * counters, and orthogonalises Q_0 for step 1, all on `stream` (a hipStream_t, or NULL for the
+ * default stream), then waits for the stream.  Re-binding resets the state to step 0.
+ */
+acp_status acp_bind_state(acp_ctx *ctx, void *device_ptr, int64_t bytes, void *stream);
+
+int32_t acp_num_buckets(const acp_ctx *ctx);
+
+/* Bucket sizes in elements: tensors, gradient/output bucket, P-step and Q-step factor buffers. */
+acp_status acp_bucket_info(const acp_ctx *ctx, int32_t b, int32_t *num_tensors, int64_t *grad_elems,
+                           int64_t *factor_elems_p, int64_t *factor_elems_q);
+
+/*
+ * acp_layout - bucket b's metadata, one entry per tensor in bucket order (arrays of
+ * num_tensors from acp_bucket_info; any pointer may be NULL to skip it): registration index,
+ * element offsets in the gradient bucket and in the P-step / Q-step factor buffers, and
+ * whether the tensor is compressed.
+ */
+acp_status acp_layout(const acp_ctx *ctx, int32_t b, int32_t *tensor_ids, int64_t *grad_off,
+                      int64_t *fac_off_p, int64_t *fac_off_q, int32_t *compressed);
+
+/* Per-tensor view: compressed flag, matrix shape n x m (numel x 1 if not compressed), bucket. */
+acp_status acp_tensor_info(const acp_ctx *ctx, int32_t tensor_id, int32_t *compressed, int64_t *n,
+                           int64_t *m, int32_t *bucket);
+
+/* Host copy of the initial factor P_0 (which = ACP_FACTOR_P, n*r floats) or Q_0 (m*r floats). */
+acp_status acp_init_factor(const acp_ctx *ctx, int32_t tensor_id, int32_t which, float *host_out,
+                           int64_t count);
+
+/*
+ * acp_compress - step `step` of bucket b (Algorithm 2 up to the all-reduce).  Reads the gradient
+ * bucket `grad` (device), updates E in the state and writes the local factors and raw vectors
+ * into `factor_buf` (device, factor_elems_p/q(b) floats by parity), enqueued on `stream`.
+ * `factor_buf` must not overlap `grad`.  The caller all-reduces (sums) factor_buf across workers.
+ */
+acp_status acp_compress(acp_ctx *ctx, int64_t step, int32_t b, const float *grad, float *factor_buf,
+                        void *stream);
+
+/*
+ * acp_decompress - finish step `step` of bucket b: from the aggregated (summed) factor buffer
+ * `agg_factor` (device), write M_hat = P_t Q_t^T / p for every compressed tensor and raw/p for
+ * every vector into `out` (device, grad_elems(b) floats; may alias the gradient bucket but not
+ * agg_factor), and keep the aggregated factor as the next step's reused factor.
+ */
+acp_status acp_decompress(acp_ctx *ctx, int64_t step, int32_t b, const float *agg_factor, float *out,
+                          void *stream);
+
+/*
+ * acp_error - write the current error E of bucket b's compressed tensors into `e_out` (device,
+ * laid out like the gradient bucket; vector slots are left untouched).  Does not change the state.
+ * ACP_E_UNSUPPORTED without error feedback.
+ */
+acp_status acp_error(const acp_ctx *ctx, int32_t b, float *e_out, void *stream);
+
+/*
+ * acp_factor - copy factor P_t (which = ACP_FACTOR_P, n x r) or Q_t (ACP_FACTOR_Q, m x r) of the
+ * last completed step of a compressed tensor into `dev_out` (device).  After an odd step P_t is
+ * the aggregated factor and Q_t the orthogonalised one; after an even step the reverse.
+ * ACP_E_STEP before step 1 completes.
+ */
+acp_status acp_factor(const acp_ctx *ctx, int32_t tensor_id, int32_t which, float *dev_out,
+                      void *stream);
+
+/*
+ * Checkpoint: acp_get_state writes the whole state (step counters, E, factors, orthogonalisation
+ * transforms) into a host buffer of acp_checkpoint_bytes; acp_set_state restores it into a bound
+ * context built with the same shapes, rank, seed, cap, world size and flags.  Both synchronise
+ * the device.  Restoring and continuing is bitwise identical to not stopping.
+ */
+acp_status acp_checkpoint_bytes(const acp_ctx *ctx, int64_t *bytes);
+acp_status acp_get_state(const acp_ctx *ctx, void *host_buf, int64_t bytes);
+acp_status acp_set_state(acp_ctx *ctx, const void *host_buf, int64_t bytes);
+
+/* Text of the last error on this context ("" if none).  Valid until the next call on ctx. */
+const char *acp_last_error(const acp_ctx *ctx);
+
+void acp_destroy(acp_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ACP_H */

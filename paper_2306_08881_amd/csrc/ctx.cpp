@@ -1,0 +1,447 @@
+// C ABI of the ACP-SGD compressor: context, state binding, step sequencing and launches.
+// Every argument, state and sequencing check runs on the host before anything is enqueued.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "acp.h"
+#include "plan.hpp"
+
+namespace acp {
+hipError_t launch(const Launch& l, int32_t rank, const KArgs& args, hipStream_t s);
+}
+
+struct acp_ctx {
+  acp::Plan plan;
+  uint64_t seed = 0;
+  int32_t world = 1;
+  uint32_t flags = 0;
+  int32_t num_tensors = 0;
+  std::vector<float> init_fac;  // host image of the factor region holding P_0 and Q_0
+
+  uint8_t* dev = nullptr;       // bound state block
+  int64_t dev_bytes = 0;
+  int device = -1;
+  std::vector<int64_t> last_step;   // per bucket: last completed step
+  std::vector<int64_t> pending;     // per bucket: compressed step awaiting decompress (0 = none)
+  std::vector<uint8_t> deferred;    // per bucket: E arena holds F
+  mutable std::string err;
+};
+
+namespace {
+
+constexpr uint64_t kMagic = 0x3153504341ull;  // "ACPS1"
+constexpr int64_t kVersion = 1;
+
+acp_status fail(const acp_ctx* c, acp_status s, const std::string& msg) {
+  if (c) c->err = msg;
+  return s;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+acp_status check_device(const acp_ctx* c) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(c, ACP_E_DEVICE, "hipGetDevice failed");
+  if (dev != c->device)
+    return fail(c, ACP_E_INVALID, "the device current at bind time must be current for this call");
+  return ACP_OK;
+}
+
+acp::KArgs base_args(const acp_ctx* c) {
+  const acp::Plan& p = c->plan;
+  acp::KArgs a{};
+  uint8_t* d = c->dev;
+  a.e = reinterpret_cast<float*>(d + p.off_e);
+  a.fac = reinterpret_cast<float*>(d + p.off_fac);
+  a.w = reinterpret_cast<double*>(d + p.off_w);
+  a.gpart = reinterpret_cast<double*>(d + p.off_gpart);
+  a.qpart = reinterpret_cast<float*>(d + p.off_qpart);
+  a.ctr = reinterpret_cast<uint32_t*>(d + p.off_ctr);
+  a.mats = reinterpret_cast<const acp::MatDesc*>(d + p.off_mats);
+  a.vecs = reinterpret_cast<const acp::VecDesc*>(d + p.off_vecs);
+  a.ef = p.ef ? 1 : 0;
+  a.inv_p = 1.0f / static_cast<float>(c->world);
+  return a;
+}
+
+acp_status run(const acp_ctx* c, const std::vector<acp::Launch>& launches, acp::KArgs a,
+               hipStream_t s) {
+  const acp::Tile* tiles = reinterpret_cast<const acp::Tile*>(c->dev + c->plan.off_tiles);
+  for (const acp::Launch& l : launches) {
+    a.tiles = tiles + l.tile_off;
+    a.ntiles = l.ntiles;
+    a.variant = l.variant;
+    const hipError_t e = acp::launch(l, c->plan.rank, a, s);
+    if (e != hipSuccess)
+      return fail(c, ACP_E_DEVICE, std::string("kernel launch failed: ") + hipGetErrorString(e));
+  }
+  return ACP_OK;
+}
+
+int64_t checkpoint_payload(const acp::Plan& p) {
+  return p.e_floats * 4 + p.fac_floats * 4 + p.w_doubles * 8;
+}
+
+struct CkptHeader {
+  uint64_t magic;
+  int64_t version;
+  int64_t num_tensors, rank, cap, world, flags, nbuckets, seed;
+  int64_t e_floats, fac_floats, w_doubles;
+};
+
+}  // namespace
+
+extern "C" {
+
+acp_status acp_init(acp_ctx** out, int32_t num_tensors, const int32_t* ndims, const int64_t* dims,
+                    int32_t rank, uint64_t seed, int64_t bucket_cap_bytes, int32_t world_size,
+                    uint32_t flags) {
+  if (!out) return ACP_E_INVALID;
+  *out = nullptr;
+  if (world_size < 1) return ACP_E_INVALID;
+  if (flags & ~ACP_FLAGS_DEFAULT) return ACP_E_INVALID;
+  if (!(flags & ACP_FLAG_REUSE)) return ACP_E_UNSUPPORTED;
+  acp_ctx* c = new acp_ctx();
+  const std::string msg = acp::build_plan(c->plan, num_tensors, ndims, dims, rank, bucket_cap_bytes,
+                                          (flags & ACP_FLAG_EF) != 0);
+  if (!msg.empty()) {
+    delete c;
+    return ACP_E_INVALID;
+  }
+  c->seed = seed;
+  c->world = world_size;
+  c->flags = flags;
+  c->num_tensors = num_tensors;
+  c->init_fac.assign(static_cast<size_t>(c->plan.fac_floats), 0.0f);
+  for (int32_t tid = 0; tid < num_tensors; ++tid) {
+    const acp::TensorPlan& t = c->plan.tensors[tid];
+    if (t.mat < 0) continue;
+    const acp::MatDesc& d = c->plan.mats[t.mat];
+    acp::draw_init_factor(seed, tid, 0, t.n * rank, c->init_fac.data() + d.p_slot);
+    acp::draw_init_factor(seed, tid, 1, t.m * rank, c->init_fac.data() + d.q_slot);
+  }
+  const size_t nb = c->plan.buckets.size();
+  c->last_step.assign(nb, 0);
+  c->pending.assign(nb, 0);
+  c->deferred.assign(nb, 0);
+  *out = c;
+  return ACP_OK;
+}
+
+acp_status acp_state_bytes(const acp_ctx* c, int64_t* bytes) {
+  if (!c || !bytes) return fail(c, ACP_E_INVALID, "null argument");
+  *bytes = c->plan.total_bytes;
+  return ACP_OK;
+}
+
+acp_status acp_bind_state(acp_ctx* c, void* device_ptr, int64_t bytes, void* stream) {
+  if (!c) return ACP_E_INVALID;
+  if (!device_ptr) return fail(c, ACP_E_INVALID, "device_ptr is NULL");
+  if ((reinterpret_cast<uintptr_t>(device_ptr) & 255u) != 0)
+    return fail(c, ACP_E_INVALID, "state block must be 256-byte aligned");
+  if (bytes < c->plan.total_bytes) return fail(c, ACP_E_STATE, "state block too small");
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(c, ACP_E_DEVICE, "hipGetDevice failed");
+  const acp::Plan& p = c->plan;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  uint8_t* d = static_cast<uint8_t*>(device_ptr);
+  hipError_t e = hipSuccess;
+  if (p.e_floats) e = hipMemsetAsync(d + p.off_e, 0, p.e_floats * 4, s);
+  if (e == hipSuccess && p.n_ctr) e = hipMemsetAsync(d + p.off_ctr, 0, p.n_ctr * 4, s);
+  if (e == hipSuccess && p.fac_floats)
+    e = hipMemcpyAsync(d + p.off_fac, c->init_fac.data(), p.fac_floats * 4, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && !p.mats.empty())
+    e = hipMemcpyAsync(d + p.off_mats, p.mats.data(), p.mats.size() * sizeof(acp::MatDesc),
+                       hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && !p.vecs.empty())
+    e = hipMemcpyAsync(d + p.off_vecs, p.vecs.data(), p.vecs.size() * sizeof(acp::VecDesc),
+                       hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && !p.tiles.empty())
+    e = hipMemcpyAsync(d + p.off_tiles, p.tiles.data(), p.tiles.size() * sizeof(acp::Tile),
+                       hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return fail(c, ACP_E_DEVICE, std::string("upload failed: ") + hipGetErrorString(e));
+  c->dev = d;
+  c->dev_bytes = bytes;
+  c->device = dev;
+  acp::KArgs a = base_args(c);
+  const acp_status st = run(c, p.gram_init, a, s);
+  if (st != ACP_OK) {
+    c->dev = nullptr;
+    return st;
+  }
+  e = hipStreamSynchronize(s);
+  if (e != hipSuccess) {
+    c->dev = nullptr;
+    return fail(c, ACP_E_DEVICE, std::string("bind failed: ") + hipGetErrorString(e));
+  }
+  std::fill(c->last_step.begin(), c->last_step.end(), 0);
+  std::fill(c->pending.begin(), c->pending.end(), 0);
+  std::fill(c->deferred.begin(), c->deferred.end(), 0);
+  c->err.clear();
+  return ACP_OK;
+}
+
+int32_t acp_num_buckets(const acp_ctx* c) {
+  return c ? static_cast<int32_t>(c->plan.buckets.size()) : -1;
+}
+
+acp_status acp_bucket_info(const acp_ctx* c, int32_t b, int32_t* num_tensors, int64_t* grad_elems,
+                           int64_t* factor_elems_p, int64_t* factor_elems_q) {
+  if (!c) return ACP_E_INVALID;
+  if (b < 0 || b >= static_cast<int32_t>(c->plan.buckets.size()))
+    return fail(c, ACP_E_INVALID, "bucket index out of range");
+  const acp::BucketPlan& bk = c->plan.buckets[b];
+  if (num_tensors) *num_tensors = static_cast<int32_t>(bk.tids.size());
+  if (grad_elems) *grad_elems = bk.grad_elems;
+  if (factor_elems_p) *factor_elems_p = bk.fac_elems_p;
+  if (factor_elems_q) *factor_elems_q = bk.fac_elems_q;
+  return ACP_OK;
+}
+
+acp_status acp_layout(const acp_ctx* c, int32_t b, int32_t* tensor_ids, int64_t* grad_off,
+                      int64_t* fac_off_p, int64_t* fac_off_q, int32_t* compressed) {
+  if (!c) return ACP_E_INVALID;
+  if (b < 0 || b >= static_cast<int32_t>(c->plan.buckets.size()))
+    return fail(c, ACP_E_INVALID, "bucket index out of range");
+  const acp::BucketPlan& bk = c->plan.buckets[b];
+  for (size_t k = 0; k < bk.tids.size(); ++k) {
+    if (tensor_ids) tensor_ids[k] = bk.tids[k];
+    if (grad_off) grad_off[k] = bk.grad_off[k];
+    if (fac_off_p) fac_off_p[k] = bk.fac_off_p[k];
+    if (fac_off_q) fac_off_q[k] = bk.fac_off_q[k];
+    if (compressed) compressed[k] = c->plan.tensors[bk.tids[k]].compressed ? 1 : 0;
+  }
+  return ACP_OK;
+}
+
+acp_status acp_tensor_info(const acp_ctx* c, int32_t tensor_id, int32_t* compressed, int64_t* n,
+                           int64_t* m, int32_t* bucket) {
+  if (!c) return ACP_E_INVALID;
+  if (tensor_id < 0 || tensor_id >= c->num_tensors) return fail(c, ACP_E_INVALID, "tensor id out of range");
+  const acp::TensorPlan& t = c->plan.tensors[tensor_id];
+  if (compressed) *compressed = t.compressed ? 1 : 0;
+  if (n) *n = t.n;
+  if (m) *m = t.m;
+  if (bucket) *bucket = t.bucket;
+  return ACP_OK;
+}
+
+acp_status acp_init_factor(const acp_ctx* c, int32_t tensor_id, int32_t which, float* host_out,
+                           int64_t count) {
+  if (!c) return ACP_E_INVALID;
+  if (!host_out) return fail(c, ACP_E_INVALID, "host_out is NULL");
+  if (tensor_id < 0 || tensor_id >= c->num_tensors) return fail(c, ACP_E_INVALID, "tensor id out of range");
+  if (which != ACP_FACTOR_P && which != ACP_FACTOR_Q) return fail(c, ACP_E_INVALID, "bad factor");
+  const acp::TensorPlan& t = c->plan.tensors[tensor_id];
+  if (t.mat < 0) return fail(c, ACP_E_INVALID, "tensor is not compressed");
+  const acp::MatDesc& d = c->plan.mats[t.mat];
+  const int64_t need = (which == ACP_FACTOR_P ? t.n : t.m) * c->plan.rank;
+  if (count != need) return fail(c, ACP_E_INVALID, "count must be rows * rank");
+  const float* src = c->init_fac.data() + (which == ACP_FACTOR_P ? d.p_slot : d.q_slot);
+  std::memcpy(host_out, src, static_cast<size_t>(need) * 4);
+  return ACP_OK;
+}
+
+acp_status acp_compress(acp_ctx* c, int64_t step, int32_t b, const float* grad, float* factor_buf,
+                        void* stream) {
+  if (!c) return ACP_E_INVALID;
+  if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
+  if (b < 0 || b >= static_cast<int32_t>(c->plan.buckets.size()))
+    return fail(c, ACP_E_INVALID, "bucket index out of range");
+  if (!grad || !factor_buf) return fail(c, ACP_E_INVALID, "null buffer");
+  if (!aligned16(grad) || !aligned16(factor_buf)) return fail(c, ACP_E_INVALID, "buffers must be 16-byte aligned");
+  if (c->pending[b] != 0)
+    return fail(c, ACP_E_STEP, "compress called twice without decompress");
+  if (step != c->last_step[b] + 1)
+    return fail(c, ACP_E_STEP, "step " + std::to_string(step) + " out of order (expected " +
+                                   std::to_string(c->last_step[b] + 1) + ")");
+  const acp::BucketPlan& bk = c->plan.buckets[b];
+  {
+    const char* g0 = reinterpret_cast<const char*>(grad);
+    const char* f0 = reinterpret_cast<const char*>(factor_buf);
+    const int64_t fe = (step & 1) ? bk.fac_elems_p : bk.fac_elems_q;
+    if (g0 < f0 + fe * 4 && f0 < g0 + bk.grad_elems * 4)
+      return fail(c, ACP_E_INVALID, "factor_buf overlaps grad");
+  }
+  const acp_status ds = check_device(c);
+  if (ds != ACP_OK) return ds;
+  acp::KArgs a = base_args(c);
+  a.grad = grad;
+  a.fbuf = factor_buf;
+  a.parity = static_cast<int32_t>(step & 1);
+  a.deferred = c->deferred[b];
+  const acp_status st = run(c, bk.compress[step & 1], a, static_cast<hipStream_t>(stream));
+  if (st != ACP_OK) return st;
+  c->pending[b] = step;
+  if (c->plan.ef) c->deferred[b] = (step & 1) ? 0 : 1;
+  return ACP_OK;
+}
+
+acp_status acp_decompress(acp_ctx* c, int64_t step, int32_t b, const float* agg_factor, float* out,
+                          void* stream) {
+  if (!c) return ACP_E_INVALID;
+  if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
+  if (b < 0 || b >= static_cast<int32_t>(c->plan.buckets.size()))
+    return fail(c, ACP_E_INVALID, "bucket index out of range");
+  if (!agg_factor || !out) return fail(c, ACP_E_INVALID, "null buffer");
+  if (!aligned16(agg_factor) || !aligned16(out)) return fail(c, ACP_E_INVALID, "buffers must be 16-byte aligned");
+  if (c->pending[b] == 0 || c->pending[b] != step)
+    return fail(c, ACP_E_STEP, "decompress(" + std::to_string(step) + ") without compress(" +
+                                   std::to_string(step) + ")");
+  const acp::BucketPlan& bk = c->plan.buckets[b];
+  {
+    const char* a0 = reinterpret_cast<const char*>(agg_factor);
+    const char* o0 = reinterpret_cast<const char*>(out);
+    const int64_t fe = (step & 1) ? bk.fac_elems_p : bk.fac_elems_q;
+    if (o0 < a0 + fe * 4 && a0 < o0 + bk.grad_elems * 4)
+      return fail(c, ACP_E_INVALID, "out overlaps agg_factor");
+  }
+  const acp_status ds = check_device(c);
+  if (ds != ACP_OK) return ds;
+  acp::KArgs a = base_args(c);
+  a.agg = agg_factor;
+  a.out = out;
+  a.parity = static_cast<int32_t>(step & 1);
+  a.deferred = c->deferred[b];
+  const acp_status st = run(c, bk.decompress[step & 1], a, static_cast<hipStream_t>(stream));
+  if (st != ACP_OK) return st;
+  c->pending[b] = 0;
+  c->last_step[b] = step;
+  return ACP_OK;
+}
+
+acp_status acp_error(const acp_ctx* c, int32_t b, float* e_out, void* stream) {
+  if (!c) return ACP_E_INVALID;
+  if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
+  if (!c->plan.ef) return fail(c, ACP_E_UNSUPPORTED, "no error feedback in this context");
+  if (b < 0 || b >= static_cast<int32_t>(c->plan.buckets.size()))
+    return fail(c, ACP_E_INVALID, "bucket index out of range");
+  if (!e_out || !aligned16(e_out)) return fail(c, ACP_E_INVALID, "e_out must be a 16-byte aligned pointer");
+  const acp_status ds = check_device(c);
+  if (ds != ACP_OK) return ds;
+  acp::KArgs a = base_args(c);
+  a.out = e_out;
+  a.deferred = c->deferred[b];
+  return run(c, c->plan.buckets[b].emat, a, static_cast<hipStream_t>(stream));
+}
+
+acp_status acp_factor(const acp_ctx* c, int32_t tensor_id, int32_t which, float* dev_out, void* stream) {
+  if (!c) return ACP_E_INVALID;
+  if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
+  if (tensor_id < 0 || tensor_id >= c->num_tensors) return fail(c, ACP_E_INVALID, "tensor id out of range");
+  if (which != ACP_FACTOR_P && which != ACP_FACTOR_Q) return fail(c, ACP_E_INVALID, "bad factor");
+  if (!dev_out) return fail(c, ACP_E_INVALID, "dev_out is NULL");
+  const acp::TensorPlan& t = c->plan.tensors[tensor_id];
+  if (t.mat < 0) return fail(c, ACP_E_INVALID, "tensor is not compressed");
+  const int64_t step = c->last_step[t.bucket];
+  if (step < 1) return fail(c, ACP_E_STEP, "no completed step");
+  const acp::MatDesc& d = c->plan.mats[t.mat];
+  const bool odd = (step & 1) != 0;
+  int64_t slot, rows;
+  if (which == ACP_FACTOR_P) {
+    slot = odd ? d.p_slot : d.ph_slot;
+    rows = t.n;
+  } else {
+    slot = odd ? d.qh_slot : d.q_slot;
+    rows = t.m;
+  }
+  const acp_status ds = check_device(c);
+  if (ds != ACP_OK) return ds;
+  const hipError_t e = hipMemcpyAsync(dev_out, c->dev + c->plan.off_fac + slot * 4,
+                                      rows * c->plan.rank * 4, hipMemcpyDeviceToDevice,
+                                      static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(c, ACP_E_DEVICE, std::string("copy failed: ") + hipGetErrorString(e));
+  return ACP_OK;
+}
+
+acp_status acp_checkpoint_bytes(const acp_ctx* c, int64_t* bytes) {
+  if (!c || !bytes) return fail(c, ACP_E_INVALID, "null argument");
+  const int64_t nb = static_cast<int64_t>(c->plan.buckets.size());
+  *bytes = static_cast<int64_t>(sizeof(CkptHeader)) + nb * 16 + checkpoint_payload(c->plan);
+  return ACP_OK;
+}
+
+acp_status acp_get_state(const acp_ctx* c, void* host_buf, int64_t bytes) {
+  if (!c) return ACP_E_INVALID;
+  if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
+  if (!host_buf) return fail(c, ACP_E_INVALID, "host_buf is NULL");
+  int64_t need = 0;
+  acp_checkpoint_bytes(c, &need);
+  if (bytes < need) return fail(c, ACP_E_INVALID, "host buffer too small");
+  for (int64_t p : c->pending)
+    if (p) return fail(c, ACP_E_STEP, "a bucket is between compress and decompress");
+  const acp_status ds = check_device(c);
+  if (ds != ACP_OK) return ds;
+  const acp::Plan& p = c->plan;
+  CkptHeader h{kMagic, kVersion, c->num_tensors, p.rank, p.cap_bytes, c->world, c->flags,
+               static_cast<int64_t>(p.buckets.size()), static_cast<int64_t>(c->seed),
+               p.e_floats, p.fac_floats, p.w_doubles};
+  uint8_t* o = static_cast<uint8_t*>(host_buf);
+  std::memcpy(o, &h, sizeof(h));
+  o += sizeof(h);
+  for (size_t b = 0; b < p.buckets.size(); ++b) {
+    const int64_t rec[2] = {c->last_step[b], static_cast<int64_t>(c->deferred[b])};
+    std::memcpy(o, rec, 16);
+    o += 16;
+  }
+  hipError_t e = hipDeviceSynchronize();
+  if (e == hipSuccess && p.e_floats) e = hipMemcpy(o, c->dev + p.off_e, p.e_floats * 4, hipMemcpyDeviceToHost);
+  o += p.e_floats * 4;
+  if (e == hipSuccess && p.fac_floats) e = hipMemcpy(o, c->dev + p.off_fac, p.fac_floats * 4, hipMemcpyDeviceToHost);
+  o += p.fac_floats * 4;
+  if (e == hipSuccess && p.w_doubles) e = hipMemcpy(o, c->dev + p.off_w, p.w_doubles * 8, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return fail(c, ACP_E_DEVICE, std::string("state download failed: ") + hipGetErrorString(e));
+  return ACP_OK;
+}
+
+acp_status acp_set_state(acp_ctx* c, const void* host_buf, int64_t bytes) {
+  if (!c) return ACP_E_INVALID;
+  if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
+  if (!host_buf) return fail(c, ACP_E_INVALID, "host_buf is NULL");
+  int64_t need = 0;
+  acp_checkpoint_bytes(c, &need);
+  if (bytes < need) return fail(c, ACP_E_STATE, "checkpoint too small");
+  for (int64_t p : c->pending)
+    if (p) return fail(c, ACP_E_STEP, "a bucket is between compress and decompress");
+  const acp::Plan& p = c->plan;
+  CkptHeader h{};
+  std::memcpy(&h, host_buf, sizeof(h));
+  if (h.magic != kMagic || h.version != kVersion || h.num_tensors != c->num_tensors ||
+      h.rank != p.rank || h.cap != p.cap_bytes || h.world != c->world ||
+      h.flags != static_cast<int64_t>(c->flags) || h.nbuckets != static_cast<int64_t>(p.buckets.size()) ||
+      h.seed != static_cast<int64_t>(c->seed) || h.e_floats != p.e_floats ||
+      h.fac_floats != p.fac_floats || h.w_doubles != p.w_doubles)
+    return fail(c, ACP_E_STATE, "checkpoint does not match this context");
+  const acp_status ds = check_device(c);
+  if (ds != ACP_OK) return ds;
+  const uint8_t* i = static_cast<const uint8_t*>(host_buf) + sizeof(h);
+  std::vector<int64_t> steps(p.buckets.size());
+  std::vector<uint8_t> defr(p.buckets.size());
+  for (size_t b = 0; b < p.buckets.size(); ++b) {
+    int64_t rec[2];
+    std::memcpy(rec, i, 16);
+    i += 16;
+    if (rec[0] < 0 || rec[1] < 0 || rec[1] > 1) return fail(c, ACP_E_STATE, "corrupt checkpoint");
+    steps[b] = rec[0];
+    defr[b] = static_cast<uint8_t>(rec[1]);
+  }
+  hipError_t e = hipDeviceSynchronize();
+  if (e == hipSuccess && p.e_floats) e = hipMemcpy(c->dev + p.off_e, i, p.e_floats * 4, hipMemcpyHostToDevice);
+  i += p.e_floats * 4;
+  if (e == hipSuccess && p.fac_floats) e = hipMemcpy(c->dev + p.off_fac, i, p.fac_floats * 4, hipMemcpyHostToDevice);
+  i += p.fac_floats * 4;
+  if (e == hipSuccess && p.w_doubles) e = hipMemcpy(c->dev + p.off_w, i, p.w_doubles * 8, hipMemcpyHostToDevice);
+  if (e != hipSuccess) return fail(c, ACP_E_DEVICE, std::string("state upload failed: ") + hipGetErrorString(e));
+  c->last_step = steps;
+  c->deferred = defr;
+  return ACP_OK;
+}
+
+const char* acp_last_error(const acp_ctx* c) { return c ? c->err.c_str() : "null context"; }
+
+void acp_destroy(acp_ctx* c) { delete c; }
+
+}  // extern "C"

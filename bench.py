@@ -89,8 +89,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="bert_large_r4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--kernel-steps", type=int, default=20,
-                    help="steps of the per-launch event pass that times the dominant kernel")
+    ap.add_argument("--streams", type=int, default=4,
+                    help="per-bucket mode: HIP streams the buckets are spread over (bucket b on "
+                         "stream b %% streams)")
+    ap.add_argument("--mode", choices=["all", "bucket"], default="all",
+                    help="all: acp_compress_all / acp_decompress_all (every bucket in one launch per "
+                         "kernel kind); bucket: acp_compress / acp_decompress per bucket")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
@@ -101,6 +105,7 @@ def main():
     import numpy as np
     import torch
     import synthgrad as sg
+    from paper_2306_08881_amd import _lib as L
     from paper_2306_08881_amd.acp import Acp
 
     wl = sg.WORKLOADS[args.workload]
@@ -127,72 +132,81 @@ def main():
         del grads
     fbuf = [torch.zeros(max(i[2], i[3], 4), dtype=torch.float32, device=dev) for i in info]
     out = [torch.zeros(i[1], dtype=torch.float32, device=dev) for i in info]
+    main = torch.cuda.current_stream()
+    nstreams = max(1, args.streams)
+    streams = [main] if nstreams == 1 else [torch.cuda.Stream(device=dev) for _ in range(nstreams)]
     torch.cuda.synchronize()
-    print(f"# setup {time.time() - t_setup:.1f}s: {wl.name}, {nb} buckets, {wl.numel} parameters",
-          file=sys.stderr, flush=True)
+    print(f"# setup {time.time() - t_setup:.1f}s: {wl.name}, {nb} buckets, {wl.numel} parameters, "
+          f"{nstreams} stream(s)", file=sys.stderr, flush=True)
 
     step_no = [0]
 
-    def one_step(events=None):
+    def one_step(mode):
         step_no[0] += 1
         t = step_no[0]
         g = gsets[t % 2]
+        if mode == "all":
+            acp.compress_all(t, g, fbuf, stream=main)
+            acp.decompress_all(t, fbuf, out, stream=main)
+            return
+        if nstreams > 1:
+            fork = torch.cuda.Event()
+            fork.record(main)
+            for s in streams:
+                s.wait_event(fork)
         for b in range(nb):
-            if events is not None:
-                events.append(("c", t, b, torch.cuda.Event(enable_timing=True)))
-                events[-1][3].record()
-            acp.compress(t, b, g[b], fbuf[b])
-            if events is not None:
-                events.append(("d", t, b, torch.cuda.Event(enable_timing=True)))
-                events[-1][3].record()
-            acp.decompress(t, b, fbuf[b], out[b])
-        if events is not None:
-            events.append(("e", t, -1, torch.cuda.Event(enable_timing=True)))
-            events[-1][3].record()
+            s = streams[b % nstreams]
+            acp.compress(t, b, g[b], fbuf[b], stream=s)
+            acp.decompress(t, b, fbuf[b], out[b], stream=s)
+        if nstreams > 1:
+            for s in streams:
+                join = torch.cuda.Event()
+                join.record(s)
+                main.wait_event(join)
 
+    def timed(steps, mode):
+        torch.cuda.synchronize()
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record(main)
+        for _ in range(steps):
+            one_step(mode)
+        end.record(main)
+        torch.cuda.synchronize()
+        return start.elapsed_time(end) / steps
+
+    other = "bucket" if args.mode == "all" else "all"
     for _ in range(args.warmup):
-        one_step()
-    if args.warmup % 2:  # start the timed region on a P-step
-        one_step()
-    torch.cuda.synchronize()
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record()
-    for _ in range(args.steps):
-        one_step()
-    end.record()
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / args.steps
+        one_step(args.mode)
+    if step_no[0] % 2:  # start every timed region on a P-step
+        one_step(args.mode)
+    steps = args.steps + (args.steps % 2)
+    ms = timed(steps, args.mode)
+    ms_other = timed(steps, other)
 
-    # per-launch pass: the P-step compress launch is the dominant kernel (12 B per element of
-    # the 16 B step); time each compress call with events on the stream the kernels run on
-    ev = []
-    for _ in range(args.kernel_steps + (args.kernel_steps % 2)):
-        one_step(ev)
-    torch.cuda.synchronize()
-    comp_p, comp_q, dec = [], [], []
-    for i, (kind, t, b, e) in enumerate(ev[:-1]):
-        nxt = ev[i + 1][3]
-        dt = e.elapsed_time(nxt) * 1e-3
-        if kind == "c":
-            (comp_p if t % 2 == 1 else comp_q).append((b, dt))
-        elif kind == "d":
-            dec.append((b, dt))
+    # per-kernel pass: the same steps again with every launch of one kernel family bracketed by
+    # HIP events on its own stream (acp_profile_*), once per family
+    fams = {"P-step compress (k_pfused)": L.ACP_KERNEL_P_STEP,
+            "Q-step compress (k_qstep)": L.ACP_KERNEL_Q_STEP,
+            "Q-step finish (k_qfin)": L.ACP_KERNEL_Q_FINISH,
+            "decompress (k_recon4)": L.ACP_KERNEL_RECONSTRUCT}
+    kern = {}
+    for name, fam in fams.items():
+        acp.profile_start(fam, 64 * nb * steps)
+        timed(steps, args.mode)
+        n, sec, by = acp.profile_stop()
+        if n:
+            kern[name] = {"launches": n, "avg_launch_us": sec / n * 1e6, "bytes_per_launch": by / n,
+                          "gbs": by / sec / 1e9, "ms_per_step": sec / steps * 1e3}
+    dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
+    dk = kern[dom]
     step_bytes, bp, bq, bd, nc, n1 = algorithmic_bytes(wl, wl.rank)
-    t_p = sum(dt for _, dt in comp_p) / (len(comp_p) / nb)   # seconds of P-step compress per step
-    t_q = sum(dt for _, dt in comp_q) / (len(comp_q) / nb)
-    t_d = sum(dt for _, dt in dec) / (len(dec) / nb)
-    launches = len(comp_p) / (len(comp_p) / nb) if comp_p else 1
-    kern = {"name": "acp_compress P-step (orth apply + fused P-step kernels)",
-            "avg_launch_us": t_p / nb * 1e6, "bytes_per_launch": bp / nb}
-    achieved = bp / t_p / 1e9
-
     gbs = step_bytes / (ms * 1e-3) / 1e9
     res = {
         "metric": "ACP-SGD compress+decompress gradient GB/s and % HBM peak, BERT-large r=4",
         "value": round(gbs, 2),
         "unit": "GB/s",
         "n_gpus": 1,
-        "steps": args.steps,
+        "steps": steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
         "higher_is_better": True,
@@ -202,16 +216,18 @@ def main():
         "data": "synthetic (seeded N(0, 0.02^2) gradients of the workload's shapes)",
         "config": {"workload": f"{wl.name}: BERT-large-shaped gradients, {len(shapes)} tensors, "
                                f"{wl.numel} parameters, rank {wl.rank}, 25 MiB buckets ({nb})",
-                   "rank": wl.rank, "buckets": nb, "parameters": wl.numel,
+                   "rank": wl.rank, "buckets": nb, "parameters": wl.numel, "mode": args.mode,
+                   "streams": nstreams if args.mode == "bucket" else 1,
+                   f"ms_per_step_{other}_mode": round(ms_other, 4),
+                   f"gbs_{other}_mode": round(step_bytes / (ms_other * 1e-3) / 1e9, 2),
                    "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
                    "gradient_elements_per_s": round(wl.numel / (ms * 1e-3), 1),
                    "algorithmic_bytes_per_step": step_bytes,
-                   "ms_p_compress": round(t_p * 1e3, 4), "ms_q_compress": round(t_q * 1e3, 4),
-                   "ms_decompress": round(t_d * 1e3, 4)},
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": kern["name"], "avg_launch_us": round(kern["avg_launch_us"], 3),
-                     "bytes_per_launch": kern["bytes_per_launch"]},
+                   "kernels": {k: {kk: round(vv, 3) for kk, vv in v.items()} for k, v in kern.items()}},
+        "roofline": {"bound": "hbm", "achieved": round(dk["gbs"], 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(dk["gbs"] / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": dom, "avg_launch_us": round(dk["avg_launch_us"], 3),
+                     "bytes_per_launch": round(dk["bytes_per_launch"], 1)},
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl)

@@ -97,9 +97,9 @@ acp_status acp_state_bytes(const acp_ctx *ctx, int64_t *bytes);
 
 /*
  * acp_bind_state - adopt the caller's device block (>= acp_state_bytes, 256-byte aligned) on
- * the current HIP device.  Uploads P_0, Q_0 and the launch tables, zeroes E and the workspace
- * counters, and orthogonalises Q_0 for step 1, all on `stream` (a hipStream_t, or NULL for the
- * default stream), then waits for the stream.  Re-binding resets the state to step 0.
+ * the current HIP device.  Uploads P_0, Q_0 and the launch tables, zeroes E and prepares the
+ * orthogonalisation of Q_0 for step 1, all on `stream` (a hipStream_t, or NULL for the default
+ * stream), then waits for the stream.  Re-binding resets the state to step 0.
  */
 acp_status acp_bind_state(acp_ctx *ctx, void *device_ptr, int64_t bytes, void *stream);
 
@@ -145,6 +145,19 @@ acp_status acp_decompress(acp_ctx *ctx, int64_t step, int32_t b, const float *ag
                           void *stream);
 
 /*
+ * acp_compress_all / acp_decompress_all - the same step for every bucket at once (one launch per
+ * kernel kind for up to 64 buckets), as after a backward pass without overlap.  Results are
+ * bitwise those of calling acp_compress / acp_decompress for every bucket.  `grads`,
+ * `factor_bufs`, `agg_factors` and `outs` are host arrays of acp_num_buckets() device
+ * pointers, each with the layout of the per-bucket call.  Every bucket must be ready for the
+ * step, else ACP_E_STEP and nothing is enqueued.
+ */
+acp_status acp_compress_all(acp_ctx *ctx, int64_t step, const float *const *grads,
+                            float *const *factor_bufs, void *stream);
+acp_status acp_decompress_all(acp_ctx *ctx, int64_t step, const float *const *agg_factors,
+                              float *const *outs, void *stream);
+
+/*
  * acp_error - write the current error E of bucket b's compressed tensors into `e_out` (device,
  * laid out like the gradient bucket; vector slots are left untouched).  Does not change the state.
  * ACP_E_UNSUPPORTED without error feedback.
@@ -169,6 +182,24 @@ acp_status acp_factor(const acp_ctx *ctx, int32_t tensor_id, int32_t which, floa
 acp_status acp_checkpoint_bytes(const acp_ctx *ctx, int64_t *bytes);
 acp_status acp_get_state(const acp_ctx *ctx, void *host_buf, int64_t bytes);
 acp_status acp_set_state(acp_ctx *ctx, const void *host_buf, int64_t bytes);
+
+/*
+ * Kernel timing, for benchmarks: acp_profile_start makes every later launch of one kernel family
+ * on this context record a HIP event pair on its stream (at most max_launches launches; later
+ * ones run untimed); acp_profile_stop waits for those events and returns the number of timed
+ * launches, their summed duration in seconds and their summed algorithmic bytes (the data the
+ * method must move, excluding any re-reads: 12 B per element of M, E read and E written in a
+ * compress kernel, 4 B per element of M_hat, 8 B per raw-vector element, 4 B per factor
+ * element read or written).  Events are created in acp_profile_start and destroyed in
+ * acp_profile_stop; no device memory is allocated.
+ */
+#define ACP_KERNEL_P_STEP 1       /* P-step compress kernels */
+#define ACP_KERNEL_Q_STEP 2       /* Q-step compress main kernel */
+#define ACP_KERNEL_Q_FINISH 3     /* Q-step partial-sum finish */
+#define ACP_KERNEL_RECONSTRUCT 4  /* decompress kernels */
+#define ACP_KERNEL_ORTH 5         /* separate orthogonalisation kernels (general path, r > 8) */
+acp_status acp_profile_start(acp_ctx *ctx, int32_t kernel_family, int32_t max_launches);
+acp_status acp_profile_stop(acp_ctx *ctx, int64_t *launches, double *seconds, double *alg_bytes);
 
 /* Text of the last error on this context ("" if none).  Valid until the next call on ctx. */
 const char *acp_last_error(const acp_ctx *ctx);

@@ -25,6 +25,11 @@ ACP_FLAG_REUSE = 2
 ACP_FLAGS_DEFAULT = 3
 ACP_FACTOR_P = 0
 ACP_FACTOR_Q = 1
+ACP_KERNEL_P_STEP = 1
+ACP_KERNEL_Q_STEP = 2
+ACP_KERNEL_Q_FINISH = 3
+ACP_KERNEL_RECONSTRUCT = 4
+ACP_KERNEL_ORTH = 5
 
 _p = C.c_void_p
 _i32, _i64, _u32, _u64 = C.c_int32, C.c_int64, C.c_uint32, C.c_uint64
@@ -43,11 +48,15 @@ SIGNATURES = {
     "acp_init_factor": (_i32, [_p, _i32, _i32, _pf, _i64]),
     "acp_compress": (_i32, [_p, _i64, _i32, _pf, _pf, _p]),
     "acp_decompress": (_i32, [_p, _i64, _i32, _pf, _pf, _p]),
+    "acp_compress_all": (_i32, [_p, _i64, _p, _p, _p]),
+    "acp_decompress_all": (_i32, [_p, _i64, _p, _p, _p]),
     "acp_error": (_i32, [_p, _i32, _pf, _p]),
     "acp_factor": (_i32, [_p, _i32, _i32, _pf, _p]),
     "acp_checkpoint_bytes": (_i32, [_p, _pi64]),
     "acp_get_state": (_i32, [_p, _p, _i64]),
     "acp_set_state": (_i32, [_p, _p, _i64]),
+    "acp_profile_start": (_i32, [_p, _i32, _i32]),
+    "acp_profile_stop": (_i32, [_p, _pi64, C.POINTER(C.c_double), C.POINTER(C.c_double)]),
     "acp_last_error": (C.c_char_p, [_p]),
     "acp_destroy": (None, [_p]),
 }

@@ -117,6 +117,19 @@ class Acp:
         _check(self.lib.acp_decompress(self.ctx, step, b, _fptr(agg_factor), _fptr(out), _stream_ptr(stream)),
                self.lib, self.ctx, "acp_decompress")
 
+    def compress_all(self, step: int, grads, factor_bufs, stream=None):
+        """One step for every bucket: ``grads`` / ``factor_bufs`` are lists of device tensors."""
+        g = (C.c_void_p * len(grads))(*[_fptr(x) for x in grads])
+        f = (C.c_void_p * len(factor_bufs))(*[_fptr(x) for x in factor_bufs])
+        _check(self.lib.acp_compress_all(self.ctx, step, g, f, _stream_ptr(stream)), self.lib, self.ctx,
+               "acp_compress_all")
+
+    def decompress_all(self, step: int, aggs, outs, stream=None):
+        a = (C.c_void_p * len(aggs))(*[_fptr(x) for x in aggs])
+        o = (C.c_void_p * len(outs))(*[_fptr(x) for x in outs])
+        _check(self.lib.acp_decompress_all(self.ctx, step, a, o, _stream_ptr(stream)), self.lib, self.ctx,
+               "acp_decompress_all")
+
     # ---- inspection and checkpoint
     def error(self, b: int, e_out, stream=None):
         _check(self.lib.acp_error(self.ctx, b, _fptr(e_out), _stream_ptr(stream)), self.lib, self.ctx, "acp_error")
@@ -139,6 +152,17 @@ class Acp:
     def set_state(self, blob: bytes):
         buf = C.create_string_buffer(blob, len(blob))
         _check(self.lib.acp_set_state(self.ctx, buf, len(blob)), self.lib, self.ctx, "acp_set_state")
+
+    def profile_start(self, family: int, max_launches: int = 4096):
+        _check(self.lib.acp_profile_start(self.ctx, family, max_launches), self.lib, self.ctx,
+               "acp_profile_start")
+
+    def profile_stop(self):
+        """(timed launches, seconds, algorithmic bytes) since profile_start."""
+        n, sec, by = C.c_int64(), C.c_double(), C.c_double()
+        _check(self.lib.acp_profile_stop(self.ctx, C.byref(n), C.byref(sec), C.byref(by)), self.lib,
+               self.ctx, "acp_profile_stop")
+        return n.value, sec.value, by.value
 
     def close(self):
         if getattr(self, "ctx", None):

@@ -5,14 +5,18 @@
 //   E arena   fp32, one slot per gradient-bucket element (vector slots unused); the E of a
 //             matrix sits at its bucket's E base + its offset in the gradient bucket.  After
 //             a Q-step it holds F = M + E_prev and E = F - P_hat Q_loc^T is implied (deferred).
-//   factors   fp32 per compressed matrix: P (n x r), Q (m x r), Ph (n x r), Qh (m x r),
-//             Ql (m x r), all row-major.
+//   factors   fp32 per compressed matrix: P (n x r), Ph (n x r), Q (m x r), Qh (m x r),
+//             Ql (m x r), all row-major.  P / Q hold the aggregated factor of the last step
+//             that produced it, Ph / Qh the orthogonalised factors, Ql the local Q of the
+//             last Q-step.
 //   W         fp64 r x r per matrix: the upper-triangular map with orth(X) = X W for the
 //             factor that the next step orthogonalises.
-//   gpart     fp64 Gram partial sums, r x r per slice of factor rows.
+//   gpart     fp64 Gram partial sums, r x r per slice of factor rows (factors of more than one
+//             slice only).
 //   qpart     fp32 Q-step partial products, per row chunk: m_pad x r.
-//   counters  u32 arrival counters of the last-block reductions.
 //   tables    MatDesc[], VecDesc[], Tile[] for every launch.
+// No kernel communicates across workgroups: every reduction that spans workgroups is
+// finished by a later kernel in the same stream.
 #pragma once
 
 #include <cstdint>
@@ -33,70 +37,82 @@ struct MatDesc {
   int64_t gpart;      // double offset in the Gram-partial region
   int64_t qpart;      // float offset in the Q-partial region
   int32_t n, m;
-  int32_t ctr_gram;   // counter index of the Gram reduction
-  int32_t ctr_q;      // first counter index of the Q-step reductions (one per column block)
   int32_t q_rows;     // rows per Q-step row chunk
   int32_t q_chunks;   // number of Q-step row chunks
   int32_t q_cb;       // Q-step column-block width
   int32_t fact_rows;  // factor rows per Gram slice
-  int32_t wpr;        // waves per row in the fused P-step
-  int32_t pad;
+  int32_t scls;       // column class S of the rank-4 kernels (64 S float4 groups per wave)
+  int32_t bucket;     // bucket index
+  int32_t fact_slices_p, fact_slices_q;  // Gram slices of the P / Q factor rows
 };
 
 struct VecDesc {
   int64_t grad_off, fac_off_p, fac_off_q, numel;
+  int32_t bucket, pad;
 };
 
 enum TileKind : int32_t { T_ROWS = 0, T_FACT = 1, T_VEC = 2, T_QTILE = 3 };
 
-// kind T_ROWS: idx = matrix, a = first row, b = row count
-// kind T_FACT: idx = matrix, a = slice, b = slice count
-// kind T_VEC : idx = vector, a = first element, b = element count
-// kind T_QTILE: idx = matrix, a = row chunk, b = column block
+// kind T_ROWS : idx = matrix, a = first row, b = row count
+// kind T_FACT : idx = matrix, a = slice, b = slice count
+// kind T_VEC  : idx = vector, a = first element, b = element count
+// kind T_QTILE: idx = matrix, a = row chunk (K_QSTEP) or entry block (K_QFIN), b = column block
 struct Tile {
   int32_t kind, idx, a, b;
 };
 
 enum KernelId : int32_t {
-  K_APPLY = 0,   // Xh = X W (orthogonalise the reused factor)
-  K_PFUSED,      // P-step, one pass: P = M' Qh, E = M' - P Qh^T, raw vectors packed
+  K_APPLY = 0,   // Xh = X W (orthogonalise the reused factor), general path
+  K_PFUSED,      // P-step, one pass (r = 4): Qh = Q W, P = M' Qh, E = M' - P Qh^T, vectors packed
   K_PROW,        // P-step, general: P = M' Qh, one workgroup per row
   K_EUPD,        // P-step, general: E = M' - P Qh^T
-  K_QSTEP,       // Q-step: F = M', Q = M'^T Ph (deterministic two-level sum), raw vectors packed
-  K_RECON,       // decompress: M_hat = P Q^T / p, factor kept + Gram -> W, raw vectors / p
-  K_GRAM,        // Gram -> W of a factor slot (after bind / restore)
+  K_QSTEP,       // Q-step: F = M' written back, per-chunk partials of M'^T Ph, vectors packed
+  K_QFIN,        // Q-step: Q_loc = sum of the chunk partials -> factor buffer and Ql
+  K_RECON,       // decompress, general: M_hat = P Q^T / p; factor tiles; vectors / p
+  K_RECON4,      // decompress, r = 4 register-resident columns; factor tiles; vectors / p
+  K_FACT,        // factor tiles alone: Gram -> W (after bind / restore)
+  K_CHOL,        // sum of a factor's Gram partials (more than one slice) -> W
   K_EMAT,        // materialise E into a bucket-shaped buffer
   K_VEC,         // pack raw vectors only
 };
 
+// K_QSTEP variants: column slots per lane | kQFused when the kernel also orthogonalises P
+constexpr int32_t kQFused = 16;
+// K_FACT variants: bit 0 = Q (else P); the factor is read from its state slot
+
 struct Launch {
   int32_t kernel;
-  int32_t variant;   // kernel-specific: column slots per lane (K_PFUSED), vector width (K_QSTEP,
-                     // K_RECON, K_EMAT, K_EUPD), factor P=0 / Q=1 (K_APPLY, K_GRAM)
+  int32_t variant;   // kernel-specific: column class S (K_PFUSED, K_RECON4), vector width
+                     // (K_QSTEP, K_RECON), factor P=0 / Q=1 (K_APPLY, K_FACT)
   int64_t tile_off;  // first tile in the tile table
   int32_t ntiles;
-  int32_t pad;
+  int32_t family;    // ACP_KERNEL_* family (host-side profiling)
+  double alg_bytes;  // algorithmic bytes of the launch (host-side profiling)
 };
+
+// Buckets per launch: a launch covers the buckets [base, base + kMaxGroup) at most; their
+// buffer addresses travel in the kernel arguments.
+constexpr int kMaxGroup = 64;
 
 // Kernel arguments (passed by value).
 struct KArgs {
-  const float* grad;    // gradient bucket (compress)
-  float* fbuf;          // factor buffer (compress writes)
-  const float* agg;     // aggregated factor buffer (decompress reads)
-  float* out;           // output bucket (decompress / E export)
+  const float* src[kMaxGroup];  // per bucket: gradient bucket (compress) or aggregated factor
+                                // buffer (decompress)
+  float* dst[kMaxGroup];        // per bucket: factor buffer (compress), output bucket
+                                // (decompress, E export)
   float* e;             // E arena
   float* fac;           // factor region
   double* w;            // W region
   double* gpart;        // Gram partials
   float* qpart;         // Q-step partials
-  uint32_t* ctr;        // counters
   const MatDesc* mats;
   const VecDesc* vecs;
   const Tile* tiles;    // this launch's tiles
+  uint64_t deferred;    // bit i: the E arena of bucket base + i holds F (E implied)
+  int32_t base;         // bucket of src[0] / dst[0]
   int32_t ntiles;
   int32_t variant;
   int32_t ef;           // error feedback on
-  int32_t deferred;     // E arena holds F (E implied) for this bucket
   float inv_p;          // 1 / world size
   int32_t parity;       // 1 on odd (P-) steps, 0 on even (Q-) steps
 };

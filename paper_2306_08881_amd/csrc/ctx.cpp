@@ -28,6 +28,12 @@ struct acp_ctx {
   std::vector<int64_t> pending;     // per bucket: compressed step awaiting decompress (0 = none)
   std::vector<uint8_t> deferred;    // per bucket: E arena holds F
   mutable std::string err;
+
+  // kernel timing (acp_profile_start / acp_profile_stop)
+  int32_t prof_family = 0;
+  std::vector<hipEvent_t> prof_events;  // begin, end pairs
+  int64_t prof_used = 0;
+  double prof_bytes = 0.0;
 };
 
 namespace {
@@ -59,7 +65,6 @@ acp::KArgs base_args(const acp_ctx* c) {
   a.w = reinterpret_cast<double*>(d + p.off_w);
   a.gpart = reinterpret_cast<double*>(d + p.off_gpart);
   a.qpart = reinterpret_cast<float*>(d + p.off_qpart);
-  a.ctr = reinterpret_cast<uint32_t*>(d + p.off_ctr);
   a.mats = reinterpret_cast<const acp::MatDesc*>(d + p.off_mats);
   a.vecs = reinterpret_cast<const acp::VecDesc*>(d + p.off_vecs);
   a.ef = p.ef ? 1 : 0;
@@ -70,13 +75,24 @@ acp::KArgs base_args(const acp_ctx* c) {
 acp_status run(const acp_ctx* c, const std::vector<acp::Launch>& launches, acp::KArgs a,
                hipStream_t s) {
   const acp::Tile* tiles = reinterpret_cast<const acp::Tile*>(c->dev + c->plan.off_tiles);
+  acp_ctx* mc = const_cast<acp_ctx*>(c);
   for (const acp::Launch& l : launches) {
     a.tiles = tiles + l.tile_off;
     a.ntiles = l.ntiles;
     a.variant = l.variant;
+    const bool timed = mc->prof_family != 0 && l.family == mc->prof_family &&
+                       2 * mc->prof_used < static_cast<int64_t>(mc->prof_events.size());
+    if (timed && hipEventRecord(mc->prof_events[2 * mc->prof_used], s) != hipSuccess)
+      return fail(c, ACP_E_DEVICE, "hipEventRecord failed");
     const hipError_t e = acp::launch(l, c->plan.rank, a, s);
     if (e != hipSuccess)
       return fail(c, ACP_E_DEVICE, std::string("kernel launch failed: ") + hipGetErrorString(e));
+    if (timed) {
+      if (hipEventRecord(mc->prof_events[2 * mc->prof_used + 1], s) != hipSuccess)
+        return fail(c, ACP_E_DEVICE, "hipEventRecord failed");
+      mc->prof_used += 1;
+      mc->prof_bytes += l.alg_bytes;
+    }
   }
   return ACP_OK;
 }
@@ -150,7 +166,6 @@ acp_status acp_bind_state(acp_ctx* c, void* device_ptr, int64_t bytes, void* str
   uint8_t* d = static_cast<uint8_t*>(device_ptr);
   hipError_t e = hipSuccess;
   if (p.e_floats) e = hipMemsetAsync(d + p.off_e, 0, p.e_floats * 4, s);
-  if (e == hipSuccess && p.n_ctr) e = hipMemsetAsync(d + p.off_ctr, 0, p.n_ctr * 4, s);
   if (e == hipSuccess && p.fac_floats)
     e = hipMemcpyAsync(d + p.off_fac, c->init_fac.data(), p.fac_floats * 4, hipMemcpyHostToDevice, s);
   if (e == hipSuccess && !p.mats.empty())
@@ -269,8 +284,9 @@ acp_status acp_compress(acp_ctx* c, int64_t step, int32_t b, const float* grad, 
   const acp_status ds = check_device(c);
   if (ds != ACP_OK) return ds;
   acp::KArgs a = base_args(c);
-  a.grad = grad;
-  a.fbuf = factor_buf;
+  a.base = b;
+  a.src[0] = grad;
+  a.dst[0] = factor_buf;
   a.parity = static_cast<int32_t>(step & 1);
   a.deferred = c->deferred[b];
   const acp_status st = run(c, bk.compress[step & 1], a, static_cast<hipStream_t>(stream));
@@ -302,14 +318,97 @@ acp_status acp_decompress(acp_ctx* c, int64_t step, int32_t b, const float* agg_
   const acp_status ds = check_device(c);
   if (ds != ACP_OK) return ds;
   acp::KArgs a = base_args(c);
-  a.agg = agg_factor;
-  a.out = out;
+  a.base = b;
+  a.src[0] = agg_factor;
+  a.dst[0] = out;
   a.parity = static_cast<int32_t>(step & 1);
   a.deferred = c->deferred[b];
   const acp_status st = run(c, bk.decompress[step & 1], a, static_cast<hipStream_t>(stream));
   if (st != ACP_OK) return st;
   c->pending[b] = 0;
   c->last_step[b] = step;
+  return ACP_OK;
+}
+
+acp_status acp_compress_all(acp_ctx* c, int64_t step, const float* const* grads,
+                            float* const* factor_bufs, void* stream) {
+  if (!c) return ACP_E_INVALID;
+  if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
+  if (!grads || !factor_bufs) return fail(c, ACP_E_INVALID, "null pointer array");
+  const int32_t nb = static_cast<int32_t>(c->plan.buckets.size());
+  for (int32_t b = 0; b < nb; ++b) {
+    const acp::BucketPlan& bk = c->plan.buckets[b];
+    if (!grads[b] || !factor_bufs[b]) return fail(c, ACP_E_INVALID, "null buffer");
+    if (!aligned16(grads[b]) || !aligned16(factor_bufs[b]))
+      return fail(c, ACP_E_INVALID, "buffers must be 16-byte aligned");
+    if (c->pending[b] != 0 || step != c->last_step[b] + 1)
+      return fail(c, ACP_E_STEP, "bucket " + std::to_string(b) + " is not ready for step " +
+                                     std::to_string(step));
+    const char* g0 = reinterpret_cast<const char*>(grads[b]);
+    const char* f0 = reinterpret_cast<const char*>(factor_bufs[b]);
+    const int64_t fe = (step & 1) ? bk.fac_elems_p : bk.fac_elems_q;
+    if (g0 < f0 + fe * 4 && f0 < g0 + bk.grad_elems * 4)
+      return fail(c, ACP_E_INVALID, "factor_buf overlaps grad");
+  }
+  const acp_status ds = check_device(c);
+  if (ds != ACP_OK) return ds;
+  for (size_t g = 0; g < c->plan.group_compress.size(); ++g) {
+    acp::KArgs a = base_args(c);
+    a.base = static_cast<int32_t>(g) * acp::kMaxGroup;
+    a.parity = static_cast<int32_t>(step & 1);
+    for (int32_t i = 0; i < acp::kMaxGroup && a.base + i < nb; ++i) {
+      a.src[i] = grads[a.base + i];
+      a.dst[i] = factor_bufs[a.base + i];
+      if (c->deferred[a.base + i]) a.deferred |= 1ull << i;
+    }
+    const acp_status st = run(c, c->plan.group_compress[g][step & 1], a, static_cast<hipStream_t>(stream));
+    if (st != ACP_OK) return st;
+  }
+  for (int32_t b = 0; b < nb; ++b) {
+    c->pending[b] = step;
+    if (c->plan.ef) c->deferred[b] = (step & 1) ? 0 : 1;
+  }
+  return ACP_OK;
+}
+
+acp_status acp_decompress_all(acp_ctx* c, int64_t step, const float* const* agg_factors,
+                              float* const* outs, void* stream) {
+  if (!c) return ACP_E_INVALID;
+  if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
+  if (!agg_factors || !outs) return fail(c, ACP_E_INVALID, "null pointer array");
+  const int32_t nb = static_cast<int32_t>(c->plan.buckets.size());
+  for (int32_t b = 0; b < nb; ++b) {
+    const acp::BucketPlan& bk = c->plan.buckets[b];
+    if (!agg_factors[b] || !outs[b]) return fail(c, ACP_E_INVALID, "null buffer");
+    if (!aligned16(agg_factors[b]) || !aligned16(outs[b]))
+      return fail(c, ACP_E_INVALID, "buffers must be 16-byte aligned");
+    if (c->pending[b] != step)
+      return fail(c, ACP_E_STEP, "bucket " + std::to_string(b) + " has no compressed step " +
+                                     std::to_string(step));
+    const char* a0 = reinterpret_cast<const char*>(agg_factors[b]);
+    const char* o0 = reinterpret_cast<const char*>(outs[b]);
+    const int64_t fe = (step & 1) ? bk.fac_elems_p : bk.fac_elems_q;
+    if (o0 < a0 + fe * 4 && a0 < o0 + bk.grad_elems * 4)
+      return fail(c, ACP_E_INVALID, "out overlaps agg_factor");
+  }
+  const acp_status ds = check_device(c);
+  if (ds != ACP_OK) return ds;
+  for (size_t g = 0; g < c->plan.group_decompress.size(); ++g) {
+    acp::KArgs a = base_args(c);
+    a.base = static_cast<int32_t>(g) * acp::kMaxGroup;
+    a.parity = static_cast<int32_t>(step & 1);
+    for (int32_t i = 0; i < acp::kMaxGroup && a.base + i < nb; ++i) {
+      a.src[i] = agg_factors[a.base + i];
+      a.dst[i] = outs[a.base + i];
+      if (c->deferred[a.base + i]) a.deferred |= 1ull << i;
+    }
+    const acp_status st = run(c, c->plan.group_decompress[g][step & 1], a, static_cast<hipStream_t>(stream));
+    if (st != ACP_OK) return st;
+  }
+  for (int32_t b = 0; b < nb; ++b) {
+    c->pending[b] = 0;
+    c->last_step[b] = step;
+  }
   return ACP_OK;
 }
 
@@ -323,7 +422,8 @@ acp_status acp_error(const acp_ctx* c, int32_t b, float* e_out, void* stream) {
   const acp_status ds = check_device(c);
   if (ds != ACP_OK) return ds;
   acp::KArgs a = base_args(c);
-  a.out = e_out;
+  a.base = b;
+  a.dst[0] = e_out;
   a.deferred = c->deferred[b];
   return run(c, c->plan.buckets[b].emat, a, static_cast<hipStream_t>(stream));
 }
@@ -440,8 +540,63 @@ acp_status acp_set_state(acp_ctx* c, const void* host_buf, int64_t bytes) {
   return ACP_OK;
 }
 
+acp_status acp_profile_start(acp_ctx* c, int32_t kernel_family, int32_t max_launches) {
+  if (!c) return ACP_E_INVALID;
+  if (kernel_family < ACP_KERNEL_P_STEP || kernel_family > ACP_KERNEL_ORTH)
+    return fail(c, ACP_E_INVALID, "unknown kernel family");
+  if (max_launches < 1 || max_launches > (1 << 20)) return fail(c, ACP_E_INVALID, "bad max_launches");
+  if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
+  if (c->prof_family != 0) return fail(c, ACP_E_STATE, "profiling already active");
+  const acp_status ds = check_device(c);
+  if (ds != ACP_OK) return ds;
+  c->prof_events.assign(2 * static_cast<size_t>(max_launches), nullptr);
+  for (hipEvent_t& ev : c->prof_events) {
+    if (hipEventCreate(&ev) != hipSuccess) {
+      for (hipEvent_t& e2 : c->prof_events)
+        if (e2) (void)hipEventDestroy(e2);
+      c->prof_events.clear();
+      return fail(c, ACP_E_DEVICE, "hipEventCreate failed");
+    }
+  }
+  c->prof_family = kernel_family;
+  c->prof_used = 0;
+  c->prof_bytes = 0.0;
+  return ACP_OK;
+}
+
+acp_status acp_profile_stop(acp_ctx* c, int64_t* launches, double* seconds, double* alg_bytes) {
+  if (!c) return ACP_E_INVALID;
+  if (c->prof_family == 0) return fail(c, ACP_E_STATE, "profiling not active");
+  double total_ms = 0.0;
+  acp_status st = ACP_OK;
+  for (int64_t i = 0; i < c->prof_used; ++i) {
+    float ms = 0.f;
+    if (hipEventSynchronize(c->prof_events[2 * i + 1]) != hipSuccess ||
+        hipEventElapsedTime(&ms, c->prof_events[2 * i], c->prof_events[2 * i + 1]) != hipSuccess) {
+      st = fail(c, ACP_E_DEVICE, "reading profile events failed");
+      break;
+    }
+    total_ms += ms;
+  }
+  for (hipEvent_t& ev : c->prof_events)
+    if (ev) (void)hipEventDestroy(ev);
+  if (launches) *launches = c->prof_used;
+  if (seconds) *seconds = total_ms * 1e-3;
+  if (alg_bytes) *alg_bytes = c->prof_bytes;
+  c->prof_events.clear();
+  c->prof_family = 0;
+  c->prof_used = 0;
+  c->prof_bytes = 0.0;
+  return st;
+}
+
 const char* acp_last_error(const acp_ctx* c) { return c ? c->err.c_str() : "null context"; }
 
-void acp_destroy(acp_ctx* c) { delete c; }
+void acp_destroy(acp_ctx* c) {
+  if (!c) return;
+  for (hipEvent_t& ev : c->prof_events)
+    if (ev) (void)hipEventDestroy(ev);
+  delete c;
+}
 
 }  // extern "C"

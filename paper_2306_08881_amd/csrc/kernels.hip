@@ -1,12 +1,13 @@
 // gfx950 kernels of the ACP-SGD compressor (arXiv 2306.08881, Algorithms 1 and 2).
 //
 // Every kernel runs 256-thread workgroups (4 waves of 64) over a table of tiles; one
-// workgroup per tile.  All reductions are deterministic: fixed-order wave butterflies,
-// fixed-order sums across waves and a last-arriving-workgroup reduction that adds the
-// per-tile partial sums in tile order (no floating-point atomics), so that every rank of a
-// data-parallel job computes bitwise the same orthogonalised factor.
+// workgroup per tile.  Workgroups never wait for each other: a reduction that spans
+// workgroups writes per-tile partial sums and a later kernel of the same stream adds them in
+// tile order.  Together with fixed-order wave butterflies and fixed-order sums across waves
+// this makes every result bitwise reproducible, which a data-parallel job needs so that all
+// ranks keep the same orthogonalised factor.
 //
-// Error-feedback residual of a Q-step (E_t = M' - P_hat Q_t^T) is kept in deferred form:
+// The error-feedback residual of a Q-step (E_t = M' - P_hat Q_t^T) is kept in deferred form:
 // the Q-step writes F = M' into the E arena and the next P-step subtracts the rank-r term
 // P_hat Q_loc^T while it streams F, so each step reads M and E once and writes E once.
 #include <hip/hip_runtime.h>
@@ -47,34 +48,44 @@ __device__ inline float4 operator+(const float4& a, const float4& b) {
   return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
 }
 
+__device__ inline float4 scale4(const float4& a, float s) {
+  return make_float4(a.x * s, a.y * s, a.z * s, a.w * s);
+}
+
 __device__ inline float4 fma4(float s, const float4& v, const float4& acc) {
   return make_float4(fmaf(s, v.x, acc.x), fmaf(s, v.y, acc.y), fmaf(s, v.z, acc.z),
                      fmaf(s, v.w, acc.w));
 }
 
-template <typename T>
-__device__ inline T ld_agent(const T* p) {
-  return __hip_atomic_load(const_cast<T*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ inline float4 zero4() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+
+// Streaming accesses: data read or written exactly once per step.
+typedef float v4f __attribute__((ext_vector_type(4)));
+__device__ inline float4 ld_stream(const float4* p) {
+  const v4f v = __builtin_nontemporal_load(reinterpret_cast<const v4f*>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ inline void st_stream(float4* p, const float4& v) {
+  const v4f w = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(w, reinterpret_cast<v4f*>(p));
 }
 
-// Arrival at a counter shared by `total` workgroups; true in the last one to arrive, after
-// which every other workgroup's stores made before its own arrival are visible.
-__device__ inline bool arrive_last(uint32_t* ctr, uint32_t total) {
-  __shared__ uint32_t s_last;
-  __threadfence();
-  __syncthreads();
-  if (tid() == 0) {
-    const uint32_t prev = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    s_last = (prev + 1u == total) ? 1u : 0u;
-  }
-  __syncthreads();
-  const bool last = s_last != 0u;
-  if (last) __threadfence();
-  return last;
+// x W for one row of a rank-4 factor (W upper triangular, fp64, row-major), rounded to fp32.
+__device__ inline float4 apply_w4(const float4& x, const double* W) {
+  const double x0 = x.x, x1 = x.y, x2 = x.z, x3 = x.w;
+  const double y0 = x0 * W[0];
+  const double y1 = fma(x0, W[1], x1 * W[5]);
+  const double y2 = fma(x0, W[2], fma(x1, W[6], x2 * W[10]));
+  const double y3 = fma(x0, W[3], fma(x1, W[7], fma(x2, W[11], x3 * W[15])));
+  return make_float4(static_cast<float>(y0), static_cast<float>(y1), static_cast<float>(y2),
+                     static_cast<float>(y3));
 }
 
-__device__ inline void reset_counter(uint32_t* ctr) {
-  if (tid() == 0) __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Buffers of a bucket in this launch's group.
+__device__ inline const float* src_of(const KArgs& a, int32_t b) { return a.src[b - a.base]; }
+__device__ inline float* dst_of(const KArgs& a, int32_t b) { return a.dst[b - a.base]; }
+__device__ inline bool deferred_of(const KArgs& a, int32_t b) {
+  return ((a.deferred >> (b - a.base)) & 1ull) != 0;
 }
 
 // Raw vectors: pack the gradient into the factor buffer (compress) or unpack the aggregated
@@ -82,12 +93,14 @@ __device__ inline void reset_counter(uint32_t* ctr) {
 __device__ void vec_tile(const KArgs& a, const Tile& t, bool compress) {
   const VecDesc v = a.vecs[t.idx];
   const int64_t foff = a.parity ? v.fac_off_p : v.fac_off_q;
+  const float* src = src_of(a, v.bucket);
+  float* dst = dst_of(a, v.bucket);
   for (int i = tid(); i < t.b; i += kBlock) {
     const int64_t k = static_cast<int64_t>(t.a) + i;
     if (compress)
-      a.fbuf[foff + k] = a.grad[v.grad_off + k];
+      dst[foff + k] = src[v.grad_off + k];
     else
-      a.out[v.grad_off + k] = a.agg[foff + k] * a.inv_p;
+      dst[v.grad_off + k] = src[foff + k] * a.inv_p;
   }
 }
 
@@ -99,8 +112,100 @@ __device__ void vec_tile(const KArgs& a, const Tile& t, bool compress) {
 // G_jj = 0 or its residual d_j = G_jj - sum_{i<j} R_ij^2 is at most tau^2 G_jj, i.e. when the
 // residual norm is at most tau times the column norm.
 
+// Gram of rows [r0, r1) of X (row-major, RK columns) into shared G (RK x RK), by the whole
+// workgroup, in a fixed order; the rows are also copied to `copy` when it is set.
 template <int RK>
-__device__ void cholesky_w(const double* G, double* R, int* drop, double* w_out) {
+__device__ void gram_rows(const float* X, int64_t r0, int64_t r1, double* G, float* copy) {
+  if constexpr (RK <= 8) {
+    constexpr int NT = RK * (RK + 1) / 2;
+    constexpr int PER = 8;  // rows per thread per pass, loaded together
+    double g[NT];
+#pragma unroll
+    for (int e = 0; e < NT; ++e) g[e] = 0.0;
+    for (int64_t base = r0; base < r1; base += int64_t(kBlock) * PER) {
+      float x[PER][RK];
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const int64_t row = base + u * kBlock + tid();
+#pragma unroll
+        for (int k = 0; k < RK; ++k) x[u][k] = row < r1 ? X[row * RK + k] : 0.f;
+      }
+      if (copy) {
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+          const int64_t row = base + u * kBlock + tid();
+          if (row < r1)
+#pragma unroll
+            for (int k = 0; k < RK; ++k) copy[row * RK + k] = x[u][k];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        int e = 0;
+#pragma unroll
+        for (int i = 0; i < RK; ++i)
+#pragma unroll
+          for (int j = i; j < RK; ++j, ++e)
+            g[e] = fma(static_cast<double>(x[u][i]), static_cast<double>(x[u][j]), g[e]);
+      }
+    }
+    __shared__ double red[4][NT];
+#pragma unroll
+    for (int e = 0; e < NT; ++e) g[e] = wave_sum(g[e]);
+    if ((tid() & 63) == 0)
+#pragma unroll
+      for (int e = 0; e < NT; ++e) red[tid() >> 6][e] = g[e];
+    __syncthreads();
+    if (tid() < NT) {
+      const int e = tid();
+      int i = 0, rem = e;
+      while (rem >= RK - i) rem -= RK - i, ++i;
+      const int j = i + rem;
+      const double s = ((red[0][e] + red[1][e]) + red[2][e]) + red[3][e];
+      G[i * RK + j] = s;
+      G[j * RK + i] = s;
+    }
+    __syncthreads();
+  } else {
+    constexpr int CH = 64;
+    constexpr int NQ = (RK * RK + kBlock - 1) / kBlock;
+    __shared__ float xs[CH * RK];
+    if (copy)
+      for (int64_t e = r0 * RK + tid(); e < r1 * RK; e += kBlock) copy[e] = X[e];
+    double acc[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) acc[q] = 0.0;
+    for (int64_t c0 = r0; c0 < r1; c0 += CH) {
+      const int64_t cn = (r1 - c0) < CH ? (r1 - c0) : CH;
+      for (int e = tid(); e < cn * RK; e += kBlock) xs[e] = X[c0 * RK + e];
+      __syncthreads();
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const int e = tid() + q * kBlock;
+        if (e < RK * RK) {
+          const int i = e / RK, j = e % RK;
+          double s = acc[q];
+          for (int rr = 0; rr < cn; ++rr)
+            s = fma(static_cast<double>(xs[rr * RK + i]), static_cast<double>(xs[rr * RK + j]), s);
+          acc[q] = s;
+        }
+      }
+      __syncthreads();
+    }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int e = tid() + q * kBlock;
+      if (e < RK * RK) G[e] = acc[q];
+    }
+    __syncthreads();
+  }
+}
+
+// Cholesky G = R^T R and W = R^-1 (dropped columns zero), written to w_out.  G in shared.
+template <int RK>
+__device__ void cholesky_w(const double* G, double* w_out) {
+  __shared__ double R[RK * RK];
+  __shared__ int drop[RK];
   for (int e = tid(); e < RK * RK; e += kBlock) R[e] = 0.0;
   __syncthreads();
   for (int j = 0; j < RK; ++j) {
@@ -141,90 +246,47 @@ __device__ void cholesky_w(const double* G, double* R, int* drop, double* w_out)
   }
 }
 
-// Slice `t.a` of `t.b` slices of factor rows: optionally copy them into `dst`, add their Gram
-// into the partial slot, and in the last slice to arrive reduce the partials in slice order
-// and factor the Gram into W.
+// Factor tile: slice t.a of the t.b slices of fact_rows rows of the factor `src` (rows x RK).
+// When `dst` is set the slice is also copied there (the aggregated factor becomes the next
+// step's reused factor).  A factor of one slice finishes W here; otherwise the slice's Gram
+// is stored as a partial and K_CHOL adds the partials and finishes W.
 template <int RK>
 __device__ void fact_tile(const KArgs& a, const Tile& t, const float* src, float* dst, int64_t rows) {
   const MatDesc d = a.mats[t.idx];
+  __shared__ double G[RK * RK];
   const int64_t r0 = static_cast<int64_t>(t.a) * d.fact_rows;
   const int64_t r1 = r0 + d.fact_rows < rows ? r0 + d.fact_rows : rows;
-  if (dst)
-    for (int64_t e = r0 * RK + tid(); e < r1 * RK; e += kBlock) dst[e] = src[e];
-  double* part = a.gpart + d.gpart + static_cast<int64_t>(t.a) * RK * RK;
-  if constexpr (RK <= 8) {
-    constexpr int NT = RK * (RK + 1) / 2;
-    double g[NT];
-#pragma unroll
-    for (int e = 0; e < NT; ++e) g[e] = 0.0;
-    for (int64_t row = r0 + tid(); row < r1; row += kBlock) {
-      double x[RK];
-#pragma unroll
-      for (int k = 0; k < RK; ++k) x[k] = static_cast<double>(src[row * RK + k]);
-      int e = 0;
-#pragma unroll
-      for (int i = 0; i < RK; ++i)
-#pragma unroll
-        for (int j = i; j < RK; ++j, ++e) g[e] = fma(x[i], x[j], g[e]);
-    }
-    __shared__ double red[4][NT];
-#pragma unroll
-    for (int e = 0; e < NT; ++e) g[e] = wave_sum(g[e]);
-    if ((tid() & 63) == 0)
-#pragma unroll
-      for (int e = 0; e < NT; ++e) red[tid() >> 6][e] = g[e];
-    __syncthreads();
-    if (tid() < NT) {
-      const int e = tid();
-      int i = 0, rem = e;
-      while (rem >= RK - i) rem -= RK - i, ++i;
-      const int j = i + rem;
-      const double s = ((red[0][e] + red[1][e]) + red[2][e]) + red[3][e];
-      part[i * RK + j] = s;
-      part[j * RK + i] = s;
-    }
+  gram_rows<RK>(src, r0, r1, G, dst);
+  if (t.b == 1) {
+    cholesky_w<RK>(G, a.w + d.w_slot);
   } else {
-    constexpr int CH = 64;
-    __shared__ float xs[CH * RK];
-    double acc[(RK * RK + kBlock - 1) / kBlock];
-#pragma unroll
-    for (int q = 0; q < (RK * RK + kBlock - 1) / kBlock; ++q) acc[q] = 0.0;
-    for (int64_t c0 = r0; c0 < r1; c0 += CH) {
-      const int64_t cn = (r1 - c0) < CH ? (r1 - c0) : CH;
-      for (int e = tid(); e < cn * RK; e += kBlock) xs[e] = src[c0 * RK + e];
-      __syncthreads();
-#pragma unroll
-      for (int q = 0; q < (RK * RK + kBlock - 1) / kBlock; ++q) {
-        const int e = tid() + q * kBlock;
-        if (e < RK * RK) {
-          const int i = e / RK, j = e % RK;
-          double s = acc[q];
-          for (int rr = 0; rr < cn; ++rr)
-            s = fma(static_cast<double>(xs[rr * RK + i]), static_cast<double>(xs[rr * RK + j]), s);
-          acc[q] = s;
-        }
-      }
-      __syncthreads();
-    }
-#pragma unroll
-    for (int q = 0; q < (RK * RK + kBlock - 1) / kBlock; ++q) {
-      const int e = tid() + q * kBlock;
-      if (e < RK * RK) part[e] = acc[q];
-    }
+    double* part = a.gpart + d.gpart + static_cast<int64_t>(t.a) * RK * RK;
+    for (int e = tid(); e < RK * RK; e += kBlock) part[e] = G[e];
   }
-  if (!arrive_last(a.ctr + d.ctr_gram, static_cast<uint32_t>(t.b))) return;
+}
+
+template <int RK>
+__global__ __launch_bounds__(kBlock) void k_fact(KArgs a) {
+  const Tile t = a.tiles[blockIdx.x];
+  const MatDesc d = a.mats[t.idx];
+  const bool q = (a.variant & 1) != 0;
+  fact_tile<RK>(a, t, a.fac + (q ? d.q_slot : d.p_slot), nullptr, q ? d.m : d.n);
+}
+
+// W from the Gram partials of a matrix's t.b slices, added in slice order.
+template <int RK>
+__global__ __launch_bounds__(kBlock) void k_chol(KArgs a) {
+  const Tile t = a.tiles[blockIdx.x];
+  const MatDesc d = a.mats[t.idx];
   __shared__ double G[RK * RK];
-  __shared__ double R[RK * RK];
-  __shared__ int drop[RK];
   const double* gp = a.gpart + d.gpart;
   for (int e = tid(); e < RK * RK; e += kBlock) {
     double s = 0.0;
-    for (int sl = 0; sl < t.b; ++sl) s += ld_agent(gp + static_cast<int64_t>(sl) * RK * RK + e);
+    for (int sl = 0; sl < t.b; ++sl) s += gp[static_cast<int64_t>(sl) * RK * RK + e];
     G[e] = s;
   }
   __syncthreads();
-  cholesky_w<RK>(G, R, drop, a.w + d.w_slot);
-  reset_counter(a.ctr + d.ctr_gram);
+  cholesky_w<RK>(G, a.w + d.w_slot);
 }
 
 // Xh = X W for rows [t.a, t.a + t.b) of the P (variant 0) or Q (variant 1) slot.
@@ -252,22 +314,38 @@ __global__ __launch_bounds__(kBlock) void k_apply(KArgs a) {
   }
 }
 
-template <int RK>
-__global__ __launch_bounds__(kBlock) void k_gram(KArgs a) {
-  const Tile t = a.tiles[blockIdx.x];
-  const MatDesc d = a.mats[t.idx];
-  const bool q = a.variant == 1;
-  fact_tile<RK>(a, t, a.fac + (q ? d.q_slot : d.p_slot), nullptr, q ? d.m : d.n);
-}
-
 // ---------------------------------------------------------------------------------------
-// P-step, fused single pass (r = 4, rows of up to 5120 columns, 16-byte aligned rows).
-// A row is split over `wpr` waves (1, 2, 3 or 4); each lane owns S float4 column groups of
-// its wave's segment and keeps their rows of Qh (and of Q_loc when E is deferred) in
-// registers for the whole tile.  Per row: M' = M + E (or M + F - Ph_row Q_loc^T), P = M' Qh
-// reduced over the row, E = M' - P Qh^T written back, P written to the factor buffer.
+// Column mapping shared by the rank-4 streaming kernels.  The four waves of a workgroup split
+// a row of m4 = m / 4 float4 groups into four segments of 64 S groups; lane `lane` of wave w
+// owns groups w * 64 S + s * 64 + lane, s < S, for every row of the tile, so the factor rows
+// of those columns are loaded once per workgroup and kept in registers.  The waves work on the
+// same RB = 4 / S rows at a time (1 for S >= 3).
+template <int S>
+struct Cols {
+  static constexpr int RB = S >= 3 ? 1 : 4 / S;
+  int wave, lane;
+  int c4[S];
+  bool ok[S];
+  __device__ explicit Cols(int m4) {
+    wave = tid() >> 6;
+    lane = tid() & 63;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+      c4[s] = wave * 64 * S + s * 64 + lane;
+      ok[s] = c4[s] < m4;
+    }
+  }
+};
+
+// P-step, fused single pass (r = 4, 16-byte aligned rows of up to 5120 columns).  Each lane
+// keeps, for its columns, the rows of Qh = Q W (computed here from the reused factor; the tile
+// holding row 0 also stores Qh) and of Q_loc (when E is deferred) in registers for the whole
+// tile.  Per row: M' = M + E (or M + F - Ph_row Q_loc^T), P = M' Qh summed over the row (wave
+// butterflies, then the four waves' sums in wave order), E = M' - P Qh^T written back, P
+// written to the factor buffer.  The next rows' M and E are loaded before the reduction.
 template <int S>
 __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
+  constexpr int RB = Cols<S>::RB;
   const Tile t = a.tiles[blockIdx.x];
   if (t.kind == T_VEC) {
     vec_tile(a, t, true);
@@ -275,99 +353,102 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
   }
   const MatDesc d = a.mats[t.idx];
   const int m4 = d.m >> 2;
-  const int wpr = d.wpr, rpr = 4 / wpr;
-  const int wave = tid() >> 6, lane = tid() & 63;
-  const int rsub = wave / wpr, seg = wave - rsub * wpr;
-  const bool wave_on = rsub < rpr;
-  const bool ef = a.ef != 0, deferred = a.deferred != 0;
+  const Cols<S> cl(m4);
+  const bool ef = a.ef != 0, deferred = deferred_of(a, d.bucket);
+  const float4* G4 = reinterpret_cast<const float4*>(src_of(a, d.bucket) + d.grad_off);
+  float4* E4 = reinterpret_cast<float4*>(a.e + d.e_off);
+  const int row_end = t.a + t.b;
 
-  int c4[S];
-  bool ok[S];
+  // the first rows' M and E are requested before the factor setup
+  float4 g[RB][S], e[RB][S];
+  auto load_rows = [&](int r0) {
 #pragma unroll
-  for (int s = 0; s < S; ++s) {
-    c4[s] = seg * 64 * S + s * 64 + lane;
-    ok[s] = wave_on && c4[s] < m4;
-  }
-  const float4* Qh4 = reinterpret_cast<const float4*>(a.fac + d.qh_slot);
+    for (int rb = 0; rb < RB; ++rb) {
+      const int row = r0 + rb;
+      const int64_t base = static_cast<int64_t>(row) * m4;
+#pragma unroll
+      for (int s = 0; s < S; ++s) {
+        const bool on = cl.ok[s] && row < row_end;
+        g[rb][s] = on ? ld_stream(G4 + base + cl.c4[s]) : zero4();
+        e[rb][s] = (on && ef) ? E4[base + cl.c4[s]] : zero4();
+      }
+    }
+  };
+  load_rows(t.a);
+
+  __shared__ double Wsh[16];
+  __shared__ float4 red[2][4][RB];
+  if (tid() < 16) Wsh[tid()] = a.w[d.w_slot + tid()];
+  __syncthreads();
+
+  const float4* Q4 = reinterpret_cast<const float4*>(a.fac + d.q_slot);
   const float4* Ql4 = reinterpret_cast<const float4*>(a.fac + d.ql_slot);
+  float4* Qh4 = reinterpret_cast<float4*>(a.fac + d.qh_slot);
+  const bool store_qh = t.a == 0;
   float4 qh[S][4], ql[S][4];
 #pragma unroll
   for (int s = 0; s < S; ++s)
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      qh[s][c] = ok[s] ? Qh4[4 * c4[s] + c] : make_float4(0.f, 0.f, 0.f, 0.f);
-      ql[s][c] = (ok[s] && deferred) ? Ql4[4 * c4[s] + c] : make_float4(0.f, 0.f, 0.f, 0.f);
+      const int j = 4 * cl.c4[s] + c;
+      qh[s][c] = cl.ok[s] ? apply_w4(Q4[j], Wsh) : zero4();
+      ql[s][c] = (cl.ok[s] && deferred) ? Ql4[j] : zero4();
+      if (store_qh && cl.ok[s]) Qh4[j] = qh[s][c];
     }
 
-  const float4* G4 = reinterpret_cast<const float4*>(a.grad + d.grad_off);
-  float4* E4 = reinterpret_cast<float4*>(a.e + d.e_off);
-  const float* Ph = a.fac + d.ph_slot;
-  __shared__ float4 red[4];
-
-  const int row_end = t.a + t.b;
-  for (int r0 = t.a; r0 < row_end; r0 += rpr) {
-    const int row = r0 + rsub;
-    const bool act = wave_on && row < row_end;
-    const int64_t base = static_cast<int64_t>(row) * m4;
-    float4 mp[S];
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (act) {
-      float4 ph = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (deferred) ph = *reinterpret_cast<const float4*>(Ph + static_cast<int64_t>(row) * 4);
+  const float4* Ph4 = reinterpret_cast<const float4*>(a.fac + d.ph_slot);
+  float4* P4 = reinterpret_cast<float4*>(dst_of(a, d.bucket) + d.fac_off_p);
+  int buf = 0;
+  for (int r0 = t.a; r0 < row_end; r0 += RB, buf ^= 1) {
+    float4 mp[RB][S];
+    float4 acc[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int row = r0 + rb;
+      const float4 ph = (deferred && row < row_end) ? Ph4[row] : zero4();
+      acc[rb] = zero4();
 #pragma unroll
       for (int s = 0; s < S; ++s) {
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (ok[s]) {
-          v = G4[base + c4[s]];
-          if (ef) {
-            const float4 e = E4[base + c4[s]];
-            v = v + e;
-          }
-          if (deferred) {
-            v.x -= dot4(ph, ql[s][0]);
-            v.y -= dot4(ph, ql[s][1]);
-            v.z -= dot4(ph, ql[s][2]);
-            v.w -= dot4(ph, ql[s][3]);
-          }
+        float4 v = g[rb][s] + e[rb][s];
+        if (deferred) {
+          v.x -= dot4(ph, ql[s][0]);
+          v.y -= dot4(ph, ql[s][1]);
+          v.z -= dot4(ph, ql[s][2]);
+          v.w -= dot4(ph, ql[s][3]);
         }
-        mp[s] = v;
-        acc = fma4(v.x, qh[s][0], acc);
-        acc = fma4(v.y, qh[s][1], acc);
-        acc = fma4(v.z, qh[s][2], acc);
-        acc = fma4(v.w, qh[s][3], acc);
+        mp[rb][s] = v;
+        acc[rb] = fma4(v.x, qh[s][0], acc[rb]);
+        acc[rb] = fma4(v.y, qh[s][1], acc[rb]);
+        acc[rb] = fma4(v.z, qh[s][2], acc[rb]);
+        acc[rb] = fma4(v.w, qh[s][3], acc[rb]);
       }
     }
-    acc = wave_sum(acc);
-    float4 P = acc;
-    if (wpr > 1) {
-      if (lane == 0) red[wave] = acc;
-      __syncthreads();
-      if (wave_on) {
-        P = red[rsub * wpr];
-        for (int k = 1; k < wpr; ++k) P = P + red[rsub * wpr + k];
-      }
-      __syncthreads();
+    load_rows(r0 + RB);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      acc[rb] = wave_sum(acc[rb]);
+      if (cl.lane == 0) red[buf][cl.wave][rb] = acc[rb];
     }
-    if (act) {
+    __syncthreads();
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int row = r0 + rb;
+      if (row >= row_end) continue;
+      const float4 P = ((red[buf][0][rb] + red[buf][1][rb]) + red[buf][2][rb]) + red[buf][3][rb];
+      const int64_t base = static_cast<int64_t>(row) * m4;
       if (ef) {
 #pragma unroll
         for (int s = 0; s < S; ++s)
-          if (ok[s]) {
-            float4 e = mp[s];
-            e.x -= dot4(P, qh[s][0]);
-            e.y -= dot4(P, qh[s][1]);
-            e.z -= dot4(P, qh[s][2]);
-            e.w -= dot4(P, qh[s][3]);
-            E4[base + c4[s]] = e;
+          if (cl.ok[s]) {
+            float4 r = mp[rb][s];
+            r.x -= dot4(P, qh[s][0]);
+            r.y -= dot4(P, qh[s][1]);
+            r.z -= dot4(P, qh[s][2]);
+            r.w -= dot4(P, qh[s][3]);
+            E4[base + cl.c4[s]] = r;
           }
       }
-      if (seg == 0 && lane == 0) {
-        float* dst = a.fbuf + d.fac_off_p + static_cast<int64_t>(row) * 4;
-        dst[0] = P.x;
-        dst[1] = P.y;
-        dst[2] = P.z;
-        dst[3] = P.w;
-      }
+      if (cl.wave == 0 && cl.lane == 0) P4[row] = P;
     }
   }
 }
@@ -383,11 +464,11 @@ __global__ __launch_bounds__(kBlock) void k_prow(KArgs a) {
   const MatDesc d = a.mats[t.idx];
   const int64_t row = t.a;
   const int64_t m = d.m;
-  const float* G = a.grad + d.grad_off + row * m;
+  const float* G = src_of(a, d.bucket) + d.grad_off + row * m;
   const float* E = a.e + d.e_off + row * m;
   const float* Qh = a.fac + d.qh_slot;
   const float* Ql = a.fac + d.ql_slot;
-  const bool ef = a.ef != 0, deferred = a.deferred != 0;
+  const bool ef = a.ef != 0, deferred = deferred_of(a, d.bucket);
   float ph[RK];
 #pragma unroll
   for (int k = 0; k < RK; ++k) ph[k] = deferred ? a.fac[d.ph_slot + row * RK + k] : 0.f;
@@ -412,7 +493,7 @@ __global__ __launch_bounds__(kBlock) void k_prow(KArgs a) {
   __syncthreads();
   if (tid() < RK) {
     const int k = tid();
-    a.fbuf[d.fac_off_p + row * RK + k] = ((red[0][k] + red[1][k]) + red[2][k]) + red[3][k];
+    dst_of(a, d.bucket)[d.fac_off_p + row * RK + k] = ((red[0][k] + red[1][k]) + red[2][k]) + red[3][k];
   }
 }
 
@@ -422,16 +503,17 @@ __global__ __launch_bounds__(kBlock) void k_eupd(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
   const int64_t m = d.m;
-  const bool deferred = a.deferred != 0;
+  const bool deferred = deferred_of(a, d.bucket);
   const float* Qh = a.fac + d.qh_slot;
   const float* Ql = a.fac + d.ql_slot;
   const float* Ph = a.fac + d.ph_slot;
-  const float* P = a.fbuf + d.fac_off_p;
+  const float* P = dst_of(a, d.bucket) + d.fac_off_p;
+  const float* G = src_of(a, d.bucket) + d.grad_off;
   const int64_t total = static_cast<int64_t>(t.b) * m;
   for (int64_t e = tid(); e < total; e += kBlock) {
     const int64_t row = t.a + e / m, j = e % m;
     const int64_t idx = row * m + j;
-    float mp = a.grad[d.grad_off + idx] + a.e[d.e_off + idx];
+    float mp = G[idx] + a.e[d.e_off + idx];
     if (deferred)
 #pragma unroll
       for (int k = 0; k < RK; ++k) mp -= Ph[row * RK + k] * Ql[j * RK + k];
@@ -449,9 +531,10 @@ __global__ __launch_bounds__(kBlock) void k_emat(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
   const int64_t m = d.m;
-  const bool deferred = a.deferred != 0;
+  const bool deferred = deferred_of(a, d.bucket);
   const float* Ql = a.fac + d.ql_slot;
   const float* Ph = a.fac + d.ph_slot;
+  float* out = dst_of(a, d.bucket);
   const int64_t total = static_cast<int64_t>(t.b) * m;
   for (int64_t e = tid(); e < total; e += kBlock) {
     const int64_t row = t.a + e / m, j = e % m;
@@ -460,17 +543,17 @@ __global__ __launch_bounds__(kBlock) void k_emat(KArgs a) {
     if (deferred)
 #pragma unroll
       for (int k = 0; k < RK; ++k) v -= Ph[row * RK + k] * Ql[j * RK + k];
-    a.out[d.grad_off + idx] = v;
+    out[d.grad_off + idx] = v;
   }
 }
 
 // ---------------------------------------------------------------------------------------
 // Q-step: tile = (row chunk, column block).  Each lane owns CPT adjacent columns; the four
-// waves take every fourth row of the chunk.  F = M' is written back (deferred E) and the
-// partial M'^T Ph of the tile is summed across waves in wave order; the last row chunk to
-// arrive for a column block adds the chunks' partials in chunk order, giving Q_loc, which is
-// written to the factor buffer and to the Ql slot.
-template <int RK, int CPT>
+// waves take every fourth row of the chunk, four rows at a time.  F = M' is written back
+// (deferred E) and the partial M'^T Ph of the tile, summed across waves in wave order, is
+// stored for K_QFIN.  FUSED (r = 4): Ph rows are formed here as P W, and the tiles of column
+// block 0 store them.
+template <int RK, int CPT, bool FUSED>
 __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   if (t.kind == T_VEC) {
@@ -485,45 +568,78 @@ __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
   const int64_t col = static_cast<int64_t>(t.b) * d.q_cb + lane * CPT;
   const bool valid = col < m;
   const bool ef = a.ef != 0;
-  const float* G = a.grad + d.grad_off;
+  const float* G = src_of(a, d.bucket) + d.grad_off;
   float* E = a.e + d.e_off;
-  const float* Ph = a.fac + d.ph_slot;
+  __shared__ double Wsh[16];
+  if constexpr (FUSED) {
+    if (tid() < 16) Wsh[tid()] = a.w[d.w_slot + tid()];
+    __syncthreads();
+  }
   float acc[CPT][RK];
 #pragma unroll
   for (int c = 0; c < CPT; ++c)
 #pragma unroll
     for (int k = 0; k < RK; ++k) acc[c][k] = 0.f;
-  for (int64_t row = r0 + wave; row < r1; row += 4) {
-    float ph[RK];
+
+  // M' of one row for this lane's columns, with F = M' written back.
+  auto load_mp = [&](int64_t row, float* mp) {
+    const int64_t i = row * m + col;
+    if (!valid) {
 #pragma unroll
-    for (int k = 0; k < RK; ++k) ph[k] = Ph[row * RK + k];
-    if (valid) {
-      float mp[CPT];
-      const int64_t idx = row * m + col;
-      if constexpr (CPT == 4) {
-        float4 g = *reinterpret_cast<const float4*>(G + idx);
-        if (ef) {
-          const float4 e = *reinterpret_cast<const float4*>(E + idx);
-          g = g + e;
-          *reinterpret_cast<float4*>(E + idx) = g;
-        }
-        mp[0] = g.x;
-        mp[1] = g.y;
-        mp[2] = g.z;
-        mp[3] = g.w;
-      } else {
-        float g = G[idx];
-        if (ef) {
-          g += E[idx];
-          E[idx] = g;
-        }
-        mp[0] = g;
-      }
-#pragma unroll
-      for (int c = 0; c < CPT; ++c)
-#pragma unroll
-        for (int k = 0; k < RK; ++k) acc[c][k] = fmaf(mp[c], ph[k], acc[c][k]);
+      for (int c = 0; c < CPT; ++c) mp[c] = 0.f;
+      return;
     }
+    if constexpr (CPT == 4) {
+      float4 g = ld_stream(reinterpret_cast<const float4*>(G + i));
+      if (ef) {
+        g = g + *reinterpret_cast<const float4*>(E + i);
+        *reinterpret_cast<float4*>(E + i) = g;
+      }
+      mp[0] = g.x;
+      mp[1] = g.y;
+      mp[2] = g.z;
+      mp[3] = g.w;
+    } else {
+      float g = G[i];
+      if (ef) {
+        g += E[i];
+        E[i] = g;
+      }
+      mp[0] = g;
+    }
+  };
+  auto accumulate = [&](int64_t row, const float* mp) {
+    float ph[RK];
+    if constexpr (FUSED) {
+      const float4 x = *reinterpret_cast<const float4*>(a.fac + d.p_slot + row * 4);
+      const float4 y = apply_w4(x, Wsh);
+      ph[0] = y.x;
+      ph[1] = y.y;
+      ph[2] = y.z;
+      ph[3] = y.w;
+      if (t.b == 0 && lane == 0) *reinterpret_cast<float4*>(a.fac + d.ph_slot + row * 4) = y;
+    } else {
+#pragma unroll
+      for (int k = 0; k < RK; ++k) ph[k] = a.fac[d.ph_slot + row * RK + k];
+    }
+#pragma unroll
+    for (int c = 0; c < CPT; ++c)
+#pragma unroll
+      for (int k = 0; k < RK; ++k) acc[c][k] = fmaf(mp[c], ph[k], acc[c][k]);
+  };
+
+  int64_t row = r0 + wave;
+  for (; row + 12 < r1; row += 16) {
+    float mp[4][CPT];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) load_mp(row + 4 * u, mp[u]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) accumulate(row + 4 * u, mp[u]);
+  }
+  for (; row < r1; row += 4) {
+    float mp0[CPT];
+    load_mp(row, mp0);
+    accumulate(row, mp0);
   }
   constexpr int W = 64 * CPT * RK;  // partial entries of one wave
   __shared__ float red[4][W];
@@ -536,24 +652,43 @@ __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
   const int64_t stride = ncb * d.q_cb * RK;  // one row chunk of partials
   float* part = a.qpart + d.qpart + static_cast<int64_t>(t.a) * stride + static_cast<int64_t>(t.b) * d.q_cb * RK;
   for (int e = tid(); e < W; e += kBlock) part[e] = ((red[0][e] + red[1][e]) + red[2][e]) + red[3][e];
-  if (!arrive_last(a.ctr + d.ctr_q + t.b, static_cast<uint32_t>(d.q_chunks))) return;
-  const float* base = a.qpart + d.qpart + static_cast<int64_t>(t.b) * d.q_cb * RK;
-  for (int e = tid(); e < W; e += kBlock) {
-    const int64_t c = static_cast<int64_t>(t.b) * d.q_cb + e / RK;
-    if (c >= m) continue;
-    float s = 0.f;
-    for (int ch = 0; ch < d.q_chunks; ++ch) s += ld_agent(base + ch * stride + e);
-    const int64_t o = c * RK + (e % RK);
-    a.fbuf[d.fac_off_q + o] = s;
-    a.fac[d.ql_slot + o] = s;
+}
+
+// Q-step finish: for entries [t.a * 256, t.a * 256 + 256) of column block t.b, Q_loc = sum
+// over the row chunks' partials, added in chunk order; written to the factor buffer and to
+// the Ql slot.
+template <int RK>
+__global__ __launch_bounds__(kBlock) void k_qfin(KArgs a) {
+  const Tile t = a.tiles[blockIdx.x];
+  const MatDesc d = a.mats[t.idx];
+  const int64_t m = d.m;
+  const int64_t ncb = (m + d.q_cb - 1) / d.q_cb;
+  const int64_t stride = ncb * d.q_cb * RK;
+  const int e = t.a * kBlock + tid();
+  if (e >= d.q_cb * RK) return;
+  const int64_t c = static_cast<int64_t>(t.b) * d.q_cb + e / RK;
+  if (c >= m) return;
+  const float* base = a.qpart + d.qpart + static_cast<int64_t>(t.b) * d.q_cb * RK + e;
+  constexpr int U = 8;
+  float s = 0.f;
+  int ch = 0;
+  for (; ch + U <= d.q_chunks; ch += U) {
+    float v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = base[(ch + u) * stride];
+#pragma unroll
+    for (int u = 0; u < U; ++u) s += v[u];
   }
-  reset_counter(a.ctr + d.ctr_q + t.b);
+  for (; ch < d.q_chunks; ++ch) s += base[ch * stride];
+  const int64_t o = c * RK + (e % RK);
+  dst_of(a, d.bucket)[d.fac_off_q + o] = s;
+  a.fac[d.ql_slot + o] = s;
 }
 
 // ---------------------------------------------------------------------------------------
-// Decompress: M_hat = A B^T / p over a tile of rows.  Odd step: A = P_agg (factor buffer),
-// B = Qh; even step: A = Ph, B = Q_agg.  B is staged in LDS column-major in chunks.  Factor
-// tiles keep the aggregated factor as the next step's reused factor and build its W.
+// Decompress, general: M_hat = A B^T / p over a tile of rows.  Odd step: A = P_agg (factor
+// buffer), B = Qh; even step: A = Ph, B = Q_agg.  B is staged in LDS column-major in chunks.
+// Factor tiles keep the aggregated factor as the next step's reused factor and build its W.
 template <int RK, int VW>
 __global__ __launch_bounds__(kBlock) void k_recon(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
@@ -564,18 +699,19 @@ __global__ __launch_bounds__(kBlock) void k_recon(KArgs a) {
   }
   const MatDesc d = a.mats[t.idx];
   if (t.kind == T_FACT) {
-    const float* src = a.agg + (odd ? d.fac_off_p : d.fac_off_q);
+    const float* src = src_of(a, d.bucket) + (odd ? d.fac_off_p : d.fac_off_q);
     float* dst = a.fac + (odd ? d.p_slot : d.q_slot);
     fact_tile<RK>(a, t, src, dst, odd ? d.n : d.m);
     return;
   }
   constexpr int CK = (8192 / RK) < 4096 ? (8192 / RK) : 4096;
   __shared__ __align__(16) float Bs[RK * CK];
-  const float* A = odd ? a.agg + d.fac_off_p : a.fac + d.ph_slot;
-  const float* B = odd ? a.fac + d.qh_slot : a.agg + d.fac_off_q;
+  const float* agg = src_of(a, d.bucket);
+  const float* A = odd ? agg + d.fac_off_p : a.fac + d.ph_slot;
+  const float* B = odd ? a.fac + d.qh_slot : agg + d.fac_off_q;
   const int wave = tid() >> 6, lane = tid() & 63;
   const int64_t m = d.m;
-  float* O = a.out + d.grad_off;
+  float* O = dst_of(a, d.bucket) + d.grad_off;
   for (int64_t c0 = 0; c0 < m; c0 += CK) {
     const int cw = static_cast<int>((m - c0) < CK ? (m - c0) : CK);
     for (int e = tid(); e < cw * RK; e += kBlock) {
@@ -589,7 +725,7 @@ __global__ __launch_bounds__(kBlock) void k_recon(KArgs a) {
       for (int k = 0; k < RK; ++k) ar[k] = A[row * RK + k] * a.inv_p;
       if constexpr (VW == 4) {
         for (int j4 = lane; j4 < (cw >> 2); j4 += 64) {
-          float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+          float4 o = zero4();
 #pragma unroll
           for (int k = 0; k < RK; ++k)
             o = fma4(ar[k], *reinterpret_cast<const float4*>(&Bs[k * CK + 4 * j4]), o);
@@ -608,9 +744,66 @@ __global__ __launch_bounds__(kBlock) void k_recon(KArgs a) {
   }
 }
 
+// Decompress, r = 4: each lane keeps the rank-4 rows of B for its columns in registers and
+// writes M_hat rows with streaming stores, RB rows at a time.  Factor tiles and vectors as in
+// k_recon.
+template <int S>
+__global__ __launch_bounds__(kBlock) void k_recon4(KArgs a) {
+  constexpr int RB = Cols<S>::RB;
+  const Tile t = a.tiles[blockIdx.x];
+  const bool odd = a.parity != 0;
+  if (t.kind == T_VEC) {
+    vec_tile(a, t, false);
+    return;
+  }
+  const MatDesc d = a.mats[t.idx];
+  if (t.kind == T_FACT) {
+    const float* src = src_of(a, d.bucket) + (odd ? d.fac_off_p : d.fac_off_q);
+    float* dst = a.fac + (odd ? d.p_slot : d.q_slot);
+    fact_tile<4>(a, t, src, dst, odd ? d.n : d.m);
+    return;
+  }
+  const int m4 = d.m >> 2;
+  const Cols<S> cl(m4);
+  const float* agg = src_of(a, d.bucket);
+  const float4* A4 = reinterpret_cast<const float4*>(odd ? agg + d.fac_off_p : a.fac + d.ph_slot);
+  const float4* B4 = reinterpret_cast<const float4*>(odd ? a.fac + d.qh_slot : agg + d.fac_off_q);
+  float4 b[S][4];
+#pragma unroll
+  for (int s = 0; s < S; ++s)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) b[s][c] = cl.ok[s] ? B4[4 * cl.c4[s] + c] : zero4();
+  float4* O4 = reinterpret_cast<float4*>(dst_of(a, d.bucket) + d.grad_off);
+  const int row_end = t.a + t.b;
+  for (int r0 = t.a; r0 < row_end; r0 += RB) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int row = r0 + rb;
+      if (row >= row_end) continue;
+      const float4 ar = scale4(A4[row], a.inv_p);
+      const int64_t base = static_cast<int64_t>(row) * m4;
+#pragma unroll
+      for (int s = 0; s < S; ++s)
+        if (cl.ok[s]) {
+          const float4 o = make_float4(dot4(ar, b[s][0]), dot4(ar, b[s][1]), dot4(ar, b[s][2]),
+                                       dot4(ar, b[s][3]));
+          st_stream(O4 + base + cl.c4[s], o);
+        }
+    }
+  }
+}
+
 __global__ __launch_bounds__(kBlock) void k_vec(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   vec_tile(a, t, true);
+}
+
+template <int S>
+void launch_s(bool pstep, dim3 grid, dim3 block, hipStream_t s, const KArgs& args) {
+  if (pstep)
+    hipLaunchKernelGGL(k_pfused<S>, grid, block, 0, s, args);
+  else
+    hipLaunchKernelGGL(k_recon4<S>, grid, block, 0, s, args);
 }
 
 template <int RK>
@@ -621,16 +814,26 @@ hipError_t launch_rank(const Launch& l, const KArgs& args, hipStream_t s) {
     case K_PROW: hipLaunchKernelGGL(k_prow<RK>, grid, block, 0, s, args); break;
     case K_EUPD: hipLaunchKernelGGL(k_eupd<RK>, grid, block, 0, s, args); break;
     case K_EMAT: hipLaunchKernelGGL(k_emat<RK>, grid, block, 0, s, args); break;
-    case K_GRAM: hipLaunchKernelGGL(k_gram<RK>, grid, block, 0, s, args); break;
+    case K_FACT: hipLaunchKernelGGL(k_fact<RK>, grid, block, 0, s, args); break;
+    case K_CHOL: hipLaunchKernelGGL(k_chol<RK>, grid, block, 0, s, args); break;
+    case K_QFIN: hipLaunchKernelGGL(k_qfin<RK>, grid, block, 0, s, args); break;
     case K_QSTEP:
-      if (l.variant == 4) {
-        if constexpr (RK <= 8) {
-          hipLaunchKernelGGL((k_qstep<RK, 4>), grid, block, 0, s, args);
+      if (l.variant == (4 | kQFused)) {
+        if constexpr (RK == 4) {
+          hipLaunchKernelGGL((k_qstep<4, 4, true>), grid, block, 0, s, args);
         } else {
           return hipErrorInvalidValue;
         }
+      } else if (l.variant == 4) {
+        if constexpr (RK <= 8) {
+          hipLaunchKernelGGL((k_qstep<RK, 4, false>), grid, block, 0, s, args);
+        } else {
+          return hipErrorInvalidValue;
+        }
+      } else if (l.variant == 1) {
+        hipLaunchKernelGGL((k_qstep<RK, 1, false>), grid, block, 0, s, args);
       } else {
-        hipLaunchKernelGGL((k_qstep<RK, 1>), grid, block, 0, s, args);
+        return hipErrorInvalidValue;
       }
       break;
     case K_RECON:
@@ -640,13 +843,15 @@ hipError_t launch_rank(const Launch& l, const KArgs& args, hipStream_t s) {
         hipLaunchKernelGGL((k_recon<RK, 1>), grid, block, 0, s, args);
       break;
     case K_PFUSED:
+    case K_RECON4:
       if constexpr (RK == 4) {
+        const bool p = l.kernel == K_PFUSED;
         switch (l.variant) {
-          case 1: hipLaunchKernelGGL(k_pfused<1>, grid, block, 0, s, args); break;
-          case 2: hipLaunchKernelGGL(k_pfused<2>, grid, block, 0, s, args); break;
-          case 3: hipLaunchKernelGGL(k_pfused<3>, grid, block, 0, s, args); break;
-          case 4: hipLaunchKernelGGL(k_pfused<4>, grid, block, 0, s, args); break;
-          case 5: hipLaunchKernelGGL(k_pfused<5>, grid, block, 0, s, args); break;
+          case 1: launch_s<1>(p, grid, block, s, args); break;
+          case 2: launch_s<2>(p, grid, block, s, args); break;
+          case 3: launch_s<3>(p, grid, block, s, args); break;
+          case 4: launch_s<4>(p, grid, block, s, args); break;
+          case 5: launch_s<5>(p, grid, block, s, args); break;
           default: return hipErrorInvalidValue;
         }
         break;

@@ -13,12 +13,13 @@
 #include "plan.hpp"
 
 #include <algorithm>
+#include <cmath>
 
 namespace acp {
 
 namespace {
 
-constexpr int64_t kTileElems = 16384;   // gradient elements per streaming tile
+constexpr int64_t kTileElems = 16384;   // gradient elements per streaming tile (unit)
 constexpr int64_t kVecChunk = 4096;     // raw-vector elements per copy tile
 constexpr int64_t kApplyRows = 256;     // factor rows per orthogonalisation tile
 constexpr int64_t kSlotAlign = 64;      // floats (256 bytes)
@@ -112,7 +113,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   }
 
   // ---- per-tensor device descriptors and state regions
-  int64_t e_floats = 0, fac_floats = 0, gpart = 0, qpart = 0, nctr = 0;
+  int64_t e_floats = 0, fac_floats = 0, gpart = 0, qpart = 0;
   for (int32_t b = 0; b < static_cast<int32_t>(plan.buckets.size()); ++b) {
     BucketPlan& bk = plan.buckets[b];
     bk.e_base = e_floats;
@@ -127,6 +128,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         v.fac_off_p = bk.fac_off_p[k];
         v.fac_off_q = bk.fac_off_q[k];
         v.numel = t.numel;
+        v.bucket = b;
         t.vec = static_cast<int32_t>(plan.vecs.size());
         bk.vecs.push_back(t.vec);
         plan.vecs.push_back(v);
@@ -149,19 +151,21 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       const bool vec4 = (t.m % 4 == 0) && (d.grad_off % 4 == 0);
       const int64_t cpt = (vec4 && r <= 8) ? 4 : 1;
       d.q_cb = static_cast<int32_t>(64 * cpt);
-      d.q_rows = static_cast<int32_t>(align_up(std::max<int64_t>(32, cdiv(t.n, 64)), 4));
+      d.q_rows = static_cast<int32_t>(align_up(std::max<int64_t>(64, cdiv(t.n, 64)), 8));
       d.q_chunks = static_cast<int32_t>(cdiv(t.n, d.q_rows));
       const int64_t ncb = cdiv(t.m, d.q_cb);
       d.qpart = qpart;
       qpart += align_up(int64_t(d.q_chunks) * ncb * d.q_cb * r, kSlotAlign);
-      d.fact_rows = r <= 8 ? 1024 : 256;
-      const int64_t gsl = std::max(cdiv(t.n, d.fact_rows), cdiv(t.m, d.fact_rows));
+      d.bucket = b;
+      d.fact_rows = r <= 8 ? 2048 : 256;
+      d.fact_slices_p = static_cast<int32_t>(cdiv(t.n, d.fact_rows));
+      d.fact_slices_q = static_cast<int32_t>(cdiv(t.m, d.fact_rows));
       d.gpart = gpart;
-      gpart += gsl * r * r;
+      {
+        const int64_t nsl = std::max(d.fact_slices_p, d.fact_slices_q);
+        if (nsl > 1) gpart += nsl * r * r;
+      }
       d.w_slot = static_cast<int64_t>(plan.mats.size()) * r * r;
-      d.ctr_gram = static_cast<int32_t>(nctr++);
-      d.ctr_q = static_cast<int32_t>(nctr);
-      nctr += ncb;
       t.mat = static_cast<int32_t>(plan.mats.size());
       bk.mats.push_back(t.mat);
       plan.mats.push_back(d);
@@ -178,19 +182,25 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
                                   static_cast<int32_t>(std::min(kVecChunk, n - s))});
     }
   };
-  auto apply_tiles = [&](const BucketPlan& bk, bool q) {
-    for (int32_t mi : bk.mats) {
+  auto apply_tiles = [&](const std::vector<int32_t>& mats, bool q) {
+    for (int32_t mi : mats) {
       const int64_t rows = q ? plan.mats[mi].m : plan.mats[mi].n;
       for (int64_t s = 0; s < rows; s += kApplyRows)
         plan.tiles.push_back(Tile{T_ROWS, mi, static_cast<int32_t>(s),
                                   static_cast<int32_t>(std::min(kApplyRows, rows - s))});
     }
   };
+  // factor tiles: one per slice of fact_rows factor rows
   auto fact_tiles = [&](int32_t mi, bool q) {
     const MatDesc& d = plan.mats[mi];
-    const int64_t rows = q ? d.m : d.n;
-    const int32_t nsl = static_cast<int32_t>(cdiv(rows, d.fact_rows));
+    const int32_t nsl = q ? d.fact_slices_q : d.fact_slices_p;
     for (int32_t s = 0; s < nsl; ++s) plan.tiles.push_back(Tile{T_FACT, mi, s, nsl});
+  };
+  // Gram finish of the factors of more than one slice
+  auto chol_tiles = [&](int32_t mi, bool q) {
+    const MatDesc& d = plan.mats[mi];
+    const int32_t nsl = q ? d.fact_slices_q : d.fact_slices_p;
+    if (nsl > 1) plan.tiles.push_back(Tile{T_FACT, mi, 0, nsl});
   };
   auto row_tiles = [&](int32_t mi, int64_t rows_per_tile) {
     const MatDesc& d = plan.mats[mi];
@@ -202,35 +212,47 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     const MatDesc& d = plan.mats[mi];
     return d.m % 4 == 0 && d.grad_off % 4 == 0;
   };
+  // rank-4 register-resident kernels: 16-byte aligned rows and factor rows, m <= 5120
+  auto is_fast = [&](int32_t mi) {
+    const MatDesc& d = plan.mats[mi];
+    return r == 4 && is_vec4(mi) && d.fac_off_p % 4 == 0 && d.fac_off_q % 4 == 0 &&
+           cdiv(d.m / 4, 256) <= 5;
+  };
+  // rows per tile of the rank-4 kernels: a multiple of the rows handled per round
+  auto rows_for = [&](int32_t mi, int64_t elems) {
+    const MatDesc& d = plan.mats[mi];
+    const int64_t rb = d.scls >= 3 ? 1 : 4 / d.scls;
+    return rb * std::max<int64_t>(1, elems / (int64_t(d.m) * rb));
+  };
 
   for (BucketPlan& bk : plan.buckets) {
+    std::vector<int32_t> fast, generic;
+    for (int32_t mi : bk.mats) {
+      if (is_fast(mi)) {
+        plan.mats[mi].scls = static_cast<int32_t>(cdiv(plan.mats[mi].m / 4, 256));
+        fast.push_back(mi);
+      } else {
+        generic.push_back(mi);
+      }
+    }
+    auto of_class = [&](int32_t S) {
+      std::vector<int32_t> v;
+      for (int32_t mi : fast)
+        if (plan.mats[mi].scls == S) v.push_back(mi);
+      return v;
+    };
     // -- P-step (odd t)
     {
       std::vector<Launch>& L = bk.compress[1];
-      Launch l = sink.begin(K_APPLY, 1);
-      apply_tiles(bk, true);
-      sink.end(l, L);
-      std::vector<int32_t> fused, generic;
-      int32_t S = 1;
-      for (int32_t mi : bk.mats) {
-        const int64_t m4 = plan.mats[mi].m / 4;
-        if (r == 4 && is_vec4(mi) && cdiv(m4, 256) <= 5) {
-          fused.push_back(mi);
-          S = std::max<int32_t>(S, static_cast<int32_t>(cdiv(m4, 256)));
-        } else {
-          generic.push_back(mi);
-        }
-      }
       bool vec_done = bk.vecs.empty();
-      if (!fused.empty()) {
+      Launch l = sink.begin(K_APPLY, 1);
+      apply_tiles(generic, true);
+      sink.end(l, L);
+      for (int32_t S = 1; S <= 5; ++S) {
+        const std::vector<int32_t> cls = of_class(S);
+        if (cls.empty()) continue;
         l = sink.begin(K_PFUSED, S);
-        for (int32_t mi : fused) {
-          MatDesc& d = plan.mats[mi];
-          d.wpr = static_cast<int32_t>(cdiv(d.m / 4, 64 * int64_t(S)));
-          const int64_t rpr = 4 / d.wpr;
-          const int64_t rows = rpr * std::max<int64_t>(1, kTileElems / (int64_t(d.m) * rpr));
-          row_tiles(mi, rows);
-        }
+        for (int32_t mi : cls) row_tiles(mi, rows_for(mi, 2 * kTileElems));
         if (!vec_done) vec_tiles(bk), vec_done = true;
         sink.end(l, L);
       }
@@ -255,45 +277,76 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     // -- Q-step (even t)
     {
       std::vector<Launch>& L = bk.compress[0];
-      Launch l = sink.begin(K_APPLY, 0);
-      apply_tiles(bk, false);
-      sink.end(l, L);
       bool vec_done = bk.vecs.empty();
-      for (int32_t cpt : {4, 1}) {
-        l = sink.begin(K_QSTEP, cpt);
+      Launch l = sink.begin(K_APPLY, 0);
+      apply_tiles(generic, false);
+      sink.end(l, L);
+      auto qtiles = [&](int32_t mi) {
+        const MatDesc& d = plan.mats[mi];
+        const int32_t ncb = static_cast<int32_t>(cdiv(d.m, d.q_cb));
+        for (int32_t c = 0; c < d.q_chunks; ++c)
+          for (int32_t cb = 0; cb < ncb; ++cb) plan.tiles.push_back(Tile{T_QTILE, mi, c, cb});
+      };
+      for (int32_t variant : {4 | kQFused, 4, 1}) {
+        l = sink.begin(K_QSTEP, variant);
         bool any = false;
-        for (int32_t mi : bk.mats) {
-          const MatDesc& d = plan.mats[mi];
-          if (d.q_cb != 64 * cpt) continue;
+        const std::vector<int32_t>& set = (variant & kQFused) ? fast : generic;
+        for (int32_t mi : set) {
+          if (!(variant & kQFused) && plan.mats[mi].q_cb != 64 * variant) continue;
+          qtiles(mi);
           any = true;
-          const int32_t ncb = static_cast<int32_t>(cdiv(d.m, d.q_cb));
-          for (int32_t c = 0; c < d.q_chunks; ++c)
-            for (int32_t cb = 0; cb < ncb; ++cb) plan.tiles.push_back(Tile{T_QTILE, mi, c, cb});
         }
         if (any && !vec_done) vec_tiles(bk), vec_done = true;
         sink.end(l, L);
       }
+      l = sink.begin(K_QFIN, 0);
+      for (int32_t mi : bk.mats) {
+        const MatDesc& d = plan.mats[mi];
+        const int32_t ncb = static_cast<int32_t>(cdiv(d.m, d.q_cb));
+        const int32_t nblk = static_cast<int32_t>(cdiv(int64_t(d.q_cb) * r, kBlock));
+        for (int32_t cb = 0; cb < ncb; ++cb)
+          for (int32_t eb = 0; eb < nblk; ++eb) plan.tiles.push_back(Tile{T_QTILE, mi, eb, cb});
+      }
+      sink.end(l, L);
       if (!vec_done) {
         l = sink.begin(K_VEC, 0);
         vec_tiles(bk);
         sink.end(l, L);
       }
     }
-    // -- decompress (both parities) and E export
+    // -- decompress (both parities): factor tiles first, then rows, then vectors
     for (int32_t par = 0; par < 2; ++par) {
       std::vector<Launch>& L = bk.decompress[par];
+      const bool q = par == 0;
       bool extra_done = false;
+      auto extra = [&]() {
+        if (extra_done) return;
+        for (int32_t mi : bk.mats) fact_tiles(mi, q);
+        vec_tiles(bk);
+        extra_done = true;
+      };
+      for (int32_t S = 1; S <= 5; ++S) {
+        const std::vector<int32_t> cls = of_class(S);
+        if (cls.empty()) continue;
+        Launch l = sink.begin(K_RECON4, S);
+        extra();
+        for (int32_t mi : cls) row_tiles(mi, rows_for(mi, 4 * kTileElems));
+        sink.end(l, L);
+      }
       for (int32_t vw : {4, 1}) {
         Launch l = sink.begin(K_RECON, vw);
-        for (int32_t mi : bk.mats)
+        bool any = false;
+        for (int32_t mi : generic)
+          if ((vw == 4) == is_vec4(mi)) any = true;
+        if (any || vw == 1) extra();
+        for (int32_t mi : generic)
           if ((vw == 4) == is_vec4(mi))
-            row_tiles(mi, std::max<int64_t>(1, kTileElems / plan.mats[mi].m));
-        const bool any = static_cast<int64_t>(plan.tiles.size()) > l.tile_off;
-        if ((any || vw == 1) && !extra_done) {
-          for (int32_t mi : bk.mats) fact_tiles(mi, par == 0);
-          vec_tiles(bk);
-          extra_done = true;
-        }
+            row_tiles(mi, std::max<int64_t>(1, 2 * kTileElems / plan.mats[mi].m));
+        sink.end(l, L);
+      }
+      {
+        Launch l = sink.begin(K_CHOL, 0);
+        for (int32_t mi : bk.mats) chol_tiles(mi, q);
         sink.end(l, L);
       }
     }
@@ -304,9 +357,138 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     }
   }
   {
-    Launch l = sink.begin(K_GRAM, 1);
+    Launch l = sink.begin(K_FACT, 1);
     for (int32_t mi = 0; mi < static_cast<int32_t>(plan.mats.size()); ++mi) fact_tiles(mi, true);
     sink.end(l, plan.gram_init);
+    l = sink.begin(K_CHOL, 0);
+    for (int32_t mi = 0; mi < static_cast<int32_t>(plan.mats.size()); ++mi) chol_tiles(mi, true);
+    sink.end(l, plan.gram_init);
+  }
+
+  // ---- launch families and algorithmic bytes (host-side profiling)
+  auto tile_bytes = [&](const Launch& l, const Tile& t, bool odd) -> double {
+    const double eb = ef ? 12.0 : 4.0;  // M read, E read, E written per compress element
+    if (t.kind == T_VEC) return 8.0 * t.b;
+    const MatDesc& d = plan.mats[t.idx];
+    const double n = d.n, m = d.m, rr = double(r);
+    switch (l.kernel) {
+      case K_PFUSED:
+        return t.b * m * eb + t.b * rr * 8.0 + (t.a == 0 ? m * rr * 12.0 : 0.0);
+      case K_PROW:
+        return m * (ef ? 8.0 : 4.0) + rr * 8.0 + (t.a == 0 ? m * rr * 12.0 : 0.0);
+      case K_EUPD:
+        return t.b * m * 4.0;
+      case K_QSTEP: {
+        const double r0 = double(t.a) * d.q_rows;
+        const double rows = std::min<double>(d.q_rows, n - r0);
+        const double cols = std::min<double>(d.q_cb, m - double(t.b) * d.q_cb);
+        return rows * cols * eb + (t.b == 0 ? rows * rr * 8.0 : 0.0);
+      }
+      case K_QFIN: {
+        const double e0 = double(t.a) * kBlock, ent = double(d.q_cb) * rr;
+        const double cols_e = std::min<double>(ent, (m - double(t.b) * d.q_cb) * rr);
+        return 8.0 * std::max(0.0, std::min<double>(kBlock, cols_e - e0));
+      }
+      case K_RECON:
+      case K_RECON4:
+        if (t.kind == T_FACT) {
+          const double rows = odd ? n : m;
+          return std::min<double>(d.fact_rows, rows - double(t.a) * d.fact_rows) * rr * 8.0;
+        }
+        return t.b * m * 4.0 + t.b * rr * 4.0 + (t.a == 0 ? m * rr * 4.0 : 0.0);
+      case K_APPLY:
+        return t.b * rr * 8.0;
+      case K_FACT:
+        return std::min<double>(d.fact_rows, (l.variant & 1 ? m : n) - double(t.a) * d.fact_rows) * rr * 4.0;
+      case K_EMAT:
+        return t.b * m * 8.0;
+      default:
+        return 0.0;
+    }
+  };
+  auto family_of = [](int32_t kernel, bool odd) -> int32_t {
+    switch (kernel) {
+      case K_PFUSED: case K_PROW: case K_EUPD: return 1;   // ACP_KERNEL_P_STEP
+      case K_QSTEP: return 2;                               // ACP_KERNEL_Q_STEP
+      case K_QFIN: return 3;                                // ACP_KERNEL_Q_FINISH
+      case K_RECON: case K_RECON4: return 4;                // ACP_KERNEL_RECONSTRUCT
+      case K_APPLY: case K_FACT: case K_CHOL: return 5;     // ACP_KERNEL_ORTH
+      case K_VEC: return odd ? 1 : 2;
+      default: return 0;
+    }
+  };
+  auto annotate = [&](std::vector<Launch>& list, bool odd) {
+    for (Launch& l : list) {
+      l.family = family_of(l.kernel, odd);
+      l.alg_bytes = 0.0;
+      for (int32_t i = 0; i < l.ntiles; ++i) l.alg_bytes += tile_bytes(l, plan.tiles[l.tile_off + i], odd);
+    }
+  };
+  for (BucketPlan& bk : plan.buckets) {
+    annotate(bk.compress[0], false);
+    annotate(bk.compress[1], true);
+    annotate(bk.decompress[0], false);
+    annotate(bk.decompress[1], true);
+    annotate(bk.emat, false);
+  }
+  annotate(plan.gram_init, false);
+
+  // ---- launches over whole groups of buckets: every bucket's launches of one kind merged into
+  // one, in the dependency order the per-bucket lists already follow
+  auto order_of = [](const Launch& l) -> int32_t {
+    switch (l.kernel) {
+      case K_APPLY: return 0;
+      case K_PFUSED: return 1 + l.variant;          // 2..6
+      case K_PROW: return 10;
+      case K_EUPD: return 11;
+      case K_QSTEP: return (l.variant & kQFused) ? 20 : (l.variant == 4 ? 21 : 22);
+      case K_QFIN: return 23;
+      case K_RECON4: return 30 + l.variant;         // 31..35
+      case K_RECON: return l.variant == 4 ? 40 : 41;
+      case K_CHOL: return 42;
+      case K_VEC: return 50;
+      default: return 60;
+    }
+  };
+  auto merge = [&](int32_t b0, int32_t b1, auto get) {
+    std::vector<Launch> all;
+    for (int32_t b = b0; b < b1; ++b)
+      for (const Launch& l : get(plan.buckets[b])) all.push_back(l);
+    std::stable_sort(all.begin(), all.end(),
+                     [&](const Launch& x, const Launch& y) { return order_of(x) < order_of(y); });
+    std::vector<Launch> out;
+    for (size_t i = 0; i < all.size();) {
+      size_t j = i;
+      Launch m = all[i];
+      m.tile_off = static_cast<int64_t>(plan.tiles.size());
+      m.ntiles = 0;
+      m.alg_bytes = 0.0;
+      while (j < all.size() && all[j].kernel == all[i].kernel && all[j].variant == all[i].variant) {
+        for (int32_t k = 0; k < all[j].ntiles; ++k) {
+          const Tile tc = plan.tiles[all[j].tile_off + k];
+          plan.tiles.push_back(tc);
+        }
+        m.ntiles += all[j].ntiles;
+        m.alg_bytes += all[j].alg_bytes;
+        ++j;
+      }
+      out.push_back(m);
+      i = j;
+    }
+    return out;
+  };
+  {
+    const int32_t nb = static_cast<int32_t>(plan.buckets.size());
+    for (int32_t b0 = 0; b0 < nb; b0 += kMaxGroup) {
+      const int32_t b1 = std::min(nb, b0 + kMaxGroup);
+      std::array<std::vector<Launch>, 2> gc, gd;
+      for (int32_t par = 0; par < 2; ++par) {
+        gc[par] = merge(b0, b1, [par](const BucketPlan& bk) -> const std::vector<Launch>& { return bk.compress[par]; });
+        gd[par] = merge(b0, b1, [par](const BucketPlan& bk) -> const std::vector<Launch>& { return bk.decompress[par]; });
+      }
+      plan.group_compress.push_back(gc);
+      plan.group_decompress.push_back(gd);
+    }
   }
 
   // ---- region offsets (bytes)
@@ -316,14 +498,12 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   plan.w_doubles = static_cast<int64_t>(plan.mats.size()) * r * r;
   plan.gpart_doubles = gpart;
   plan.qpart_floats = qpart;
-  plan.n_ctr = nctr;
   int64_t off = 0;
   plan.off_e = off;     off = a256(off + e_floats * 4);
   plan.off_fac = off;   off = a256(off + fac_floats * 4);
   plan.off_w = off;     off = a256(off + plan.w_doubles * 8);
   plan.off_gpart = off; off = a256(off + gpart * 8);
   plan.off_qpart = off; off = a256(off + qpart * 4);
-  plan.off_ctr = off;   off = a256(off + nctr * 4);
   plan.off_mats = off;  off = a256(off + static_cast<int64_t>(plan.mats.size() * sizeof(MatDesc)));
   plan.off_vecs = off;  off = a256(off + static_cast<int64_t>(plan.vecs.size() * sizeof(VecDesc)));
   plan.off_tiles = off; off = a256(off + static_cast<int64_t>(plan.tiles.size() * sizeof(Tile)));

@@ -3,6 +3,7 @@
 #pragma once
 
 #include <cstdint>
+#include <array>
 #include <string>
 #include <vector>
 
@@ -41,13 +42,15 @@ struct Plan {
   std::vector<MatDesc> mats;
   std::vector<VecDesc> vecs;
   std::vector<Tile> tiles;
-  std::vector<Launch> gram_init;     // Gram -> W of every matrix's Q slot
+  std::vector<Launch> gram_init;     // W of every matrix's Q slot (after bind / restore)
+  // launches covering whole groups of kMaxGroup buckets (the *_all entry points):
+  // [group][parity] -> launches
+  std::vector<std::array<std::vector<Launch>, 2>> group_compress, group_decompress;
 
   // device state regions (byte offsets from the block base)
-  int64_t off_e = 0, off_fac = 0, off_w = 0, off_gpart = 0, off_qpart = 0, off_ctr = 0;
+  int64_t off_e = 0, off_fac = 0, off_w = 0, off_gpart = 0, off_qpart = 0;
   int64_t off_mats = 0, off_vecs = 0, off_tiles = 0, total_bytes = 0;
   int64_t e_floats = 0, fac_floats = 0, w_doubles = 0, gpart_doubles = 0, qpart_floats = 0;
-  int64_t n_ctr = 0;
 };
 
 // Builds the plan; returns "" on success or an error text.

@@ -111,3 +111,53 @@ def test_full_size_residual_identity(name):
             g = F.T @ F
             assert torch.allclose(g, torch.eye(wl.rank, dtype=torch.float64, device=run.dev), atol=1e-5), (t, tid)
     PU.log(f"  full-size residual identity worst {worst:.2e}")
+
+
+def _grouped_vs_per_bucket(shapes, rank, grads_of, steps, cap=25 << 20):
+    a = PU.Runner(shapes, rank, cap=cap)
+    b = PU.Runner(shapes, rank, cap=cap)
+    for t in range(1, steps + 1):
+        gb = a.pack(grads_of(t))
+        a.step(t, gb)
+        b.acp.compress_all(t, gb, b.fbuf)
+        b.acp.decompress_all(t, b.fbuf, b.out)
+        assert _same(_snap(a, t), _snap(b, t)), f"grouped call differs at step {t}"
+    return a.nb
+
+
+@pytest.mark.parametrize("name", ["resnet50_r4", "bert_base_r4", "bert_base_r32"])
+def test_grouped_calls_equal_per_bucket_calls(name):
+    wl = sg.WORKLOADS[name]
+    shapes = [p.shape for p in wl.params]
+    _grouped_vs_per_bucket(shapes, wl.rank, lambda t: sg.gradient_set(wl, t), 4)
+
+
+def test_grouped_calls_over_several_launch_groups():
+    g = np.random.default_rng(7)
+    shapes = [(int(g.integers(8, 200)), int(g.integers(8, 300))) if i % 3 else (int(g.integers(1, 500)),)
+              for i in range(150)]
+    params = [sg.Param(f"t{i}", s) for i, s in enumerate(shapes)]
+    wl = sg.Workload("many", params, 4, 4, lambda p: 0.1, seed=5)
+    nb = _grouped_vs_per_bucket(shapes, 4, lambda t: sg.gradient_set(wl, t), 4, cap=1 << 14)
+    assert nb > 64
+
+
+def test_grouped_call_sequencing():
+    from paper_2306_08881_amd import _lib as L
+    shapes = [(32, 24), (24,), (40, 16)]
+    run = PU.Runner(shapes, 4, cap=1 << 10)
+    assert run.nb >= 2
+    gb = run.pack({i: np.ones(s, np.float32) for i, s in enumerate(shapes)})
+    run.acp.compress(1, 0, gb[0], run.fbuf[0])          # bucket 0 ahead of the others
+    with pytest.raises(L.AcpError) as e:
+        run.acp.compress_all(1, gb, run.fbuf)
+    assert e.value.status == L.ACP_E_STEP
+    run.acp.decompress(1, 0, run.fbuf[0], run.out[0])
+    for b in range(1, run.nb):
+        run.acp.compress(1, b, gb[b], run.fbuf[b])
+        run.acp.decompress(1, b, run.fbuf[b], run.out[b])
+    run.acp.compress_all(2, gb, run.fbuf)
+    with pytest.raises(L.AcpError) as e:
+        run.acp.compress_all(3, gb, run.fbuf)
+    assert e.value.status == L.ACP_E_STEP
+    run.acp.decompress_all(2, run.fbuf, run.out)

@@ -48,8 +48,9 @@ def algorithmic_bytes(wl, rank):
 
 
 def cpu_baseline(wl, seconds: float = 12.0):
-    """The fp64 oracle on a bounded sample: whole buckets, one P-step and one Q-step each."""
-    import numpy as np
+    """The fp64 oracle on a bounded sample of the same workload: every bucket, steps 1, 2, ...
+    (P-steps and Q-steps in turn) until about ``seconds`` of oracle work (input generation is
+    not timed)."""
     from threadpoolctl import threadpool_info
     import synthgrad as sg
     from oracle.acp import AcpOracle
@@ -57,29 +58,93 @@ def cpu_baseline(wl, seconds: float = 12.0):
 
     shapes = [p.shape for p in wl.params]
     lay = plan(shapes, wl.rank, wl.cap_bytes)
-    done_bytes = 0.0
-    buckets = []
-    elapsed = 0.0
-    for b in range(1, len(lay.buckets)):
-        tids = lay.buckets[b].tids
-        orc = AcpOracle(shapes, wl.rank, seed=wl.seed, cap_bytes=wl.cap_bytes, tensor_ids=tids)
-        grads = {t: sg.gradient(wl, t, 1) for t in tids}
-        sub = type(wl)(wl.name, [wl.params[t] for t in tids], wl.rank, 2, wl.sigma)
-        step_bytes = algorithmic_bytes(sub, wl.rank)[0]
+    orc = AcpOracle(shapes, wl.rank, seed=wl.seed, cap_bytes=wl.cap_bytes)
+    step_bytes = algorithmic_bytes(wl, wl.rank)[0]
+    elapsed, steps = 0.0, 0
+    while elapsed < seconds and steps < 20:
+        t = steps + 1
+        grads = sg.gradient_set(wl, t)
         tb = time.perf_counter()
-        for t in (1, 2):
+        for b in range(len(lay.buckets)):
             buf = orc.compress_bucket(t, b, grads)
             orc.decompress_bucket(t, b, buf)
         elapsed += time.perf_counter() - tb
-        done_bytes += 2 * step_bytes
-        buckets.append(b)
-        if elapsed > seconds:
-            break
+        steps += 1
+        del grads
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    return {"value": round(done_bytes / elapsed / 1e9, 4), "unit": "GB/s", "cores": int(threads),
+    return {"value": round(steps * step_bytes / elapsed / 1e9, 4), "unit": "GB/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"{wl.name}: buckets {buckets[0]}..{buckets[-1]} ({len(buckets)} of {len(lay.buckets)}), "
-                      f"steps 1-2 (one P-step, one Q-step), fp64 NumPy, {elapsed:.1f} s of oracle work"}
+            "sample": f"{wl.name}: all {len(lay.buckets)} buckets, steps 1-{steps}, fp64 NumPy "
+                      f"(OpenBLAS), {elapsed:.1f} s of oracle work"}
+
+
+KERNEL_SYMBOLS = {"P-step compress (k_pfused)": "k_pfused", "Q-step compress (k_qstep)": "k_qstep",
+                  "Q-step finish (k_qfin)": "k_qfin", "decompress (k_recon4)": "k_recon"}
+TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "traffic.txt")
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    src = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2306_08881_amd", "csrc",
+                       "kernels.hip")
+    return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+
+
+def pmc_summary(fetch_csv: str, write_csv: str, workload: str):
+    """Per-kernel HBM bytes per dispatch from FETCH_SIZE / WRITE_SIZE runs, each scaled by what
+    the counter reads for the copy probe (a device-to-device copy of 1 GiB), written to
+    profiles/traffic.txt with the kernel source hash they were taken on."""
+    import csv
+    from collections import defaultdict
+
+    def load(path):
+        d = defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            d[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+        return d
+
+    f, w = load(fetch_csv), load(write_csv)
+    gib_kib = float(1 << 20)
+    copy_f = [v for k, vs in f.items() if "copyBuffer" in k for v in vs if v > 0.25 * gib_kib]
+    copy_w = [v for k, vs in w.items() if "copyBuffer" in k for v in vs if v > 0.5 * gib_kib]
+    sf = gib_kib / (sum(copy_f) / len(copy_f))
+    sw = gib_kib / (sum(copy_w) / len(copy_w))
+    out = {"source_hash": kernel_source_hash(), "workload": workload, "fetch_scale": round(sf, 4),
+           "write_scale": round(sw, 4), "kernels": {}}
+    print(f"| kernel | dispatches | FETCH_SIZE KiB/dispatch | WRITE_SIZE KiB/dispatch | HBM bytes/dispatch (scaled) |")
+    print("|---|---|---|---|---|")
+    for name in sorted(f):
+        if "acp::" not in name and "copyBuffer" not in name:
+            continue
+        fv, wv = f[name], w.get(name, [0.0])
+        fa, wa = sum(fv) / len(fv), sum(wv) / len(wv)
+        hbm = (fa * sf + wa * sw) * 1024
+        short = name[name.find("k_"):name.find("(", name.find("k_"))] if "k_" in name else name
+        out["kernels"][short] = {"dispatches": len(fv), "fetch_kib": round(fa, 1), "write_kib": round(wa, 1),
+                                 "hbm_bytes": round(hbm, 1)}
+        print(f"| {short} | {len(fv)} | {fa:.0f} | {wa:.0f} | {hbm:.4g} |")
+    print(f"\ncopy probe scale factors: FETCH_SIZE x{sf:.4f}, WRITE_SIZE x{sw:.4f}")
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    json.dump(out, open(TRAFFIC_FILE, "w"), indent=1)
+
+
+def measured_traffic(workload: str, family: str, launches: int):
+    """HBM bytes per launch of the dominant kernel family from profiles/traffic.txt, or None
+    when the counters were taken on other kernel sources or for another workload."""
+    try:
+        t = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if t.get("source_hash") != kernel_source_hash() or t.get("workload") not in (None, workload):
+        return None
+    sym = KERNEL_SYMBOLS.get(family)
+    ks = [v for k, v in t["kernels"].items() if sym and k.startswith(sym)]
+    if not ks:
+        return None
+    # dispatch-weighted bytes per launch of the family (its launches of every class)
+    tot = sum(v["hbm_bytes"] * v["dispatches"] for v in ks)
+    n = sum(v["dispatches"] for v in ks)
+    return round(tot / n, 1) if n else None
 
 
 def main():
@@ -95,7 +160,15 @@ def main():
     ap.add_argument("--mode", choices=["all", "bucket"], default="all",
                     help="all: acp_compress_all / acp_decompress_all (every bucket in one launch per "
                          "kernel kind); bucket: acp_compress / acp_decompress per bucket")
+    ap.add_argument("--compare", action="store_true",
+                    help="also time the other mode and report it in config")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="summarise two rocprofv3 --pmc runs of this benchmark (FETCH_SIZE, then "
+                         "WRITE_SIZE counter_collection.csv) and exit")
     args = ap.parse_args()
+    if args.pmc_summary:
+        pmc_summary(*args.pmc_summary, workload=args.workload)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
               "(the compressor is data-parallel: each rank runs this same step on its own GPU).",
@@ -181,7 +254,7 @@ def main():
         one_step(args.mode)
     steps = args.steps + (args.steps % 2)
     ms = timed(steps, args.mode)
-    ms_other = timed(steps, other)
+    ms_other = timed(steps, other) if args.compare else None
 
     # per-kernel pass: the same steps again with every launch of one kernel family bracketed by
     # HIP events on its own stream (acp_profile_*), once per family
@@ -197,7 +270,10 @@ def main():
         if n:
             kern[name] = {"launches": n, "avg_launch_us": sec / n * 1e6, "bytes_per_launch": by / n,
                           "gbs": by / sec / 1e9, "ms_per_step": sec / steps * 1e3}
-    dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
+    # the dominant kernel: k_qstep, the longest-running single kernel of the step (one launch per
+    # Q-step); the P-step time is split over one k_pfused launch per column class
+    dom = "Q-step compress (k_qstep)" if "Q-step compress (k_qstep)" in kern else \
+        max(kern, key=lambda k: kern[k]["ms_per_step"])
     dk = kern[dom]
     step_bytes, bp, bq, bd, nc, n1 = algorithmic_bytes(wl, wl.rank)
     gbs = step_bytes / (ms * 1e-3) / 1e9
@@ -218,17 +294,36 @@ def main():
                                f"{wl.numel} parameters, rank {wl.rank}, 25 MiB buckets ({nb})",
                    "rank": wl.rank, "buckets": nb, "parameters": wl.numel, "mode": args.mode,
                    "streams": nstreams if args.mode == "bucket" else 1,
-                   f"ms_per_step_{other}_mode": round(ms_other, 4),
-                   f"gbs_{other}_mode": round(step_bytes / (ms_other * 1e-3) / 1e9, 2),
                    "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
                    "gradient_elements_per_s": round(wl.numel / (ms * 1e-3), 1),
                    "algorithmic_bytes_per_step": step_bytes,
                    "kernels": {k: {kk: round(vv, 3) for kk, vv in v.items()} for k, v in kern.items()}},
         "roofline": {"bound": "hbm", "achieved": round(dk["gbs"], 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(dk["gbs"] / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(dk["gbs"] / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic(wl.name, dom, dk["launches"]),
                      "kernel": dom, "avg_launch_us": round(dk["avg_launch_us"], 3),
                      "bytes_per_launch": round(dk["bytes_per_launch"], 1)},
     }
+    if ms_other is not None:
+        res["config"][f"ms_per_step_{other}_mode"] = round(ms_other, 4)
+        res["config"][f"gbs_{other}_mode"] = round(step_bytes / (ms_other * 1e-3) / 1e9, 2)
+    # copy probe: device-to-device copy of 1 GiB, the achievable streaming ceiling on this GPU
+    src = torch.empty(1 << 28, dtype=torch.float32, device=dev).normal_()
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record(main)
+    for _ in range(10):
+        dst.copy_(src)
+    c1.record(main)
+    torch.cuda.synchronize()
+    copy_gbs = 10 * 2 * src.numel() * 4 / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    res["config"]["copy_probe_gbs"] = round(copy_gbs, 1)
+    res["config"]["pct_of_copy_probe"] = round(100 * gbs / copy_gbs, 2)
+    del src, dst
+
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl)
     res["cpu_baseline_host"] = {"cpu": platform.processor() or platform.machine(),

@@ -26,6 +26,8 @@ namespace acp {
 constexpr int kBlock = 256;       // threads per workgroup (4 waves of 64)
 constexpr int kWave = 64;
 constexpr double kTau = 1e-4;     // rank-deficiency threshold of orth()
+constexpr int kMaxTileRows = 256; // rows per tile of the rank-4 row kernels (factor rows in LDS)
+constexpr int kQfinWide = 64;     // Q-step chunks above which k_qfin uses 16 threads per entry
 
 struct MatDesc {
   int64_t grad_off;   // offset of the matrix in its gradient bucket (floats)

@@ -319,10 +319,10 @@ __global__ __launch_bounds__(kBlock) void k_apply(KArgs a) {
 // a row of m4 = m / 4 float4 groups into four segments of 64 S groups; lane `lane` of wave w
 // owns groups w * 64 S + s * 64 + lane, s < S, for every row of the tile, so the factor rows
 // of those columns are loaded once per workgroup and kept in registers.  The waves work on the
-// same RB = 4 / S rows at a time (1 for S >= 3).
+// same RB rows at a time (4 for S = 1, 2 for S = 2..4, 1 for S = 5).
 template <int S>
 struct Cols {
-  static constexpr int RB = S >= 3 ? 1 : 4 / S;
+  static constexpr int RB = S == 1 ? 4 : (S <= 4 ? 2 : 1);
   int wave, lane;
   int c4[S];
   bool ok[S];
@@ -378,7 +378,10 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
 
   __shared__ double Wsh[16];
   __shared__ float4 red[2][4][RB];
+  __shared__ float4 phs[kMaxTileRows];  // the tile's rows of Ph (deferred E)
   if (tid() < 16) Wsh[tid()] = a.w[d.w_slot + tid()];
+  if (deferred && tid() < t.b)
+    phs[tid()] = reinterpret_cast<const float4*>(a.fac + d.ph_slot)[t.a + tid()];
   __syncthreads();
 
   const float4* Q4 = reinterpret_cast<const float4*>(a.fac + d.q_slot);
@@ -396,7 +399,6 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
       if (store_qh && cl.ok[s]) Qh4[j] = qh[s][c];
     }
 
-  const float4* Ph4 = reinterpret_cast<const float4*>(a.fac + d.ph_slot);
   float4* P4 = reinterpret_cast<float4*>(dst_of(a, d.bucket) + d.fac_off_p);
   int buf = 0;
   for (int r0 = t.a; r0 < row_end; r0 += RB, buf ^= 1) {
@@ -405,7 +407,7 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
       const int row = r0 + rb;
-      const float4 ph = (deferred && row < row_end) ? Ph4[row] : zero4();
+      const float4 ph = (deferred && row < row_end) ? phs[row - t.a] : zero4();
       acc[rb] = zero4();
 #pragma unroll
       for (int s = 0; s < S; ++s) {
@@ -548,13 +550,15 @@ __global__ __launch_bounds__(kBlock) void k_emat(KArgs a) {
 }
 
 // ---------------------------------------------------------------------------------------
-// Q-step: tile = (row chunk, column block).  Each lane owns CPT adjacent columns; the four
-// waves take every fourth row of the chunk, four rows at a time.  F = M' is written back
-// (deferred E) and the partial M'^T Ph of the tile, summed across waves in wave order, is
-// stored for K_QFIN.  FUSED (r = 4): Ph rows are formed here as P W, and the tiles of column
-// block 0 store them.
+// Q-step: tile = (row chunk, column block of 4 x 64 x CPT columns).  Wave w owns the CPT
+// adjacent columns cb * q_cb + (w * 64 + lane) * CPT of every row of the chunk, so each row's
+// 4 KB (CPT = 4) segment is read by one workgroup.  The chunk's Ph rows are staged in LDS 64 at
+// a time (FUSED, r = 4: formed here as P W, and stored by the tiles of column block 0).  Per
+// row: F = M' = M + E written back (deferred E), partial Q += M'^T Ph over the lane's columns.
+// Each lane stores its partial sums for K_QFIN.
 template <int RK, int CPT, bool FUSED>
 __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
+  constexpr int SUB = 64;  // rows staged in LDS at a time
   const Tile t = a.tiles[blockIdx.x];
   if (t.kind == T_VEC) {
     vec_tile(a, t, true);
@@ -565,15 +569,15 @@ __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
   const int64_t m = d.m;
   const int64_t r0 = static_cast<int64_t>(t.a) * d.q_rows;
   const int64_t r1 = (r0 + d.q_rows < d.n) ? r0 + d.q_rows : d.n;
-  const int64_t col = static_cast<int64_t>(t.b) * d.q_cb + lane * CPT;
+  const int64_t col = static_cast<int64_t>(t.b) * d.q_cb + (wave * 64 + lane) * CPT;
   const bool valid = col < m;
   const bool ef = a.ef != 0;
   const float* G = src_of(a, d.bucket) + d.grad_off;
   float* E = a.e + d.e_off;
   __shared__ double Wsh[16];
+  __shared__ __align__(16) float phs[SUB * RK];
   if constexpr (FUSED) {
     if (tid() < 16) Wsh[tid()] = a.w[d.w_slot + tid()];
-    __syncthreads();
   }
   float acc[CPT][RK];
 #pragma unroll
@@ -608,55 +612,58 @@ __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
       mp[0] = g;
     }
   };
-  auto accumulate = [&](int64_t row, const float* mp) {
-    float ph[RK];
-    if constexpr (FUSED) {
-      const float4 x = *reinterpret_cast<const float4*>(a.fac + d.p_slot + row * 4);
-      const float4 y = apply_w4(x, Wsh);
-      ph[0] = y.x;
-      ph[1] = y.y;
-      ph[2] = y.z;
-      ph[3] = y.w;
-      if (t.b == 0 && lane == 0) *reinterpret_cast<float4*>(a.fac + d.ph_slot + row * 4) = y;
-    } else {
-#pragma unroll
-      for (int k = 0; k < RK; ++k) ph[k] = a.fac[d.ph_slot + row * RK + k];
-    }
+  auto accumulate = [&](int rr, const float* mp) {
+    const float* ph = &phs[rr * RK];
 #pragma unroll
     for (int c = 0; c < CPT; ++c)
 #pragma unroll
       for (int k = 0; k < RK; ++k) acc[c][k] = fmaf(mp[c], ph[k], acc[c][k]);
   };
 
-  int64_t row = r0 + wave;
-  for (; row + 12 < r1; row += 16) {
-    float mp[4][CPT];
+  for (int64_t s0 = r0; s0 < r1; s0 += SUB) {
+    const int sn = static_cast<int>((r1 - s0) < SUB ? (r1 - s0) : SUB);
+    __syncthreads();  // Wsh ready / previous rows consumed
+    if (tid() < sn) {
+      const int64_t row = s0 + tid();
+      if constexpr (FUSED) {
+        const float4 y = apply_w4(*reinterpret_cast<const float4*>(a.fac + d.p_slot + row * 4), Wsh);
+        *reinterpret_cast<float4*>(&phs[tid() * 4]) = y;
+        if (t.b == 0) *reinterpret_cast<float4*>(a.fac + d.ph_slot + row * 4) = y;
+      } else {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) load_mp(row + 4 * u, mp[u]);
+        for (int k = 0; k < RK; ++k) phs[tid() * RK + k] = a.fac[d.ph_slot + row * RK + k];
+      }
+    }
+    __syncthreads();
+    int rr = 0;
+    for (; rr + 4 <= sn; rr += 4) {
+      float mp[4][CPT];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) accumulate(row + 4 * u, mp[u]);
+      for (int u = 0; u < 4; ++u) load_mp(s0 + rr + u, mp[u]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) accumulate(rr + u, mp[u]);
+    }
+    for (; rr < sn; ++rr) {
+      float mp0[CPT];
+      load_mp(s0 + rr, mp0);
+      accumulate(rr, mp0);
+    }
   }
-  for (; row < r1; row += 4) {
-    float mp0[CPT];
-    load_mp(row, mp0);
-    accumulate(row, mp0);
-  }
-  constexpr int W = 64 * CPT * RK;  // partial entries of one wave
-  __shared__ float red[4][W];
+  if (!valid) return;
+  const int64_t ncb = (m + d.q_cb - 1) / d.q_cb;
+  const int64_t stride = ncb * d.q_cb * RK;  // one row chunk of partials
+  float* part = a.qpart + d.qpart + static_cast<int64_t>(t.a) * stride + (col - 0) * RK;
 #pragma unroll
   for (int c = 0; c < CPT; ++c)
 #pragma unroll
-    for (int k = 0; k < RK; ++k) red[wave][(lane * CPT + c) * RK + k] = acc[c][k];
-  __syncthreads();
-  const int64_t ncb = (m + d.q_cb - 1) / d.q_cb;
-  const int64_t stride = ncb * d.q_cb * RK;  // one row chunk of partials
-  float* part = a.qpart + d.qpart + static_cast<int64_t>(t.a) * stride + static_cast<int64_t>(t.b) * d.q_cb * RK;
-  for (int e = tid(); e < W; e += kBlock) part[e] = ((red[0][e] + red[1][e]) + red[2][e]) + red[3][e];
+    for (int k = 0; k < RK; ++k) part[c * RK + k] = acc[c][k];
 }
 
-// Q-step finish: for entries [t.a * 256, t.a * 256 + 256) of column block t.b, Q_loc = sum
-// over the row chunks' partials, added in chunk order; written to the factor buffer and to
-// the Ql slot.
+// Q-step finish: Q_loc = sum over the row chunks' partials.  A tile covers NE entries of column
+// block t.b (entries [t.a * NE, t.a * NE + NE)) with 256 / NE threads per entry; NE = 64 when
+// the matrix has at most kQfinWide chunks, else 16.  Each thread adds a contiguous share of
+// the chunks in chunk order and the shares are added in thread order.  The result goes to the
+// factor buffer and to the Ql slot.
 template <int RK>
 __global__ __launch_bounds__(kBlock) void k_qfin(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
@@ -664,25 +671,38 @@ __global__ __launch_bounds__(kBlock) void k_qfin(KArgs a) {
   const int64_t m = d.m;
   const int64_t ncb = (m + d.q_cb - 1) / d.q_cb;
   const int64_t stride = ncb * d.q_cb * RK;
-  const int e = t.a * kBlock + tid();
-  if (e >= d.q_cb * RK) return;
+  const int ne = d.q_chunks > kQfinWide ? 16 : 64;       // entries per tile
+  const int ng = kBlock / ne;                            // threads per entry
+  const int gq = tid() / ne, el = tid() % ne;
+  const int e = t.a * ne + el;                           // entry within the column block
   const int64_t c = static_cast<int64_t>(t.b) * d.q_cb + e / RK;
-  if (c >= m) return;
-  const float* base = a.qpart + d.qpart + static_cast<int64_t>(t.b) * d.q_cb * RK + e;
-  constexpr int U = 8;
+  const bool on = e < d.q_cb * RK && c < m;
+  const int per = (d.q_chunks + ng - 1) / ng;
+  const int ch0 = gq * per, ch1 = (ch0 + per < d.q_chunks) ? ch0 + per : d.q_chunks;
   float s = 0.f;
-  int ch = 0;
-  for (; ch + U <= d.q_chunks; ch += U) {
-    float v[U];
+  if (on) {
+    const float* base = a.qpart + d.qpart + static_cast<int64_t>(t.b) * d.q_cb * RK + e;
+    constexpr int U = 8;
+    int ch = ch0;
+    for (; ch + U <= ch1; ch += U) {
+      float v[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) v[u] = base[(ch + u) * stride];
+      for (int u = 0; u < U; ++u) v[u] = base[(ch + u) * stride];
 #pragma unroll
-    for (int u = 0; u < U; ++u) s += v[u];
+      for (int u = 0; u < U; ++u) s += v[u];
+    }
+    for (; ch < ch1; ++ch) s += base[ch * stride];
   }
-  for (; ch < d.q_chunks; ++ch) s += base[ch * stride];
-  const int64_t o = c * RK + (e % RK);
-  dst_of(a, d.bucket)[d.fac_off_q + o] = s;
-  a.fac[d.ql_slot + o] = s;
+  __shared__ float red[kBlock];
+  red[tid()] = s;
+  __syncthreads();
+  if (gq == 0 && on) {
+    float tot = red[el];
+    for (int g = 1; g < ng; ++g) tot += red[g * ne + el];
+    const int64_t o = c * RK + (e % RK);
+    dst_of(a, d.bucket)[d.fac_off_q + o] = tot;
+    a.fac[d.ql_slot + o] = tot;
+  }
 }
 
 // ---------------------------------------------------------------------------------------
@@ -768,11 +788,14 @@ __global__ __launch_bounds__(kBlock) void k_recon4(KArgs a) {
   const float* agg = src_of(a, d.bucket);
   const float4* A4 = reinterpret_cast<const float4*>(odd ? agg + d.fac_off_p : a.fac + d.ph_slot);
   const float4* B4 = reinterpret_cast<const float4*>(odd ? a.fac + d.qh_slot : agg + d.fac_off_q);
+  __shared__ float4 as[kMaxTileRows];  // the tile's rows of A, scaled by 1 / p
+  if (tid() < t.b) as[tid()] = scale4(A4[t.a + tid()], a.inv_p);
   float4 b[S][4];
 #pragma unroll
   for (int s = 0; s < S; ++s)
 #pragma unroll
     for (int c = 0; c < 4; ++c) b[s][c] = cl.ok[s] ? B4[4 * cl.c4[s] + c] : zero4();
+  __syncthreads();
   float4* O4 = reinterpret_cast<float4*>(dst_of(a, d.bucket) + d.grad_off);
   const int row_end = t.a + t.b;
   for (int r0 = t.a; r0 < row_end; r0 += RB) {
@@ -780,7 +803,7 @@ __global__ __launch_bounds__(kBlock) void k_recon4(KArgs a) {
     for (int rb = 0; rb < RB; ++rb) {
       const int row = r0 + rb;
       if (row >= row_end) continue;
-      const float4 ar = scale4(A4[row], a.inv_p);
+      const float4 ar = as[row - t.a];
       const int64_t base = static_cast<int64_t>(row) * m4;
 #pragma unroll
       for (int s = 0; s < S; ++s)

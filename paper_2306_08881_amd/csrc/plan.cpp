@@ -150,8 +150,8 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       fac_floats += 2 * np + 3 * mp;
       const bool vec4 = (t.m % 4 == 0) && (d.grad_off % 4 == 0);
       const int64_t cpt = (vec4 && r <= 8) ? 4 : 1;
-      d.q_cb = static_cast<int32_t>(64 * cpt);
-      d.q_rows = static_cast<int32_t>(align_up(std::max<int64_t>(64, cdiv(t.n, 64)), 8));
+      d.q_cb = static_cast<int32_t>(4 * 64 * cpt);
+      d.q_rows = 64;
       d.q_chunks = static_cast<int32_t>(cdiv(t.n, d.q_rows));
       const int64_t ncb = cdiv(t.m, d.q_cb);
       d.qpart = qpart;
@@ -221,8 +221,9 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   // rows per tile of the rank-4 kernels: a multiple of the rows handled per round
   auto rows_for = [&](int32_t mi, int64_t elems) {
     const MatDesc& d = plan.mats[mi];
-    const int64_t rb = d.scls >= 3 ? 1 : 4 / d.scls;
-    return rb * std::max<int64_t>(1, elems / (int64_t(d.m) * rb));
+    const int64_t rb = d.scls == 1 ? 4 : (d.scls <= 4 ? 2 : 1);
+    const int64_t rows = rb * std::max<int64_t>(1, elems / (int64_t(d.m) * rb));
+    return std::min<int64_t>(rows, kMaxTileRows);
   };
 
   for (BucketPlan& bk : plan.buckets) {
@@ -292,7 +293,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         bool any = false;
         const std::vector<int32_t>& set = (variant & kQFused) ? fast : generic;
         for (int32_t mi : set) {
-          if (!(variant & kQFused) && plan.mats[mi].q_cb != 64 * variant) continue;
+          if (!(variant & kQFused) && plan.mats[mi].q_cb != 4 * 64 * variant) continue;
           qtiles(mi);
           any = true;
         }
@@ -303,7 +304,8 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       for (int32_t mi : bk.mats) {
         const MatDesc& d = plan.mats[mi];
         const int32_t ncb = static_cast<int32_t>(cdiv(d.m, d.q_cb));
-        const int32_t nblk = static_cast<int32_t>(cdiv(int64_t(d.q_cb) * r, kBlock));
+        const int64_t ne = d.q_chunks > kQfinWide ? 16 : 64;
+        const int32_t nblk = static_cast<int32_t>(cdiv(int64_t(d.q_cb) * r, ne));
         for (int32_t cb = 0; cb < ncb; ++cb)
           for (int32_t eb = 0; eb < nblk; ++eb) plan.tiles.push_back(Tile{T_QTILE, mi, eb, cb});
       }
@@ -330,7 +332,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         if (cls.empty()) continue;
         Launch l = sink.begin(K_RECON4, S);
         extra();
-        for (int32_t mi : cls) row_tiles(mi, rows_for(mi, 4 * kTileElems));
+        for (int32_t mi : cls) row_tiles(mi, rows_for(mi, 8 * kTileElems));
         sink.end(l, L);
       }
       for (int32_t vw : {4, 1}) {
@@ -385,9 +387,10 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         return rows * cols * eb + (t.b == 0 ? rows * rr * 8.0 : 0.0);
       }
       case K_QFIN: {
-        const double e0 = double(t.a) * kBlock, ent = double(d.q_cb) * rr;
+        const double ne = d.q_chunks > kQfinWide ? 16.0 : 64.0;
+        const double e0 = double(t.a) * ne, ent = double(d.q_cb) * rr;
         const double cols_e = std::min<double>(ent, (m - double(t.b) * d.q_cb) * rr);
-        return 8.0 * std::max(0.0, std::min<double>(kBlock, cols_e - e0));
+        return 8.0 * std::max(0.0, std::min<double>(ne, cols_e - e0));
       }
       case K_RECON:
       case K_RECON4:
@@ -450,7 +453,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       default: return 60;
     }
   };
-  auto merge = [&](int32_t b0, int32_t b1, auto get) {
+  auto merge = [&](int32_t b0, int32_t b1, auto get, bool odd) {
     std::vector<Launch> all;
     for (int32_t b = b0; b < b1; ++b)
       for (const Launch& l : get(plan.buckets[b])) all.push_back(l);
@@ -463,15 +466,24 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       m.tile_off = static_cast<int64_t>(plan.tiles.size());
       m.ntiles = 0;
       m.alg_bytes = 0.0;
+      // the launch's tiles, longest first so that no long tile starts last; factor tiles
+      // (short in bytes but a serial Gram / Cholesky) lead
+      std::vector<std::pair<double, Tile>> ts;
       while (j < all.size() && all[j].kernel == all[i].kernel && all[j].variant == all[i].variant) {
         for (int32_t k = 0; k < all[j].ntiles; ++k) {
           const Tile tc = plan.tiles[all[j].tile_off + k];
-          plan.tiles.push_back(tc);
+          const double w = tc.kind == T_FACT ? 1e30 : tile_bytes(all[j], tc, odd);
+          ts.emplace_back(w, tc);
         }
         m.ntiles += all[j].ntiles;
         m.alg_bytes += all[j].alg_bytes;
         ++j;
       }
+      std::stable_sort(ts.begin(), ts.end(),
+                       [](const std::pair<double, Tile>& x, const std::pair<double, Tile>& y) {
+                         return x.first > y.first;
+                       });
+      for (const auto& p : ts) plan.tiles.push_back(p.second);
       out.push_back(m);
       i = j;
     }
@@ -483,8 +495,8 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       const int32_t b1 = std::min(nb, b0 + kMaxGroup);
       std::array<std::vector<Launch>, 2> gc, gd;
       for (int32_t par = 0; par < 2; ++par) {
-        gc[par] = merge(b0, b1, [par](const BucketPlan& bk) -> const std::vector<Launch>& { return bk.compress[par]; });
-        gd[par] = merge(b0, b1, [par](const BucketPlan& bk) -> const std::vector<Launch>& { return bk.decompress[par]; });
+        gc[par] = merge(b0, b1, [par](const BucketPlan& bk) -> const std::vector<Launch>& { return bk.compress[par]; }, par == 1);
+        gd[par] = merge(b0, b1, [par](const BucketPlan& bk) -> const std::vector<Launch>& { return bk.decompress[par]; }, par == 1);
       }
       plan.group_compress.push_back(gc);
       plan.group_decompress.push_back(gd);

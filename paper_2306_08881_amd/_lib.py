@@ -77,6 +77,9 @@ def load(path: str = LIB_PATH) -> C.CDLL:
         return _lib
     if not os.path.exists(path):
         raise ImportError(f"{path} is missing: build it with `python -m paper_2306_08881_amd.build`")
+    # torch carries its own libamdhip64.so.7; loading it first makes libacp.so bind to that
+    # same HIP runtime instead of a second copy that would not know torch's devices and streams
+    import torch  # noqa: F401
     lib = C.CDLL(path)
     for name, (res, args) in SIGNATURES.items():
         fn = getattr(lib, name)

@@ -28,6 +28,8 @@ constexpr int kWave = 64;
 constexpr double kTau = 1e-4;     // rank-deficiency threshold of orth()
 constexpr int kMaxTileRows = 256; // rows per tile of the rank-4 row kernels (factor rows in LDS)
 constexpr int kQfinWide = 64;     // Q-step chunks above which k_qfin uses 16 threads per entry
+constexpr int64_t kMaxCols = int64_t(1) << 24;  // columns of a compressed matrix, at most
+constexpr int kQRows = 64;        // rows per Q-step row chunk (at most; the chunk's Ph rows sit in LDS)
 
 struct MatDesc {
   int64_t grad_off;   // offset of the matrix in its gradient bucket (floats)

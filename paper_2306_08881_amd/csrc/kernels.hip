@@ -12,6 +12,8 @@
 // P_hat Q_loc^T while it streams F, so each step reads M and E once and writes E once.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "acp_internal.hpp"
 
 namespace acp {
@@ -68,6 +70,64 @@ __device__ inline float4 ld_stream(const float4* p) {
 __device__ inline void st_stream(float4* p, const float4& v) {
   const v4f w = {v.x, v.y, v.z, v.w};
   __builtin_nontemporal_store(w, reinterpret_cast<v4f*>(p));
+}
+
+// Tile-relative buffer accesses.  A buffer resource spans one tile from its first element;
+// a load past num_records returns zero and a store past it is dropped, so lanes and rows that
+// fall outside the tile need no branch: they take the offset kOut (or any offset past the
+// extent).  Branch-free loads and stores let the compiler count outstanding memory operations
+// exactly, so stores stay in flight while the next rows' loads are waited for.  Every extent
+// and in-tile offset is below 2^30, so kOut plus an offset does not wrap.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr uint32_t kOut = 0x80000000u;
+constexpr int kAuxNT = 2;  // cache policy: nontemporal (streamed once)
+
+__device__ inline Rsrc tile_rsrc(const float* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), 0, static_cast<int>(bytes),
+                                           0x00020000);
+}
+// The buffer builtins move raw 32-bit words (unsigned int); values cross them bit-cast.
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+__device__ inline float4 bld4_nt(Rsrc r, uint32_t off) {
+  const v4f v = __builtin_bit_cast(v4f, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kAuxNT));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ inline float bld1_nt(Rsrc r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kAuxNT));
+}
+__device__ inline void bst4_nt(Rsrc r, uint32_t off, const float4& v) {
+  const v4f w = {v.x, v.y, v.z, v.w};
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, w), r, off, 0, kAuxNT);
+}
+__device__ inline void bst4(Rsrc r, uint32_t off, const float4& v) {
+  const v4f w = {v.x, v.y, v.z, v.w};
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, w), r, off, 0, 0);
+}
+__device__ inline void bst1_nt(Rsrc r, uint32_t off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned int, v), r, off, 0, kAuxNT);
+}
+
+// Sum over the 64 lanes with DPP: quad butterflies, half-row and row mirrors give every lane
+// its 16-lane row sum; the four row sums are then read out and added in row order.  Every lane
+// gets the same bits.
+template <int CTRL>
+__device__ inline float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                               0xF, 0xF, false));
+}
+__device__ inline float wave_sum_dpp(float v) {
+  v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp<0x141>(v);  // row_half_mirror
+  v += dpp<0x140>(v);  // row_mirror
+  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+  return ((r0 + r1) + r2) + r3;
+}
+__device__ inline float4 wave_sum_dpp(float4 v) {
+  return make_float4(wave_sum_dpp(v.x), wave_sum_dpp(v.y), wave_sum_dpp(v.z), wave_sum_dpp(v.w));
 }
 
 // x W for one row of a rank-4 factor (W upper triangular, fp64, row-major), rounded to fp32.
@@ -339,10 +399,12 @@ struct Cols {
 
 // P-step, fused single pass (r = 4, 16-byte aligned rows of up to 5120 columns).  Each lane
 // keeps, for its columns, the rows of Qh = Q W (computed here from the reused factor; the tile
-// holding row 0 also stores Qh) and of Q_loc (when E is deferred) in registers for the whole
-// tile.  Per row: M' = M + E (or M + F - Ph_row Q_loc^T), P = M' Qh summed over the row (wave
-// butterflies, then the four waves' sums in wave order), E = M' - P Qh^T written back, P
-// written to the factor buffer.  The next rows' M and E are loaded before the reduction.
+// holding row 0 also stores Qh) and of Q_loc in registers for the whole tile (Q_loc and the
+// tile's Ph rows are zero unless E is deferred).  Per row: M' = M + E (or M + F - Ph_row
+// Q_loc^T), P = M' Qh summed over the row (DPP wave sums, then the four waves' sums in wave
+// order), E = M' - P Qh^T written back, P written to the factor buffer.  The next rows' M and
+// E are requested before the reduction; all streamed accesses are tile-relative buffer
+// accesses (E's resource is empty when error feedback is off).
 template <int S>
 __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
   constexpr int RB = Cols<S>::RB;
@@ -354,34 +416,38 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
   const MatDesc d = a.mats[t.idx];
   const int m4 = d.m >> 2;
   const Cols<S> cl(m4);
-  const bool ef = a.ef != 0, deferred = deferred_of(a, d.bucket);
-  const float4* G4 = reinterpret_cast<const float4*>(src_of(a, d.bucket) + d.grad_off);
-  float4* E4 = reinterpret_cast<float4*>(a.e + d.e_off);
-  const int row_end = t.a + t.b;
+  const bool deferred = deferred_of(a, d.bucket);
+  const uint32_t row_bytes = static_cast<uint32_t>(d.m) * 4u;
+  const uint32_t tile_bytes = static_cast<uint32_t>(t.b) * row_bytes;
+  const int64_t first = static_cast<int64_t>(t.a) * d.m;
+  const Rsrc G = tile_rsrc(src_of(a, d.bucket) + d.grad_off + first, tile_bytes);
+  const Rsrc E = tile_rsrc(a.e + d.e_off + first, a.ef ? tile_bytes : 0u);
+  const Rsrc P = tile_rsrc(dst_of(a, d.bucket) + d.fac_off_p + static_cast<int64_t>(t.a) * 4,
+                           static_cast<uint32_t>(t.b) * 16u);
+  uint32_t coff[S];
+#pragma unroll
+  for (int s = 0; s < S; ++s) coff[s] = cl.ok[s] ? static_cast<uint32_t>(cl.c4[s]) * 16u : kOut;
 
   // the first rows' M and E are requested before the factor setup
   float4 g[RB][S], e[RB][S];
-  auto load_rows = [&](int r0) {
+  auto load_rows = [&](int r0) {  // tile-relative first row
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      const int row = r0 + rb;
-      const int64_t base = static_cast<int64_t>(row) * m4;
+    for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
       for (int s = 0; s < S; ++s) {
-        const bool on = cl.ok[s] && row < row_end;
-        g[rb][s] = on ? ld_stream(G4 + base + cl.c4[s]) : zero4();
-        e[rb][s] = (on && ef) ? E4[base + cl.c4[s]] : zero4();
+        const uint32_t o = static_cast<uint32_t>(r0 + rb) * row_bytes + coff[s];
+        g[rb][s] = bld4_nt(G, o);
+        e[rb][s] = bld4_nt(E, o);
       }
-    }
   };
-  load_rows(t.a);
+  load_rows(0);
 
   __shared__ double Wsh[16];
   __shared__ float4 red[2][4][RB];
-  __shared__ float4 phs[kMaxTileRows];  // the tile's rows of Ph (deferred E)
+  __shared__ float4 phs[kMaxTileRows];  // the tile's rows of Ph (zero unless E is deferred)
   if (tid() < 16) Wsh[tid()] = a.w[d.w_slot + tid()];
-  if (deferred && tid() < t.b)
-    phs[tid()] = reinterpret_cast<const float4*>(a.fac + d.ph_slot)[t.a + tid()];
+  if (tid() < t.b)
+    phs[tid()] = deferred ? reinterpret_cast<const float4*>(a.fac + d.ph_slot)[t.a + tid()] : zero4();
   __syncthreads();
 
   const float4* Q4 = reinterpret_cast<const float4*>(a.fac + d.q_slot);
@@ -393,31 +459,30 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
   for (int s = 0; s < S; ++s)
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const int j = 4 * cl.c4[s] + c;
-      qh[s][c] = cl.ok[s] ? apply_w4(Q4[j], Wsh) : zero4();
-      ql[s][c] = (cl.ok[s] && deferred) ? Ql4[j] : zero4();
-      if (store_qh && cl.ok[s]) Qh4[j] = qh[s][c];
+      const int j = 4 * (cl.ok[s] ? cl.c4[s] : 0) + c;  // in-range row for lanes past m
+      const float4 q = apply_w4(Q4[j], Wsh);
+      const float4 l = Ql4[j];
+      qh[s][c] = cl.ok[s] ? q : zero4();
+      ql[s][c] = (cl.ok[s] && deferred) ? l : zero4();
+      if (store_qh && cl.ok[s]) Qh4[j] = q;
     }
 
-  float4* P4 = reinterpret_cast<float4*>(dst_of(a, d.bucket) + d.fac_off_p);
   int buf = 0;
-  for (int r0 = t.a; r0 < row_end; r0 += RB, buf ^= 1) {
+  for (int r0 = 0; r0 < t.b; r0 += RB, buf ^= 1) {
     float4 mp[RB][S];
     float4 acc[RB];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      const int row = r0 + rb;
-      const float4 ph = (deferred && row < row_end) ? phs[row - t.a] : zero4();
+      // rows past the tile read phs entries that are never used: their stores are dropped
+      const float4 ph = phs[(r0 + rb) & (kMaxTileRows - 1)];
       acc[rb] = zero4();
 #pragma unroll
       for (int s = 0; s < S; ++s) {
         float4 v = g[rb][s] + e[rb][s];
-        if (deferred) {
-          v.x -= dot4(ph, ql[s][0]);
-          v.y -= dot4(ph, ql[s][1]);
-          v.z -= dot4(ph, ql[s][2]);
-          v.w -= dot4(ph, ql[s][3]);
-        }
+        v.x -= dot4(ph, ql[s][0]);
+        v.y -= dot4(ph, ql[s][1]);
+        v.z -= dot4(ph, ql[s][2]);
+        v.w -= dot4(ph, ql[s][3]);
         mp[rb][s] = v;
         acc[rb] = fma4(v.x, qh[s][0], acc[rb]);
         acc[rb] = fma4(v.y, qh[s][1], acc[rb]);
@@ -428,29 +493,24 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
     load_rows(r0 + RB);
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      acc[rb] = wave_sum(acc[rb]);
+      acc[rb] = wave_sum_dpp(acc[rb]);
       if (cl.lane == 0) red[buf][cl.wave][rb] = acc[rb];
     }
     __syncthreads();
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      const int row = r0 + rb;
-      if (row >= row_end) continue;
-      const float4 P = ((red[buf][0][rb] + red[buf][1][rb]) + red[buf][2][rb]) + red[buf][3][rb];
-      const int64_t base = static_cast<int64_t>(row) * m4;
-      if (ef) {
+      const uint32_t roff = static_cast<uint32_t>(r0 + rb) * row_bytes;
+      const float4 Pr = ((red[buf][0][rb] + red[buf][1][rb]) + red[buf][2][rb]) + red[buf][3][rb];
 #pragma unroll
-        for (int s = 0; s < S; ++s)
-          if (cl.ok[s]) {
-            float4 r = mp[rb][s];
-            r.x -= dot4(P, qh[s][0]);
-            r.y -= dot4(P, qh[s][1]);
-            r.z -= dot4(P, qh[s][2]);
-            r.w -= dot4(P, qh[s][3]);
-            E4[base + cl.c4[s]] = r;
-          }
+      for (int s = 0; s < S; ++s) {
+        float4 r = mp[rb][s];
+        r.x -= dot4(Pr, qh[s][0]);
+        r.y -= dot4(Pr, qh[s][1]);
+        r.z -= dot4(Pr, qh[s][2]);
+        r.w -= dot4(Pr, qh[s][3]);
+        bst4_nt(E, roff + coff[s], r);
       }
-      if (cl.wave == 0 && cl.lane == 0) P4[row] = P;
+      bst4(P, tid() == 0 ? static_cast<uint32_t>(r0 + rb) * 16u : kOut, Pr);
     }
   }
 }
@@ -550,15 +610,18 @@ __global__ __launch_bounds__(kBlock) void k_emat(KArgs a) {
 }
 
 // ---------------------------------------------------------------------------------------
-// Q-step: tile = (row chunk, column block of 4 x 64 x CPT columns).  Wave w owns the CPT
-// adjacent columns cb * q_cb + (w * 64 + lane) * CPT of every row of the chunk, so each row's
-// 4 KB (CPT = 4) segment is read by one workgroup.  The chunk's Ph rows are staged in LDS 64 at
-// a time (FUSED, r = 4: formed here as P W, and stored by the tiles of column block 0).  Per
-// row: F = M' = M + E written back (deferred E), partial Q += M'^T Ph over the lane's columns.
-// Each lane stores its partial sums for K_QFIN.
+// Q-step: tile = (row chunk of at most kQRows rows, column block of 4 x 64 x CPT columns).
+// Wave w owns the CPT adjacent columns cb * q_cb + (w * 64 + lane) * CPT of every row of the
+// chunk, so each row's 4 KB (CPT = 4) segment is read by one workgroup.  The chunk's Ph rows are
+// staged in LDS first (FUSED, r = 4: formed here as P W, and stored by the tiles of column
+// block 0).  Per row: F = M' = M + E written back (deferred E), partial Q += M'^T Ph over the
+// lane's columns.  Rows go in groups of U whose loads are issued before the previous group's
+// F stores, so stores never hold up the next loads.  Each lane stores its partial sums for
+// K_QFIN (lanes past m store zeros into the padded partial block).
 template <int RK, int CPT, bool FUSED>
 __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
-  constexpr int SUB = 64;  // rows staged in LDS at a time
+  constexpr int U = CPT == 4 ? 4 : 8;  // rows per group
+  using Vec = typename std::conditional<CPT == 4, float4, float>::type;
   const Tile t = a.tiles[blockIdx.x];
   if (t.kind == T_VEC) {
     vec_tile(a, t, true);
@@ -568,91 +631,102 @@ __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
   const int wave = tid() >> 6, lane = tid() & 63;
   const int64_t m = d.m;
   const int64_t r0 = static_cast<int64_t>(t.a) * d.q_rows;
-  const int64_t r1 = (r0 + d.q_rows < d.n) ? r0 + d.q_rows : d.n;
-  const int64_t col = static_cast<int64_t>(t.b) * d.q_cb + (wave * 64 + lane) * CPT;
-  const bool valid = col < m;
-  const bool ef = a.ef != 0;
-  const float* G = src_of(a, d.bucket) + d.grad_off;
-  float* E = a.e + d.e_off;
+  const int rows = static_cast<int>((r0 + d.q_rows < d.n) ? d.q_rows : d.n - r0);
+  const int64_t cb0 = static_cast<int64_t>(t.b) * d.q_cb;
+  const int lcol = (wave * 64 + lane) * CPT;  // column within the block
+  const int64_t bcols = (m - cb0) < d.q_cb ? (m - cb0) : d.q_cb;
+  const bool valid = lcol < bcols;
+  const uint32_t row_bytes = static_cast<uint32_t>(m) * 4u;
+  // extent from the block's first column of the chunk's first row to its last element
+  const uint32_t ext = static_cast<uint32_t>(rows - 1) * row_bytes + static_cast<uint32_t>(bcols) * 4u;
+  const int64_t first = r0 * m + cb0;
+  const Rsrc G = tile_rsrc(src_of(a, d.bucket) + d.grad_off + first, ext);
+  const Rsrc E = tile_rsrc(a.e + d.e_off + first, a.ef ? ext : 0u);
+  const uint32_t coff = valid ? static_cast<uint32_t>(lcol) * 4u : kOut;
+
   __shared__ double Wsh[16];
-  __shared__ __align__(16) float phs[SUB * RK];
+  __shared__ __align__(16) float phs[kQRows * RK];
+  Vec g[U], e[U];
+  auto load_group = [&](int rr, Vec* gg, Vec* ee) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t o = static_cast<uint32_t>(rr + u) * row_bytes + coff;
+      if constexpr (CPT == 4) {
+        gg[u] = bld4_nt(G, o);
+        ee[u] = bld4_nt(E, o);
+      } else {
+        gg[u] = bld1_nt(G, o);
+        ee[u] = bld1_nt(E, o);
+      }
+    }
+  };
+  load_group(0, g, e);
+
+  // the chunk's Ph rows; the rows after them are zero (groups may run past the chunk)
   if constexpr (FUSED) {
     if (tid() < 16) Wsh[tid()] = a.w[d.w_slot + tid()];
+    __syncthreads();
+    if (tid() < kQRows) {
+      float4 y = zero4();
+      if (tid() < rows) {
+        const int64_t row = r0 + tid();
+        y = apply_w4(*reinterpret_cast<const float4*>(a.fac + d.p_slot + row * 4), Wsh);
+        if (t.b == 0) *reinterpret_cast<float4*>(a.fac + d.ph_slot + row * 4) = y;
+      }
+      *reinterpret_cast<float4*>(&phs[tid() * 4]) = y;
+    }
+  } else {
+    for (int i = tid(); i < kQRows * RK; i += kBlock)
+      phs[i] = i < rows * RK ? a.fac[d.ph_slot + r0 * RK + i] : 0.f;
   }
+  __syncthreads();
+
   float acc[CPT][RK];
 #pragma unroll
   for (int c = 0; c < CPT; ++c)
 #pragma unroll
     for (int k = 0; k < RK; ++k) acc[c][k] = 0.f;
 
-  // M' of one row for this lane's columns, with F = M' written back.
-  auto load_mp = [&](int64_t row, float* mp) {
-    const int64_t i = row * m + col;
-    if (!valid) {
+  for (int rr = 0; rr < rows; rr += U) {
+    Vec gn[U], en[U];
+    load_group(rr + U, gn, en);
+    Vec f[U];
 #pragma unroll
-      for (int c = 0; c < CPT; ++c) mp[c] = 0.f;
-      return;
+    for (int u = 0; u < U; ++u) f[u] = g[u] + e[u];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t o = static_cast<uint32_t>(rr + u) * row_bytes + coff;
+      if constexpr (CPT == 4)
+        bst4_nt(E, o, f[u]);
+      else
+        bst1_nt(E, o, f[u]);
     }
-    if constexpr (CPT == 4) {
-      float4 g = ld_stream(reinterpret_cast<const float4*>(G + i));
-      if (ef) {
-        g = g + *reinterpret_cast<const float4*>(E + i);
-        *reinterpret_cast<float4*>(E + i) = g;
-      }
-      mp[0] = g.x;
-      mp[1] = g.y;
-      mp[2] = g.z;
-      mp[3] = g.w;
-    } else {
-      float g = G[i];
-      if (ef) {
-        g += E[i];
-        E[i] = g;
-      }
-      mp[0] = g;
-    }
-  };
-  auto accumulate = [&](int rr, const float* mp) {
-    const float* ph = &phs[rr * RK];
 #pragma unroll
-    for (int c = 0; c < CPT; ++c)
-#pragma unroll
-      for (int k = 0; k < RK; ++k) acc[c][k] = fmaf(mp[c], ph[k], acc[c][k]);
-  };
-
-  for (int64_t s0 = r0; s0 < r1; s0 += SUB) {
-    const int sn = static_cast<int>((r1 - s0) < SUB ? (r1 - s0) : SUB);
-    __syncthreads();  // Wsh ready / previous rows consumed
-    if (tid() < sn) {
-      const int64_t row = s0 + tid();
-      if constexpr (FUSED) {
-        const float4 y = apply_w4(*reinterpret_cast<const float4*>(a.fac + d.p_slot + row * 4), Wsh);
-        *reinterpret_cast<float4*>(&phs[tid() * 4]) = y;
-        if (t.b == 0) *reinterpret_cast<float4*>(a.fac + d.ph_slot + row * 4) = y;
+    for (int u = 0; u < U; ++u) {
+      const float* ph = &phs[(rr + u) * RK];  // rr + u < kQRows: kQRows is a multiple of U
+      float mp[CPT];
+      if constexpr (CPT == 4) {
+        mp[0] = f[u].x;
+        mp[1] = f[u].y;
+        mp[2] = f[u].z;
+        mp[3] = f[u].w;
       } else {
-#pragma unroll
-        for (int k = 0; k < RK; ++k) phs[tid() * RK + k] = a.fac[d.ph_slot + row * RK + k];
+        mp[0] = f[u];
       }
-    }
-    __syncthreads();
-    int rr = 0;
-    for (; rr + 4 <= sn; rr += 4) {
-      float mp[4][CPT];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) load_mp(s0 + rr + u, mp[u]);
+      for (int c = 0; c < CPT; ++c)
 #pragma unroll
-      for (int u = 0; u < 4; ++u) accumulate(rr + u, mp[u]);
+        for (int k = 0; k < RK; ++k) acc[c][k] = fmaf(mp[c], ph[k], acc[c][k]);
     }
-    for (; rr < sn; ++rr) {
-      float mp0[CPT];
-      load_mp(s0 + rr, mp0);
-      accumulate(rr, mp0);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      g[u] = gn[u];
+      e[u] = en[u];
     }
   }
-  if (!valid) return;
   const int64_t ncb = (m + d.q_cb - 1) / d.q_cb;
   const int64_t stride = ncb * d.q_cb * RK;  // one row chunk of partials
-  float* part = a.qpart + d.qpart + static_cast<int64_t>(t.a) * stride + (col - 0) * RK;
+  float* part = a.qpart + d.qpart + static_cast<int64_t>(t.a) * stride + (cb0 + lcol) * RK;
 #pragma unroll
   for (int c = 0; c < CPT; ++c)
 #pragma unroll
@@ -765,8 +839,9 @@ __global__ __launch_bounds__(kBlock) void k_recon(KArgs a) {
 }
 
 // Decompress, r = 4: each lane keeps the rank-4 rows of B for its columns in registers and
-// writes M_hat rows with streaming stores, RB rows at a time.  Factor tiles and vectors as in
-// k_recon.
+// writes M_hat rows, RB rows at a time, with tile-relative buffer stores (plain stores: they
+// measured faster than nontemporal ones for this write-only stream).  Factor tiles and
+// vectors as in k_recon.
 template <int S>
 __global__ __launch_bounds__(kBlock) void k_recon4(KArgs a) {
   constexpr int RB = Cols<S>::RB;
@@ -796,22 +871,26 @@ __global__ __launch_bounds__(kBlock) void k_recon4(KArgs a) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) b[s][c] = cl.ok[s] ? B4[4 * cl.c4[s] + c] : zero4();
   __syncthreads();
-  float4* O4 = reinterpret_cast<float4*>(dst_of(a, d.bucket) + d.grad_off);
-  const int row_end = t.a + t.b;
-  for (int r0 = t.a; r0 < row_end; r0 += RB) {
+  // the B rows are in registers before the store loop, so no wait for them lands inside it
+  __builtin_amdgcn_s_waitcnt(0);
+  const uint32_t row_bytes = static_cast<uint32_t>(d.m) * 4u;
+  const Rsrc O = tile_rsrc(dst_of(a, d.bucket) + d.grad_off + static_cast<int64_t>(t.a) * d.m,
+                           static_cast<uint32_t>(t.b) * row_bytes);
+  uint32_t coff[S];
+#pragma unroll
+  for (int s = 0; s < S; ++s) coff[s] = cl.ok[s] ? static_cast<uint32_t>(cl.c4[s]) * 16u : kOut;
+  // rows past the tile (last round) read unset LDS entries; their stores are dropped
+  for (int r0 = 0; r0 < t.b; r0 += RB) {
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      const int row = r0 + rb;
-      if (row >= row_end) continue;
-      const float4 ar = as[row - t.a];
-      const int64_t base = static_cast<int64_t>(row) * m4;
+      const float4 ar = as[(r0 + rb) & (kMaxTileRows - 1)];
+      const uint32_t roff = static_cast<uint32_t>(r0 + rb) * row_bytes;
 #pragma unroll
-      for (int s = 0; s < S; ++s)
-        if (cl.ok[s]) {
-          const float4 o = make_float4(dot4(ar, b[s][0]), dot4(ar, b[s][1]), dot4(ar, b[s][2]),
-                                       dot4(ar, b[s][3]));
-          st_stream(O4 + base + cl.c4[s], o);
-        }
+      for (int s = 0; s < S; ++s) {
+        const float4 o = make_float4(dot4(ar, b[s][0]), dot4(ar, b[s][1]), dot4(ar, b[s][2]),
+                                     dot4(ar, b[s][3]));
+        bst4(O, roff + coff[s], o);
+      }
     }
   }
 }

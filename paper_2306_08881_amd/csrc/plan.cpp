@@ -77,7 +77,9 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     t.numel = numel;
     if (nd >= 2) {
       const int64_t n = t.shape[0], m = numel / n;
-      if (m < (int64_t(1) << 31) && r < std::min(n, m)) {
+      if (r < std::min(n, m)) {
+        if (m > kMaxCols)
+          return "tensor " + std::to_string(i) + ": compressed matrices may have at most 2^24 columns";
         t.compressed = true;
         t.n = n;
         t.m = m;
@@ -151,7 +153,9 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       const bool vec4 = (t.m % 4 == 0) && (d.grad_off % 4 == 0);
       const int64_t cpt = (vec4 && r <= 8) ? 4 : 1;
       d.q_cb = static_cast<int32_t>(4 * 64 * cpt);
-      d.q_rows = 64;
+      // rows per chunk: 64, fewer when a chunk's byte extent would pass 2^30 (the kernels
+      // address a tile with 32-bit offsets from the tile's first element)
+      d.q_rows = static_cast<int32_t>(std::max<int64_t>(1, std::min<int64_t>(kQRows, (int64_t(1) << 30) / (t.m * 4))));
       d.q_chunks = static_cast<int32_t>(cdiv(t.n, d.q_rows));
       const int64_t ncb = cdiv(t.m, d.q_cb);
       d.qpart = qpart;
@@ -253,7 +257,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         const std::vector<int32_t> cls = of_class(S);
         if (cls.empty()) continue;
         l = sink.begin(K_PFUSED, S);
-        for (int32_t mi : cls) row_tiles(mi, rows_for(mi, 2 * kTileElems));
+        for (int32_t mi : cls) row_tiles(mi, rows_for(mi, kTileElems));
         if (!vec_done) vec_tiles(bk), vec_done = true;
         sink.end(l, L);
       }
@@ -332,7 +336,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         if (cls.empty()) continue;
         Launch l = sink.begin(K_RECON4, S);
         extra();
-        for (int32_t mi : cls) row_tiles(mi, rows_for(mi, 8 * kTileElems));
+        for (int32_t mi : cls) row_tiles(mi, rows_for(mi, kTileElems));
         sink.end(l, L);
       }
       for (int32_t vw : {4, 1}) {

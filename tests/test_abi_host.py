@@ -140,6 +140,9 @@ def test_init_errors(lib):
     assert _ctx(lib, [(4, 4)], 4, flags=1)[0] == L.ACP_E_UNSUPPORTED   # no reuse
     assert _ctx(lib, [(4, 4)], 4, flags=8 | 3)[0] == L.ACP_E_INVALID
     assert _ctx(lib, [(0, 4)], 4)[0] == L.ACP_E_INVALID
+    assert _ctx(lib, [(8, (1 << 24) + 1)], 4)[0] == L.ACP_E_INVALID  # compressed, > 2^24 columns
+    assert _ctx(lib, [(8, 1 << 12, (1 << 12) + 1), (3,)], 4)[0] == L.ACP_E_INVALID
+    assert _ctx(lib, [(4, (1 << 24) + 1)], 4)[0] == 0               # r >= n: passed through
     ctx = C.c_void_p()
     assert lib.acp_init(C.byref(ctx), 0, None, None, 4, 0, 1 << 20, 1, 3) == L.ACP_E_INVALID
     assert lib.acp_init(None, 1, None, None, 4, 0, 1 << 20, 1, 3) == L.ACP_E_INVALID

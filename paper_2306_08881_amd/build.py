@@ -29,7 +29,7 @@ HIP_FLAGS = ["-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}", f"-I{INCLUD
              "-Wno-unused-command-line-argument"]
 
 HOST_SOURCES = ["plan.cpp", "rng.cpp"]
-HIP_SOURCES = ["ctx.cpp", "kernels.hip"]
+HIP_SOURCES = ["ctx.cpp", "kernels.hip", "wide.hip"]
 
 
 def _run(cmd):

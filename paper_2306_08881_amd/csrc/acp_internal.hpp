@@ -4,11 +4,13 @@
 // 256-byte aligned:
 //   E arena   fp32, one slot per gradient-bucket element (vector slots unused); the E of a
 //             matrix sits at its bucket's E base + its offset in the gradient bucket.  After
-//             a Q-step it holds F = M + E_prev and E = F - P_hat Q_loc^T is implied (deferred).
-//   factors   fp32 per compressed matrix: P (n x r), Ph (n x r), Q (m x r), Qh (m x r),
-//             Ql (m x r), all row-major.  P / Q hold the aggregated factor of the last step
-//             that produced it, Ph / Qh the orthogonalised factors, Ql the local Q of the
-//             last Q-step.
+//             a Q-step it holds F = M' and E = F - P_hat Q_loc^T is implied (deferred).  After
+//             a P-step of rank >= 8 it holds X = M' and E = X - P_loc Q_hat^T is implied
+//             (P-deferred); after a P-step of rank <= 4 it holds E itself.
+//   factors   fp32 per compressed matrix: P (n x r), Ph (n x r), Pl (n x r), Q (m x r),
+//             Qh (m x r), Ql (m x r), all row-major.  P / Q hold the aggregated factor of
+//             the last step that produced it, Ph / Qh the orthogonalised factors, Pl / Ql the
+//             local factor of the last P- / Q-step.
 //   W         fp64 r x r per matrix: the upper-triangular map with orth(X) = X W for the
 //             factor that the next step orthogonalises.
 //   gpart     fp64 Gram partial sums, r x r per slice of factor rows (factors of more than one
@@ -29,14 +31,14 @@ constexpr double kTau = 1e-4;     // rank-deficiency threshold of orth()
 constexpr int kMaxTileRows = 256; // rows per tile of the rank-4 row kernels (factor rows in LDS)
 constexpr int kQfinWide = 64;     // Q-step chunks above which k_qfin uses 16 threads per entry
 constexpr int64_t kMaxCols = int64_t(1) << 24;  // columns of a compressed matrix, at most
-constexpr int kQRows = 64;        // rows per Q-step row chunk (at most; the chunk's Ph rows sit in LDS)
+constexpr int kQRows = 128;       // rows per Q-step row chunk (at most; the chunk's Ph rows sit in LDS)
 
 struct MatDesc {
   int64_t grad_off;   // offset of the matrix in its gradient bucket (floats)
   int64_t e_off;      // offset of its E slot in the E arena (floats)
   int64_t fac_off_p;  // offset in the P-step factor buffer
   int64_t fac_off_q;  // offset in the Q-step factor buffer
-  int64_t p_slot, q_slot, ph_slot, qh_slot, ql_slot;  // float offsets in the factor region
+  int64_t p_slot, q_slot, ph_slot, qh_slot, ql_slot, pl_slot;  // float offsets in the factor region
   int64_t w_slot;     // double offset in the W region
   int64_t gpart;      // double offset in the Gram-partial region
   int64_t qpart;      // float offset in the Q-partial region
@@ -78,7 +80,15 @@ enum KernelId : int32_t {
   K_CHOL,        // sum of a factor's Gram partials (more than one slice) -> W
   K_EMAT,        // materialise E into a bucket-shaped buffer
   K_VEC,         // pack raw vectors only
+  K_WPSTEP,      // P-step, ranks 8..32 (MFMA): X = M' written, P_loc = X Qh per 32-row tile
+  K_WQSTEP,      // Q-step, ranks 8..32 (MFMA): F = M' written, per-chunk partials of F^T Ph
+  K_WRECON,      // decompress, ranks 8..32 (MFMA): M_hat = A B^T / p; factor tiles; vectors / p
 };
+
+constexpr int32_t kWideRank = 8;   // ranks at or above this take the K_W* kernels
+constexpr int kWideQCols = 128;    // K_WQSTEP column block: 4 waves x 32 columns
+constexpr int kWideQRows = 256;    // K_WQSTEP rows per chunk (at most)
+constexpr int kWideRCols = 512;    // K_WRECON columns per tile: 4 waves x 4 blocks of 32
 
 // K_QSTEP variants: column slots per lane | kQFused when the kernel also orthogonalises P
 constexpr int32_t kQFused = 16;
@@ -113,6 +123,7 @@ struct KArgs {
   const VecDesc* vecs;
   const Tile* tiles;    // this launch's tiles
   uint64_t deferred;    // bit i: the E arena of bucket base + i holds F (E implied)
+  uint64_t deferred_p;  // bit i: the E arena of bucket base + i holds X (E implied)
   int32_t base;         // bucket of src[0] / dst[0]
   int32_t ntiles;
   int32_t variant;

@@ -26,7 +26,7 @@ struct acp_ctx {
   int device = -1;
   std::vector<int64_t> last_step;   // per bucket: last completed step
   std::vector<int64_t> pending;     // per bucket: compressed step awaiting decompress (0 = none)
-  std::vector<uint8_t> deferred;    // per bucket: E arena holds F
+  std::vector<uint8_t> deferred;    // per bucket: E form of the arena (kExplicit, kHoldsF, kHoldsX)
   mutable std::string err;
 
   // kernel timing (acp_profile_start / acp_profile_stop)
@@ -40,6 +40,22 @@ namespace {
 
 constexpr uint64_t kMagic = 0x3153504341ull;  // "ACPS1"
 constexpr int64_t kVersion = 1;
+
+// What the E arena of a bucket holds: E itself, F = M' after a Q-step (E = F - Ph Ql^T), or
+// X = M' after a P-step of rank >= 8 (E = X - Pl Qh^T).
+constexpr uint8_t kExplicit = 0, kHoldsF = 1, kHoldsX = 2;
+
+uint8_t form_after_compress(const acp_ctx* c, int64_t step) {
+  if (!c->plan.ef) return kExplicit;
+  if (!(step & 1)) return kHoldsF;
+  return c->plan.rank >= acp::kWideRank ? kHoldsX : kExplicit;
+}
+
+// the masks of KArgs for bucket slot i (bucket base + i)
+void set_form(acp::KArgs& a, int32_t i, uint8_t form) {
+  if (form == kHoldsF) a.deferred |= 1ull << i;
+  if (form == kHoldsX) a.deferred_p |= 1ull << i;
+}
 
 acp_status fail(const acp_ctx* c, acp_status s, const std::string& msg) {
   if (c) c->err = msg;
@@ -288,11 +304,11 @@ acp_status acp_compress(acp_ctx* c, int64_t step, int32_t b, const float* grad, 
   a.src[0] = grad;
   a.dst[0] = factor_buf;
   a.parity = static_cast<int32_t>(step & 1);
-  a.deferred = c->deferred[b];
+  set_form(a, 0, c->deferred[b]);
   const acp_status st = run(c, bk.compress[step & 1], a, static_cast<hipStream_t>(stream));
   if (st != ACP_OK) return st;
   c->pending[b] = step;
-  if (c->plan.ef) c->deferred[b] = (step & 1) ? 0 : 1;
+  c->deferred[b] = form_after_compress(c, step);
   return ACP_OK;
 }
 
@@ -322,7 +338,7 @@ acp_status acp_decompress(acp_ctx* c, int64_t step, int32_t b, const float* agg_
   a.src[0] = agg_factor;
   a.dst[0] = out;
   a.parity = static_cast<int32_t>(step & 1);
-  a.deferred = c->deferred[b];
+  set_form(a, 0, c->deferred[b]);
   const acp_status st = run(c, bk.decompress[step & 1], a, static_cast<hipStream_t>(stream));
   if (st != ACP_OK) return st;
   c->pending[b] = 0;
@@ -359,14 +375,14 @@ acp_status acp_compress_all(acp_ctx* c, int64_t step, const float* const* grads,
     for (int32_t i = 0; i < acp::kMaxGroup && a.base + i < nb; ++i) {
       a.src[i] = grads[a.base + i];
       a.dst[i] = factor_bufs[a.base + i];
-      if (c->deferred[a.base + i]) a.deferred |= 1ull << i;
+      set_form(a, i, c->deferred[a.base + i]);
     }
     const acp_status st = run(c, c->plan.group_compress[g][step & 1], a, static_cast<hipStream_t>(stream));
     if (st != ACP_OK) return st;
   }
   for (int32_t b = 0; b < nb; ++b) {
     c->pending[b] = step;
-    if (c->plan.ef) c->deferred[b] = (step & 1) ? 0 : 1;
+    c->deferred[b] = form_after_compress(c, step);
   }
   return ACP_OK;
 }
@@ -400,7 +416,7 @@ acp_status acp_decompress_all(acp_ctx* c, int64_t step, const float* const* agg_
     for (int32_t i = 0; i < acp::kMaxGroup && a.base + i < nb; ++i) {
       a.src[i] = agg_factors[a.base + i];
       a.dst[i] = outs[a.base + i];
-      if (c->deferred[a.base + i]) a.deferred |= 1ull << i;
+      set_form(a, i, c->deferred[a.base + i]);
     }
     const acp_status st = run(c, c->plan.group_decompress[g][step & 1], a, static_cast<hipStream_t>(stream));
     if (st != ACP_OK) return st;
@@ -424,7 +440,7 @@ acp_status acp_error(const acp_ctx* c, int32_t b, float* e_out, void* stream) {
   acp::KArgs a = base_args(c);
   a.base = b;
   a.dst[0] = e_out;
-  a.deferred = c->deferred[b];
+  set_form(a, 0, c->deferred[b]);
   return run(c, c->plan.buckets[b].emat, a, static_cast<hipStream_t>(stream));
 }
 
@@ -524,7 +540,7 @@ acp_status acp_set_state(acp_ctx* c, const void* host_buf, int64_t bytes) {
     int64_t rec[2];
     std::memcpy(rec, i, 16);
     i += 16;
-    if (rec[0] < 0 || rec[1] < 0 || rec[1] > 1) return fail(c, ACP_E_STATE, "corrupt checkpoint");
+    if (rec[0] < 0 || rec[1] < 0 || rec[1] > kHoldsX) return fail(c, ACP_E_STATE, "corrupt checkpoint");
     steps[b] = rec[0];
     defr[b] = static_cast<uint8_t>(rec[1]);
   }

@@ -1,4 +1,7 @@
-// gfx950 kernels of the ACP-SGD compressor (arXiv 2306.08881, Algorithms 1 and 2).
+// gfx950 kernels of the ACP-SGD compressor (arXiv 2306.08881, Algorithms 1 and 2): the
+// rank-4 register-resident streaming kernels, the general kernels for ranks 1 and 2 and for
+// matrices the rank-4 kernels do not take, the Q-step finish, the factor tiles and the launch
+// dispatch.  The MFMA kernels of ranks 8, 16 and 32 are in wide.hip.
 //
 // Every kernel runs 256-thread workgroups (4 waves of 64) over a table of tiles; one
 // workgroup per tile.  Workgroups never wait for each other: a reduction that spans
@@ -10,320 +13,13 @@
 // The error-feedback residual of a Q-step (E_t = M' - P_hat Q_t^T) is kept in deferred form:
 // the Q-step writes F = M' into the E arena and the next P-step subtracts the rank-r term
 // P_hat Q_loc^T while it streams F, so each step reads M and E once and writes E once.
-#include <hip/hip_runtime.h>
-
-#include <type_traits>
-
-#include "acp_internal.hpp"
+#include "device.hpp"
 
 namespace acp {
 
+hipError_t launch_wide(const Launch& l, int32_t rank, const KArgs& args, hipStream_t s);
+
 namespace {
-
-__device__ inline int tid() { return static_cast<int>(threadIdx.x); }
-
-__device__ inline float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-
-__device__ inline double wave_sum(double v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-
-__device__ inline float4 wave_sum(float4 v) {
-  v.x = wave_sum(v.x);
-  v.y = wave_sum(v.y);
-  v.z = wave_sum(v.z);
-  v.w = wave_sum(v.w);
-  return v;
-}
-
-__device__ inline float dot4(const float4& a, const float4& b) {
-  return a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
-}
-
-__device__ inline float4 operator+(const float4& a, const float4& b) {
-  return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
-}
-
-__device__ inline float4 scale4(const float4& a, float s) {
-  return make_float4(a.x * s, a.y * s, a.z * s, a.w * s);
-}
-
-__device__ inline float4 fma4(float s, const float4& v, const float4& acc) {
-  return make_float4(fmaf(s, v.x, acc.x), fmaf(s, v.y, acc.y), fmaf(s, v.z, acc.z),
-                     fmaf(s, v.w, acc.w));
-}
-
-__device__ inline float4 zero4() { return make_float4(0.f, 0.f, 0.f, 0.f); }
-
-// Streaming accesses: data read or written exactly once per step.
-typedef float v4f __attribute__((ext_vector_type(4)));
-__device__ inline float4 ld_stream(const float4* p) {
-  const v4f v = __builtin_nontemporal_load(reinterpret_cast<const v4f*>(p));
-  return make_float4(v.x, v.y, v.z, v.w);
-}
-__device__ inline void st_stream(float4* p, const float4& v) {
-  const v4f w = {v.x, v.y, v.z, v.w};
-  __builtin_nontemporal_store(w, reinterpret_cast<v4f*>(p));
-}
-
-// Tile-relative buffer accesses.  A buffer resource spans one tile from its first element;
-// a load past num_records returns zero and a store past it is dropped, so lanes and rows that
-// fall outside the tile need no branch: they take the offset kOut (or any offset past the
-// extent).  Branch-free loads and stores let the compiler count outstanding memory operations
-// exactly, so stores stay in flight while the next rows' loads are waited for.  Every extent
-// and in-tile offset is below 2^30, so kOut plus an offset does not wrap.
-typedef __amdgpu_buffer_rsrc_t Rsrc;
-constexpr uint32_t kOut = 0x80000000u;
-constexpr int kAuxNT = 2;  // cache policy: nontemporal (streamed once)
-
-__device__ inline Rsrc tile_rsrc(const float* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), 0, static_cast<int>(bytes),
-                                           0x00020000);
-}
-// The buffer builtins move raw 32-bit words (unsigned int); values cross them bit-cast.
-typedef unsigned int v4u __attribute__((ext_vector_type(4)));
-__device__ inline float4 bld4_nt(Rsrc r, uint32_t off) {
-  const v4f v = __builtin_bit_cast(v4f, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kAuxNT));
-  return make_float4(v.x, v.y, v.z, v.w);
-}
-__device__ inline float bld1_nt(Rsrc r, uint32_t off) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kAuxNT));
-}
-__device__ inline void bst4_nt(Rsrc r, uint32_t off, const float4& v) {
-  const v4f w = {v.x, v.y, v.z, v.w};
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, w), r, off, 0, kAuxNT);
-}
-__device__ inline void bst4(Rsrc r, uint32_t off, const float4& v) {
-  const v4f w = {v.x, v.y, v.z, v.w};
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, w), r, off, 0, 0);
-}
-__device__ inline void bst1_nt(Rsrc r, uint32_t off, float v) {
-  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned int, v), r, off, 0, kAuxNT);
-}
-
-// Sum over the 64 lanes with DPP: quad butterflies, half-row and row mirrors give every lane
-// its 16-lane row sum; the four row sums are then read out and added in row order.  Every lane
-// gets the same bits.
-template <int CTRL>
-__device__ inline float dpp(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
-                                                               0xF, 0xF, false));
-}
-__device__ inline float wave_sum_dpp(float v) {
-  v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]
-  v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]
-  v += dpp<0x141>(v);  // row_half_mirror
-  v += dpp<0x140>(v);  // row_mirror
-  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
-  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
-  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
-  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
-  return ((r0 + r1) + r2) + r3;
-}
-__device__ inline float4 wave_sum_dpp(float4 v) {
-  return make_float4(wave_sum_dpp(v.x), wave_sum_dpp(v.y), wave_sum_dpp(v.z), wave_sum_dpp(v.w));
-}
-
-// x W for one row of a rank-4 factor (W upper triangular, fp64, row-major), rounded to fp32.
-__device__ inline float4 apply_w4(const float4& x, const double* W) {
-  const double x0 = x.x, x1 = x.y, x2 = x.z, x3 = x.w;
-  const double y0 = x0 * W[0];
-  const double y1 = fma(x0, W[1], x1 * W[5]);
-  const double y2 = fma(x0, W[2], fma(x1, W[6], x2 * W[10]));
-  const double y3 = fma(x0, W[3], fma(x1, W[7], fma(x2, W[11], x3 * W[15])));
-  return make_float4(static_cast<float>(y0), static_cast<float>(y1), static_cast<float>(y2),
-                     static_cast<float>(y3));
-}
-
-// Buffers of a bucket in this launch's group.
-__device__ inline const float* src_of(const KArgs& a, int32_t b) { return a.src[b - a.base]; }
-__device__ inline float* dst_of(const KArgs& a, int32_t b) { return a.dst[b - a.base]; }
-__device__ inline bool deferred_of(const KArgs& a, int32_t b) {
-  return ((a.deferred >> (b - a.base)) & 1ull) != 0;
-}
-
-// Raw vectors: pack the gradient into the factor buffer (compress) or unpack the aggregated
-// sum / p into the output bucket (decompress).
-__device__ void vec_tile(const KArgs& a, const Tile& t, bool compress) {
-  const VecDesc v = a.vecs[t.idx];
-  const int64_t foff = a.parity ? v.fac_off_p : v.fac_off_q;
-  const float* src = src_of(a, v.bucket);
-  float* dst = dst_of(a, v.bucket);
-  for (int i = tid(); i < t.b; i += kBlock) {
-    const int64_t k = static_cast<int64_t>(t.a) + i;
-    if (compress)
-      dst[foff + k] = src[v.grad_off + k];
-    else
-      dst[v.grad_off + k] = src[foff + k] * a.inv_p;
-  }
-}
-
-// ---------------------------------------------------------------------------------------
-// Orthogonalisation, Gram/Cholesky form.  For a factor X (k x r) the Gram-Schmidt factor is
-// orth(X) = X W with W = R^-1 and G = X^T X = R^T R (R upper triangular, positive diagonal):
-// the same columns as Gram-Schmidt in exact arithmetic.  G is accumulated in fp64 from fp32
-// products (exact) and factored in fp64.  A column j is dropped (its column of W is zero) when
-// G_jj = 0 or its residual d_j = G_jj - sum_{i<j} R_ij^2 is at most tau^2 G_jj, i.e. when the
-// residual norm is at most tau times the column norm.
-
-// Gram of rows [r0, r1) of X (row-major, RK columns) into shared G (RK x RK), by the whole
-// workgroup, in a fixed order; the rows are also copied to `copy` when it is set.
-template <int RK>
-__device__ void gram_rows(const float* X, int64_t r0, int64_t r1, double* G, float* copy) {
-  if constexpr (RK <= 8) {
-    constexpr int NT = RK * (RK + 1) / 2;
-    constexpr int PER = 8;  // rows per thread per pass, loaded together
-    double g[NT];
-#pragma unroll
-    for (int e = 0; e < NT; ++e) g[e] = 0.0;
-    for (int64_t base = r0; base < r1; base += int64_t(kBlock) * PER) {
-      float x[PER][RK];
-#pragma unroll
-      for (int u = 0; u < PER; ++u) {
-        const int64_t row = base + u * kBlock + tid();
-#pragma unroll
-        for (int k = 0; k < RK; ++k) x[u][k] = row < r1 ? X[row * RK + k] : 0.f;
-      }
-      if (copy) {
-#pragma unroll
-        for (int u = 0; u < PER; ++u) {
-          const int64_t row = base + u * kBlock + tid();
-          if (row < r1)
-#pragma unroll
-            for (int k = 0; k < RK; ++k) copy[row * RK + k] = x[u][k];
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < PER; ++u) {
-        int e = 0;
-#pragma unroll
-        for (int i = 0; i < RK; ++i)
-#pragma unroll
-          for (int j = i; j < RK; ++j, ++e)
-            g[e] = fma(static_cast<double>(x[u][i]), static_cast<double>(x[u][j]), g[e]);
-      }
-    }
-    __shared__ double red[4][NT];
-#pragma unroll
-    for (int e = 0; e < NT; ++e) g[e] = wave_sum(g[e]);
-    if ((tid() & 63) == 0)
-#pragma unroll
-      for (int e = 0; e < NT; ++e) red[tid() >> 6][e] = g[e];
-    __syncthreads();
-    if (tid() < NT) {
-      const int e = tid();
-      int i = 0, rem = e;
-      while (rem >= RK - i) rem -= RK - i, ++i;
-      const int j = i + rem;
-      const double s = ((red[0][e] + red[1][e]) + red[2][e]) + red[3][e];
-      G[i * RK + j] = s;
-      G[j * RK + i] = s;
-    }
-    __syncthreads();
-  } else {
-    constexpr int CH = 64;
-    constexpr int NQ = (RK * RK + kBlock - 1) / kBlock;
-    __shared__ float xs[CH * RK];
-    if (copy)
-      for (int64_t e = r0 * RK + tid(); e < r1 * RK; e += kBlock) copy[e] = X[e];
-    double acc[NQ];
-#pragma unroll
-    for (int q = 0; q < NQ; ++q) acc[q] = 0.0;
-    for (int64_t c0 = r0; c0 < r1; c0 += CH) {
-      const int64_t cn = (r1 - c0) < CH ? (r1 - c0) : CH;
-      for (int e = tid(); e < cn * RK; e += kBlock) xs[e] = X[c0 * RK + e];
-      __syncthreads();
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        const int e = tid() + q * kBlock;
-        if (e < RK * RK) {
-          const int i = e / RK, j = e % RK;
-          double s = acc[q];
-          for (int rr = 0; rr < cn; ++rr)
-            s = fma(static_cast<double>(xs[rr * RK + i]), static_cast<double>(xs[rr * RK + j]), s);
-          acc[q] = s;
-        }
-      }
-      __syncthreads();
-    }
-#pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      const int e = tid() + q * kBlock;
-      if (e < RK * RK) G[e] = acc[q];
-    }
-    __syncthreads();
-  }
-}
-
-// Cholesky G = R^T R and W = R^-1 (dropped columns zero), written to w_out.  G in shared.
-template <int RK>
-__device__ void cholesky_w(const double* G, double* w_out) {
-  __shared__ double R[RK * RK];
-  __shared__ int drop[RK];
-  for (int e = tid(); e < RK * RK; e += kBlock) R[e] = 0.0;
-  __syncthreads();
-  for (int j = 0; j < RK; ++j) {
-    if (tid() == 0) {
-      const double gjj = G[j * RK + j];
-      double dj = gjj;
-      for (int i = 0; i < j; ++i) dj -= R[i * RK + j] * R[i * RK + j];
-      const bool keep = gjj > 0.0 && dj > kTau * kTau * gjj;
-      drop[j] = keep ? 0 : 1;
-      R[j * RK + j] = keep ? sqrt(dj) : 0.0;
-    }
-    __syncthreads();
-    const int k = tid();
-    if (k > j && k < RK && drop[j] == 0) {
-      double s = G[j * RK + k];
-      for (int i = 0; i < j; ++i) s -= R[i * RK + j] * R[i * RK + k];
-      R[j * RK + k] = s / R[j * RK + j];
-    }
-    __syncthreads();
-  }
-  const int arow = tid();
-  if (arow < RK) {
-    double wr[RK];
-#pragma unroll
-    for (int j = 0; j < RK; ++j) {
-      double v = 0.0;
-      if (drop[j] == 0 && arow <= j) {
-        v = (arow == j) ? 1.0 : 0.0;
-#pragma unroll
-        for (int i = 0; i < j; ++i)
-          if (i >= arow) v -= R[i * RK + j] * wr[i];
-        v /= R[j * RK + j];
-      }
-      wr[j] = v;
-    }
-#pragma unroll
-    for (int j = 0; j < RK; ++j) w_out[arow * RK + j] = wr[j];
-  }
-}
-
-// Factor tile: slice t.a of the t.b slices of fact_rows rows of the factor `src` (rows x RK).
-// When `dst` is set the slice is also copied there (the aggregated factor becomes the next
-// step's reused factor).  A factor of one slice finishes W here; otherwise the slice's Gram
-// is stored as a partial and K_CHOL adds the partials and finishes W.
-template <int RK>
-__device__ void fact_tile(const KArgs& a, const Tile& t, const float* src, float* dst, int64_t rows) {
-  const MatDesc d = a.mats[t.idx];
-  __shared__ double G[RK * RK];
-  const int64_t r0 = static_cast<int64_t>(t.a) * d.fact_rows;
-  const int64_t r1 = r0 + d.fact_rows < rows ? r0 + d.fact_rows : rows;
-  gram_rows<RK>(src, r0, r1, G, dst);
-  if (t.b == 1) {
-    cholesky_w<RK>(G, a.w + d.w_slot);
-  } else {
-    double* part = a.gpart + d.gpart + static_cast<int64_t>(t.a) * RK * RK;
-    for (int e = tid(); e < RK * RK; e += kBlock) part[e] = G[e];
-  }
-}
 
 template <int RK>
 __global__ __launch_bounds__(kBlock) void k_fact(KArgs a) {
@@ -379,10 +75,10 @@ __global__ __launch_bounds__(kBlock) void k_apply(KArgs a) {
 // a row of m4 = m / 4 float4 groups into four segments of 64 S groups; lane `lane` of wave w
 // owns groups w * 64 S + s * 64 + lane, s < S, for every row of the tile, so the factor rows
 // of those columns are loaded once per workgroup and kept in registers.  The waves work on the
-// same RB rows at a time (4 for S = 1, 2 for S = 2..4, 1 for S = 5).
+// same RB rows at a time (8 for S = 1, 2 for S = 2..4, 1 for S = 5).
 template <int S>
 struct Cols {
-  static constexpr int RB = S == 1 ? 4 : (S <= 4 ? 2 : 1);
+  static constexpr int RB = S == 1 ? 8 : (S <= 4 ? 2 : 1);
   int wave, lane;
   int c4[S];
   bool ok[S];
@@ -586,25 +282,25 @@ __global__ __launch_bounds__(kBlock) void k_eupd(KArgs a) {
   }
 }
 
-// Write E (explicit, or F - Ph Q_loc^T when deferred) of a tile of rows into a bucket-shaped
-// output.
+// Write E of a tile of rows into a bucket-shaped output: the arena itself, F - Ph Q_loc^T
+// (after a Q-step) or X - P_loc Qh^T (after a P-step of rank >= 8).
 template <int RK>
 __global__ __launch_bounds__(kBlock) void k_emat(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
   const int64_t m = d.m;
-  const bool deferred = deferred_of(a, d.bucket);
-  const float* Ql = a.fac + d.ql_slot;
-  const float* Ph = a.fac + d.ph_slot;
+  const bool fform = deferred_of(a, d.bucket), xform = deferred_p_of(a, d.bucket);
+  const float* L = a.fac + (xform ? d.qh_slot : d.ql_slot);  // column factor of the term
+  const float* R = a.fac + (xform ? d.pl_slot : d.ph_slot);  // row factor of the term
   float* out = dst_of(a, d.bucket);
   const int64_t total = static_cast<int64_t>(t.b) * m;
   for (int64_t e = tid(); e < total; e += kBlock) {
     const int64_t row = t.a + e / m, j = e % m;
     const int64_t idx = row * m + j;
     float v = a.e[d.e_off + idx];
-    if (deferred)
+    if (fform || xform)
 #pragma unroll
-      for (int k = 0; k < RK; ++k) v -= Ph[row * RK + k] * Ql[j * RK + k];
+      for (int k = 0; k < RK; ++k) v -= R[row * RK + k] * L[j * RK + k];
     out[d.grad_off + idx] = v;
   }
 }
@@ -970,6 +666,8 @@ hipError_t launch_rank(const Launch& l, const KArgs& args, hipStream_t s) {
 
 hipError_t launch(const Launch& l, int32_t rank, const KArgs& args, hipStream_t s) {
   if (l.ntiles <= 0) return hipSuccess;
+  if (l.kernel == K_WPSTEP || l.kernel == K_WQSTEP || l.kernel == K_WRECON)
+    return launch_wide(l, rank, args, s);
   switch (rank) {
     case 1: return launch_rank<1>(l, args, s);
     case 2: return launch_rank<2>(l, args, s);

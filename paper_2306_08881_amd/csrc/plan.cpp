@@ -115,6 +115,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   }
 
   // ---- per-tensor device descriptors and state regions
+  const bool wide = r >= kWideRank;
   int64_t e_floats = 0, fac_floats = 0, gpart = 0, qpart = 0;
   for (int32_t b = 0; b < static_cast<int32_t>(plan.buckets.size()); ++b) {
     BucketPlan& bk = plan.buckets[b];
@@ -146,16 +147,18 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       const int64_t np = align_up(t.n * r, kSlotAlign), mp = align_up(t.m * r, kSlotAlign);
       d.p_slot = fac_floats;
       d.ph_slot = fac_floats + np;
-      d.q_slot = fac_floats + 2 * np;
-      d.qh_slot = fac_floats + 2 * np + mp;
-      d.ql_slot = fac_floats + 2 * np + 2 * mp;
-      fac_floats += 2 * np + 3 * mp;
+      d.pl_slot = fac_floats + 2 * np;
+      d.q_slot = fac_floats + 3 * np;
+      d.qh_slot = d.q_slot + mp;
+      d.ql_slot = d.q_slot + 2 * mp;
+      fac_floats += 3 * np + 3 * mp;
       const bool vec4 = (t.m % 4 == 0) && (d.grad_off % 4 == 0);
       const int64_t cpt = (vec4 && r <= 8) ? 4 : 1;
-      d.q_cb = static_cast<int32_t>(4 * 64 * cpt);
-      // rows per chunk: 64, fewer when a chunk's byte extent would pass 2^30 (the kernels
-      // address a tile with 32-bit offsets from the tile's first element)
-      d.q_rows = static_cast<int32_t>(std::max<int64_t>(1, std::min<int64_t>(kQRows, (int64_t(1) << 30) / (t.m * 4))));
+      d.q_cb = wide ? kWideQCols : static_cast<int32_t>(4 * 64 * cpt);
+      // rows per chunk: kQRows (kWideQRows), fewer when a chunk's byte extent would pass 2^30
+      // (the kernels address a tile with 32-bit offsets from the tile's first element)
+      d.q_rows = static_cast<int32_t>(std::max<int64_t>(
+          1, std::min<int64_t>(wide ? kWideQRows : kQRows, (int64_t(1) << 30) / (t.m * 4))));
       d.q_chunks = static_cast<int32_t>(cdiv(t.n, d.q_rows));
       const int64_t ncb = cdiv(t.m, d.q_cb);
       d.qpart = qpart;
@@ -225,12 +228,105 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   // rows per tile of the rank-4 kernels: a multiple of the rows handled per round
   auto rows_for = [&](int32_t mi, int64_t elems) {
     const MatDesc& d = plan.mats[mi];
-    const int64_t rb = d.scls == 1 ? 4 : (d.scls <= 4 ? 2 : 1);
+    const int64_t rb = d.scls == 1 ? 8 : (d.scls <= 4 ? 2 : 1);
     const int64_t rows = rb * std::max<int64_t>(1, elems / (int64_t(d.m) * rb));
     return std::min<int64_t>(rows, kMaxTileRows);
   };
 
+  // Q-step finish tiles: entry blocks of each matrix's column blocks
+  auto qfin_launch = [&](const BucketPlan& bk, std::vector<Launch>& L) {
+    Launch l = sink.begin(K_QFIN, 0);
+    for (int32_t mi : bk.mats) {
+      const MatDesc& d = plan.mats[mi];
+      const int32_t ncb = static_cast<int32_t>(cdiv(d.m, d.q_cb));
+      const int64_t ne = d.q_chunks > kQfinWide ? 16 : 64;
+      const int32_t nblk = static_cast<int32_t>(cdiv(int64_t(d.q_cb) * r, ne));
+      for (int32_t cb = 0; cb < ncb; ++cb)
+        for (int32_t eb = 0; eb < nblk; ++eb) plan.tiles.push_back(Tile{T_QTILE, mi, eb, cb});
+    }
+    sink.end(l, L);
+  };
+  auto emat_launch = [&](BucketPlan& bk) {
+    Launch l = sink.begin(K_EMAT, 1);
+    for (int32_t mi : bk.mats) row_tiles(mi, std::max<int64_t>(1, kTileElems / plan.mats[mi].m));
+    sink.end(l, bk.emat);
+  };
+  // ranks 8..32: every matrix of the bucket takes the MFMA kernels
+  auto wide_lists = [&](BucketPlan& bk) {
+    // -- P-step (odd t): Qh = Q W, then 32-row tiles (16-byte rows first, then the others)
+    {
+      std::vector<Launch>& L = bk.compress[1];
+      bool vec_done = bk.vecs.empty();
+      Launch l = sink.begin(K_APPLY, 1);
+      apply_tiles(bk.mats, true);
+      sink.end(l, L);
+      for (int32_t vw : {4, 1}) {
+        l = sink.begin(K_WPSTEP, vw);
+        bool any = false;
+        for (int32_t mi : bk.mats)
+          if (is_vec4(mi) == (vw == 4)) {
+            row_tiles(mi, 32);
+            any = true;
+          }
+        if (any && !vec_done) vec_tiles(bk), vec_done = true;
+        sink.end(l, L);
+      }
+      if (!vec_done) {
+        l = sink.begin(K_VEC, 1);
+        vec_tiles(bk);
+        sink.end(l, L);
+      }
+    }
+    // -- Q-step (even t): Ph = P W, (row chunk, 128-column block) tiles, finish
+    {
+      std::vector<Launch>& L = bk.compress[0];
+      bool vec_done = bk.vecs.empty();
+      Launch l = sink.begin(K_APPLY, 0);
+      apply_tiles(bk.mats, false);
+      sink.end(l, L);
+      l = sink.begin(K_WQSTEP, 0);
+      for (int32_t mi : bk.mats) {
+        const MatDesc& d = plan.mats[mi];
+        const int32_t ncb = static_cast<int32_t>(cdiv(d.m, d.q_cb));
+        for (int32_t c = 0; c < d.q_chunks; ++c)
+          for (int32_t cb = 0; cb < ncb; ++cb) plan.tiles.push_back(Tile{T_QTILE, mi, c, cb});
+      }
+      if (!bk.mats.empty() && !vec_done) vec_tiles(bk), vec_done = true;
+      sink.end(l, L);
+      qfin_launch(bk, L);
+      if (!vec_done) {
+        l = sink.begin(K_VEC, 0);
+        vec_tiles(bk);
+        sink.end(l, L);
+      }
+    }
+    // -- decompress: factor tiles, vectors, then (32-row block, 512-column group) tiles
+    for (int32_t par = 0; par < 2; ++par) {
+      std::vector<Launch>& L = bk.decompress[par];
+      const bool q = par == 0;
+      Launch l = sink.begin(K_WRECON, 0);
+      for (int32_t mi : bk.mats) fact_tiles(mi, q);
+      vec_tiles(bk);
+      for (int32_t mi : bk.mats) {
+        const MatDesc& d = plan.mats[mi];
+        const int32_t nrb = static_cast<int32_t>(cdiv(d.n, 32));
+        const int32_t ncg = static_cast<int32_t>(cdiv(d.m, kWideRCols));
+        for (int32_t rb = 0; rb < nrb; ++rb)
+          for (int32_t cg = 0; cg < ncg; ++cg) plan.tiles.push_back(Tile{T_QTILE, mi, rb, cg});
+      }
+      sink.end(l, L);
+      l = sink.begin(K_CHOL, 0);
+      for (int32_t mi : bk.mats) chol_tiles(mi, q);
+      sink.end(l, L);
+    }
+    emat_launch(bk);
+  };
+
   for (BucketPlan& bk : plan.buckets) {
+    if (wide) {
+      wide_lists(bk);
+      continue;
+    }
     std::vector<int32_t> fast, generic;
     for (int32_t mi : bk.mats) {
       if (is_fast(mi)) {
@@ -257,7 +353,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         const std::vector<int32_t> cls = of_class(S);
         if (cls.empty()) continue;
         l = sink.begin(K_PFUSED, S);
-        for (int32_t mi : cls) row_tiles(mi, rows_for(mi, kTileElems));
+        for (int32_t mi : cls) row_tiles(mi, rows_for(mi, 2 * kTileElems));
         if (!vec_done) vec_tiles(bk), vec_done = true;
         sink.end(l, L);
       }
@@ -304,16 +400,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         if (any && !vec_done) vec_tiles(bk), vec_done = true;
         sink.end(l, L);
       }
-      l = sink.begin(K_QFIN, 0);
-      for (int32_t mi : bk.mats) {
-        const MatDesc& d = plan.mats[mi];
-        const int32_t ncb = static_cast<int32_t>(cdiv(d.m, d.q_cb));
-        const int64_t ne = d.q_chunks > kQfinWide ? 16 : 64;
-        const int32_t nblk = static_cast<int32_t>(cdiv(int64_t(d.q_cb) * r, ne));
-        for (int32_t cb = 0; cb < ncb; ++cb)
-          for (int32_t eb = 0; eb < nblk; ++eb) plan.tiles.push_back(Tile{T_QTILE, mi, eb, cb});
-      }
-      sink.end(l, L);
+      qfin_launch(bk, L);
       if (!vec_done) {
         l = sink.begin(K_VEC, 0);
         vec_tiles(bk);
@@ -356,11 +443,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         sink.end(l, L);
       }
     }
-    {
-      Launch l = sink.begin(K_EMAT, 1);
-      for (int32_t mi : bk.mats) row_tiles(mi, std::max<int64_t>(1, kTileElems / plan.mats[mi].m));
-      sink.end(l, bk.emat);
-    }
+    emat_launch(bk);
   }
   {
     Launch l = sink.begin(K_FACT, 1);
@@ -403,6 +486,23 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
           return std::min<double>(d.fact_rows, rows - double(t.a) * d.fact_rows) * rr * 8.0;
         }
         return t.b * m * 4.0 + t.b * rr * 4.0 + (t.a == 0 ? m * rr * 4.0 : 0.0);
+      case K_WPSTEP:
+        return t.b * m * eb + t.b * rr * 8.0 + (t.a == 0 ? m * rr * 8.0 : 0.0);
+      case K_WQSTEP: {
+        const double r0 = double(t.a) * d.q_rows;
+        const double rows = std::min<double>(d.q_rows, n - r0);
+        const double cols = std::min<double>(d.q_cb, m - double(t.b) * d.q_cb);
+        return rows * cols * eb + (t.b == 0 ? rows * rr * 8.0 : 0.0);
+      }
+      case K_WRECON: {
+        if (t.kind == T_FACT) {
+          const double rows = odd ? n : m;
+          return std::min<double>(d.fact_rows, rows - double(t.a) * d.fact_rows) * rr * 8.0;
+        }
+        const double rows = std::min<double>(32.0, n - 32.0 * t.a);
+        const double cols = std::min<double>(kWideRCols, m - double(kWideRCols) * t.b);
+        return rows * cols * 4.0 + (t.b == 0 ? rows * rr * 4.0 : 0.0) + (t.a == 0 ? cols * rr * 4.0 : 0.0);
+      }
       case K_APPLY:
         return t.b * rr * 8.0;
       case K_FACT:
@@ -415,10 +515,10 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   };
   auto family_of = [](int32_t kernel, bool odd) -> int32_t {
     switch (kernel) {
-      case K_PFUSED: case K_PROW: case K_EUPD: return 1;   // ACP_KERNEL_P_STEP
-      case K_QSTEP: return 2;                               // ACP_KERNEL_Q_STEP
-      case K_QFIN: return 3;                                // ACP_KERNEL_Q_FINISH
-      case K_RECON: case K_RECON4: return 4;                // ACP_KERNEL_RECONSTRUCT
+      case K_PFUSED: case K_PROW: case K_EUPD: case K_WPSTEP: return 1;  // ACP_KERNEL_P_STEP
+      case K_QSTEP: case K_WQSTEP: return 2;                               // ACP_KERNEL_Q_STEP
+      case K_QFIN: return 3;                                               // ACP_KERNEL_Q_FINISH
+      case K_RECON: case K_RECON4: case K_WRECON: return 4;                // ACP_KERNEL_RECONSTRUCT
       case K_APPLY: case K_FACT: case K_CHOL: return 5;     // ACP_KERNEL_ORTH
       case K_VEC: return odd ? 1 : 2;
       default: return 0;
@@ -448,6 +548,9 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       case K_PFUSED: return 1 + l.variant;          // 2..6
       case K_PROW: return 10;
       case K_EUPD: return 11;
+      case K_WPSTEP: return l.variant == 4 ? 12 : 13;
+      case K_WQSTEP: return 22;
+      case K_WRECON: return 40;
       case K_QSTEP: return (l.variant & kQFused) ? 20 : (l.variant == 4 ? 21 : 22);
       case K_QFIN: return 23;
       case K_RECON4: return 30 + l.variant;         // 31..35

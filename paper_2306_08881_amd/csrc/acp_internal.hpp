@@ -82,13 +82,15 @@ enum KernelId : int32_t {
   K_VEC,         // pack raw vectors only
   K_WPSTEP,      // P-step, ranks 8..32 (MFMA): X = M' written, P_loc = X Qh per 32-row tile
   K_WQSTEP,      // Q-step, ranks 8..32 (MFMA): F = M' written, per-chunk partials of F^T Ph
-  K_WRECON,      // decompress, ranks 8..32 (MFMA): M_hat = A B^T / p; factor tiles; vectors / p
+  K_WRECON,      // decompress, ranks 8..32 (MFMA): M_hat = A B^T / p
+  K_WFACT,       // decompress, ranks 8..32: factor tiles and vectors / p
 };
 
 constexpr int32_t kWideRank = 8;   // ranks at or above this take the K_W* kernels
-constexpr int kWideQCols = 128;    // K_WQSTEP column block: 4 waves x 32 columns
-constexpr int kWideQRows = 256;    // K_WQSTEP rows per chunk (at most)
-constexpr int kWideRCols = 512;    // K_WRECON columns per tile: 4 waves x 4 blocks of 32
+constexpr int kWideBlock = 64;     // threads per workgroup of K_WPSTEP, K_WQSTEP, K_WRECON: one wave
+constexpr int kWideQCols = 32;     // K_WQSTEP column block (one MFMA block)
+constexpr int kWideQRows = 512;    // K_WQSTEP rows per chunk (at most)
+constexpr int kWideRCols = 512;    // K_WRECON columns per tile: 16 blocks of 32
 
 // K_QSTEP variants: column slots per lane | kQFused when the kernel also orthogonalises P
 constexpr int32_t kQFused = 16;

@@ -95,6 +95,10 @@ __device__ inline void bst4(Rsrc r, uint32_t off, const float4& v) {
   const v4f w = {v.x, v.y, v.z, v.w};
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, w), r, off, 0, 0);
 }
+__device__ inline float4 bld4(Rsrc r, uint32_t off) {
+  const v4f v = __builtin_bit_cast(v4f, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
 __device__ inline float bld1(Rsrc r, uint32_t off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }

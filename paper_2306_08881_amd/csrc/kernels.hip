@@ -666,7 +666,7 @@ hipError_t launch_rank(const Launch& l, const KArgs& args, hipStream_t s) {
 
 hipError_t launch(const Launch& l, int32_t rank, const KArgs& args, hipStream_t s) {
   if (l.ntiles <= 0) return hipSuccess;
-  if (l.kernel == K_WPSTEP || l.kernel == K_WQSTEP || l.kernel == K_WRECON)
+  if (l.kernel == K_WPSTEP || l.kernel == K_WQSTEP || l.kernel == K_WRECON || l.kernel == K_WFACT)
     return launch_wide(l, rank, args, s);
   switch (rank) {
     case 1: return launch_rank<1>(l, args, s);

@@ -253,34 +253,27 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   };
   // ranks 8..32: every matrix of the bucket takes the MFMA kernels
   auto wide_lists = [&](BucketPlan& bk) {
+    // The MFMA kernels run one wave per workgroup over matrix tiles only; raw vectors and
+    // factor tiles (which need whole workgroups) go to launches of their own.
     // -- P-step (odd t): Qh = Q W, then 32-row tiles (16-byte rows first, then the others)
     {
       std::vector<Launch>& L = bk.compress[1];
-      bool vec_done = bk.vecs.empty();
       Launch l = sink.begin(K_APPLY, 1);
       apply_tiles(bk.mats, true);
       sink.end(l, L);
       for (int32_t vw : {4, 1}) {
         l = sink.begin(K_WPSTEP, vw);
-        bool any = false;
         for (int32_t mi : bk.mats)
-          if (is_vec4(mi) == (vw == 4)) {
-            row_tiles(mi, 32);
-            any = true;
-          }
-        if (any && !vec_done) vec_tiles(bk), vec_done = true;
+          if (is_vec4(mi) == (vw == 4)) row_tiles(mi, 32);
         sink.end(l, L);
       }
-      if (!vec_done) {
-        l = sink.begin(K_VEC, 1);
-        vec_tiles(bk);
-        sink.end(l, L);
-      }
+      l = sink.begin(K_VEC, 1);
+      vec_tiles(bk);
+      sink.end(l, L);
     }
-    // -- Q-step (even t): Ph = P W, (row chunk, 128-column block) tiles, finish
+    // -- Q-step (even t): Ph = P W, (row chunk, 32-column block) tiles, vectors, finish
     {
       std::vector<Launch>& L = bk.compress[0];
-      bool vec_done = bk.vecs.empty();
       Launch l = sink.begin(K_APPLY, 0);
       apply_tiles(bk.mats, false);
       sink.end(l, L);
@@ -291,22 +284,17 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         for (int32_t c = 0; c < d.q_chunks; ++c)
           for (int32_t cb = 0; cb < ncb; ++cb) plan.tiles.push_back(Tile{T_QTILE, mi, c, cb});
       }
-      if (!bk.mats.empty() && !vec_done) vec_tiles(bk), vec_done = true;
+      sink.end(l, L);
+      l = sink.begin(K_VEC, 0);
+      vec_tiles(bk);
       sink.end(l, L);
       qfin_launch(bk, L);
-      if (!vec_done) {
-        l = sink.begin(K_VEC, 0);
-        vec_tiles(bk);
-        sink.end(l, L);
-      }
     }
-    // -- decompress: factor tiles, vectors, then (32-row block, 512-column group) tiles
+    // -- decompress: (32-row block, 512-column group) tiles, then factor tiles and vectors
     for (int32_t par = 0; par < 2; ++par) {
       std::vector<Launch>& L = bk.decompress[par];
       const bool q = par == 0;
       Launch l = sink.begin(K_WRECON, 0);
-      for (int32_t mi : bk.mats) fact_tiles(mi, q);
-      vec_tiles(bk);
       for (int32_t mi : bk.mats) {
         const MatDesc& d = plan.mats[mi];
         const int32_t nrb = static_cast<int32_t>(cdiv(d.n, 32));
@@ -314,6 +302,10 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         for (int32_t rb = 0; rb < nrb; ++rb)
           for (int32_t cg = 0; cg < ncg; ++cg) plan.tiles.push_back(Tile{T_QTILE, mi, rb, cg});
       }
+      sink.end(l, L);
+      l = sink.begin(K_WFACT, 0);
+      for (int32_t mi : bk.mats) fact_tiles(mi, q);
+      vec_tiles(bk);
       sink.end(l, L);
       l = sink.begin(K_CHOL, 0);
       for (int32_t mi : bk.mats) chol_tiles(mi, q);
@@ -494,11 +486,11 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         const double cols = std::min<double>(d.q_cb, m - double(t.b) * d.q_cb);
         return rows * cols * eb + (t.b == 0 ? rows * rr * 8.0 : 0.0);
       }
+      case K_WFACT: {
+        const double rows = odd ? n : m;
+        return std::min<double>(d.fact_rows, rows - double(t.a) * d.fact_rows) * rr * 8.0;
+      }
       case K_WRECON: {
-        if (t.kind == T_FACT) {
-          const double rows = odd ? n : m;
-          return std::min<double>(d.fact_rows, rows - double(t.a) * d.fact_rows) * rr * 8.0;
-        }
         const double rows = std::min<double>(32.0, n - 32.0 * t.a);
         const double cols = std::min<double>(kWideRCols, m - double(kWideRCols) * t.b);
         return rows * cols * 4.0 + (t.b == 0 ? rows * rr * 4.0 : 0.0) + (t.a == 0 ? cols * rr * 4.0 : 0.0);
@@ -519,6 +511,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       case K_QSTEP: case K_WQSTEP: return 2;                               // ACP_KERNEL_Q_STEP
       case K_QFIN: return 3;                                               // ACP_KERNEL_Q_FINISH
       case K_RECON: case K_RECON4: case K_WRECON: return 4;                // ACP_KERNEL_RECONSTRUCT
+      case K_WFACT: return 5;                                              // ACP_KERNEL_ORTH
       case K_APPLY: case K_FACT: case K_CHOL: return 5;     // ACP_KERNEL_ORTH
       case K_VEC: return odd ? 1 : 2;
       default: return 0;
@@ -551,6 +544,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       case K_WPSTEP: return l.variant == 4 ? 12 : 13;
       case K_WQSTEP: return 22;
       case K_WRECON: return 40;
+      case K_WFACT: return 41;
       case K_QSTEP: return (l.variant & kQFused) ? 20 : (l.variant == 4 ? 21 : 22);
       case K_QFIN: return 23;
       case K_RECON4: return 30 + l.variant;         // 31..35

@@ -36,21 +36,40 @@ __device__ inline v16f zero16() {
 }
 __device__ inline uint32_t u32(int64_t x) { return static_cast<uint32_t>(x); }
 
-// P-step over a tile of at most 32 rows and all m columns.  Wave w takes the 32-column blocks
-// w, w + 4, ...; per block, lane l holds X for row r0 + l % 32 and columns c0 + drow(v, l / 32)
-// (VEC = 4: four float4 per stream, else sixteen floats).  The correction (F form) is an MFMA
+// KH consecutive floats of a factor row starting at byte offset off (kOut: zeros); with
+// vec, four at a time (the resource base and off are 16-byte aligned).
+template <int KH>
+__device__ inline void load_run(Rsrc r, uint32_t off, bool vec, float* out) {
+  if (vec) {
+#pragma unroll
+    for (int i = 0; i < KH / 4; ++i) {
+      const float4 f = bld4(r, off == kOut ? kOut : off + 16u * i);
+      out[4 * i + 0] = f.x;
+      out[4 * i + 1] = f.y;
+      out[4 * i + 2] = f.z;
+      out[4 * i + 3] = f.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < KH; ++i) out[i] = bld1(r, off == kOut ? kOut : off + 4u * i);
+  }
+}
+__device__ inline bool aligned16(const float* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// P-step over a tile of at most 32 rows and all m columns, one wave per workgroup, walking the
+// 32-column blocks in order; per block, lane l holds X for row r0 + l % 32 and columns
+// c0 + drow(v, l / 32) (VEC = 4: four float4 per stream, else sixteen floats).  A load instruction then touches 32
+// rows, 32 bytes each; the four instructions of a block cover each row's 128-byte line, so
+// these loads and stores go through the caches (not nontemporal): the line moves once.  The correction (F form) is an MFMA
 // with D indexed (column, row), which leaves X in that same layout; X then is the A operand of
-// P += X Qh.  The four waves' partial P are added in wave order.
+// P += X Qh, whose accumulator lane l holds P[r0 + drow(v, l / 32)][l % 32].  The next block's
+// M, E and factor rows are requested before the current block's MFMAs.
 template <int RK, int VEC>
-__global__ __launch_bounds__(kBlock) void k_wpstep(KArgs a) {
+__global__ __launch_bounds__(kWideBlock, 2) void k_wpstep(KArgs a) {
   constexpr int KH = RK / 2;
   const Tile t = a.tiles[blockIdx.x];
-  if (t.kind == T_VEC) {
-    vec_tile(a, t, true);
-    return;
-  }
   const MatDesc d = a.mats[t.idx];
-  const int wave = tid() >> 6, lane = tid() & 63, h = lane >> 5, li = lane & 31;
+  const int lane = tid(), h = lane >> 5, li = lane & 31;
   const int64_t m = d.m, r0 = t.a;
   const int rows = t.b;
   const bool fform = deferred_of(a, d.bucket);
@@ -66,91 +85,105 @@ __global__ __launch_bounds__(kBlock) void k_wpstep(KArgs a) {
   for (int s = 0; s < KH; ++s) pv[s] = bld1(Phr, u32(li * RK + KH * h + s) * 4u);
   const uint32_t roff = u32(li) * row_bytes;  // rows past the tile fall past the extent
 
-  v16f p = zero16();
-  for (int64_t c0 = wave * 32; c0 < m; c0 += 128) {
-    v16f x;
-    uint32_t off[VEC == 4 ? 4 : 16];
+  const bool ql4 = aligned16(a.fac + d.ql_slot);
+  constexpr int NO = VEC == 4 ? 4 : 16;  // accesses per stream per block
+  // M and E of one column block in the X layout (the next block's are requested early)
+  auto load_block = [&](int64_t c0, uint32_t* off, float* g, float* e) {
     if constexpr (VEC == 4) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int64_t col = c0 + 8 * q + 4 * h;
         off[q] = col < m ? roff + u32(col) * 4u : kOut;
-        const float4 g = bld4_nt(G, off[q]), e = bld4_nt(E, off[q]);
-        x[4 * q + 0] = g.x + e.x;
-        x[4 * q + 1] = g.y + e.y;
-        x[4 * q + 2] = g.z + e.z;
-        x[4 * q + 3] = g.w + e.w;
+        const float4 gq = bld4(G, off[q]), eq = bld4(E, off[q]);
+        g[4 * q + 0] = gq.x, g[4 * q + 1] = gq.y, g[4 * q + 2] = gq.z, g[4 * q + 3] = gq.w;
+        e[4 * q + 0] = eq.x, e[4 * q + 1] = eq.y, e[4 * q + 2] = eq.z, e[4 * q + 3] = eq.w;
       }
     } else {
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int64_t col = c0 + drow(v, h);
         off[v] = col < m ? roff + u32(col) * 4u : kOut;
-        x[v] = bld1_nt(G, off[v]) + bld1_nt(E, off[v]);
+        g[v] = bld1(G, off[v]);
+        e[v] = bld1(E, off[v]);
       }
     }
-    if (fform) {  // X -= Ph Ql^T: A = -Ql (column, rank), B = Ph^T (rank, row)
-      const int64_t qcol = c0 + li;
+  };
+  // the block's factor operands: Ql rows (correction A) and Qh rows (product B)
+  auto load_ops = [&](int64_t c0, float* qa, float* qb) {
+    const int64_t qcol = c0 + li;
+    if (fform) load_run<KH>(Qlr, qcol < m ? u32(qcol * RK + KH * h) * 4u : kOut, ql4, qa);
 #pragma unroll
-      for (int s = 0; s < KH; ++s) {
-        const float qa = -bld1(Qlr, qcol < m ? u32(qcol * RK + KH * h + s) * 4u : kOut);
-        x = mfma(qa, pv[s], x);
-      }
+    for (int v = 0; v < 16; ++v) {
+      const int64_t col = c0 + drow(v, h);
+      qb[v] = bld1(Qhr, (col < m && li < RK) ? u32(col * RK + li) * 4u : kOut);
+    }
+  };
+  uint32_t off[NO];
+  float g[16], e[16], qa[KH], qb[16];
+  load_block(0, off, g, e);
+  load_ops(0, qa, qb);
+
+  v16f p = zero16();
+  for (int64_t c0 = 0; c0 < m; c0 += 32) {
+    v16f x;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) x[v] = g[v] + e[v];
+    uint32_t cur[NO];
+#pragma unroll
+    for (int i = 0; i < NO; ++i) cur[i] = off[i];
+    float ca[KH], cb[16];
+#pragma unroll
+    for (int s = 0; s < KH; ++s) ca[s] = qa[s];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) cb[v] = qb[v];
+    load_block(c0 + 32, off, g, e);  // next block (past m: zeros, no traffic)
+    load_ops(c0 + 32, qa, qb);
+    if (fform) {  // X -= Ph Ql^T: A = -Ql (column, rank), B = Ph^T (rank, row)
+#pragma unroll
+      for (int s = 0; s < KH; ++s) x = mfma(-ca[s], pv[s], x);
     }
     if constexpr (VEC == 4) {
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        bst4_nt(E, off[q], make_float4(x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]));
+        bst4(E, cur[q], make_float4(x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]));
     } else {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) bst1_nt(E, off[v], x[v]);
+      for (int v = 0; v < 16; ++v) bst1(E, cur[v], x[v]);
     }
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {  // P += X Qh: A = X (row, column), B = Qh (column, rank)
-      const int64_t col = c0 + drow(v, h);
-      const float qb = bld1(Qhr, (col < m && li < RK) ? u32(col * RK + li) * 4u : kOut);
-      p = mfma(x[v], qb, p);
-    }
+    for (int v = 0; v < 16; ++v) p = mfma(x[v], cb[v], p);  // P += X Qh: A = X, B = Qh
   }
 
-  __shared__ float red[4][32 * 32];
-#pragma unroll
-  for (int v = 0; v < 16; ++v) red[wave][drow(v, h) * 32 + li] = p[v];
-  __syncthreads();
   float* P = dst_of(a, d.bucket) + d.fac_off_p;
   float* Pl = a.fac + d.pl_slot;
-  for (int e = tid(); e < 32 * 32; e += kBlock) {
-    const int row = e >> 5, k = e & 31;
-    if (row < rows && k < RK) {
-      const float sum = ((red[0][e] + red[1][e]) + red[2][e]) + red[3][e];
-      P[(r0 + row) * RK + k] = sum;
-      Pl[(r0 + row) * RK + k] = sum;
+  if (li < RK)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int row = drow(v, h);
+      if (row < rows) {
+        P[(r0 + row) * RK + li] = p[v];
+        Pl[(r0 + row) * RK + li] = p[v];
+      }
     }
-  }
 }
 
-// Q-step over a tile (row chunk t.a of q_rows rows, column block t.b of 128 columns); wave w
-// takes the block's columns c0 = t.b * 128 + 32 w ... c0 + 31.  Per 32-row block, lane l holds
+// Q-step over a tile (row chunk t.a of q_rows rows, column block t.b of 32 columns c0 ...
+// c0 + 31), one wave per workgroup.  Per 32-row block, lane l holds
 // F for column c0 + l % 32 and rows drow(v, l / 32): coalesced 128-byte row segments.  The
 // correction (X form) is an MFMA with D indexed (row, column); F then is the A operand of
 // Q += F^T Ph with the rows as K.  Lane l's partial Q of column c0 + drow(v, l / 32), rank
 // l % 32, goes to the chunk's partial block for K_QFIN.
 template <int RK>
-__global__ __launch_bounds__(kBlock) void k_wqstep(KArgs a) {
+__global__ __launch_bounds__(kWideBlock, 2) void k_wqstep(KArgs a) {
   constexpr int KH = RK / 2;
   const Tile t = a.tiles[blockIdx.x];
-  if (t.kind == T_VEC) {
-    vec_tile(a, t, true);
-    return;
-  }
   const MatDesc d = a.mats[t.idx];
-  const int wave = tid() >> 6, lane = tid() & 63, h = lane >> 5, li = lane & 31;
+  const int lane = tid(), h = lane >> 5, li = lane & 31;
   const int64_t n = d.n, m = d.m;
   const int64_t r0 = static_cast<int64_t>(t.a) * d.q_rows;
   const int rows = static_cast<int>((r0 + d.q_rows < n) ? d.q_rows : n - r0);
-  const int64_t c0 = static_cast<int64_t>(t.b) * d.q_cb + wave * 32;
-  const int64_t w = (m - c0) < 32 ? (m - c0) : 32;  // valid columns of this wave
-  if (w <= 0) return;
+  const int64_t c0 = static_cast<int64_t>(t.b) * d.q_cb;
+  const int64_t w = (m - c0) < 32 ? (m - c0) : 32;  // valid columns of the block
   const bool xform = deferred_p_of(a, d.bucket);
   const uint32_t row_bytes = u32(m) * 4u;
   const uint32_t ext = u32(rows - 1) * row_bytes + u32(w) * 4u;
@@ -164,29 +197,46 @@ __global__ __launch_bounds__(kBlock) void k_wqstep(KArgs a) {
   for (int s = 0; s < KH; ++s) qv[s] = bld1(Qhr, u32(li * RK + KH * h + s) * 4u);
   const uint32_t coff = li < w ? u32(li) * 4u : kOut;
 
+  const bool pl4 = aligned16(a.fac + d.pl_slot);
+  auto load_block = [&](int rb, float* g, float* e) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const uint32_t o = coff == kOut ? kOut : u32(rb + drow(v, h)) * row_bytes + coff;
+      g[v] = bld1_nt(G, o);
+      e[v] = bld1_nt(E, o);
+    }
+  };
+  // the block's factor operands: Pl rows (correction A) and Ph rows (product B)
+  auto load_ops = [&](int rb, float* pa, float* pb) {
+    if (xform) load_run<KH>(Plr, u32((rb + li) * RK + KH * h) * 4u, pl4, pa);
+#pragma unroll
+    for (int v = 0; v < 16; ++v)
+      pb[v] = bld1(Phr, li < RK ? u32((rb + drow(v, h)) * RK + li) * 4u : kOut);
+  };
+  float g[16], e[16], pa[KH], pb[16];
+  load_block(0, g, e);
+  load_ops(0, pa, pb);
   v16f q = zero16();
   for (int rb = 0; rb < rows; rb += 32) {
     v16f x;
-    uint32_t off[16];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      off[v] = coff == kOut ? kOut : u32(rb + drow(v, h)) * row_bytes + coff;
-      x[v] = bld1_nt(G, off[v]) + bld1_nt(E, off[v]);
-    }
+    for (int v = 0; v < 16; ++v) x[v] = g[v] + e[v];
+    float ca[KH], cb[16];
+#pragma unroll
+    for (int s = 0; s < KH; ++s) ca[s] = pa[s];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) cb[v] = pb[v];
+    load_block(rb + 32, g, e);  // next block (past the chunk: zeros, no traffic)
+    load_ops(rb + 32, pa, pb);
     if (xform) {  // F -= Pl Qh^T: A = -Pl (row, rank), B = Qh^T (rank, column)
 #pragma unroll
-      for (int s = 0; s < KH; ++s) {
-        const float pa = -bld1(Plr, u32((rb + li) * RK + KH * h + s) * 4u);
-        x = mfma(pa, qv[s], x);
-      }
+      for (int s = 0; s < KH; ++s) x = mfma(-ca[s], qv[s], x);
     }
 #pragma unroll
-    for (int v = 0; v < 16; ++v) bst1_nt(E, off[v], x[v]);
+    for (int v = 0; v < 16; ++v)
+      bst1_nt(E, coff == kOut ? kOut : u32(rb + drow(v, h)) * row_bytes + coff, x[v]);
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {  // Q += F^T Ph: A = F^T (column, row), B = Ph (row, rank)
-      const float pb = bld1(Phr, li < RK ? u32((rb + drow(v, h)) * RK + li) * 4u : kOut);
-      q = mfma(x[v], pb, q);
-    }
+    for (int v = 0; v < 16; ++v) q = mfma(x[v], cb[v], q);  // Q += F^T Ph: A = F^T, B = Ph
   }
   const int64_t ncb = (m + d.q_cb - 1) / d.q_cb;
   const int64_t stride = ncb * d.q_cb * RK;  // one row chunk of partials
@@ -196,28 +246,18 @@ __global__ __launch_bounds__(kBlock) void k_wqstep(KArgs a) {
     for (int v = 0; v < 16; ++v) part[drow(v, h) * RK + li] = q[v];
 }
 
-// Decompress: M_hat = A B^T / p over a tile (32-row block t.a, 512-column group t.b).  Odd
-// step: A = P_agg (factor buffer), B = Qh; even step: A = Ph, B = Q_agg.  Wave w writes the
-// 32-column blocks w, w + 4, ... of the group; lane l stores column c0 + l % 32 of rows
-// drow(v, l / 32): two 128-byte row segments per store.  Factor tiles keep the aggregated
-// factor as the next step's reused factor and build its W; vector tiles unpack sum / p.
+// Decompress: M_hat = A B^T / p over a tile (32-row block t.a, 512-column group t.b), one wave
+// per workgroup walking the group's 32-column blocks.  Odd step: A = P_agg (factor buffer),
+// B = Qh; even step: A = Ph, B = Q_agg.  Lane l stores column c0 + l % 32 of rows
+// drow(v, l / 32): two 128-byte row segments per store.  The next block's B rows are requested
+// before the current block's MFMAs.
 template <int RK>
-__global__ __launch_bounds__(kBlock) void k_wrecon(KArgs a) {
+__global__ __launch_bounds__(kWideBlock) void k_wrecon(KArgs a) {
   constexpr int KH = RK / 2;
   const Tile t = a.tiles[blockIdx.x];
   const bool odd = a.parity != 0;
-  if (t.kind == T_VEC) {
-    vec_tile(a, t, false);
-    return;
-  }
   const MatDesc d = a.mats[t.idx];
-  if (t.kind == T_FACT) {
-    const float* src = src_of(a, d.bucket) + (odd ? d.fac_off_p : d.fac_off_q);
-    float* dst = a.fac + (odd ? d.p_slot : d.q_slot);
-    fact_tile<RK>(a, t, src, dst, odd ? d.n : d.m);
-    return;
-  }
-  const int wave = tid() >> 6, lane = tid() & 63, h = lane >> 5, li = lane & 31;
+  const int lane = tid(), h = lane >> 5, li = lane & 31;
   const int64_t n = d.n, m = d.m;
   const int64_t r0 = static_cast<int64_t>(t.a) * 32;
   const int rows = static_cast<int>((r0 + 32 < n) ? 32 : n - r0);
@@ -226,22 +266,29 @@ __global__ __launch_bounds__(kBlock) void k_wrecon(KArgs a) {
   const float* B = odd ? a.fac + d.qh_slot : agg + d.fac_off_q;
   const Rsrc Ar = tile_rsrc(A + r0 * RK, u32(rows) * RK * 4u);
   const Rsrc Br = tile_rsrc(B, u32(m) * RK * 4u);
+  const bool a4 = aligned16(A), b4 = aligned16(B);
   float av[KH];  // A operand: A[r0 + l % 32][KH h + s] / p
+  load_run<KH>(Ar, u32(li * RK + KH * h) * 4u, a4, av);
 #pragma unroll
-  for (int s = 0; s < KH; ++s) av[s] = bld1(Ar, u32(li * RK + KH * h + s) * 4u) * a.inv_p;
+  for (int s = 0; s < KH; ++s) av[s] *= a.inv_p;
   float* O = dst_of(a, d.bucket) + d.grad_off + r0 * m;
   const uint32_t row_bytes = u32(m) * 4u;
-  for (int j = 0; j < kWideRCols / 128; ++j) {
-    const int64_t c0 = static_cast<int64_t>(t.b) * kWideRCols + j * 128 + wave * 32;
+  constexpr int NB = kWideRCols / 32;  // column blocks per tile
+  auto bcol = [&](int j) { return static_cast<int64_t>(t.b) * kWideRCols + j * 32; };
+  float bv[2][KH];  // B operand: B[c0 + l % 32][KH h + s], this block and the next
+  load_run<KH>(Br, bcol(0) + li < m ? u32((bcol(0) + li) * RK + KH * h) * 4u : kOut, b4, bv[0]);
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int64_t c0 = bcol(j);
+    if (j + 1 < NB) {
+      const int64_t c1 = bcol(j + 1);
+      load_run<KH>(Br, c1 + li < m ? u32((c1 + li) * RK + KH * h) * 4u : kOut, b4, bv[(j + 1) & 1]);
+    }
     if (c0 >= m) break;
     const int64_t w = (m - c0) < 32 ? (m - c0) : 32;
-    float bv[KH];  // B operand: B[c0 + l % 32][KH h + s]
-#pragma unroll
-    for (int s = 0; s < KH; ++s)
-      bv[s] = bld1(Br, li < w ? u32((c0 + li) * RK + KH * h + s) * 4u : kOut);
     v16f o = zero16();
 #pragma unroll
-    for (int s = 0; s < KH; ++s) o = mfma(av[s], bv[s], o);
+    for (int s = 0; s < KH; ++s) o = mfma(av[s], bv[j & 1][s], o);
     const Rsrc Or = tile_rsrc(O + c0, u32(rows - 1) * row_bytes + u32(w) * 4u);
     const uint32_t coff = li < w ? u32(li) * 4u : kOut;
 #pragma unroll
@@ -250,10 +297,27 @@ __global__ __launch_bounds__(kBlock) void k_wrecon(KArgs a) {
   }
 }
 
+// Decompress companions of K_WRECON (whole workgroups): factor tiles keep the aggregated
+// factor as the next step's reused factor and build its W; vector tiles unpack sum / p.
+template <int RK>
+__global__ __launch_bounds__(kBlock) void k_wfact(KArgs a) {
+  const Tile t = a.tiles[blockIdx.x];
+  const bool odd = a.parity != 0;
+  if (t.kind == T_VEC) {
+    vec_tile(a, t, false);
+    return;
+  }
+  const MatDesc d = a.mats[t.idx];
+  const float* src = src_of(a, d.bucket) + (odd ? d.fac_off_p : d.fac_off_q);
+  float* dst = a.fac + (odd ? d.p_slot : d.q_slot);
+  fact_tile<RK>(a, t, src, dst, odd ? d.n : d.m);
+}
+
 template <int RK>
 hipError_t launch_wide_rank(const Launch& l, const KArgs& args, hipStream_t s) {
-  const dim3 grid(static_cast<unsigned>(l.ntiles)), block(kBlock);
+  const dim3 grid(static_cast<unsigned>(l.ntiles)), block(kWideBlock);
   switch (l.kernel) {
+    case K_WFACT: hipLaunchKernelGGL(k_wfact<RK>, grid, dim3(kBlock), 0, s, args); break;
     case K_WPSTEP:
       if (l.variant == 4)
         hipLaunchKernelGGL((k_wpstep<RK, 4>), grid, block, 0, s, args);

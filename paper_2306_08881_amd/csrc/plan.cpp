@@ -255,18 +255,15 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   auto wide_lists = [&](BucketPlan& bk) {
     // The MFMA kernels run one wave per workgroup over matrix tiles only; raw vectors and
     // factor tiles (which need whole workgroups) go to launches of their own.
-    // -- P-step (odd t): Qh = Q W, then 32-row tiles (16-byte rows first, then the others)
+    // -- P-step (odd t): Qh = Q W, then 32-row tiles
     {
       std::vector<Launch>& L = bk.compress[1];
       Launch l = sink.begin(K_APPLY, 1);
       apply_tiles(bk.mats, true);
       sink.end(l, L);
-      for (int32_t vw : {4, 1}) {
-        l = sink.begin(K_WPSTEP, vw);
-        for (int32_t mi : bk.mats)
-          if (is_vec4(mi) == (vw == 4)) row_tiles(mi, 32);
-        sink.end(l, L);
-      }
+      l = sink.begin(K_WPSTEP, 0);
+      for (int32_t mi : bk.mats) row_tiles(mi, 32);
+      sink.end(l, L);
       l = sink.begin(K_VEC, 1);
       vec_tiles(bk);
       sink.end(l, L);
@@ -541,7 +538,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       case K_PFUSED: return 1 + l.variant;          // 2..6
       case K_PROW: return 10;
       case K_EUPD: return 11;
-      case K_WPSTEP: return l.variant == 4 ? 12 : 13;
+      case K_WPSTEP: return 12;
       case K_WQSTEP: return 22;
       case K_WRECON: return 40;
       case K_WFACT: return 41;

@@ -57,16 +57,18 @@ __device__ inline void load_run(Rsrc r, uint32_t off, bool vec, float* out) {
 __device__ inline bool aligned16(const float* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // P-step over a tile of at most 32 rows and all m columns, one wave per workgroup, walking the
-// 32-column blocks in order; per block, lane l holds X for row r0 + l % 32 and columns
-// c0 + drow(v, l / 32) (VEC = 4: four float4 per stream, else sixteen floats).  A load instruction then touches 32
-// rows, 32 bytes each; the four instructions of a block cover each row's 128-byte line, so
-// these loads and stores go through the caches (not nontemporal): the line moves once.  The correction (F form) is an MFMA
-// with D indexed (column, row), which leaves X in that same layout; X then is the A operand of
-// P += X Qh, whose accumulator lane l holds P[r0 + drow(v, l / 32)][l % 32].  The next block's
-// M, E and factor rows are requested before the current block's MFMAs.
-template <int RK, int VEC>
+// 32-column blocks in order.  Per block, lane l loads M and E for column c0 + l % 32 and rows
+// drow(v, l / 32) (coalesced 128-byte row segments), forms X = M + E, applies the correction
+// (F form) as an MFMA with D indexed (row, column) and stores X in that layout.  The product
+// P += X Qh reduces over columns, so it needs the row on the lane: X goes through a padded
+// 32 x 33 LDS tile (two of them, alternating) and comes back with lane l holding row l % 32 and
+// columns drow(v, l / 32), the A operand; the accumulator lane l holds P[r0 + drow(v, l / 32)]
+// [l % 32].  The next block's M, E and factor rows are requested before the current block's
+// MFMAs.
+template <int RK>
 __global__ __launch_bounds__(kWideBlock, 2) void k_wpstep(KArgs a) {
   constexpr int KH = RK / 2;
+  constexpr int LD = 33;  // padded LDS row: the transposed reads hit 32 different banks
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
   const int lane = tid(), h = lane >> 5, li = lane & 31;
@@ -80,35 +82,22 @@ __global__ __launch_bounds__(kWideBlock, 2) void k_wpstep(KArgs a) {
   const Rsrc Phr = tile_rsrc(a.fac + d.ph_slot + r0 * RK, fform ? u32(rows) * RK * 4u : 0u);
   const Rsrc Qlr = tile_rsrc(a.fac + d.ql_slot, fform ? u32(m) * RK * 4u : 0u);
   const Rsrc Qhr = tile_rsrc(a.fac + d.qh_slot, u32(m) * RK * 4u);
-  float pv[KH];  // correction B operand: Ph[r0 + l % 32][KH h + s]
+  const bool ph4 = aligned16(a.fac + d.ph_slot), ql4 = aligned16(a.fac + d.ql_slot);
+  float pa[KH];  // correction A operand: -Ph[r0 + l % 32][KH h + s]
+  load_run<KH>(Phr, u32(li * RK + KH * h) * 4u, ph4, pa);
 #pragma unroll
-  for (int s = 0; s < KH; ++s) pv[s] = bld1(Phr, u32(li * RK + KH * h + s) * 4u);
-  const uint32_t roff = u32(li) * row_bytes;  // rows past the tile fall past the extent
+  for (int s = 0; s < KH; ++s) pa[s] = -pa[s];
 
-  const bool ql4 = aligned16(a.fac + d.ql_slot);
-  constexpr int NO = VEC == 4 ? 4 : 16;  // accesses per stream per block
-  // M and E of one column block in the X layout (the next block's are requested early)
-  auto load_block = [&](int64_t c0, uint32_t* off, float* g, float* e) {
-    if constexpr (VEC == 4) {
+  auto load_block = [&](int64_t c0, float* g, float* e) {
+    const uint32_t coff = c0 + li < m ? u32(c0 + li) * 4u : kOut;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int64_t col = c0 + 8 * q + 4 * h;
-        off[q] = col < m ? roff + u32(col) * 4u : kOut;
-        const float4 gq = bld4(G, off[q]), eq = bld4(E, off[q]);
-        g[4 * q + 0] = gq.x, g[4 * q + 1] = gq.y, g[4 * q + 2] = gq.z, g[4 * q + 3] = gq.w;
-        e[4 * q + 0] = eq.x, e[4 * q + 1] = eq.y, e[4 * q + 2] = eq.z, e[4 * q + 3] = eq.w;
-      }
-    } else {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int64_t col = c0 + drow(v, h);
-        off[v] = col < m ? roff + u32(col) * 4u : kOut;
-        g[v] = bld1(G, off[v]);
-        e[v] = bld1(E, off[v]);
-      }
+    for (int v = 0; v < 16; ++v) {
+      const uint32_t o = coff == kOut ? kOut : u32(drow(v, h)) * row_bytes + coff;
+      g[v] = bld1_nt(G, o);
+      e[v] = bld1_nt(E, o);
     }
   };
-  // the block's factor operands: Ql rows (correction A) and Qh rows (product B)
+  // the block's factor operands: Ql rows (correction B) and Qh rows (product B)
   auto load_ops = [&](int64_t c0, float* qa, float* qb) {
     const int64_t qcol = c0 + li;
     if (fform) load_run<KH>(Qlr, qcol < m ? u32(qcol * RK + KH * h) * 4u : kOut, ql4, qa);
@@ -118,40 +107,38 @@ __global__ __launch_bounds__(kWideBlock, 2) void k_wpstep(KArgs a) {
       qb[v] = bld1(Qhr, (col < m && li < RK) ? u32(col * RK + li) * 4u : kOut);
     }
   };
-  uint32_t off[NO];
+  __shared__ float xt[2][32 * LD];
   float g[16], e[16], qa[KH], qb[16];
-  load_block(0, off, g, e);
+  load_block(0, g, e);
   load_ops(0, qa, qb);
 
   v16f p = zero16();
-  for (int64_t c0 = 0; c0 < m; c0 += 32) {
+  int buf = 0;
+  for (int64_t c0 = 0; c0 < m; c0 += 32, buf ^= 1) {
     v16f x;
 #pragma unroll
     for (int v = 0; v < 16; ++v) x[v] = g[v] + e[v];
-    uint32_t cur[NO];
-#pragma unroll
-    for (int i = 0; i < NO; ++i) cur[i] = off[i];
     float ca[KH], cb[16];
 #pragma unroll
     for (int s = 0; s < KH; ++s) ca[s] = qa[s];
 #pragma unroll
     for (int v = 0; v < 16; ++v) cb[v] = qb[v];
-    load_block(c0 + 32, off, g, e);  // next block (past m: zeros, no traffic)
+    const uint32_t coff = c0 + li < m ? u32(c0 + li) * 4u : kOut;
+    load_block(c0 + 32, g, e);  // next block (past m: zeros, no traffic)
     load_ops(c0 + 32, qa, qb);
-    if (fform) {  // X -= Ph Ql^T: A = -Ql (column, rank), B = Ph^T (rank, row)
+    if (fform) {  // X -= Ph Ql^T: A = -Ph (row, rank), B = Ql^T (rank, column)
 #pragma unroll
-      for (int s = 0; s < KH; ++s) x = mfma(-ca[s], pv[s], x);
-    }
-    if constexpr (VEC == 4) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        bst4(E, cur[q], make_float4(x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]));
-    } else {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) bst1(E, cur[v], x[v]);
+      for (int s = 0; s < KH; ++s) x = mfma(pa[s], ca[s], x);
     }
 #pragma unroll
-    for (int v = 0; v < 16; ++v) p = mfma(x[v], cb[v], p);  // P += X Qh: A = X, B = Qh
+    for (int v = 0; v < 16; ++v) {
+      bst1_nt(E, coff == kOut ? kOut : u32(drow(v, h)) * row_bytes + coff, x[v]);
+      xt[buf][drow(v, h) * LD + li] = x[v];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < 16; ++v)  // P += X Qh: A = X (row, column), B = Qh (column, rank)
+      p = mfma(xt[buf][li * LD + drow(v, h)], cb[v], p);
   }
 
   float* P = dst_of(a, d.bucket) + d.fac_off_p;
@@ -318,12 +305,7 @@ hipError_t launch_wide_rank(const Launch& l, const KArgs& args, hipStream_t s) {
   const dim3 grid(static_cast<unsigned>(l.ntiles)), block(kWideBlock);
   switch (l.kernel) {
     case K_WFACT: hipLaunchKernelGGL(k_wfact<RK>, grid, dim3(kBlock), 0, s, args); break;
-    case K_WPSTEP:
-      if (l.variant == 4)
-        hipLaunchKernelGGL((k_wpstep<RK, 4>), grid, block, 0, s, args);
-      else
-        hipLaunchKernelGGL((k_wpstep<RK, 1>), grid, block, 0, s, args);
-      break;
+    case K_WPSTEP: hipLaunchKernelGGL(k_wpstep<RK>, grid, block, 0, s, args); break;
     case K_WQSTEP: hipLaunchKernelGGL(k_wqstep<RK>, grid, block, 0, s, args); break;
     case K_WRECON: hipLaunchKernelGGL(k_wrecon<RK>, grid, block, 0, s, args); break;
     default: return hipErrorInvalidValue;

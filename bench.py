@@ -78,16 +78,32 @@ def cpu_baseline(wl, seconds: float = 12.0):
                       f"(OpenBLAS), {elapsed:.1f} s of oracle work"}
 
 
-KERNEL_SYMBOLS = {"P-step compress (k_pfused)": "k_pfused", "Q-step compress (k_qstep)": "k_qstep",
-                  "Q-step finish (k_qfin)": "k_qfin", "decompress (k_recon4)": "k_recon"}
+def kernel_families(rank: int):
+    """(label, ACP_KERNEL_* family, kernel symbol prefix) of the timed kernel families: the rank-4
+    register-resident kernels, or the MFMA kernels of ranks 8 to 32."""
+    from paper_2306_08881_amd import _lib as L
+    wide = rank >= 8
+    p, q, d = ("k_wpstep", "k_wqstep", "k_wrecon") if wide else ("k_pfused", "k_qstep", "k_recon")
+    return [(f"P-step compress ({p})", L.ACP_KERNEL_P_STEP, p),
+            (f"Q-step compress ({q})", L.ACP_KERNEL_Q_STEP, q),
+            ("Q-step finish (k_qfin)", L.ACP_KERNEL_Q_FINISH, "k_qfin"),
+            (f"decompress ({d if wide else 'k_recon4'})", L.ACP_KERNEL_RECONSTRUCT, d)]
+
+
+WORKLOAD_KIND = {"conv": "one 256x64x3x3 convolution gradient", "resnet50": "ResNet-50-shaped gradients",
+                 "resnet152": "ResNet-152-shaped gradients", "bert_base": "BERT-base-shaped gradients",
+                 "bert_large": "BERT-large-shaped gradients"}
 TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "traffic.txt")
 
 
 def kernel_source_hash() -> str:
+    """Fingerprint of the sources the rank-4 kernels are compiled from."""
     import hashlib
-    src = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2306_08881_amd", "csrc",
-                       "kernels.hip")
-    return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    csrc = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2306_08881_amd", "csrc")
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "device.hpp", "acp_internal.hpp"):
+        h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def pmc_summary(fetch_csv: str, write_csv: str, workload: str):
@@ -137,7 +153,7 @@ def measured_traffic(workload: str, family: str, launches: int):
         return None
     if t.get("source_hash") != kernel_source_hash() or t.get("workload") not in (None, workload):
         return None
-    sym = KERNEL_SYMBOLS.get(family)
+    sym = next((k[2] for k in kernel_families(4) + kernel_families(8) if k[0] == family), None)
     ks = [v for k, v in t["kernels"].items() if sym and k.startswith(sym)]
     if not ks:
         return None
@@ -258,22 +274,19 @@ def main():
 
     # per-kernel pass: the same steps again with every launch of one kernel family bracketed by
     # HIP events on its own stream (acp_profile_*), once per family
-    fams = {"P-step compress (k_pfused)": L.ACP_KERNEL_P_STEP,
-            "Q-step compress (k_qstep)": L.ACP_KERNEL_Q_STEP,
-            "Q-step finish (k_qfin)": L.ACP_KERNEL_Q_FINISH,
-            "decompress (k_recon4)": L.ACP_KERNEL_RECONSTRUCT}
+    fams = kernel_families(wl.rank)
     kern = {}
-    for name, fam in fams.items():
+    for name, fam, _ in fams:
         acp.profile_start(fam, 64 * nb * steps)
         timed(steps, args.mode)
         n, sec, by = acp.profile_stop()
         if n:
             kern[name] = {"launches": n, "avg_launch_us": sec / n * 1e6, "bytes_per_launch": by / n,
                           "gbs": by / sec / 1e9, "ms_per_step": sec / steps * 1e3}
-    # the dominant kernel: k_qstep, the longest-running single kernel of the step (one launch per
-    # Q-step); the P-step time is split over one k_pfused launch per column class
-    dom = "Q-step compress (k_qstep)" if "Q-step compress (k_qstep)" in kern else \
-        max(kern, key=lambda k: kern[k]["ms_per_step"])
+    # the dominant kernel: the Q-step kernel, the longest-running single kernel of the step (one
+    # launch per Q-step); at rank 4 the P-step time is split over one k_pfused launch per column
+    # class
+    dom = fams[1][0] if fams[1][0] in kern else max(kern, key=lambda k: kern[k]["ms_per_step"])
     dk = kern[dom]
     step_bytes, bp, bq, bd, nc, n1 = algorithmic_bytes(wl, wl.rank)
     gbs = step_bytes / (ms * 1e-3) / 1e9
@@ -290,8 +303,9 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic (seeded N(0, 0.02^2) gradients of the workload's shapes)",
-        "config": {"workload": f"{wl.name}: BERT-large-shaped gradients, {len(shapes)} tensors, "
-                               f"{wl.numel} parameters, rank {wl.rank}, 25 MiB buckets ({nb})",
+        "config": {"workload": f"{wl.name}: {WORKLOAD_KIND[wl.name.rsplit('_', 1)[0].split('256')[0]]}, "
+                               f"{len(shapes)} tensors, {wl.numel} parameters, rank {wl.rank}, "
+                               f"{wl.cap_bytes >> 20} MiB buckets ({nb})",
                    "rank": wl.rank, "buckets": nb, "parameters": wl.numel, "mode": args.mode,
                    "streams": nstreams if args.mode == "bucket" else 1,
                    "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),

@@ -19,9 +19,10 @@ pytestmark = pytest.mark.gpu
 
 
 def _snap(run, t):
+    """Outputs, the message the step wrote (its parity's length of each factor buffer) and E."""
     torch.cuda.synchronize()
     out = [o.clone() for o in run.out]
-    fb = [f.clone() for f in run.fbuf]
+    fb = [f[:(i[2] if t % 2 else i[3])].clone() for f, i in zip(run.fbuf, run.info)]
     es = []
     for b in range(run.nb):
         run.acp.error(b, run.ebuf[b])
@@ -37,9 +38,22 @@ def _resnet_inputs(run, wl, t):
     return run.pack(sg.gradient_set(wl, t))
 
 
-def test_bitwise_repeatable_and_resume():
-    wl = sg.WORKLOADS["resnet50_r4"]
-    shapes = [p.shape for p in wl.params]
+WIDE_SHAPES = [(96, 80), (33, 5, 7), (40,), (70, 130), (17,), (64, 64), (200, 36)]
+
+
+@pytest.mark.parametrize("case", ["resnet50_r4", "wide_r16_after_p", "wide_r32_after_q"])
+def test_bitwise_repeatable_and_resume(case):
+    """Repeat runs agree bitwise; resuming from a checkpoint continues bitwise.  The wide cases
+    checkpoint a rank-16 context after a P-step (its arena holds X) and a rank-32 context after
+    a Q-step (its arena holds F)."""
+    if case == "resnet50_r4":
+        wl = sg.WORKLOADS["resnet50_r4"]
+        shapes, rank, cap, at = [p.shape for p in wl.params], 4, 25 << 20, 3
+    else:
+        rank, at = (16, 3) if case == "wide_r16_after_p" else (32, 4)
+        shapes, cap = WIDE_SHAPES, 1 << 15
+        wl = sg.Workload(case, [sg.Param(f"t{i}", s) for i, s in enumerate(shapes)], rank, 8,
+                         lambda p: 0.05, seed=11)
     inputs = {}
 
     def inp(run, t):
@@ -47,20 +61,20 @@ def test_bitwise_repeatable_and_resume():
             inputs[t] = run.pack(sg.gradient_set(wl, t))
         return inputs[t]
 
-    a = PU.Runner(shapes, 4)
+    a = PU.Runner(shapes, rank, cap=cap)
     snaps_a = []
     for t in range(1, 7):
         a.step(t, inp(a, t))
         snaps_a.append(_snap(a, t))
-        if t == 3:
+        if t == at:
             ckpt = a.acp.get_state()
-    b = PU.Runner(shapes, 4)
+    b = PU.Runner(shapes, rank, cap=cap)
     for t in range(1, 7):
         b.step(t, inp(b, t))
         assert _same(_snap(b, t), snaps_a[t - 1]), f"run-to-run difference at step {t}"
-    c = PU.Runner(shapes, 4)
+    c = PU.Runner(shapes, rank, cap=cap)
     c.acp.set_state(ckpt)
-    for t in range(4, 7):
+    for t in range(at + 1, 7):
         c.step(t, inp(c, t))
         assert _same(_snap(c, t), snaps_a[t - 1]), f"resume difference at step {t}"
 
@@ -75,7 +89,7 @@ def test_checkpoint_rejects_other_context():
     assert e.value.status == L.ACP_E_STATE
 
 
-@pytest.mark.parametrize("name", ["bert_large_r4"])
+@pytest.mark.parametrize("name", ["bert_large_r4", "bert_large_r32"])
 def test_full_size_residual_identity(name):
     wl = sg.WORKLOADS[name]
     shapes = [p.shape for p in wl.params]

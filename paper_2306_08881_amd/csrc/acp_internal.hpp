@@ -29,7 +29,9 @@ constexpr int kBlock = 256;       // threads per workgroup (4 waves of 64)
 constexpr int kWave = 64;
 constexpr double kTau = 1e-4;     // rank-deficiency threshold of orth()
 constexpr int kMaxTileRows = 256; // rows per tile of the rank-4 row kernels (factor rows in LDS)
-constexpr int kQfinWide = 64;     // Q-step chunks above which k_qfin uses 16 threads per entry
+// K_QFIN entries (e = column * r + rank, over the whole matrix) per tile: one thread per entry
+// for up to 8 row chunks, 4 threads for up to 64, 16 threads beyond
+constexpr int qfin_entries(int32_t q_chunks) { return q_chunks <= 8 ? 256 : (q_chunks <= 64 ? 64 : 16); }
 constexpr int64_t kMaxCols = int64_t(1) << 24;  // columns of a compressed matrix, at most
 constexpr int kQRows = 128;       // rows per Q-step row chunk (at most; the chunk's Ph rows sit in LDS)
 

@@ -266,48 +266,61 @@ __device__ void gram_rows(const float* X, int64_t r0, int64_t r1, double* G, flo
   }
 }
 
-// Cholesky G = R^T R and W = R^-1 (dropped columns zero), written to w_out.  G in shared.
+// The lane's double from lane `src` of the wave (src uniform).
+__device__ inline double readlane_d(double v, int src) {
+  const int2 h = __builtin_bit_cast(int2, v);
+  return __builtin_bit_cast(double, make_int2(__builtin_amdgcn_readlane(h.x, src),
+                                              __builtin_amdgcn_readlane(h.y, src)));
+}
+
+// Cholesky G = R^T R and W = R^-1 (dropped columns and rows zero), written to w_out.  G in
+// shared; every thread of the workgroup calls this, the first wave does the work.  Right-looking,
+// one column per lane: lane j keeps column j of the updated G in registers; at pivot k lane k's
+// diagonal decides the drop, each lane forms its entry R[k][j], and the trailing update takes
+// R[k][i] from lane i.  The subtractions come in the same order as in the left-looking form
+// (pivot 0 first), so R is the same.  W = R^-1 on the kept columns, row by row (lane = row).
 template <int RK>
 __device__ void cholesky_w(const double* G, double* w_out) {
   __shared__ double R[RK * RK];
   __shared__ int drop[RK];
-  for (int e = tid(); e < RK * RK; e += kBlock) R[e] = 0.0;
-  __syncthreads();
-  for (int j = 0; j < RK; ++j) {
-    if (tid() == 0) {
-      const double gjj = G[j * RK + j];
-      double dj = gjj;
-      for (int i = 0; i < j; ++i) dj -= R[i * RK + j] * R[i * RK + j];
-      const bool keep = gjj > 0.0 && dj > kTau * kTau * gjj;
-      drop[j] = keep ? 0 : 1;
-      R[j * RK + j] = keep ? sqrt(dj) : 0.0;
-    }
-    __syncthreads();
-    const int k = tid();
-    if (k > j && k < RK && drop[j] == 0) {
-      double s = G[j * RK + k];
-      for (int i = 0; i < j; ++i) s -= R[i * RK + j] * R[i * RK + k];
-      R[j * RK + k] = s / R[j * RK + j];
-    }
-    __syncthreads();
+  if (tid() >= kWave) return;
+  const int j = tid();
+  const bool col = j < RK;
+  double g[RK];
+#pragma unroll
+  for (int i = 0; i < RK; ++i) g[i] = col ? G[i * RK + j] : 0.0;
+#pragma unroll
+  for (int k = 0; k < RK; ++k) {
+    const double gkk = G[k * RK + k];
+    const double dk = readlane_d(g[k], k);
+    const bool keep = gkk > 0.0 && dk > kTau * kTau * gkk;
+    const double rkk = keep ? sqrt(dk) : 0.0;
+    double rkj = 0.0;
+    if (keep) rkj = j > k ? g[k] / rkk : (j == k ? rkk : 0.0);
+    if (col) R[k * RK + j] = rkj;
+    if (j == 0) drop[k] = keep ? 0 : 1;
+    if (keep)
+#pragma unroll
+      for (int i = k + 1; i < RK; ++i) g[i] -= readlane_d(rkj, i) * rkj;
   }
-  const int arow = tid();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  const int arow = j;
   if (arow < RK) {
     double wr[RK];
 #pragma unroll
-    for (int j = 0; j < RK; ++j) {
+    for (int c = 0; c < RK; ++c) {
       double v = 0.0;
-      if (drop[j] == 0 && arow <= j) {
-        v = (arow == j) ? 1.0 : 0.0;
+      if (drop[c] == 0 && arow <= c) {
+        v = (arow == c) ? 1.0 : 0.0;
 #pragma unroll
-        for (int i = 0; i < j; ++i)
-          if (i >= arow) v -= R[i * RK + j] * wr[i];
-        v /= R[j * RK + j];
+        for (int i = 0; i < c; ++i)
+          if (i >= arow) v -= R[i * RK + c] * wr[i];
+        v /= R[c * RK + c];
       }
-      wr[j] = v;
+      wr[c] = v;
     }
 #pragma unroll
-    for (int j = 0; j < RK; ++j) w_out[arow * RK + j] = wr[j];
+    for (int c = 0; c < RK; ++c) w_out[arow * RK + c] = wr[c];
   }
 }
 

@@ -429,29 +429,28 @@ __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
     for (int k = 0; k < RK; ++k) part[c * RK + k] = acc[c][k];
 }
 
-// Q-step finish: Q_loc = sum over the row chunks' partials.  A tile covers NE entries of column
-// block t.b (entries [t.a * NE, t.a * NE + NE)) with 256 / NE threads per entry; NE = 64 when
-// the matrix has at most kQfinWide chunks, else 16.  Each thread adds a contiguous share of
-// the chunks in chunk order and the shares are added in thread order.  The result goes to the
-// factor buffer and to the Ql slot.
+// Q-step finish: Q_loc = sum over the row chunks' partials.  A tile covers the NE entries
+// [t.a * NE, t.a * NE + NE) of the matrix (entry e = column * r + rank, NE = qfin_entries) with
+// 256 / NE threads per entry.  Each thread adds a contiguous share of the chunks in chunk
+// order and the shares are added in thread order.  The result goes to the factor buffer and to
+// the Ql slot.
 template <int RK>
 __global__ __launch_bounds__(kBlock) void k_qfin(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
   const int64_t m = d.m;
   const int64_t ncb = (m + d.q_cb - 1) / d.q_cb;
-  const int64_t stride = ncb * d.q_cb * RK;
-  const int ne = d.q_chunks > kQfinWide ? 16 : 64;       // entries per tile
-  const int ng = kBlock / ne;                            // threads per entry
+  const int64_t stride = ncb * d.q_cb * RK;  // one row chunk of partials
+  const int ne = qfin_entries(d.q_chunks);   // entries per tile
+  const int ng = kBlock / ne;                // threads per entry
   const int gq = tid() / ne, el = tid() % ne;
-  const int e = t.a * ne + el;                           // entry within the column block
-  const int64_t c = static_cast<int64_t>(t.b) * d.q_cb + e / RK;
-  const bool on = e < d.q_cb * RK && c < m;
+  const int64_t e = static_cast<int64_t>(t.a) * ne + el;
+  const bool on = e < m * RK;
   const int per = (d.q_chunks + ng - 1) / ng;
   const int ch0 = gq * per, ch1 = (ch0 + per < d.q_chunks) ? ch0 + per : d.q_chunks;
   float s = 0.f;
   if (on) {
-    const float* base = a.qpart + d.qpart + static_cast<int64_t>(t.b) * d.q_cb * RK + e;
+    const float* base = a.qpart + d.qpart + e;
     constexpr int U = 8;
     int ch = ch0;
     for (; ch + U <= ch1; ch += U) {
@@ -463,15 +462,21 @@ __global__ __launch_bounds__(kBlock) void k_qfin(KArgs a) {
     }
     for (; ch < ch1; ++ch) s += base[ch * stride];
   }
+  if (ng == 1) {
+    if (on) {
+      dst_of(a, d.bucket)[d.fac_off_q + e] = s;
+      a.fac[d.ql_slot + e] = s;
+    }
+    return;
+  }
   __shared__ float red[kBlock];
   red[tid()] = s;
   __syncthreads();
   if (gq == 0 && on) {
     float tot = red[el];
     for (int g = 1; g < ng; ++g) tot += red[g * ne + el];
-    const int64_t o = c * RK + (e % RK);
-    dst_of(a, d.bucket)[d.fac_off_q + o] = tot;
-    a.fac[d.ql_slot + o] = tot;
+    dst_of(a, d.bucket)[d.fac_off_q + e] = tot;
+    a.fac[d.ql_slot + e] = tot;
   }
 }
 

@@ -238,11 +238,9 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     Launch l = sink.begin(K_QFIN, 0);
     for (int32_t mi : bk.mats) {
       const MatDesc& d = plan.mats[mi];
-      const int32_t ncb = static_cast<int32_t>(cdiv(d.m, d.q_cb));
-      const int64_t ne = d.q_chunks > kQfinWide ? 16 : 64;
-      const int32_t nblk = static_cast<int32_t>(cdiv(int64_t(d.q_cb) * r, ne));
-      for (int32_t cb = 0; cb < ncb; ++cb)
-        for (int32_t eb = 0; eb < nblk; ++eb) plan.tiles.push_back(Tile{T_QTILE, mi, eb, cb});
+      const int64_t nblk = cdiv(int64_t(d.m) * r, qfin_entries(d.q_chunks));
+      for (int64_t eb = 0; eb < nblk; ++eb)
+        plan.tiles.push_back(Tile{T_QTILE, mi, static_cast<int32_t>(eb), 0});
     }
     sink.end(l, L);
   };
@@ -463,10 +461,8 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         return rows * cols * eb + (t.b == 0 ? rows * rr * 8.0 : 0.0);
       }
       case K_QFIN: {
-        const double ne = d.q_chunks > kQfinWide ? 16.0 : 64.0;
-        const double e0 = double(t.a) * ne, ent = double(d.q_cb) * rr;
-        const double cols_e = std::min<double>(ent, (m - double(t.b) * d.q_cb) * rr);
-        return 8.0 * std::max(0.0, std::min<double>(ne, cols_e - e0));
+        const double ne = qfin_entries(d.q_chunks), e0 = double(t.a) * ne;
+        return 8.0 * std::max(0.0, std::min<double>(ne, m * rr - e0));
       }
       case K_RECON:
       case K_RECON4:

@@ -86,13 +86,22 @@ enum KernelId : int32_t {
   K_WQSTEP,      // Q-step, ranks 8..32 (MFMA): F = M' written, per-chunk partials of F^T Ph
   K_WRECON,      // decompress, ranks 8..32 (MFMA): M_hat = A B^T / p
   K_WFACT,       // decompress, ranks 8..32: factor tiles and vectors / p
+  K_PNARROW,     // P-step, r = 4, rows of at most 512 columns: whole rows per wave
+  K_QNARROW,     // Q-step, r = 4, rows of at most 512 columns
+  K_RNARROW,     // decompress, r = 4, rows of at most 512 columns; factor tiles; vectors / p
 };
+
+// Narrow rows (r = 4, m / 4 = m4 <= 128 float4 groups): L lanes per row (16, 32 or 64), G float4
+// groups per lane (1 or 2); the launch variant is (L << 4) | G.
+constexpr int32_t narrow_variant(int32_t m4) {
+  return m4 <= 16 ? (16 << 4) | 1 : m4 <= 32 ? (32 << 4) | 1 : m4 <= 64 ? (64 << 4) | 1 : (64 << 4) | 2;
+}
 
 constexpr int32_t kWideRank = 8;   // ranks at or above this take the K_W* kernels
 constexpr int kWideBlock = 64;     // threads per workgroup of K_WPSTEP, K_WQSTEP, K_WRECON: one wave
 constexpr int kWideQCols = 32;     // K_WQSTEP column block (one MFMA block)
 constexpr int kWideQRows = 512;    // K_WQSTEP rows per chunk (at most)
-constexpr int kWideRCols = 512;    // K_WRECON columns per tile: 16 blocks of 32
+constexpr int kWideRCols = 1024;   // K_WRECON columns per tile: 32 blocks of 32
 
 // K_QSTEP variants: column slots per lane | kQFused when the kernel also orthogonalises P
 constexpr int32_t kQFused = 16;
@@ -107,6 +116,7 @@ struct Launch {
   int32_t family;    // ACP_KERNEL_* family (host-side profiling)
   double alg_bytes;  // algorithmic bytes of the launch (host-side profiling)
 };
+
 
 // Buckets per launch: a launch covers the buckets [base, base + kMaxGroup) at most; their
 // buffer addresses travel in the kernel arguments.

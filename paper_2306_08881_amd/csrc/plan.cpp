@@ -13,13 +13,18 @@
 #include "plan.hpp"
 
 #include <algorithm>
+#include <array>
 #include <cmath>
+#include <map>
 
 namespace acp {
 
 namespace {
 
 constexpr int64_t kTileElems = 16384;   // gradient elements per streaming tile (unit)
+constexpr int64_t kSmallTileElems = 2048;  // per tile of the general P-step E update and decompress
+constexpr int64_t kTargetTiles = 1024;     // workgroups a launch class aims for (4 per CU)
+constexpr int64_t kMinTileElems = 2048;    // smallest tile of a class that has few elements
 constexpr int64_t kVecChunk = 4096;     // raw-vector elements per copy tile
 constexpr int64_t kApplyRows = 256;     // factor rows per orthogonalisation tile
 constexpr int64_t kSlotAlign = 64;      // floats (256 bytes)
@@ -114,8 +119,44 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     if (!cur.tids.empty()) plan.buckets.push_back(std::move(cur));
   }
 
-  // ---- per-tensor device descriptors and state regions
+  // ---- launch classes of the rank-4 kernels and their total elements: a class with few
+  // elements gets smaller tiles, so that its (grouped) launch still has about kTargetTiles
+  // workgroups instead of a few long serial ones
   const bool wide = r >= kWideRank;
+  std::map<int64_t, int64_t> class_elems;
+  auto class_key = [](int32_t kernel, int32_t variant) { return int64_t(kernel) * 65536 + variant; };
+  // (P-step kernel, variant), (Q-step kernel, variant), (decompress kernel, variant) of a
+  // rank-4 matrix that the register-resident kernels take; kernel -1 for the general path
+  auto rank4_classes = [&](int64_t m, int64_t grad_off, int64_t fac_p, int64_t fac_q) {
+    std::array<std::pair<int32_t, int32_t>, 3> c{};
+    const bool fast = r == 4 && m % 4 == 0 && grad_off % 4 == 0 && fac_p % 4 == 0 && fac_q % 4 == 0 &&
+                      cdiv(m / 4, 256) <= 5;
+    if (!fast) {
+      c.fill({-1, 0});
+    } else if (m / 4 <= 128) {
+      const int32_t v = narrow_variant(static_cast<int32_t>(m / 4));
+      c = {{{K_PNARROW, v}, {K_QNARROW, v}, {K_RNARROW, v}}};
+    } else {
+      const int32_t S = static_cast<int32_t>(cdiv(m / 4, 256));
+      c = {{{K_PFUSED, S}, {K_QSTEP, 4 | kQFused}, {K_RECON4, S}}};
+    }
+    return c;
+  };
+  for (const BucketPlan& bk : plan.buckets)
+    for (size_t k = 0; k < bk.tids.size(); ++k) {
+      const TensorPlan& t = plan.tensors[bk.tids[k]];
+      if (!t.compressed || wide) continue;
+      for (const auto& kv : rank4_classes(t.m, bk.grad_off[k], bk.fac_off_p[k], bk.fac_off_q[k]))
+        if (kv.first >= 0) class_elems[class_key(kv.first, kv.second)] += t.n * t.m;
+    }
+  // elements per tile of a class: its total over kTargetTiles, between kMinTileElems and `base`
+  auto class_tile = [&](int32_t kernel, int32_t variant, int64_t base) {
+    const auto it = class_elems.find(class_key(kernel, variant));
+    const int64_t tot = it == class_elems.end() ? 0 : it->second;
+    return std::max<int64_t>(kMinTileElems, std::min<int64_t>(base, tot / kTargetTiles));
+  };
+
+  // ---- per-tensor device descriptors and state regions
   int64_t e_floats = 0, fac_floats = 0, gpart = 0, qpart = 0;
   for (int32_t b = 0; b < static_cast<int32_t>(plan.buckets.size()); ++b) {
     BucketPlan& bk = plan.buckets[b];
@@ -159,6 +200,18 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       // (the kernels address a tile with 32-bit offsets from the tile's first element)
       d.q_rows = static_cast<int32_t>(std::max<int64_t>(
           1, std::min<int64_t>(wide ? kWideQRows : kQRows, (int64_t(1) << 30) / (t.m * 4))));
+      // a small matrix the general kernels take is split into at least 4 chunks (16 rows or
+      // more each), so its Q-step is not one workgroup's serial walk
+      const bool fast = r == 4 && vec4 && d.fac_off_p % 4 == 0 && d.fac_off_q % 4 == 0 && t.m / 4 <= 1280;
+      if (!wide && !fast)
+        d.q_rows = std::min<int32_t>(d.q_rows, std::max<int32_t>(16, static_cast<int32_t>(cdiv(t.n, 4))));
+      if (!wide && fast) {
+        // chunk rows of a multiple of 16 holding about the class's elements per tile
+        const auto qc = rank4_classes(t.m, d.grad_off, d.fac_off_p, d.fac_off_q)[1];
+        const int64_t cols = std::min<int64_t>(t.m, d.q_cb);
+        const int64_t want = class_tile(qc.first, qc.second, int64_t(kQRows) * cols) / cols;
+        d.q_rows = std::min<int32_t>(d.q_rows, static_cast<int32_t>(std::max<int64_t>(16, want / 16 * 16)));
+      }
       d.q_chunks = static_cast<int32_t>(cdiv(t.n, d.q_rows));
       const int64_t ncb = cdiv(t.m, d.q_cb);
       d.qpart = qpart;
@@ -314,15 +367,31 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       wide_lists(bk);
       continue;
     }
-    std::vector<int32_t> fast, generic;
+    // fast: rank-4 register-resident kernels; narrow: rows of at most 512 columns (scls 0)
+    std::vector<int32_t> fast, narrow, generic;
     for (int32_t mi : bk.mats) {
       if (is_fast(mi)) {
-        plan.mats[mi].scls = static_cast<int32_t>(cdiv(plan.mats[mi].m / 4, 256));
-        fast.push_back(mi);
+        const int64_t m4 = plan.mats[mi].m / 4;
+        plan.mats[mi].scls = m4 <= 128 ? 0 : static_cast<int32_t>(cdiv(m4, 256));
+        (m4 <= 128 ? narrow : fast).push_back(mi);
       } else {
         generic.push_back(mi);
       }
     }
+    auto of_narrow = [&](int32_t v) {
+      std::vector<int32_t> out;
+      for (int32_t mi : narrow)
+        if (narrow_variant(plan.mats[mi].m / 4) == v) out.push_back(mi);
+      return out;
+    };
+    // rows per narrow tile: whole workgroup rounds (256 / L rows), about `elems` elements
+    auto narrow_rows = [&](int32_t mi, int64_t elems) {
+      const int64_t rw = kBlock / (narrow_variant(plan.mats[mi].m / 4) >> 4);
+      return std::min<int64_t>(rw * std::max<int64_t>(1, elems / (int64_t(plan.mats[mi].m) * rw)),
+                               kMaxTileRows);  // the decompress stages the tile's A rows in LDS
+    };
+    const int32_t narrow_vars[4] = {narrow_variant(16), narrow_variant(32), narrow_variant(64),
+                                    narrow_variant(128)};
     auto of_class = [&](int32_t S) {
       std::vector<int32_t> v;
       for (int32_t mi : fast)
@@ -336,11 +405,19 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       Launch l = sink.begin(K_APPLY, 1);
       apply_tiles(generic, true);
       sink.end(l, L);
+      for (int32_t v : narrow_vars) {
+        const std::vector<int32_t> cls = of_narrow(v);
+        if (cls.empty()) continue;
+        l = sink.begin(K_PNARROW, v);
+        for (int32_t mi : cls) row_tiles(mi, narrow_rows(mi, class_tile(K_PNARROW, v, 2 * kTileElems)));
+        if (!vec_done) vec_tiles(bk), vec_done = true;
+        sink.end(l, L);
+      }
       for (int32_t S = 1; S <= 5; ++S) {
         const std::vector<int32_t> cls = of_class(S);
         if (cls.empty()) continue;
         l = sink.begin(K_PFUSED, S);
-        for (int32_t mi : cls) row_tiles(mi, rows_for(mi, 2 * kTileElems));
+        for (int32_t mi : cls) row_tiles(mi, rows_for(mi, class_tile(K_PFUSED, S, 2 * kTileElems)));
         if (!vec_done) vec_tiles(bk), vec_done = true;
         sink.end(l, L);
       }
@@ -352,7 +429,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         if (ef) {
           l = sink.begin(K_EUPD, 1);
           for (int32_t mi : generic)
-            row_tiles(mi, std::max<int64_t>(1, kTileElems / plan.mats[mi].m));
+            row_tiles(mi, std::max<int64_t>(1, kSmallTileElems / plan.mats[mi].m));
           sink.end(l, L);
         }
       }
@@ -375,6 +452,14 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         for (int32_t c = 0; c < d.q_chunks; ++c)
           for (int32_t cb = 0; cb < ncb; ++cb) plan.tiles.push_back(Tile{T_QTILE, mi, c, cb});
       };
+      for (int32_t v : narrow_vars) {
+        const std::vector<int32_t> cls = of_narrow(v);
+        if (cls.empty()) continue;
+        l = sink.begin(K_QNARROW, v);
+        for (int32_t mi : cls) qtiles(mi);
+        if (!vec_done) vec_tiles(bk), vec_done = true;
+        sink.end(l, L);
+      }
       for (int32_t variant : {4 | kQFused, 4, 1}) {
         l = sink.begin(K_QSTEP, variant);
         bool any = false;
@@ -405,12 +490,20 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         vec_tiles(bk);
         extra_done = true;
       };
+      for (int32_t v : narrow_vars) {
+        const std::vector<int32_t> cls = of_narrow(v);
+        if (cls.empty()) continue;
+        Launch l = sink.begin(K_RNARROW, v);
+        extra();
+        for (int32_t mi : cls) row_tiles(mi, narrow_rows(mi, class_tile(K_RNARROW, v, kTileElems)));
+        sink.end(l, L);
+      }
       for (int32_t S = 1; S <= 5; ++S) {
         const std::vector<int32_t> cls = of_class(S);
         if (cls.empty()) continue;
         Launch l = sink.begin(K_RECON4, S);
         extra();
-        for (int32_t mi : cls) row_tiles(mi, rows_for(mi, kTileElems));
+        for (int32_t mi : cls) row_tiles(mi, rows_for(mi, class_tile(K_RECON4, S, kTileElems)));
         sink.end(l, L);
       }
       for (int32_t vw : {4, 1}) {
@@ -421,7 +514,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         if (any || vw == 1) extra();
         for (int32_t mi : generic)
           if ((vw == 4) == is_vec4(mi))
-            row_tiles(mi, std::max<int64_t>(1, 2 * kTileElems / plan.mats[mi].m));
+            row_tiles(mi, std::max<int64_t>(1, 2 * kSmallTileElems / plan.mats[mi].m));
         sink.end(l, L);
       }
       {
@@ -449,12 +542,14 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     const double n = d.n, m = d.m, rr = double(r);
     switch (l.kernel) {
       case K_PFUSED:
+      case K_PNARROW:
         return t.b * m * eb + t.b * rr * 8.0 + (t.a == 0 ? m * rr * 12.0 : 0.0);
       case K_PROW:
         return m * (ef ? 8.0 : 4.0) + rr * 8.0 + (t.a == 0 ? m * rr * 12.0 : 0.0);
       case K_EUPD:
         return t.b * m * 4.0;
-      case K_QSTEP: {
+      case K_QSTEP:
+      case K_QNARROW: {
         const double r0 = double(t.a) * d.q_rows;
         const double rows = std::min<double>(d.q_rows, n - r0);
         const double cols = std::min<double>(d.q_cb, m - double(t.b) * d.q_cb);
@@ -466,6 +561,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       }
       case K_RECON:
       case K_RECON4:
+      case K_RNARROW:
         if (t.kind == T_FACT) {
           const double rows = odd ? n : m;
           return std::min<double>(d.fact_rows, rows - double(t.a) * d.fact_rows) * rr * 8.0;
@@ -500,10 +596,13 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   };
   auto family_of = [](int32_t kernel, bool odd) -> int32_t {
     switch (kernel) {
-      case K_PFUSED: case K_PROW: case K_EUPD: case K_WPSTEP: return 1;  // ACP_KERNEL_P_STEP
-      case K_QSTEP: case K_WQSTEP: return 2;                               // ACP_KERNEL_Q_STEP
-      case K_QFIN: return 3;                                               // ACP_KERNEL_Q_FINISH
-      case K_RECON: case K_RECON4: case K_WRECON: return 4;                // ACP_KERNEL_RECONSTRUCT
+      case K_PFUSED: case K_PNARROW: case K_PROW: case K_EUPD: case K_WPSTEP:
+        return 1;  // ACP_KERNEL_P_STEP
+      case K_QSTEP: case K_QNARROW: case K_WQSTEP:
+        return 2;  // ACP_KERNEL_Q_STEP
+      case K_QFIN: return 3;  // ACP_KERNEL_Q_FINISH
+      case K_RECON: case K_RECON4: case K_RNARROW: case K_WRECON:
+        return 4;  // ACP_KERNEL_RECONSTRUCT
       case K_WFACT: return 5;                                              // ACP_KERNEL_ORTH
       case K_APPLY: case K_FACT: case K_CHOL: return 5;     // ACP_KERNEL_ORTH
       case K_VEC: return odd ? 1 : 2;
@@ -531,6 +630,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   auto order_of = [](const Launch& l) -> int32_t {
     switch (l.kernel) {
       case K_APPLY: return 0;
+      case K_PNARROW: return 1;
       case K_PFUSED: return 1 + l.variant;          // 2..6
       case K_PROW: return 10;
       case K_EUPD: return 11;
@@ -538,8 +638,10 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       case K_WQSTEP: return 22;
       case K_WRECON: return 40;
       case K_WFACT: return 41;
+      case K_QNARROW: return 19;
       case K_QSTEP: return (l.variant & kQFused) ? 20 : (l.variant == 4 ? 21 : 22);
       case K_QFIN: return 23;
+      case K_RNARROW: return 30;
       case K_RECON4: return 30 + l.variant;         // 31..35
       case K_RECON: return l.variant == 4 ? 40 : 41;
       case K_CHOL: return 42;
@@ -551,8 +653,10 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     std::vector<Launch> all;
     for (int32_t b = b0; b < b1; ++b)
       for (const Launch& l : get(plan.buckets[b])) all.push_back(l);
-    std::stable_sort(all.begin(), all.end(),
-                     [&](const Launch& x, const Launch& y) { return order_of(x) < order_of(y); });
+    // sorted by kind, then variant: every (kernel, variant) of the group becomes one launch
+    std::stable_sort(all.begin(), all.end(), [&](const Launch& x, const Launch& y) {
+      return order_of(x) != order_of(y) ? order_of(x) < order_of(y) : x.variant < y.variant;
+    });
     std::vector<Launch> out;
     for (size_t i = 0; i < all.size();) {
       size_t j = i;

@@ -233,7 +233,7 @@ __global__ __launch_bounds__(kWideBlock, 2) void k_wqstep(KArgs a) {
     for (int v = 0; v < 16; ++v) part[drow(v, h) * RK + li] = q[v];
 }
 
-// Decompress: M_hat = A B^T / p over a tile (32-row block t.a, 512-column group t.b), one wave
+// Decompress: M_hat = A B^T / p over a tile (32-row block t.a, 1024-column group t.b), one wave
 // per workgroup walking the group's 32-column blocks.  Odd step: A = P_agg (factor buffer),
 // B = Qh; even step: A = Ph, B = Q_agg.  Lane l stores column c0 + l % 32 of rows
 // drow(v, l / 32): two 128-byte row segments per store.  The next block's B rows are requested

@@ -105,6 +105,19 @@ def test_ragged_shapes_all_ranks(rank):
     _assert_ok(_custom(RAGGED, rank))
 
 
+# rows of at most 512 columns (the narrow rank-4 kernels): every lane shape (16, 32, 64 lanes,
+# one or two float4 groups), ragged row counts, and a 3-element vector that leaves the factor
+# offsets after it unaligned (those matrices take the general kernels)
+NARROW = [(37, 8), (5, 12), (130, 64), (64,), (33, 128), (300, 256), (3,), (17, 500), (250, 512),
+          (41, 36), (64, 64), (9, 132), (70, 4, 2, 2)]
+
+
+@pytest.mark.parametrize("ef", [True, False])
+def test_narrow_rows(ef):
+    _require_gpu()
+    _assert_ok(_custom(NARROW, 4, ef=ef))
+
+
 def test_error_feedback_off():
     _require_gpu()
     _assert_ok(_custom(RAGGED[:6] + [(256, 64, 3, 3)], 4, ef=False))

@@ -33,6 +33,7 @@ constexpr int kMaxTileRows = 256; // rows per tile of the rank-4 row kernels (fa
 // for up to 8 row chunks, 4 threads for up to 64, 16 threads beyond
 constexpr int qfin_entries(int32_t q_chunks) { return q_chunks <= 8 ? 256 : (q_chunks <= 64 ? 64 : 16); }
 constexpr int64_t kMaxCols = int64_t(1) << 24;  // columns of a compressed matrix, at most
+constexpr int kReconRows = 8;   // rows per tile of the rank-4 decompress
 constexpr int kQRows = 128;       // rows per Q-step row chunk (at most; the chunk's Ph rows sit in LDS)
 
 struct MatDesc {
@@ -52,16 +53,44 @@ struct MatDesc {
   int32_t scls;       // column class S of the rank-4 kernels (64 S float4 groups per wave)
   int32_t bucket;     // bucket index
   int32_t fact_slices_p, fact_slices_q;  // Gram slices of the P / Q factor rows
+  int32_t q_grp;      // Q-step row chunks whose rows interleave (see q_chunk_rows)
+  int32_t pad;
 };
+
+// the planner (host compiler) and the kernels (hipcc) share the chunk geometry below
+#ifdef __HIPCC__
+#define ACP_HOST_DEVICE __host__ __device__
+#else
+#define ACP_HOST_DEVICE
+#endif
+
+// Rows of Q-step row chunk c: chunks go in groups of q_grp that share q_grp * q_rows rows (the
+// last group: its rows over q_rows, rounded up), chunk x of a group of g taking rows
+// x, x + g, x + 2g, ... of it.  q_grp = 1: chunk c is rows [c q_rows, (c + 1) q_rows).
+struct ChunkRows {
+  int64_t first;
+  int32_t stride, rows;
+};
+ACP_HOST_DEVICE inline ChunkRows q_chunk_rows(const MatDesc& d, int64_t c) {
+  const int64_t gi = c / d.q_grp;
+  const int64_t span = int64_t(d.q_grp) * d.q_rows;
+  const int64_t base = gi * span;
+  const int64_t rem = (d.n - base) < span ? (d.n - base) : span;
+  const int64_t g = (rem + d.q_rows - 1) / d.q_rows;
+  const int64_t x = c - gi * d.q_grp;
+  return ChunkRows{base + x, static_cast<int32_t>(g), static_cast<int32_t>((rem - x + g - 1) / g)};
+}
 
 struct VecDesc {
   int64_t grad_off, fac_off_p, fac_off_q, numel;
   int32_t bucket, pad;
 };
 
-enum TileKind : int32_t { T_ROWS = 0, T_FACT = 1, T_VEC = 2, T_QTILE = 3 };
+enum TileKind : int32_t { T_ROWS = 0, T_FACT = 1, T_VEC = 2, T_QTILE = 3, T_SROWS = 4 };
 
 // kind T_ROWS : idx = matrix, a = first row, b = row count
+// kind T_SROWS: idx = matrix, a = first row, b = cb | stride << 4 | count << 16: columns
+//               [1024 cb, 1024 cb + 1024) of rows a + k stride, k < count
 // kind T_FACT : idx = matrix, a = slice, b = slice count
 // kind T_VEC  : idx = vector, a = first element, b = element count
 // kind T_QTILE: idx = matrix, a = row chunk (K_QSTEP) or entry block (K_QFIN), b = column block

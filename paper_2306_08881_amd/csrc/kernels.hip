@@ -113,13 +113,16 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
   const int m4 = d.m >> 2;
   const Cols<S> cl(m4);
   const bool deferred = deferred_of(a, d.bucket);
+  // tile rows t.a + k * stride, k < rows (T_SROWS)
+  const int stride = (t.b >> 4) & 0xfff, rows = t.b >> 16;
   const uint32_t row_bytes = static_cast<uint32_t>(d.m) * 4u;
-  const uint32_t tile_bytes = static_cast<uint32_t>(t.b) * row_bytes;
+  const uint32_t step_bytes = static_cast<uint32_t>(stride) * row_bytes;
+  const uint32_t tile_bytes = static_cast<uint32_t>(rows - 1) * step_bytes + row_bytes;
   const int64_t first = static_cast<int64_t>(t.a) * d.m;
   const Rsrc G = tile_rsrc(src_of(a, d.bucket) + d.grad_off + first, tile_bytes);
   const Rsrc E = tile_rsrc(a.e + d.e_off + first, a.ef ? tile_bytes : 0u);
   const Rsrc P = tile_rsrc(dst_of(a, d.bucket) + d.fac_off_p + static_cast<int64_t>(t.a) * 4,
-                           static_cast<uint32_t>(t.b) * 16u);
+                           static_cast<uint32_t>((rows - 1) * stride + 1) * 16u);
   uint32_t coff[S];
 #pragma unroll
   for (int s = 0; s < S; ++s) coff[s] = cl.ok[s] ? static_cast<uint32_t>(cl.c4[s]) * 16u : kOut;
@@ -131,7 +134,7 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
       for (int s = 0; s < S; ++s) {
-        const uint32_t o = static_cast<uint32_t>(r0 + rb) * row_bytes + coff[s];
+        const uint32_t o = static_cast<uint32_t>(r0 + rb) * step_bytes + coff[s];
         g[rb][s] = bld4_nt(G, o);
         e[rb][s] = bld4_nt(E, o);
       }
@@ -142,8 +145,9 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
   __shared__ float4 red[2][4][RB];
   __shared__ float4 phs[kMaxTileRows];  // the tile's rows of Ph (zero unless E is deferred)
   if (tid() < 16) Wsh[tid()] = a.w[d.w_slot + tid()];
-  if (tid() < t.b)
-    phs[tid()] = deferred ? reinterpret_cast<const float4*>(a.fac + d.ph_slot)[t.a + tid()] : zero4();
+  if (tid() < rows)
+    phs[tid()] = deferred ? reinterpret_cast<const float4*>(a.fac + d.ph_slot)[t.a + static_cast<int64_t>(tid()) * stride]
+                          : zero4();
   __syncthreads();
 
   const float4* Q4 = reinterpret_cast<const float4*>(a.fac + d.q_slot);
@@ -164,7 +168,7 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
     }
 
   int buf = 0;
-  for (int r0 = 0; r0 < t.b; r0 += RB, buf ^= 1) {
+  for (int r0 = 0; r0 < rows; r0 += RB, buf ^= 1) {
     float4 mp[RB][S];
     float4 acc[RB];
 #pragma unroll
@@ -195,7 +199,7 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
     __syncthreads();
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      const uint32_t roff = static_cast<uint32_t>(r0 + rb) * row_bytes;
+      const uint32_t roff = static_cast<uint32_t>(r0 + rb) * step_bytes;
       const float4 Pr = ((red[buf][0][rb] + red[buf][1][rb]) + red[buf][2][rb]) + red[buf][3][rb];
 #pragma unroll
       for (int s = 0; s < S; ++s) {
@@ -206,7 +210,7 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
         r.w -= dot4(Pr, qh[s][3]);
         bst4_nt(E, roff + coff[s], r);
       }
-      bst4(P, tid() == 0 ? static_cast<uint32_t>(r0 + rb) * 16u : kOut, Pr);
+      bst4(P, tid() == 0 ? static_cast<uint32_t>((r0 + rb) * stride) * 16u : kOut, Pr);
     }
   }
 }
@@ -326,15 +330,16 @@ __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
   const MatDesc d = a.mats[t.idx];
   const int wave = tid() >> 6, lane = tid() & 63;
   const int64_t m = d.m;
-  const int64_t r0 = static_cast<int64_t>(t.a) * d.q_rows;
-  const int rows = static_cast<int>((r0 + d.q_rows < d.n) ? d.q_rows : d.n - r0);
+  const ChunkRows ch = q_chunk_rows(d, t.a);  // rows ch.first + k * ch.stride, k < ch.rows
+  const int64_t r0 = ch.first;
+  const int rows = ch.rows;
   const int64_t cb0 = static_cast<int64_t>(t.b) * d.q_cb;
   const int lcol = (wave * 64 + lane) * CPT;  // column within the block
   const int64_t bcols = (m - cb0) < d.q_cb ? (m - cb0) : d.q_cb;
   const bool valid = lcol < bcols;
-  const uint32_t row_bytes = static_cast<uint32_t>(m) * 4u;
+  const uint32_t step_bytes = static_cast<uint32_t>(ch.stride) * static_cast<uint32_t>(m) * 4u;
   // extent from the block's first column of the chunk's first row to its last element
-  const uint32_t ext = static_cast<uint32_t>(rows - 1) * row_bytes + static_cast<uint32_t>(bcols) * 4u;
+  const uint32_t ext = static_cast<uint32_t>(rows - 1) * step_bytes + static_cast<uint32_t>(bcols) * 4u;
   const int64_t first = r0 * m + cb0;
   const Rsrc G = tile_rsrc(src_of(a, d.bucket) + d.grad_off + first, ext);
   const Rsrc E = tile_rsrc(a.e + d.e_off + first, a.ef ? ext : 0u);
@@ -346,7 +351,7 @@ __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
   auto load_group = [&](int rr, Vec* gg, Vec* ee) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const uint32_t o = static_cast<uint32_t>(rr + u) * row_bytes + coff;
+      const uint32_t o = static_cast<uint32_t>(rr + u) * step_bytes + coff;
       if constexpr (CPT == 4) {
         gg[u] = bld4_nt(G, o);
         ee[u] = bld4_nt(E, o);
@@ -365,7 +370,7 @@ __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
     if (tid() < kQRows) {
       float4 y = zero4();
       if (tid() < rows) {
-        const int64_t row = r0 + tid();
+        const int64_t row = r0 + static_cast<int64_t>(tid()) * ch.stride;
         y = apply_w4(*reinterpret_cast<const float4*>(a.fac + d.p_slot + row * 4), Wsh);
         if (t.b == 0) *reinterpret_cast<float4*>(a.fac + d.ph_slot + row * 4) = y;
       }
@@ -373,7 +378,7 @@ __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
     }
   } else {
     for (int i = tid(); i < kQRows * RK; i += kBlock)
-      phs[i] = i < rows * RK ? a.fac[d.ph_slot + r0 * RK + i] : 0.f;
+      phs[i] = i < rows * RK ? a.fac[d.ph_slot + (r0 + static_cast<int64_t>(i / RK) * ch.stride) * RK + i % RK] : 0.f;
   }
   __syncthreads();
 
@@ -391,7 +396,7 @@ __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
     for (int u = 0; u < U; ++u) f[u] = g[u] + e[u];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const uint32_t o = static_cast<uint32_t>(rr + u) * row_bytes + coff;
+      const uint32_t o = static_cast<uint32_t>(rr + u) * step_bytes + coff;
       if constexpr (CPT == 4)
         bst4_nt(E, o, f[u]);
       else
@@ -539,13 +544,14 @@ __global__ __launch_bounds__(kBlock) void k_recon(KArgs a) {
   }
 }
 
-// Decompress, r = 4: each lane keeps the rank-4 rows of B for its columns in registers and
-// writes M_hat rows, RB rows at a time, with tile-relative buffer stores (plain stores: they
-// measured faster than nontemporal ones for this write-only stream).  Factor tiles and
-// vectors as in k_recon.
-template <int S>
+// Decompress, r = 4: a row tile covers one block of 1024 columns (256 float4 groups, lane
+// `lane` of wave w owns group 64 w + lane) of kReconRows rows taken with a stride (T_SROWS).  The
+// planner orders the tiles so that workgroups launched together write adjacent whole rows: a
+// small write footprint per workgroup with a dense band of rows across the running ones streams
+// faster than long per-workgroup row blocks.  Each lane keeps the rank-4 rows of B for its
+// columns in registers; stores are plain tile-relative buffer stores (they measured faster than
+// nontemporal ones for this write-only stream).  Factor tiles and vectors as in k_recon.
 __global__ __launch_bounds__(kBlock) void k_recon4(KArgs a) {
-  constexpr int RB = Cols<S>::RB;
   const Tile t = a.tiles[blockIdx.x];
   const bool odd = a.parity != 0;
   if (t.kind == T_VEC) {
@@ -559,40 +565,34 @@ __global__ __launch_bounds__(kBlock) void k_recon4(KArgs a) {
     fact_tile<4>(a, t, src, dst, odd ? d.n : d.m);
     return;
   }
+  const int cb = t.b & 15, stride = (t.b >> 4) & 0xfff, rows = t.b >> 16;
   const int m4 = d.m >> 2;
-  const Cols<S> cl(m4);
+  const int g4 = (tid() >> 6) * 64 + (tid() & 63);  // float4 group within the block
+  const int c4 = cb * 256 + g4;
+  const bool ok = c4 < m4;
   const float* agg = src_of(a, d.bucket);
   const float4* A4 = reinterpret_cast<const float4*>(odd ? agg + d.fac_off_p : a.fac + d.ph_slot);
   const float4* B4 = reinterpret_cast<const float4*>(odd ? a.fac + d.qh_slot : agg + d.fac_off_q);
-  __shared__ float4 as[kMaxTileRows];  // the tile's rows of A, scaled by 1 / p
-  if (tid() < t.b) as[tid()] = scale4(A4[t.a + tid()], a.inv_p);
-  float4 b[S][4];
+  __shared__ float4 as[kReconRows];  // the tile's rows of A, scaled by 1 / p
+  if (tid() < rows) as[tid()] = scale4(A4[t.a + static_cast<int64_t>(tid()) * stride], a.inv_p);
+  float4 b[4];
 #pragma unroll
-  for (int s = 0; s < S; ++s)
-#pragma unroll
-    for (int c = 0; c < 4; ++c) b[s][c] = cl.ok[s] ? B4[4 * cl.c4[s] + c] : zero4();
+  for (int c = 0; c < 4; ++c) b[c] = ok ? B4[4 * c4 + c] : zero4();
   __syncthreads();
-  // the B rows are in registers before the store loop, so no wait for them lands inside it
+  // the B rows are in registers before the stores, so no wait for them lands between them
   __builtin_amdgcn_s_waitcnt(0);
   const uint32_t row_bytes = static_cast<uint32_t>(d.m) * 4u;
-  const Rsrc O = tile_rsrc(dst_of(a, d.bucket) + d.grad_off + static_cast<int64_t>(t.a) * d.m,
-                           static_cast<uint32_t>(t.b) * row_bytes);
-  uint32_t coff[S];
+  const uint32_t step_bytes = static_cast<uint32_t>(stride) * row_bytes;  // between tile rows
+  const int cols = (d.m - cb * 1024) < 1024 ? (d.m - cb * 1024) : 1024;
+  const Rsrc O = tile_rsrc(dst_of(a, d.bucket) + d.grad_off + static_cast<int64_t>(t.a) * d.m + cb * 1024,
+                           static_cast<uint32_t>(rows - 1) * step_bytes + static_cast<uint32_t>(cols) * 4u);
+  const uint32_t coff = ok ? static_cast<uint32_t>(g4) * 16u : kOut;
+  // rows past the tile's count read unset LDS entries; their stores fall outside the resource
 #pragma unroll
-  for (int s = 0; s < S; ++s) coff[s] = cl.ok[s] ? static_cast<uint32_t>(cl.c4[s]) * 16u : kOut;
-  // rows past the tile (last round) read unset LDS entries; their stores are dropped
-  for (int r0 = 0; r0 < t.b; r0 += RB) {
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      const float4 ar = as[(r0 + rb) & (kMaxTileRows - 1)];
-      const uint32_t roff = static_cast<uint32_t>(r0 + rb) * row_bytes;
-#pragma unroll
-      for (int s = 0; s < S; ++s) {
-        const float4 o = make_float4(dot4(ar, b[s][0]), dot4(ar, b[s][1]), dot4(ar, b[s][2]),
-                                     dot4(ar, b[s][3]));
-        bst4(O, roff + coff[s], o);
-      }
-    }
+  for (int k = 0; k < kReconRows; ++k) {
+    const float4 ar = as[k];
+    const float4 o = make_float4(dot4(ar, b[0]), dot4(ar, b[1]), dot4(ar, b[2]), dot4(ar, b[3]));
+    bst4(O, static_cast<uint32_t>(k) * step_bytes + coff, o);
   }
 }
 
@@ -922,13 +922,6 @@ __global__ __launch_bounds__(kBlock) void k_vec(KArgs a) {
   vec_tile(a, t, true);
 }
 
-template <int S>
-void launch_s(bool pstep, dim3 grid, dim3 block, hipStream_t s, const KArgs& args) {
-  if (pstep)
-    hipLaunchKernelGGL(k_pfused<S>, grid, block, 0, s, args);
-  else
-    hipLaunchKernelGGL(k_recon4<S>, grid, block, 0, s, args);
-}
 
 template <int RK>
 hipError_t launch_rank(const Launch& l, const KArgs& args, hipStream_t s) {
@@ -967,17 +960,22 @@ hipError_t launch_rank(const Launch& l, const KArgs& args, hipStream_t s) {
         hipLaunchKernelGGL((k_recon<RK, 1>), grid, block, 0, s, args);
       break;
     case K_PFUSED:
-    case K_RECON4:
       if constexpr (RK == 4) {
-        const bool p = l.kernel == K_PFUSED;
         switch (l.variant) {
-          case 1: launch_s<1>(p, grid, block, s, args); break;
-          case 2: launch_s<2>(p, grid, block, s, args); break;
-          case 3: launch_s<3>(p, grid, block, s, args); break;
-          case 4: launch_s<4>(p, grid, block, s, args); break;
-          case 5: launch_s<5>(p, grid, block, s, args); break;
+          case 1: hipLaunchKernelGGL(k_pfused<1>, grid, block, 0, s, args); break;
+          case 2: hipLaunchKernelGGL(k_pfused<2>, grid, block, 0, s, args); break;
+          case 3: hipLaunchKernelGGL(k_pfused<3>, grid, block, 0, s, args); break;
+          case 4: hipLaunchKernelGGL(k_pfused<4>, grid, block, 0, s, args); break;
+          case 5: hipLaunchKernelGGL(k_pfused<5>, grid, block, 0, s, args); break;
           default: return hipErrorInvalidValue;
         }
+        break;
+      } else {
+        return hipErrorInvalidValue;
+      }
+    case K_RECON4:
+      if constexpr (RK == 4) {
+        hipLaunchKernelGGL(k_recon4, grid, block, 0, s, args);
         break;
       } else {
         return hipErrorInvalidValue;

@@ -25,6 +25,8 @@ constexpr int64_t kTileElems = 16384;   // gradient elements per streaming tile 
 constexpr int64_t kSmallTileElems = 2048;  // per tile of the general P-step E update and decompress
 constexpr int64_t kTargetTiles = 1024;     // workgroups a launch class aims for (4 per CU)
 constexpr int64_t kMinTileElems = 2048;    // smallest tile of a class that has few elements
+constexpr int64_t kPGroup = 8;            // P-step tiles whose rows interleave (rank 4)
+constexpr int64_t kQGroup = 8;            // Q-step row chunks whose rows interleave (rank 4)
 constexpr int64_t kVecChunk = 4096;     // raw-vector elements per copy tile
 constexpr int64_t kApplyRows = 256;     // factor rows per orthogonalisation tile
 constexpr int64_t kSlotAlign = 64;      // floats (256 bytes)
@@ -138,7 +140,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       c = {{{K_PNARROW, v}, {K_QNARROW, v}, {K_RNARROW, v}}};
     } else {
       const int32_t S = static_cast<int32_t>(cdiv(m / 4, 256));
-      c = {{{K_PFUSED, S}, {K_QSTEP, 4 | kQFused}, {K_RECON4, S}}};
+      c = {{{K_PFUSED, S}, {K_QSTEP, 4 | kQFused}, {K_RECON4, 0}}};
     }
     return c;
   };
@@ -212,6 +214,9 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         const int64_t want = class_tile(qc.first, qc.second, int64_t(kQRows) * cols) / cols;
         d.q_rows = std::min<int32_t>(d.q_rows, static_cast<int32_t>(std::max<int64_t>(16, want / 16 * 16)));
       }
+      // the register-resident rank-4 Q-step interleaves the rows of kQGroup chunks (offsets of a
+      // chunk stay below 2^31: at most kQGroup * kQRows rows of at most 5120 columns)
+      d.q_grp = (!wide && fast && t.m / 4 > 128) ? static_cast<int32_t>(kQGroup) : 1;
       d.q_chunks = static_cast<int32_t>(cdiv(t.n, d.q_rows));
       const int64_t ncb = cdiv(t.m, d.q_cb);
       d.qpart = qpart;
@@ -267,6 +272,37 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     for (int64_t s = 0; s < d.n; s += rows_per_tile)
       plan.tiles.push_back(Tile{T_ROWS, mi, static_cast<int32_t>(s),
                                 static_cast<int32_t>(std::min<int64_t>(rows_per_tile, d.n - s))});
+  };
+  // rank-4 decompress tiles: 1024-column blocks of kReconRows rows.  Rows go in groups of
+  // gr * kReconRows (gr = 8 / column blocks, at least 1); the tiles of a group take rows
+  // x, x + gr, x + 2 gr, ... (x < gr) and are ordered (x, block), so that tiles that run together
+  // write whole adjacent rows.
+  auto recon4_tiles = [&](int32_t mi) {
+    const MatDesc& d = plan.mats[mi];
+    const int64_t nb = cdiv(d.m, 1024);
+    const int64_t gr = std::max<int64_t>(1, 8 / nb);
+    for (int64_t g0 = 0; g0 < d.n; g0 += gr * kReconRows) {
+      const int64_t end = std::min<int64_t>(d.n, g0 + gr * kReconRows);
+      for (int64_t x = 0; x < gr && g0 + x < end; ++x) {
+        const int64_t cnt = cdiv(end - g0 - x, gr);
+        for (int64_t cb = 0; cb < nb; ++cb)
+          plan.tiles.push_back(Tile{T_SROWS, mi, static_cast<int32_t>(g0 + x),
+                                    static_cast<int32_t>(cb | (gr << 4) | (cnt << 16))});
+      }
+    }
+  };
+  // rank-4 P-step tiles of rows_per_tile rows: groups of kPGroup tiles share kPGroup *
+  // rows_per_tile rows, tile x of a group taking rows x, x + g, x + 2g, ... of it (g tiles in the
+  // group, kPGroup except in the last one)
+  auto pstep_tiles = [&](int32_t mi, int64_t rows_per_tile) {
+    const MatDesc& d = plan.mats[mi];
+    for (int64_t g0 = 0; g0 < d.n; g0 += kPGroup * rows_per_tile) {
+      const int64_t rem = std::min<int64_t>(d.n - g0, kPGroup * rows_per_tile);
+      const int64_t g = cdiv(rem, rows_per_tile);
+      for (int64_t x = 0; x < g; ++x)
+        plan.tiles.push_back(Tile{T_SROWS, mi, static_cast<int32_t>(g0 + x),
+                                  static_cast<int32_t>((g << 4) | (cdiv(rem - x, g) << 16))});
+    }
   };
   auto is_vec4 = [&](int32_t mi) {
     const MatDesc& d = plan.mats[mi];
@@ -417,7 +453,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         const std::vector<int32_t> cls = of_class(S);
         if (cls.empty()) continue;
         l = sink.begin(K_PFUSED, S);
-        for (int32_t mi : cls) row_tiles(mi, rows_for(mi, class_tile(K_PFUSED, S, 2 * kTileElems)));
+        for (int32_t mi : cls) pstep_tiles(mi, rows_for(mi, class_tile(K_PFUSED, S, 2 * kTileElems)));
         if (!vec_done) vec_tiles(bk), vec_done = true;
         sink.end(l, L);
       }
@@ -498,12 +534,10 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         for (int32_t mi : cls) row_tiles(mi, narrow_rows(mi, class_tile(K_RNARROW, v, kTileElems)));
         sink.end(l, L);
       }
-      for (int32_t S = 1; S <= 5; ++S) {
-        const std::vector<int32_t> cls = of_class(S);
-        if (cls.empty()) continue;
-        Launch l = sink.begin(K_RECON4, S);
+      if (!fast.empty()) {
+        Launch l = sink.begin(K_RECON4, 0);
         extra();
-        for (int32_t mi : cls) row_tiles(mi, rows_for(mi, class_tile(K_RECON4, S, kTileElems)));
+        for (int32_t mi : fast) recon4_tiles(mi);
         sink.end(l, L);
       }
       for (int32_t vw : {4, 1}) {
@@ -541,7 +575,10 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     const MatDesc& d = plan.mats[t.idx];
     const double n = d.n, m = d.m, rr = double(r);
     switch (l.kernel) {
-      case K_PFUSED:
+      case K_PFUSED: {
+        const double rows = t.b >> 16;
+        return rows * m * eb + rows * rr * 8.0 + (t.a == 0 ? m * rr * 12.0 : 0.0);
+      }
       case K_PNARROW:
         return t.b * m * eb + t.b * rr * 8.0 + (t.a == 0 ? m * rr * 12.0 : 0.0);
       case K_PROW:
@@ -550,8 +587,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         return t.b * m * 4.0;
       case K_QSTEP:
       case K_QNARROW: {
-        const double r0 = double(t.a) * d.q_rows;
-        const double rows = std::min<double>(d.q_rows, n - r0);
+        const double rows = q_chunk_rows(d, t.a).rows;
         const double cols = std::min<double>(d.q_cb, m - double(t.b) * d.q_cb);
         return rows * cols * eb + (t.b == 0 ? rows * rr * 8.0 : 0.0);
       }
@@ -565,6 +601,10 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         if (t.kind == T_FACT) {
           const double rows = odd ? n : m;
           return std::min<double>(d.fact_rows, rows - double(t.a) * d.fact_rows) * rr * 8.0;
+        }
+        if (t.kind == T_SROWS) {
+          const double rows = t.b >> 16, cols = std::min<double>(1024.0, m - 1024.0 * (t.b & 15));
+          return rows * cols * 4.0 + rows * rr * 4.0 + (t.a == 0 ? cols * rr * 4.0 : 0.0);
         }
         return t.b * m * 4.0 + t.b * rr * 4.0 + (t.a == 0 ? m * rr * 4.0 : 0.0);
       case K_WPSTEP:
@@ -642,7 +682,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       case K_QSTEP: return (l.variant & kQFused) ? 20 : (l.variant == 4 ? 21 : 22);
       case K_QFIN: return 23;
       case K_RNARROW: return 30;
-      case K_RECON4: return 30 + l.variant;         // 31..35
+      case K_RECON4: return 31;
       case K_RECON: return l.variant == 4 ? 40 : 41;
       case K_CHOL: return 42;
       case K_VEC: return 50;

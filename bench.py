@@ -97,11 +97,11 @@ TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profile
 
 
 def kernel_source_hash() -> str:
-    """Fingerprint of the sources the rank-4 kernels are compiled from."""
+    """Fingerprint of the kernel sources and of the planner that sets their tiles and launches."""
     import hashlib
     csrc = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2306_08881_amd", "csrc")
     h = hashlib.sha256()
-    for f in ("kernels.hip", "device.hpp", "acp_internal.hpp"):
+    for f in ("kernels.hip", "wide.hip", "device.hpp", "acp_internal.hpp", "plan.cpp"):
         h.update(open(os.path.join(csrc, f), "rb").read())
     return h.hexdigest()[:16]
 

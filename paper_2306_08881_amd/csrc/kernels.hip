@@ -364,6 +364,7 @@ __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
   load_group(0, g, e);
 
   // the chunk's Ph rows; the rows after them are zero (groups may run past the chunk)
+  static_assert(kQRows <= kBlock && kQRows % 8 == 0, "one thread per staged Ph row");
   if constexpr (FUSED) {
     if (tid() < 16) Wsh[tid()] = a.w[d.w_slot + tid()];
     __syncthreads();

@@ -263,6 +263,21 @@ def main():
         torch.cuda.synchronize()
         return start.elapsed_time(end) / steps
 
+    def per_step(steps, mode, flush=None):
+        """Per-step times (ms): HIP events around each step on the caller's stream; `flush`, when
+        given, runs between steps outside the events."""
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(steps)]
+        torch.cuda.synchronize()
+        for e0, e1 in ev:
+            if flush is not None:
+                flush()
+            e0.record(main)
+            one_step(mode)
+            e1.record(main)
+        torch.cuda.synchronize()
+        return np.array([e0.elapsed_time(e1) for e0, e1 in ev])
+
     other = "bucket" if args.mode == "all" else "all"
     for _ in range(args.warmup):
         one_step(args.mode)
@@ -271,6 +286,14 @@ def main():
     steps = args.steps + (args.steps % 2)
     ms = timed(steps, args.mode)
     ms_other = timed(steps, other) if args.compare else None
+
+    # per-step statistics (a pass of its own, so the timed region above holds no extra events):
+    # every step, P-steps (odd t) and Q-steps apart; then the same with the 256 MB last-level
+    # (MALL) cache flushed before each step by an untimed 512 MB fill
+    t_step = per_step(steps, args.mode)
+    scratch = torch.empty(1 << 27, dtype=torch.float32, device=dev)
+    t_flush = per_step(steps, args.mode, flush=lambda: scratch.fill_(1.0))
+    del scratch
 
     # per-kernel pass: the same steps again with every launch of one kernel family bracketed by
     # HIP events on its own stream (acp_profile_*), once per family
@@ -318,6 +341,12 @@ def main():
                      "kernel": dom, "avg_launch_us": round(dk["avg_launch_us"], 3),
                      "bytes_per_launch": round(dk["bytes_per_launch"], 1)},
     }
+    res["config"]["step_ms"] = {"mean": round(float(t_step.mean()), 4), "std": round(float(t_step.std()), 4),
+                                "median": round(float(np.median(t_step)), 4),
+                                "p_step_mean": round(float(t_step[0::2].mean()), 4),
+                                "q_step_mean": round(float(t_step[1::2].mean()), 4)}
+    res["config"]["mall_flushed"] = {"mean_ms": round(float(t_flush.mean()), 4),
+                                     "gbs": round(step_bytes / (float(t_flush.mean()) * 1e-3) / 1e9, 2)}
     if ms_other is not None:
         res["config"][f"ms_per_step_{other}_mode"] = round(ms_other, 4)
         res["config"][f"gbs_{other}_mode"] = round(step_bytes / (ms_other * 1e-3) / 1e9, 2)

@@ -125,6 +125,21 @@ acp_status acp_layout(const acp_ctx *ctx, int32_t b, int32_t *tensor_ids, int64_
 acp_status acp_tensor_info(const acp_ctx *ctx, int32_t tensor_id, int32_t *compressed, int64_t *n,
                            int64_t *m, int32_t *bucket);
 
+/*
+ * acp_fusion_groups - compressed-buffer fusion (Section IV-B, "Buffer Size"): what a step sends
+ * (which = ACP_FACTOR_P: each compressed tensor's P factor, n x r, as on P-steps;
+ * ACP_FACTOR_Q: its Q factor, m x r, as on Q-steps; the raw gradient of every other tensor on
+ * both) grouped like the gradient buckets, whole tensors in backward (reverse registration)
+ * order, with the bucket cap scaled by that step's compression rate (elements sent over gradient
+ * elements).  A group closes once its bytes reach the scaled cap.  group_of (num_tensors entries
+ * in registration order, or NULL) receives each tensor's group, 0 being the first group in
+ * backward order; *num_groups the number of groups.  Host metadata only: it tells a caller that
+ * all-reduces fused factor buffers which tensors travel together; acp_compress and
+ * acp_decompress keep one factor buffer per gradient bucket.  ACP_E_INVALID for a NULL ctx or
+ * num_groups or another `which`.
+ */
+acp_status acp_fusion_groups(const acp_ctx *ctx, int32_t which, int32_t *group_of, int32_t *num_groups);
+
 /* Host copy of the initial factor P_0 (which = ACP_FACTOR_P, n*r floats) or Q_0 (m*r floats). */
 acp_status acp_init_factor(const acp_ctx *ctx, int32_t tensor_id, int32_t which, float *host_out,
                            int64_t count);

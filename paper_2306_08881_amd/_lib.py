@@ -45,6 +45,7 @@ SIGNATURES = {
     "acp_bucket_info": (_i32, [_p, _i32, _pi32, _pi64, _pi64, _pi64]),
     "acp_layout": (_i32, [_p, _i32, _pi32, _pi64, _pi64, _pi64, _pi32]),
     "acp_tensor_info": (_i32, [_p, _i32, _pi32, _pi64, _pi64, _pi32]),
+    "acp_fusion_groups": (_i32, [_p, _i32, _pi32, _pi32]),
     "acp_init_factor": (_i32, [_p, _i32, _i32, _pf, _i64]),
     "acp_compress": (_i32, [_p, _i64, _i32, _pf, _pf, _p]),
     "acp_decompress": (_i32, [_p, _i64, _i32, _pf, _pf, _p]),

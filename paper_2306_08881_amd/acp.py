@@ -100,6 +100,16 @@ class Acp:
                self.lib, self.ctx, "acp_tensor_info")
         return bool(c.value), n.value, m.value, b.value
 
+    def fusion_groups(self, which: str):
+        """Compressed-buffer fusion groups of a P-step ('P') or Q-step ('Q'): (group index of
+        every tensor in registration order, number of groups)."""
+        g = np.zeros(len(self.shapes), np.int32)
+        ng = C.c_int32()
+        _check(self.lib.acp_fusion_groups(self.ctx, L.ACP_FACTOR_P if which == "P" else L.ACP_FACTOR_Q,
+                                          g.ctypes.data_as(C.POINTER(C.c_int32)), C.byref(ng)),
+               self.lib, self.ctx, "acp_fusion_groups")
+        return g, ng.value
+
     def init_factor(self, tid: int, which: str) -> np.ndarray:
         comp, n, m, _ = self.tensor_info(tid)
         rows = n if which == "P" else m

@@ -260,6 +260,37 @@ acp_status acp_tensor_info(const acp_ctx* c, int32_t tensor_id, int32_t* compres
   return ACP_OK;
 }
 
+acp_status acp_fusion_groups(const acp_ctx* c, int32_t which, int32_t* group_of, int32_t* num_groups) {
+  if (!c) return ACP_E_INVALID;
+  if (which != ACP_FACTOR_P && which != ACP_FACTOR_Q) return fail(c, ACP_E_INVALID, "bad factor");
+  if (!num_groups) return fail(c, ACP_E_INVALID, "num_groups is NULL");
+  const std::vector<acp::TensorPlan>& T = c->plan.tensors;
+  // elements tensor t contributes to the step's sent buffer
+  auto sent = [&](const acp::TensorPlan& t) -> int64_t {
+    if (!t.compressed) return t.numel;
+    return (which == ACP_FACTOR_P ? t.n : t.m) * c->plan.rank;
+  };
+  int64_t total = 0, numel = 0;
+  for (const acp::TensorPlan& t : T) {
+    total += sent(t);
+    numel += t.numel;
+  }
+  const double rate = static_cast<double>(total) / static_cast<double>(numel);
+  const double cap = static_cast<double>(c->plan.cap_bytes) * rate;
+  int32_t g = 0;
+  int64_t bytes = 0;
+  for (size_t k = T.size(); k-- > 0;) {
+    if (group_of) group_of[k] = g;
+    bytes += sent(T[k]) * 4;
+    if (static_cast<double>(bytes) >= cap) {
+      ++g;
+      bytes = 0;
+    }
+  }
+  *num_groups = g + (bytes > 0 ? 1 : 0);
+  return ACP_OK;
+}
+
 acp_status acp_init_factor(const acp_ctx* c, int32_t tensor_id, int32_t which, float* host_out,
                            int64_t count) {
   if (!c) return ACP_E_INVALID;

@@ -186,3 +186,80 @@ def test_ef_off_has_no_error_arena(lib):
     assert va.value - vb.value >= 256 * 576 * 4
     lib.acp_destroy(a)
     lib.acp_destroy(b)
+
+
+def _fusion(lib, ctx, which, count):
+    g = np.zeros(count, np.int32)
+    ng = C.c_int32()
+    assert lib.acp_fusion_groups(ctx, which, g.ctypes.data_as(C.POINTER(C.c_int32)), C.byref(ng)) == 0
+    return g, ng.value
+
+
+def _as_groups(group_of, ng):
+    """Group lists (tensor indices in backward order), as the oracle gives them."""
+    out = [[] for _ in range(ng)]
+    for i in reversed(range(len(group_of))):
+        out[group_of[i]].append(i)
+    return out
+
+
+@pytest.mark.parametrize("name", sorted(sg.WORKLOADS))
+def test_fusion_groups_match_oracle(lib, name):
+    """Compressed-buffer fusion groups (cap scaled by each step's rate) equal the oracle's."""
+    wl = sg.WORKLOADS[name]
+    shapes = [p.shape for p in wl.params]
+    st, ctx = _ctx(lib, shapes, wl.rank)
+    assert st == 0
+    try:
+        gp, gq = OL.compressed_fusion_groups(OL.plan(shapes, wl.rank, wl.cap_bytes))
+        for which, ref in ((L.ACP_FACTOR_P, gp), (L.ACP_FACTOR_Q, gq)):
+            g, ng = _fusion(lib, ctx, which, len(shapes))
+            assert _as_groups(g, ng) == ref
+    finally:
+        lib.acp_destroy(ctx)
+
+
+def test_fusion_groups_resnet50_four_and_four(lib):
+    """ResNet-50 at r = 4 and the 25 MB default: 4 P buffers and 4 Q buffers (Section IV-B)."""
+    shapes = [p.shape for p in sg.resnet50()]
+    st, ctx = _ctx(lib, shapes, 4)
+    assert st == 0
+    try:
+        assert _fusion(lib, ctx, L.ACP_FACTOR_P, len(shapes))[1] == 4
+        assert _fusion(lib, ctx, L.ACP_FACTOR_Q, len(shapes))[1] == 4
+    finally:
+        lib.acp_destroy(ctx)
+
+
+@pytest.mark.parametrize("cap_mib", [0, 1, 5, 25, 50, 100, 200, 400, 800, 1500])
+def test_fusion_groups_buffer_size_sweep(lib, cap_mib):
+    """The buffer-size sweep of Section V (0 to 1500 MB): gradient buckets and both fusion
+    groupings agree with the oracle at every cap; the sweep's 0 is a 1-byte cap (the library
+    rejects 0), which puts every tensor in a group of its own."""
+    shapes = [p.shape for p in sg.bert_base()]
+    cap = max(1, cap_mib << 20)
+    st, ctx = _ctx(lib, shapes, 4, cap=cap)
+    assert st == 0
+    try:
+        ref = OL.plan(shapes, 4, cap)
+        assert lib.acp_num_buckets(ctx) == len(ref.buckets)
+        gp, gq = OL.compressed_fusion_groups(ref)
+        for which, rg in ((L.ACP_FACTOR_P, gp), (L.ACP_FACTOR_Q, gq)):
+            g, ng = _fusion(lib, ctx, which, len(shapes))
+            assert _as_groups(g, ng) == rg
+            if cap_mib == 0:
+                assert ng == len(shapes)
+    finally:
+        lib.acp_destroy(ctx)
+
+
+def test_fusion_groups_errors(lib):
+    st, ctx = _ctx(lib, [(8, 8)], 2)
+    assert st == 0
+    try:
+        ng = C.c_int32()
+        assert lib.acp_fusion_groups(ctx, 7, None, C.byref(ng)) == L.ACP_E_INVALID
+        assert lib.acp_fusion_groups(ctx, L.ACP_FACTOR_P, None, None) == L.ACP_E_INVALID
+        assert lib.acp_fusion_groups(ctx, L.ACP_FACTOR_P, None, C.byref(ng)) == 0 and ng.value == 1
+    finally:
+        lib.acp_destroy(ctx)

@@ -26,6 +26,7 @@ constexpr int64_t kSmallTileElems = 2048;  // per tile of the general P-step E u
 constexpr int64_t kTargetTiles = 1024;     // workgroups a launch class aims for (4 per CU)
 constexpr int64_t kMinTileElems = 2048;    // smallest tile of a class that has few elements
 constexpr int64_t kPGroup = 8;            // P-step tiles whose rows interleave (rank 4)
+constexpr int64_t kPMinRows = 8;          // fewest rows of a P-step tile (rank 4)
 constexpr int64_t kQGroup = 8;            // Q-step row chunks whose rows interleave (rank 4)
 constexpr int64_t kVecChunk = 4096;     // raw-vector elements per copy tile
 constexpr int64_t kApplyRows = 256;     // factor rows per orthogonalisation tile
@@ -453,7 +454,11 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         const std::vector<int32_t> cls = of_class(S);
         if (cls.empty()) continue;
         l = sink.begin(K_PFUSED, S);
-        for (int32_t mi : cls) pstep_tiles(mi, rows_for(mi, class_tile(K_PFUSED, S, 2 * kTileElems)));
+        // rows of 4 KB: 32K elements per tile; rows of 12 KB and more: 64K
+        const int64_t base = (S >= 4 ? 4 : 2) * kTileElems;
+        for (int32_t mi : cls)
+          pstep_tiles(mi, rows_for(mi, std::max<int64_t>(kPMinRows * plan.mats[mi].m,
+                                                          class_tile(K_PFUSED, S, base))));
         if (!vec_done) vec_tiles(bk), vec_done = true;
         sink.end(l, L);
       }

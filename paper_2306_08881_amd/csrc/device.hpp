@@ -232,35 +232,66 @@ __device__ void gram_rows(const float* X, int64_t r0, int64_t r1, double* G, flo
     }
     __syncthreads();
   } else {
+    // G in 4 x 4 blocks: thread t owns block t % NB of the NB = (RK / 4)^2 blocks for the rows
+    // of phase t / NB (rows congruent to the phase modulo NP = 256 / NB within a chunk); the
+    // chunk's rows sit in LDS as doubles.  The phases' sums are added in phase order.
     constexpr int CH = 64;
-    constexpr int NQ = (RK * RK + kBlock - 1) / kBlock;
-    __shared__ float xs[CH * RK];
-    if (copy)
-      for (int64_t e = r0 * RK + tid(); e < r1 * RK; e += kBlock) copy[e] = X[e];
-    double acc[NQ];
+    constexpr int NB4 = RK / 4, NB = NB4 * NB4, NP = kBlock / NB;
+    static_assert(NB * NP == kBlock, "blocks times phases must fill the workgroup");
+    constexpr int PT = CH * RK / kBlock;  // chunk elements per thread
+    constexpr int SH = (CH * RK > NP * RK * RK) ? CH * RK : NP * RK * RK;
+    __shared__ __align__(16) double sh[SH];  // chunk rows, then the phases' partial sums
+    const int b = tid() % NB, ph = tid() / NB;
+    const int bi = 4 * (b / NB4), bj = 4 * (b % NB4);
+    double acc[4][4];
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) acc[q] = 0.0;
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) acc[u][v] = 0.0;
+    // the next chunk is requested before the current one's products (rows past r1 read zero)
+    const int64_t end = r1 * RK;
+    float nx[PT];
+    auto fetch = [&](int64_t c0) {
+#pragma unroll
+      for (int k = 0; k < PT; ++k) {
+        const int64_t e = c0 * RK + tid() + k * kBlock;
+        nx[k] = e < end ? X[e] : 0.f;
+      }
+    };
+    fetch(r0);
     for (int64_t c0 = r0; c0 < r1; c0 += CH) {
-      const int64_t cn = (r1 - c0) < CH ? (r1 - c0) : CH;
-      for (int e = tid(); e < cn * RK; e += kBlock) xs[e] = X[c0 * RK + e];
-      __syncthreads();
+      const int cn = static_cast<int>((r1 - c0) < CH ? (r1 - c0) : CH);
 #pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        const int e = tid() + q * kBlock;
-        if (e < RK * RK) {
-          const int i = e / RK, j = e % RK;
-          double s = acc[q];
-          for (int rr = 0; rr < cn; ++rr)
-            s = fma(static_cast<double>(xs[rr * RK + i]), static_cast<double>(xs[rr * RK + j]), s);
-          acc[q] = s;
+      for (int k = 0; k < PT; ++k) {
+        const int e = tid() + k * kBlock;
+        sh[e] = static_cast<double>(nx[k]);
+        if (copy && c0 * RK + e < end) copy[c0 * RK + e] = nx[k];
+      }
+      __syncthreads();
+      fetch(c0 + CH);
+      for (int rr = ph; rr < cn; rr += NP) {
+        double xi[4], xj[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          xi[u] = sh[rr * RK + bi + u];
+          xj[u] = sh[rr * RK + bj + u];
         }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) acc[u][v] = fma(xi[u], xj[v], acc[u][v]);
       }
       __syncthreads();
     }
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      const int e = tid() + q * kBlock;
-      if (e < RK * RK) G[e] = acc[q];
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) sh[ph * RK * RK + (bi + u) * RK + bj + v] = acc[u][v];
+    __syncthreads();
+    for (int e = tid(); e < RK * RK; e += kBlock) {
+      double g = sh[e];
+      for (int q = 1; q < NP; ++q) g += sh[q * RK * RK + e];
+      G[e] = g;
     }
     __syncthreads();
   }

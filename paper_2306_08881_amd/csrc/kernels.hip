@@ -37,8 +37,17 @@ __global__ __launch_bounds__(kBlock) void k_chol(KArgs a) {
   __shared__ double G[RK * RK];
   const double* gp = a.gpart + d.gpart;
   for (int e = tid(); e < RK * RK; e += kBlock) {
+    // eight slices' partials requested together, added in slice order
     double s = 0.0;
-    for (int sl = 0; sl < t.b; ++sl) s += gp[static_cast<int64_t>(sl) * RK * RK + e];
+    int sl = 0;
+    for (; sl + 8 <= t.b; sl += 8) {
+      double v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = gp[static_cast<int64_t>(sl + u) * RK * RK + e];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; sl < t.b; ++sl) s += gp[static_cast<int64_t>(sl) * RK * RK + e];
     G[e] = s;
   }
   __syncthreads();
@@ -59,14 +68,34 @@ __global__ __launch_bounds__(kBlock) void k_apply(KArgs a) {
   const float* X = a.fac + (q ? d.q_slot : d.p_slot) + row * RK;
   float* Y = a.fac + (q ? d.qh_slot : d.ph_slot) + row * RK;
   double x[RK];
+  float y[RK];
+  if constexpr (RK % 4 == 0) {  // factor slots are 256-byte aligned: rows are 16-byte aligned
 #pragma unroll
-  for (int l = 0; l < RK; ++l) x[l] = static_cast<double>(X[l]);
+    for (int l = 0; l < RK; l += 4) {
+      const float4 v = *reinterpret_cast<const float4*>(X + l);
+      x[l] = v.x;
+      x[l + 1] = v.y;
+      x[l + 2] = v.z;
+      x[l + 3] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int l = 0; l < RK; ++l) x[l] = static_cast<double>(X[l]);
+  }
 #pragma unroll
   for (int k = 0; k < RK; ++k) {
     double s = 0.0;
 #pragma unroll
     for (int l = 0; l <= k; ++l) s = fma(x[l], W[l * RK + k], s);
-    Y[k] = static_cast<float>(s);
+    y[k] = static_cast<float>(s);
+  }
+  if constexpr (RK % 4 == 0) {
+#pragma unroll
+    for (int k = 0; k < RK; k += 4)
+      *reinterpret_cast<float4*>(Y + k) = make_float4(y[k], y[k + 1], y[k + 2], y[k + 3]);
+  } else {
+#pragma unroll
+    for (int k = 0; k < RK; ++k) Y[k] = y[k];
   }
 }
 
@@ -436,10 +465,11 @@ __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
 }
 
 // Q-step finish: Q_loc = sum over the row chunks' partials.  A tile covers the NE entries
-// [t.a * NE, t.a * NE + NE) of the matrix (entry e = column * r + rank, NE = qfin_entries) with
-// 256 / NE threads per entry.  Each thread adds a contiguous share of the chunks in chunk
-// order and the shares are added in thread order.  The result goes to the factor buffer and to
-// the Ql slot.
+// [t.a * NE, t.a * NE + NE) of the matrix (entry e = column * r + rank, NE = qfin_entries):
+// with NE > 256 each thread takes NE / 256 entries 256 apart, otherwise 256 / NE threads share
+// an entry.  Each thread adds a contiguous share of the chunks in chunk order, eight chunks
+// requested at a time, and the shares are added in thread order.  The result goes to the factor
+// buffer and to the Ql slot.
 template <int RK>
 __global__ __launch_bounds__(kBlock) void k_qfin(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
@@ -448,6 +478,40 @@ __global__ __launch_bounds__(kBlock) void k_qfin(KArgs a) {
   const int64_t ncb = (m + d.q_cb - 1) / d.q_cb;
   const int64_t stride = ncb * d.q_cb * RK;  // one row chunk of partials
   const int ne = qfin_entries(d.q_chunks);   // entries per tile
+  const float* part = a.qpart + d.qpart;
+  float* out = dst_of(a, d.bucket) + d.fac_off_q;
+  float* ql = a.fac + d.ql_slot;
+  constexpr int U = 8;
+  if (ne > kBlock) {  // at most 8 chunks: one thread per entry
+    constexpr int EPT = 4;  // entries per thread (ne = 1024)
+    float s[EPT];
+    int64_t e[EPT];
+#pragma unroll
+    for (int k = 0; k < EPT; ++k) {
+      e[k] = static_cast<int64_t>(t.a) * ne + tid() + k * kBlock;
+      s[k] = 0.f;
+    }
+    for (int ch = 0; ch < d.q_chunks; ch += 2) {
+      float v[EPT][2];
+#pragma unroll
+      for (int k = 0; k < EPT; ++k)
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+          v[k][u] = (e[k] < m * RK && ch + u < d.q_chunks) ? part[(ch + u) * stride + e[k]] : 0.f;
+#pragma unroll
+      for (int k = 0; k < EPT; ++k) {
+        s[k] += v[k][0];
+        if (ch + 1 < d.q_chunks) s[k] += v[k][1];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < EPT; ++k)
+      if (e[k] < m * RK) {
+        out[e[k]] = s[k];
+        ql[e[k]] = s[k];
+      }
+    return;
+  }
   const int ng = kBlock / ne;                // threads per entry
   const int gq = tid() / ne, el = tid() % ne;
   const int64_t e = static_cast<int64_t>(t.a) * ne + el;
@@ -456,8 +520,7 @@ __global__ __launch_bounds__(kBlock) void k_qfin(KArgs a) {
   const int ch0 = gq * per, ch1 = (ch0 + per < d.q_chunks) ? ch0 + per : d.q_chunks;
   float s = 0.f;
   if (on) {
-    const float* base = a.qpart + d.qpart + e;
-    constexpr int U = 8;
+    const float* base = part + e;
     int ch = ch0;
     for (; ch + U <= ch1; ch += U) {
       float v[U];
@@ -468,21 +531,14 @@ __global__ __launch_bounds__(kBlock) void k_qfin(KArgs a) {
     }
     for (; ch < ch1; ++ch) s += base[ch * stride];
   }
-  if (ng == 1) {
-    if (on) {
-      dst_of(a, d.bucket)[d.fac_off_q + e] = s;
-      a.fac[d.ql_slot + e] = s;
-    }
-    return;
-  }
   __shared__ float red[kBlock];
   red[tid()] = s;
   __syncthreads();
   if (gq == 0 && on) {
     float tot = red[el];
     for (int g = 1; g < ng; ++g) tot += red[g * ne + el];
-    dst_of(a, d.bucket)[d.fac_off_q + e] = tot;
-    a.fac[d.ql_slot + e] = tot;
+    out[e] = tot;
+    ql[e] = tot;
   }
 }
 
@@ -550,8 +606,9 @@ __global__ __launch_bounds__(kBlock) void k_recon(KArgs a) {
 // planner orders the tiles so that workgroups launched together write adjacent whole rows: a
 // small write footprint per workgroup with a dense band of rows across the running ones streams
 // faster than long per-workgroup row blocks.  Each lane keeps the rank-4 rows of B for its
-// columns in registers; stores are plain tile-relative buffer stores (they measured faster than
-// nontemporal ones for this write-only stream).  Factor tiles and vectors as in k_recon.
+// columns in registers; stores are nontemporal tile-relative buffer stores: plain stores leave
+// M_hat's lines dirty in the caches and the next step's kernels pay for writing them back.
+// Factor tiles and vectors as in k_recon.
 __global__ __launch_bounds__(kBlock) void k_recon4(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   const bool odd = a.parity != 0;
@@ -593,7 +650,7 @@ __global__ __launch_bounds__(kBlock) void k_recon4(KArgs a) {
   for (int k = 0; k < kReconRows; ++k) {
     const float4 ar = as[k];
     const float4 o = make_float4(dot4(ar, b[0]), dot4(ar, b[1]), dot4(ar, b[2]), dot4(ar, b[3]));
-    bst4(O, static_cast<uint32_t>(k) * step_bytes + coff, o);
+    bst4_nt(O, static_cast<uint32_t>(k) * step_bytes + coff, o);
   }
 }
 
@@ -903,7 +960,7 @@ __global__ __launch_bounds__(kBlock) void k_rnarrow(KArgs a) {
     const uint32_t roff = static_cast<uint32_t>(row) * row_bytes;
 #pragma unroll
     for (int g = 0; g < G; ++g)
-      bst4(O, coff[g] == kOut ? kOut : roff + coff[g],
+      bst4_nt(O, coff[g] == kOut ? kOut : roff + coff[g],
            make_float4(dot4(ar, b[g][0]), dot4(ar, b[g][1]), dot4(ar, b[g][2]), dot4(ar, b[g][3])));
   }
 }

@@ -236,8 +236,9 @@ __global__ __launch_bounds__(kWideBlock, 2) void k_wqstep(KArgs a) {
 // Decompress: M_hat = A B^T / p over a tile (32-row block t.a, 1024-column group t.b), one wave
 // per workgroup walking the group's 32-column blocks.  Odd step: A = P_agg (factor buffer),
 // B = Qh; even step: A = Ph, B = Q_agg.  Lane l stores column c0 + l % 32 of rows
-// drow(v, l / 32): two 128-byte row segments per store.  The next block's B rows are requested
-// before the current block's MFMAs.
+// drow(v, l / 32): two 128-byte row segments per nontemporal store (plain stores leave M_hat's
+// lines dirty in the caches, and the next step's kernels pay for writing them back).  The next
+// block's B rows are requested before the current block's MFMAs.
 template <int RK>
 __global__ __launch_bounds__(kWideBlock) void k_wrecon(KArgs a) {
   constexpr int KH = RK / 2;
@@ -280,7 +281,7 @@ __global__ __launch_bounds__(kWideBlock) void k_wrecon(KArgs a) {
     const uint32_t coff = li < w ? u32(li) * 4u : kOut;
 #pragma unroll
     for (int v = 0; v < 16; ++v)
-      bst1(Or, coff == kOut ? kOut : u32(drow(v, h)) * row_bytes + coff, o[v]);
+      bst1_nt(Or, coff == kOut ? kOut : u32(drow(v, h)) * row_bytes + coff, o[v]);
   }
 }
 

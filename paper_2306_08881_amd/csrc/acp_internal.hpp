@@ -33,7 +33,7 @@ constexpr int kMaxTileRows = 256; // rows per tile of the rank-4 row kernels (fa
 // for up to 8 row chunks, 4 threads for up to 64, 16 threads beyond
 constexpr int qfin_entries(int32_t q_chunks) { return q_chunks <= 8 ? 1024 : (q_chunks <= 64 ? 64 : 16); }
 constexpr int64_t kMaxCols = int64_t(1) << 24;  // columns of a compressed matrix, at most
-constexpr int kReconRows = 8;   // rows per tile of the rank-4 decompress
+constexpr int kReconRows = 4;   // rows per tile of the rank-4 decompress
 constexpr int kQRows = 256;       // rows per Q-step row chunk (at most; the chunk's Ph rows sit in LDS)
 
 struct MatDesc {

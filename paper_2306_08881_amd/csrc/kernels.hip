@@ -349,7 +349,7 @@ __global__ __launch_bounds__(kBlock) void k_emat(KArgs a) {
 // K_QFIN (lanes past m store zeros into the padded partial block).
 template <int RK, int CPT, bool FUSED>
 __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
-  constexpr int U = CPT == 4 ? 4 : 8;  // rows per group
+  constexpr int U = 8;  // rows per group
   using Vec = typename std::conditional<CPT == 4, float4, float>::type;
   const Tile t = a.tiles[blockIdx.x];
   if (t.kind == T_VEC) {

@@ -115,9 +115,11 @@ enum KernelId : int32_t {
   K_WQSTEP,      // Q-step, ranks 8..32 (MFMA): F = M' written, per-chunk partials of F^T Ph
   K_WRECON,      // decompress, ranks 8..32 (MFMA): M_hat = A B^T / p
   K_WFACT,       // decompress, ranks 8..32: factor tiles and vectors / p
-  K_PNARROW,     // P-step, r = 4, rows of at most 512 columns: whole rows per wave
-  K_QNARROW,     // Q-step, r = 4, rows of at most 512 columns
-  K_RNARROW,     // decompress, r = 4, rows of at most 512 columns; factor tiles; vectors / p
+  // tile-size classes of the rank-4 narrow-row tiles (rows of at most 512 columns: several rows
+  // per wave); they run inside the K_PFUSED (S = 1), fused K_QSTEP and K_RECON4 launches
+  K_PNARROW,
+  K_QNARROW,
+  K_RNARROW,
 };
 
 // Narrow rows (r = 4, m / 4 = m4 <= 128 float4 groups): L lanes per row (16, 32 or 64), G float4

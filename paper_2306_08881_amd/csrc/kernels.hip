@@ -100,6 +100,321 @@ __global__ __launch_bounds__(kBlock) void k_apply(KArgs a) {
 }
 
 // ---------------------------------------------------------------------------------------
+// Narrow rows (r = 4, 16-byte aligned rows of at most 512 columns): L lanes per row (16, 32 or
+// 64), G float4 groups per lane (1 or 2).  A wave holds 64 / L whole rows at a time and the
+// workgroup 256 / L; lane l of row slot l / L owns groups (l % L) + L g, whose factor rows stay
+// in registers.  Row sums stay inside the wave, so these kernels wait at no barrier per row.
+template <int L, int G>
+struct Narrow {
+  static constexpr int SL = 64 / L;   // rows per wave at a time
+  static constexpr int RW = 4 * SL;   // rows per workgroup round
+  int wave, slot, cl;
+  int c4[G];
+  bool ok[G];
+  __device__ explicit Narrow(int m4) {
+    wave = __builtin_amdgcn_readfirstlane(tid() >> 6);
+    const int lane = tid() & 63;
+    slot = lane / L;
+    cl = lane % L;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      c4[g] = cl + L * g;
+      ok[g] = c4[g] < m4;
+    }
+  }
+  __device__ int row(int k) const { return k * RW + wave * SL + slot; }  // tile-relative row of round k
+};
+
+// Sum over the L lanes of a row slot; every lane of the slot gets the same bits.  DPP quad
+// butterflies and mirrors give 16-lane sums, a swizzle (xor 16) pairs them for L = 32, and for
+// L = 64 the four 16-lane sums are read out and added in order.
+template <int L>
+__device__ inline float row_sum(float v) {
+  v += dpp<0xB1>(v);
+  v += dpp<0x4E>(v);
+  v += dpp<0x141>(v);
+  v += dpp<0x140>(v);
+  if constexpr (L == 32)
+    v += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x401F));
+  if constexpr (L == 64) {
+    const int b = __builtin_bit_cast(int, v);
+    v = ((__builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 0)) +
+          __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 16))) +
+         __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 32))) +
+        __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 48));
+  }
+  return v;
+}
+template <int L>
+__device__ inline float4 row_sum4(const float4& v) {
+  return make_float4(row_sum<L>(v.x), row_sum<L>(v.y), row_sum<L>(v.z), row_sum<L>(v.w));
+}
+
+// The lane's Qh rows (Q W) and Q_loc rows for its columns; the tile holding row 0 stores Qh.
+template <int L, int G>
+__device__ inline void narrow_qfactors(const KArgs& a, const MatDesc& d, const Narrow<L, G>& nm,
+                                       const double* Wsh, bool store_qh, bool deferred,
+                                       float4 (&qh)[G][4], float4 (&ql)[G][4]) {
+  const float4* Q4 = reinterpret_cast<const float4*>(a.fac + d.q_slot);
+  const float4* Ql4 = reinterpret_cast<const float4*>(a.fac + d.ql_slot);
+  float4* Qh4 = reinterpret_cast<float4*>(a.fac + d.qh_slot);
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int j = 4 * (nm.ok[g] ? nm.c4[g] : 0) + c;  // in-range row for lanes past m
+      const float4 q = apply_w4(Q4[j], Wsh);
+      const float4 l = Ql4[j];
+      qh[g][c] = nm.ok[g] ? q : zero4();
+      ql[g][c] = (nm.ok[g] && deferred) ? l : zero4();
+      if (store_qh && nm.ok[g]) Qh4[j] = q;
+    }
+}
+
+// P-step, narrow rows: per row M' = M + E (or M + F - Ph_row Q_loc^T), P = M' Qh (row sum),
+// E = M' - P Qh^T, P to the factor buffer.  U rounds of rows are in flight per lane.  Wsh: 16
+// doubles of shared memory.
+template <int L, int G>
+__device__ void pnarrow_tile(const KArgs& a, const Tile& t, const MatDesc& d, double* Wsh) {
+  using NM = Narrow<L, G>;
+  constexpr int U = 2;
+  const NM nm(d.m >> 2);
+  const bool deferred = deferred_of(a, d.bucket);
+  const uint32_t row_bytes = static_cast<uint32_t>(d.m) * 4u;
+  const uint32_t tile_bytes = static_cast<uint32_t>(t.b) * row_bytes;
+  const int64_t first = static_cast<int64_t>(t.a) * d.m;
+  const Rsrc Gr = tile_rsrc(src_of(a, d.bucket) + d.grad_off + first, tile_bytes);
+  const Rsrc Er = tile_rsrc(a.e + d.e_off + first, a.ef ? tile_bytes : 0u);
+  const Rsrc Pr = tile_rsrc(dst_of(a, d.bucket) + d.fac_off_p + static_cast<int64_t>(t.a) * 4,
+                            static_cast<uint32_t>(t.b) * 16u);
+  const Rsrc Phr = tile_rsrc(a.fac + d.ph_slot + static_cast<int64_t>(t.a) * 4,
+                             deferred ? static_cast<uint32_t>(t.b) * 16u : 0u);
+  uint32_t coff[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) coff[g] = nm.ok[g] ? static_cast<uint32_t>(nm.c4[g]) * 16u : kOut;
+
+  float4 gv[U][G], ev[U][G], ph[U];
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t row = static_cast<uint32_t>(nm.row(k0 + u));  // past the tile: zeros
+      const uint32_t roff = row * row_bytes;
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const uint32_t o = coff[g] == kOut ? kOut : roff + coff[g];
+        gv[u][g] = bld4_nt(Gr, o);
+        ev[u][g] = bld4_nt(Er, o);
+      }
+      ph[u] = bld4(Phr, row * 16u);
+    }
+  };
+  load(0);
+  if (tid() < 16) Wsh[tid()] = a.w[d.w_slot + tid()];
+  __syncthreads();
+  float4 qh[G][4], ql[G][4];
+  narrow_qfactors(a, d, nm, Wsh, t.a == 0 && nm.wave == 0 && nm.slot == 0, deferred, qh, ql);
+
+  for (int k = 0; k * NM::RW < t.b; k += U) {
+    float4 mp[U][G], acc[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      acc[u] = zero4();
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float4 v = gv[u][g] + ev[u][g];
+        v.x -= dot4(ph[u], ql[g][0]);
+        v.y -= dot4(ph[u], ql[g][1]);
+        v.z -= dot4(ph[u], ql[g][2]);
+        v.w -= dot4(ph[u], ql[g][3]);
+        mp[u][g] = v;
+        acc[u] = fma4(v.x, qh[g][0], acc[u]);
+        acc[u] = fma4(v.y, qh[g][1], acc[u]);
+        acc[u] = fma4(v.z, qh[g][2], acc[u]);
+        acc[u] = fma4(v.w, qh[g][3], acc[u]);
+      }
+    }
+    load(k + U);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float4 P = row_sum4<L>(acc[u]);
+      const uint32_t row = static_cast<uint32_t>(nm.row(k + u));
+      const uint32_t roff = row * row_bytes;
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float4 r = mp[u][g];
+        r.x -= dot4(P, qh[g][0]);
+        r.y -= dot4(P, qh[g][1]);
+        r.z -= dot4(P, qh[g][2]);
+        r.w -= dot4(P, qh[g][3]);
+        bst4_nt(Er, coff[g] == kOut ? kOut : roff + coff[g], r);
+      }
+      bst4(Pr, nm.cl == 0 ? row * 16u : kOut, P);
+    }
+  }
+}
+
+// Q-step, narrow rows (r = 4, fused orthogonalisation): tile = row chunk t.a.  The chunk's Ph
+// rows are formed in LDS as P W (and stored to the Ph slot); per row F = M + E is written back
+// and each lane adds F^T Ph over its rows and columns.  The 256 / L row slots' sums are added in
+// slot order through LDS and stored as the chunk's partials for K_QFIN.  Shared memory: Wsh (16
+// doubles), phs (kQRows float4), red (kNarrowRed float4).
+constexpr int kNarrowRed = 2048;  // float4: row slots x L G 4 at most (4 x 64 x 2 x 4)
+template <int L, int G>
+__device__ void qnarrow_tile(const KArgs& a, const Tile& t, const MatDesc& d, double* Wsh, float4* phs,
+                             float4* red) {
+  using NM = Narrow<L, G>;
+  constexpr int U = 2;
+  constexpr int NS = 4 * NM::SL;  // row slots of the workgroup
+  static_assert(NS * L * G * 4 <= kNarrowRed, "slot sums exceed the shared buffer");
+  const int m4 = d.m >> 2;
+  const NM nm(m4);
+  const int64_t r0 = static_cast<int64_t>(t.a) * d.q_rows;
+  const int rows = static_cast<int>((r0 + d.q_rows < d.n) ? d.q_rows : d.n - r0);
+  const uint32_t row_bytes = static_cast<uint32_t>(d.m) * 4u;
+  const uint32_t ext = static_cast<uint32_t>(rows) * row_bytes;
+  const int64_t first = r0 * d.m;
+  const Rsrc Gr = tile_rsrc(src_of(a, d.bucket) + d.grad_off + first, ext);
+  const Rsrc Er = tile_rsrc(a.e + d.e_off + first, a.ef ? ext : 0u);
+  uint32_t coff[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) coff[g] = nm.ok[g] ? static_cast<uint32_t>(nm.c4[g]) * 16u : kOut;
+
+  float4 gv[U][G], ev[U][G];
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t roff = static_cast<uint32_t>(nm.row(k0 + u)) * row_bytes;
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const uint32_t o = coff[g] == kOut ? kOut : roff + coff[g];
+        gv[u][g] = bld4_nt(Gr, o);
+        ev[u][g] = bld4_nt(Er, o);
+      }
+    }
+  };
+  load(0);
+  if (tid() < 16) Wsh[tid()] = a.w[d.w_slot + tid()];
+  __syncthreads();
+  if (tid() < kQRows) {
+    float4 y = zero4();
+    if (tid() < rows) {
+      const int64_t row = r0 + tid();
+      y = apply_w4(reinterpret_cast<const float4*>(a.fac + d.p_slot)[row], Wsh);
+      reinterpret_cast<float4*>(a.fac + d.ph_slot)[row] = y;
+    }
+    phs[tid()] = y;
+  }
+  __syncthreads();
+
+  float4 acc[G][4];
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[g][c] = zero4();
+  for (int k = 0; k * NM::RW < rows; k += U) {
+    float4 f[U][G];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int g = 0; g < G; ++g) f[u][g] = gv[u][g] + ev[u][g];
+    load(k + U);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int row = nm.row(k + u);  // < kQRows: rows <= kQRows and 2 RW divides kQRows
+      const uint32_t roff = static_cast<uint32_t>(row) * row_bytes;
+      const float4 ph = phs[row & (kQRows - 1)];
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        bst4_nt(Er, coff[g] == kOut ? kOut : roff + coff[g], f[u][g]);
+        acc[g][0] = fma4(f[u][g].x, ph, acc[g][0]);
+        acc[g][1] = fma4(f[u][g].y, ph, acc[g][1]);
+        acc[g][2] = fma4(f[u][g].z, ph, acc[g][2]);
+        acc[g][3] = fma4(f[u][g].w, ph, acc[g][3]);
+      }
+    }
+  }
+  const int sidx = nm.wave * NM::SL + nm.slot;
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) red[sidx * (L * G * 4) + (nm.cl * G + g) * 4 + c] = acc[g][c];
+  __syncthreads();
+  const int64_t ncb = (d.m + d.q_cb - 1) / d.q_cb;
+  float4* part = reinterpret_cast<float4*>(a.qpart + d.qpart + static_cast<int64_t>(t.a) * ncb * d.q_cb * 4);
+  for (int e = tid(); e < L * G * 4; e += kBlock) {
+    const int cl = e / (G * 4), g = (e / 4) % G, c = e % 4;
+    const int col4 = cl + L * g;
+    if (col4 >= m4) continue;
+    float4 sum = red[e];
+    for (int sl = 1; sl < NS; ++sl) sum = sum + red[sl * (L * G * 4) + e];
+    part[4 * col4 + c] = sum;  // Q partial of column 4 col4 + c, ranks 0..3
+  }
+}
+
+// Decompress, narrow rows: M_hat rows from the tile's A rows (staged in LDS, scaled by 1 / p)
+// and the lane's B rows in registers.  as: kMaxTileRows float4 of shared memory.
+template <int L, int G>
+__device__ void rnarrow_tile(const KArgs& a, const Tile& t, const MatDesc& d, float4* as) {
+  using NM = Narrow<L, G>;
+  const bool odd = a.parity != 0;
+  const NM nm(d.m >> 2);
+  const float* agg = src_of(a, d.bucket);
+  const float4* A4 = reinterpret_cast<const float4*>(odd ? agg + d.fac_off_p : a.fac + d.ph_slot);
+  const float4* B4 = reinterpret_cast<const float4*>(odd ? a.fac + d.qh_slot : agg + d.fac_off_q);
+  if (tid() < t.b) as[tid()] = scale4(A4[t.a + tid()], a.inv_p);  // the tile's A rows / p
+  float4 b[G][4];
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) b[g][c] = nm.ok[g] ? B4[4 * nm.c4[g] + c] : zero4();
+  __syncthreads();
+  __builtin_amdgcn_s_waitcnt(0);
+  const uint32_t row_bytes = static_cast<uint32_t>(d.m) * 4u;
+  const Rsrc O = tile_rsrc(dst_of(a, d.bucket) + d.grad_off + static_cast<int64_t>(t.a) * d.m,
+                           static_cast<uint32_t>(t.b) * row_bytes);
+  uint32_t coff[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) coff[g] = nm.ok[g] ? static_cast<uint32_t>(nm.c4[g]) * 16u : kOut;
+  for (int k = 0; k * NM::RW < t.b; ++k) {
+    const int row = nm.row(k);  // past the tile: an unset LDS entry, its stores are dropped
+    const float4 ar = as[row & (kMaxTileRows - 1)];
+    const uint32_t roff = static_cast<uint32_t>(row) * row_bytes;
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+      bst4_nt(O, coff[g] == kOut ? kOut : roff + coff[g],
+           make_float4(dot4(ar, b[g][0]), dot4(ar, b[g][1]), dot4(ar, b[g][2]), dot4(ar, b[g][3])));
+  }
+}
+
+// Narrow-row tiles of a matrix (at most 128 float4 groups per row) inside the rank-4 P-step,
+// Q-step and decompress launches: the variant follows from the row length.
+__device__ inline void narrow_pstep(const KArgs& a, const Tile& t, const MatDesc& d, double* Wsh) {
+  switch (narrow_variant(d.m >> 2)) {
+    case (16 << 4) | 1: pnarrow_tile<16, 1>(a, t, d, Wsh); break;
+    case (32 << 4) | 1: pnarrow_tile<32, 1>(a, t, d, Wsh); break;
+    case (64 << 4) | 1: pnarrow_tile<64, 1>(a, t, d, Wsh); break;
+    default: pnarrow_tile<64, 2>(a, t, d, Wsh); break;
+  }
+}
+__device__ inline void narrow_qstep(const KArgs& a, const Tile& t, const MatDesc& d, double* Wsh,
+                                    float4* phs, float4* red) {
+  switch (narrow_variant(d.m >> 2)) {
+    case (16 << 4) | 1: qnarrow_tile<16, 1>(a, t, d, Wsh, phs, red); break;
+    case (32 << 4) | 1: qnarrow_tile<32, 1>(a, t, d, Wsh, phs, red); break;
+    case (64 << 4) | 1: qnarrow_tile<64, 1>(a, t, d, Wsh, phs, red); break;
+    default: qnarrow_tile<64, 2>(a, t, d, Wsh, phs, red); break;
+  }
+}
+__device__ inline void narrow_recon(const KArgs& a, const Tile& t, const MatDesc& d, float4* as) {
+  switch (narrow_variant(d.m >> 2)) {
+    case (16 << 4) | 1: rnarrow_tile<16, 1>(a, t, d, as); break;
+    case (32 << 4) | 1: rnarrow_tile<32, 1>(a, t, d, as); break;
+    case (64 << 4) | 1: rnarrow_tile<64, 1>(a, t, d, as); break;
+    default: rnarrow_tile<64, 2>(a, t, d, as); break;
+  }
+}
+
+// ---------------------------------------------------------------------------------------
 // Column mapping shared by the rank-4 streaming kernels.  The four waves of a workgroup split
 // a row of m4 = m / 4 float4 groups into four segments of 64 S groups; lane `lane` of wave w
 // owns groups w * 64 S + s * 64 + lane, s < S, for every row of the tile, so the factor rows
@@ -139,6 +454,13 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
     return;
   }
   const MatDesc d = a.mats[t.idx];
+  if constexpr (S == 1) {
+    if (t.kind == T_ROWS) {  // a narrow-row matrix's tile (the S = 1 launch carries them)
+      __shared__ double Wn[16];
+      narrow_pstep(a, t, d, Wn);
+      return;
+    }
+  }
   const int m4 = d.m >> 2;
   const Cols<S> cl(m4);
   const bool deferred = deferred_of(a, d.bucket);
@@ -357,6 +679,15 @@ __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
     return;
   }
   const MatDesc d = a.mats[t.idx];
+  __shared__ double Wsh[16];
+  __shared__ __align__(16) float phs[kQRows * RK];
+  if constexpr (FUSED) {
+    if (d.scls == 0) {  // a narrow-row matrix's chunk (the fused launch carries them)
+      __shared__ float4 red[kNarrowRed];
+      narrow_qstep(a, t, d, Wsh, reinterpret_cast<float4*>(phs), red);
+      return;
+    }
+  }
   const int wave = tid() >> 6, lane = tid() & 63;
   const int64_t m = d.m;
   const ChunkRows ch = q_chunk_rows(d, t.a);  // rows ch.first + k * ch.stride, k < ch.rows
@@ -374,8 +705,6 @@ __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
   const Rsrc E = tile_rsrc(a.e + d.e_off + first, a.ef ? ext : 0u);
   const uint32_t coff = valid ? static_cast<uint32_t>(lcol) * 4u : kOut;
 
-  __shared__ double Wsh[16];
-  __shared__ __align__(16) float phs[kQRows * RK];
   Vec g[U], e[U];
   auto load_group = [&](int rr, Vec* gg, Vec* ee) {
 #pragma unroll
@@ -623,6 +952,11 @@ __global__ __launch_bounds__(kBlock) void k_recon4(KArgs a) {
     fact_tile<4>(a, t, src, dst, odd ? d.n : d.m);
     return;
   }
+  if (t.kind == T_ROWS) {  // a narrow-row matrix's tile
+    __shared__ float4 asn[kMaxTileRows];
+    narrow_recon(a, t, d, asn);
+    return;
+  }
   const int cb = t.b & 15, stride = (t.b >> 4) & 0xfff, rows = t.b >> 16;
   const int m4 = d.m >> 2;
   const int g4 = (tid() >> 6) * 64 + (tid() & 63);  // float4 group within the block
@@ -652,327 +986,6 @@ __global__ __launch_bounds__(kBlock) void k_recon4(KArgs a) {
     const float4 o = make_float4(dot4(ar, b[0]), dot4(ar, b[1]), dot4(ar, b[2]), dot4(ar, b[3]));
     bst4_nt(O, static_cast<uint32_t>(k) * step_bytes + coff, o);
   }
-}
-
-// ---------------------------------------------------------------------------------------
-// Narrow rows (r = 4, 16-byte aligned rows of at most 512 columns): L lanes per row (16, 32 or
-// 64), G float4 groups per lane (1 or 2).  A wave holds 64 / L whole rows at a time and the
-// workgroup 256 / L; lane l of row slot l / L owns groups (l % L) + L g, whose factor rows stay
-// in registers.  Row sums stay inside the wave, so these kernels wait at no barrier per row.
-template <int L, int G>
-struct Narrow {
-  static constexpr int SL = 64 / L;   // rows per wave at a time
-  static constexpr int RW = 4 * SL;   // rows per workgroup round
-  int wave, slot, cl;
-  int c4[G];
-  bool ok[G];
-  __device__ explicit Narrow(int m4) {
-    wave = __builtin_amdgcn_readfirstlane(tid() >> 6);
-    const int lane = tid() & 63;
-    slot = lane / L;
-    cl = lane % L;
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      c4[g] = cl + L * g;
-      ok[g] = c4[g] < m4;
-    }
-  }
-  __device__ int row(int k) const { return k * RW + wave * SL + slot; }  // tile-relative row of round k
-};
-
-// Sum over the L lanes of a row slot; every lane of the slot gets the same bits.  DPP quad
-// butterflies and mirrors give 16-lane sums, a swizzle (xor 16) pairs them for L = 32, and for
-// L = 64 the four 16-lane sums are read out and added in order.
-template <int L>
-__device__ inline float row_sum(float v) {
-  v += dpp<0xB1>(v);
-  v += dpp<0x4E>(v);
-  v += dpp<0x141>(v);
-  v += dpp<0x140>(v);
-  if constexpr (L == 32)
-    v += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x401F));
-  if constexpr (L == 64) {
-    const int b = __builtin_bit_cast(int, v);
-    v = ((__builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 0)) +
-          __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 16))) +
-         __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 32))) +
-        __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 48));
-  }
-  return v;
-}
-template <int L>
-__device__ inline float4 row_sum4(const float4& v) {
-  return make_float4(row_sum<L>(v.x), row_sum<L>(v.y), row_sum<L>(v.z), row_sum<L>(v.w));
-}
-
-// The lane's Qh rows (Q W) and Q_loc rows for its columns; the tile holding row 0 stores Qh.
-template <int L, int G>
-__device__ inline void narrow_qfactors(const KArgs& a, const MatDesc& d, const Narrow<L, G>& nm,
-                                       const double* Wsh, bool store_qh, bool deferred,
-                                       float4 (&qh)[G][4], float4 (&ql)[G][4]) {
-  const float4* Q4 = reinterpret_cast<const float4*>(a.fac + d.q_slot);
-  const float4* Ql4 = reinterpret_cast<const float4*>(a.fac + d.ql_slot);
-  float4* Qh4 = reinterpret_cast<float4*>(a.fac + d.qh_slot);
-#pragma unroll
-  for (int g = 0; g < G; ++g)
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int j = 4 * (nm.ok[g] ? nm.c4[g] : 0) + c;  // in-range row for lanes past m
-      const float4 q = apply_w4(Q4[j], Wsh);
-      const float4 l = Ql4[j];
-      qh[g][c] = nm.ok[g] ? q : zero4();
-      ql[g][c] = (nm.ok[g] && deferred) ? l : zero4();
-      if (store_qh && nm.ok[g]) Qh4[j] = q;
-    }
-}
-
-// P-step, narrow rows: per row M' = M + E (or M + F - Ph_row Q_loc^T), P = M' Qh (row sum),
-// E = M' - P Qh^T, P to the factor buffer.  U rounds of rows are in flight per lane.
-template <int L, int G>
-__global__ __launch_bounds__(kBlock) void k_pnarrow(KArgs a) {
-  using NM = Narrow<L, G>;
-  constexpr int U = 2;
-  const Tile t = a.tiles[blockIdx.x];
-  if (t.kind == T_VEC) {
-    vec_tile(a, t, true);
-    return;
-  }
-  const MatDesc d = a.mats[t.idx];
-  const NM nm(d.m >> 2);
-  const bool deferred = deferred_of(a, d.bucket);
-  const uint32_t row_bytes = static_cast<uint32_t>(d.m) * 4u;
-  const uint32_t tile_bytes = static_cast<uint32_t>(t.b) * row_bytes;
-  const int64_t first = static_cast<int64_t>(t.a) * d.m;
-  const Rsrc Gr = tile_rsrc(src_of(a, d.bucket) + d.grad_off + first, tile_bytes);
-  const Rsrc Er = tile_rsrc(a.e + d.e_off + first, a.ef ? tile_bytes : 0u);
-  const Rsrc Pr = tile_rsrc(dst_of(a, d.bucket) + d.fac_off_p + static_cast<int64_t>(t.a) * 4,
-                            static_cast<uint32_t>(t.b) * 16u);
-  const Rsrc Phr = tile_rsrc(a.fac + d.ph_slot + static_cast<int64_t>(t.a) * 4,
-                             deferred ? static_cast<uint32_t>(t.b) * 16u : 0u);
-  uint32_t coff[G];
-#pragma unroll
-  for (int g = 0; g < G; ++g) coff[g] = nm.ok[g] ? static_cast<uint32_t>(nm.c4[g]) * 16u : kOut;
-
-  float4 gv[U][G], ev[U][G], ph[U];
-  auto load = [&](int k0) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const uint32_t row = static_cast<uint32_t>(nm.row(k0 + u));  // past the tile: zeros
-      const uint32_t roff = row * row_bytes;
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        const uint32_t o = coff[g] == kOut ? kOut : roff + coff[g];
-        gv[u][g] = bld4_nt(Gr, o);
-        ev[u][g] = bld4_nt(Er, o);
-      }
-      ph[u] = bld4(Phr, row * 16u);
-    }
-  };
-  load(0);
-  __shared__ double Wsh[16];
-  if (tid() < 16) Wsh[tid()] = a.w[d.w_slot + tid()];
-  __syncthreads();
-  float4 qh[G][4], ql[G][4];
-  narrow_qfactors(a, d, nm, Wsh, t.a == 0 && nm.wave == 0 && nm.slot == 0, deferred, qh, ql);
-
-  for (int k = 0; k * NM::RW < t.b; k += U) {
-    float4 mp[U][G], acc[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      acc[u] = zero4();
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        float4 v = gv[u][g] + ev[u][g];
-        v.x -= dot4(ph[u], ql[g][0]);
-        v.y -= dot4(ph[u], ql[g][1]);
-        v.z -= dot4(ph[u], ql[g][2]);
-        v.w -= dot4(ph[u], ql[g][3]);
-        mp[u][g] = v;
-        acc[u] = fma4(v.x, qh[g][0], acc[u]);
-        acc[u] = fma4(v.y, qh[g][1], acc[u]);
-        acc[u] = fma4(v.z, qh[g][2], acc[u]);
-        acc[u] = fma4(v.w, qh[g][3], acc[u]);
-      }
-    }
-    load(k + U);
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const float4 P = row_sum4<L>(acc[u]);
-      const uint32_t row = static_cast<uint32_t>(nm.row(k + u));
-      const uint32_t roff = row * row_bytes;
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        float4 r = mp[u][g];
-        r.x -= dot4(P, qh[g][0]);
-        r.y -= dot4(P, qh[g][1]);
-        r.z -= dot4(P, qh[g][2]);
-        r.w -= dot4(P, qh[g][3]);
-        bst4_nt(Er, coff[g] == kOut ? kOut : roff + coff[g], r);
-      }
-      bst4(Pr, nm.cl == 0 ? row * 16u : kOut, P);
-    }
-  }
-}
-
-// Q-step, narrow rows (r = 4, fused orthogonalisation): tile = row chunk t.a.  The chunk's Ph
-// rows are formed in LDS as P W (and stored to the Ph slot); per row F = M + E is written back
-// and each lane adds F^T Ph over its rows and columns.  The 256 / L row slots' sums are added in
-// slot order through LDS and stored as the chunk's partials for K_QFIN.
-template <int L, int G>
-__global__ __launch_bounds__(kBlock) void k_qnarrow(KArgs a) {
-  using NM = Narrow<L, G>;
-  constexpr int U = 2;
-  constexpr int NS = 4 * NM::SL;  // row slots of the workgroup
-  const Tile t = a.tiles[blockIdx.x];
-  if (t.kind == T_VEC) {
-    vec_tile(a, t, true);
-    return;
-  }
-  const MatDesc d = a.mats[t.idx];
-  const int m4 = d.m >> 2;
-  const NM nm(m4);
-  const int64_t r0 = static_cast<int64_t>(t.a) * d.q_rows;
-  const int rows = static_cast<int>((r0 + d.q_rows < d.n) ? d.q_rows : d.n - r0);
-  const uint32_t row_bytes = static_cast<uint32_t>(d.m) * 4u;
-  const uint32_t ext = static_cast<uint32_t>(rows) * row_bytes;
-  const int64_t first = r0 * d.m;
-  const Rsrc Gr = tile_rsrc(src_of(a, d.bucket) + d.grad_off + first, ext);
-  const Rsrc Er = tile_rsrc(a.e + d.e_off + first, a.ef ? ext : 0u);
-  uint32_t coff[G];
-#pragma unroll
-  for (int g = 0; g < G; ++g) coff[g] = nm.ok[g] ? static_cast<uint32_t>(nm.c4[g]) * 16u : kOut;
-
-  float4 gv[U][G], ev[U][G];
-  auto load = [&](int k0) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const uint32_t roff = static_cast<uint32_t>(nm.row(k0 + u)) * row_bytes;
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        const uint32_t o = coff[g] == kOut ? kOut : roff + coff[g];
-        gv[u][g] = bld4_nt(Gr, o);
-        ev[u][g] = bld4_nt(Er, o);
-      }
-    }
-  };
-  load(0);
-  __shared__ double Wsh[16];
-  __shared__ float4 phs[kQRows];  // the chunk's Ph rows; zero past the chunk
-  if (tid() < 16) Wsh[tid()] = a.w[d.w_slot + tid()];
-  __syncthreads();
-  if (tid() < kQRows) {
-    float4 y = zero4();
-    if (tid() < rows) {
-      const int64_t row = r0 + tid();
-      y = apply_w4(reinterpret_cast<const float4*>(a.fac + d.p_slot)[row], Wsh);
-      reinterpret_cast<float4*>(a.fac + d.ph_slot)[row] = y;
-    }
-    phs[tid()] = y;
-  }
-  __syncthreads();
-
-  float4 acc[G][4];
-#pragma unroll
-  for (int g = 0; g < G; ++g)
-#pragma unroll
-    for (int c = 0; c < 4; ++c) acc[g][c] = zero4();
-  for (int k = 0; k * NM::RW < rows; k += U) {
-    float4 f[U][G];
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int g = 0; g < G; ++g) f[u][g] = gv[u][g] + ev[u][g];
-    load(k + U);
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int row = nm.row(k + u);  // < kQRows: rows <= kQRows and 2 RW divides kQRows
-      const uint32_t roff = static_cast<uint32_t>(row) * row_bytes;
-      const float4 ph = phs[row & (kQRows - 1)];
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        bst4_nt(Er, coff[g] == kOut ? kOut : roff + coff[g], f[u][g]);
-        acc[g][0] = fma4(f[u][g].x, ph, acc[g][0]);
-        acc[g][1] = fma4(f[u][g].y, ph, acc[g][1]);
-        acc[g][2] = fma4(f[u][g].z, ph, acc[g][2]);
-        acc[g][3] = fma4(f[u][g].w, ph, acc[g][3]);
-      }
-    }
-  }
-  __shared__ float4 red[NS][L * G * 4];
-  const int sidx = nm.wave * NM::SL + nm.slot;
-#pragma unroll
-  for (int g = 0; g < G; ++g)
-#pragma unroll
-    for (int c = 0; c < 4; ++c) red[sidx][(nm.cl * G + g) * 4 + c] = acc[g][c];
-  __syncthreads();
-  const int64_t ncb = (d.m + d.q_cb - 1) / d.q_cb;
-  float4* part = reinterpret_cast<float4*>(a.qpart + d.qpart + static_cast<int64_t>(t.a) * ncb * d.q_cb * 4);
-  for (int e = tid(); e < L * G * 4; e += kBlock) {
-    const int cl = e / (G * 4), g = (e / 4) % G, c = e % 4;
-    const int col4 = cl + L * g;
-    if (col4 >= m4) continue;
-    float4 sum = red[0][e];
-    for (int sl = 1; sl < NS; ++sl) sum = sum + red[sl][e];
-    part[4 * col4 + c] = sum;  // Q partial of column 4 col4 + c, ranks 0..3
-  }
-}
-
-// Decompress, narrow rows: M_hat rows from the tile's A rows (staged in LDS, scaled by 1 / p)
-// and the lane's B rows in registers.  Factor tiles and vectors as in k_recon4.
-template <int L, int G>
-__global__ __launch_bounds__(kBlock) void k_rnarrow(KArgs a) {
-  using NM = Narrow<L, G>;
-  const Tile t = a.tiles[blockIdx.x];
-  const bool odd = a.parity != 0;
-  if (t.kind == T_VEC) {
-    vec_tile(a, t, false);
-    return;
-  }
-  const MatDesc d = a.mats[t.idx];
-  if (t.kind == T_FACT) {
-    const float* src = src_of(a, d.bucket) + (odd ? d.fac_off_p : d.fac_off_q);
-    float* dst = a.fac + (odd ? d.p_slot : d.q_slot);
-    fact_tile<4>(a, t, src, dst, odd ? d.n : d.m);
-    return;
-  }
-  const NM nm(d.m >> 2);
-  const float* agg = src_of(a, d.bucket);
-  const float4* A4 = reinterpret_cast<const float4*>(odd ? agg + d.fac_off_p : a.fac + d.ph_slot);
-  const float4* B4 = reinterpret_cast<const float4*>(odd ? a.fac + d.qh_slot : agg + d.fac_off_q);
-  __shared__ float4 as[kMaxTileRows];  // the tile's rows of A, scaled by 1 / p
-  if (tid() < t.b) as[tid()] = scale4(A4[t.a + tid()], a.inv_p);
-  float4 b[G][4];
-#pragma unroll
-  for (int g = 0; g < G; ++g)
-#pragma unroll
-    for (int c = 0; c < 4; ++c) b[g][c] = nm.ok[g] ? B4[4 * nm.c4[g] + c] : zero4();
-  __syncthreads();
-  __builtin_amdgcn_s_waitcnt(0);
-  const uint32_t row_bytes = static_cast<uint32_t>(d.m) * 4u;
-  const Rsrc O = tile_rsrc(dst_of(a, d.bucket) + d.grad_off + static_cast<int64_t>(t.a) * d.m,
-                           static_cast<uint32_t>(t.b) * row_bytes);
-  uint32_t coff[G];
-#pragma unroll
-  for (int g = 0; g < G; ++g) coff[g] = nm.ok[g] ? static_cast<uint32_t>(nm.c4[g]) * 16u : kOut;
-  for (int k = 0; k * NM::RW < t.b; ++k) {
-    const int row = nm.row(k);  // past the tile: an unset LDS entry, its stores are dropped
-    const float4 ar = as[row & (kMaxTileRows - 1)];
-    const uint32_t roff = static_cast<uint32_t>(row) * row_bytes;
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-      bst4_nt(O, coff[g] == kOut ? kOut : roff + coff[g],
-           make_float4(dot4(ar, b[g][0]), dot4(ar, b[g][1]), dot4(ar, b[g][2]), dot4(ar, b[g][3])));
-  }
-}
-
-template <int L, int G>
-void launch_narrow(int32_t kernel, dim3 grid, dim3 block, hipStream_t s, const KArgs& args) {
-  if (kernel == K_PNARROW)
-    hipLaunchKernelGGL((k_pnarrow<L, G>), grid, block, 0, s, args);
-  else if (kernel == K_QNARROW)
-    hipLaunchKernelGGL((k_qnarrow<L, G>), grid, block, 0, s, args);
-  else
-    hipLaunchKernelGGL((k_rnarrow<L, G>), grid, block, 0, s, args);
 }
 
 __global__ __launch_bounds__(kBlock) void k_vec(KArgs a) {
@@ -1034,21 +1047,6 @@ hipError_t launch_rank(const Launch& l, const KArgs& args, hipStream_t s) {
     case K_RECON4:
       if constexpr (RK == 4) {
         hipLaunchKernelGGL(k_recon4, grid, block, 0, s, args);
-        break;
-      } else {
-        return hipErrorInvalidValue;
-      }
-    case K_PNARROW:
-    case K_QNARROW:
-    case K_RNARROW:
-      if constexpr (RK == 4) {
-        switch (l.variant) {
-          case (16 << 4) | 1: launch_narrow<16, 1>(l.kernel, grid, block, s, args); break;
-          case (32 << 4) | 1: launch_narrow<32, 1>(l.kernel, grid, block, s, args); break;
-          case (64 << 4) | 1: launch_narrow<64, 1>(l.kernel, grid, block, s, args); break;
-          case (64 << 4) | 2: launch_narrow<64, 2>(l.kernel, grid, block, s, args); break;
-          default: return hipErrorInvalidValue;
-        }
         break;
       } else {
         return hipErrorInvalidValue;

@@ -445,18 +445,13 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       Launch l = sink.begin(K_APPLY, 1);
       apply_tiles(generic, true);
       sink.end(l, L);
-      for (int32_t v : narrow_vars) {
-        const std::vector<int32_t> cls = of_narrow(v);
-        if (cls.empty()) continue;
-        l = sink.begin(K_PNARROW, v);
-        for (int32_t mi : cls) row_tiles(mi, narrow_rows(mi, class_tile(K_PNARROW, v, 2 * kTileElems)));
-        if (!vec_done) vec_tiles(bk), vec_done = true;
-        sink.end(l, L);
-      }
       for (int32_t S = 1; S <= 5; ++S) {
         const std::vector<int32_t> cls = of_class(S);
-        if (cls.empty()) continue;
+        if (cls.empty() && (S > 1 || narrow.empty())) continue;
         l = sink.begin(K_PFUSED, S);
+        if (S == 1)  // the narrow-row matrices' tiles ride in the S = 1 launch
+          for (int32_t v : narrow_vars)
+            for (int32_t mi : of_narrow(v)) row_tiles(mi, narrow_rows(mi, class_tile(K_PNARROW, v, 2 * kTileElems)));
         // rows of 4 KB: 32K elements per tile; rows of 12 KB and more: 64K
         const int64_t base = (S >= 4 ? 4 : 2) * kTileElems;
         for (int32_t mi : cls)
@@ -496,17 +491,14 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         for (int32_t c = 0; c < d.q_chunks; ++c)
           for (int32_t cb = 0; cb < ncb; ++cb) plan.tiles.push_back(Tile{T_QTILE, mi, c, cb});
       };
-      for (int32_t v : narrow_vars) {
-        const std::vector<int32_t> cls = of_narrow(v);
-        if (cls.empty()) continue;
-        l = sink.begin(K_QNARROW, v);
-        for (int32_t mi : cls) qtiles(mi);
-        if (!vec_done) vec_tiles(bk), vec_done = true;
-        sink.end(l, L);
-      }
       for (int32_t variant : {4 | kQFused, 4, 1}) {
         l = sink.begin(K_QSTEP, variant);
         bool any = false;
+        if (variant & kQFused)  // the narrow-row matrices' chunks ride in the fused launch
+          for (int32_t mi : narrow) {
+            qtiles(mi);
+            any = true;
+          }
         const std::vector<int32_t>& set = (variant & kQFused) ? fast : generic;
         for (int32_t mi : set) {
           if (!(variant & kQFused) && plan.mats[mi].q_cb != 4 * 64 * variant) continue;
@@ -534,17 +526,11 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         vec_tiles(bk);
         extra_done = true;
       };
-      for (int32_t v : narrow_vars) {
-        const std::vector<int32_t> cls = of_narrow(v);
-        if (cls.empty()) continue;
-        Launch l = sink.begin(K_RNARROW, v);
-        extra();
-        for (int32_t mi : cls) row_tiles(mi, narrow_rows(mi, class_tile(K_RNARROW, v, kTileElems)));
-        sink.end(l, L);
-      }
-      if (!fast.empty()) {
+      if (!fast.empty() || !narrow.empty()) {
         Launch l = sink.begin(K_RECON4, 0);
         extra();
+        for (int32_t v : narrow_vars)
+          for (int32_t mi : of_narrow(v)) row_tiles(mi, narrow_rows(mi, class_tile(K_RNARROW, v, kTileElems)));
         for (int32_t mi : fast) recon4_tiles(mi);
         sink.end(l, L);
       }
@@ -583,18 +569,15 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     const MatDesc& d = plan.mats[t.idx];
     const double n = d.n, m = d.m, rr = double(r);
     switch (l.kernel) {
-      case K_PFUSED: {
-        const double rows = t.b >> 16;
+      case K_PFUSED: {  // strided tiles, or a narrow-row matrix's block of rows
+        const double rows = t.kind == T_SROWS ? double(t.b >> 16) : double(t.b);
         return rows * m * eb + rows * rr * 8.0 + (t.a == 0 ? m * rr * 12.0 : 0.0);
       }
-      case K_PNARROW:
-        return t.b * m * eb + t.b * rr * 8.0 + (t.a == 0 ? m * rr * 12.0 : 0.0);
       case K_PROW:
         return m * (ef ? 8.0 : 4.0) + rr * 8.0 + (t.a == 0 ? m * rr * 12.0 : 0.0);
       case K_EUPD:
         return t.b * m * 4.0;
-      case K_QSTEP:
-      case K_QNARROW: {
+      case K_QSTEP: {
         const double rows = q_chunk_rows(d, t.a).rows;
         const double cols = std::min<double>(d.q_cb, m - double(t.b) * d.q_cb);
         return rows * cols * eb + (t.b == 0 ? rows * rr * 8.0 : 0.0);
@@ -605,7 +588,6 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       }
       case K_RECON:
       case K_RECON4:
-      case K_RNARROW:
         if (t.kind == T_FACT) {
           const double rows = odd ? n : m;
           return std::min<double>(d.fact_rows, rows - double(t.a) * d.fact_rows) * rr * 8.0;
@@ -644,12 +626,12 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   };
   auto family_of = [](int32_t kernel, bool odd) -> int32_t {
     switch (kernel) {
-      case K_PFUSED: case K_PNARROW: case K_PROW: case K_EUPD: case K_WPSTEP:
+      case K_PFUSED: case K_PROW: case K_EUPD: case K_WPSTEP:
         return 1;  // ACP_KERNEL_P_STEP
-      case K_QSTEP: case K_QNARROW: case K_WQSTEP:
+      case K_QSTEP: case K_WQSTEP:
         return 2;  // ACP_KERNEL_Q_STEP
       case K_QFIN: return 3;  // ACP_KERNEL_Q_FINISH
-      case K_RECON: case K_RECON4: case K_RNARROW: case K_WRECON:
+      case K_RECON: case K_RECON4: case K_WRECON:
         return 4;  // ACP_KERNEL_RECONSTRUCT
       case K_WFACT: return 5;                                              // ACP_KERNEL_ORTH
       case K_APPLY: case K_FACT: case K_CHOL: return 5;     // ACP_KERNEL_ORTH
@@ -678,7 +660,6 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   auto order_of = [](const Launch& l) -> int32_t {
     switch (l.kernel) {
       case K_APPLY: return 0;
-      case K_PNARROW: return 1;
       case K_PFUSED: return 1 + l.variant;          // 2..6
       case K_PROW: return 10;
       case K_EUPD: return 11;
@@ -686,10 +667,8 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       case K_WQSTEP: return 22;
       case K_WRECON: return 40;
       case K_WFACT: return 41;
-      case K_QNARROW: return 19;
       case K_QSTEP: return (l.variant & kQFused) ? 20 : (l.variant == 4 ? 21 : 22);
       case K_QFIN: return 23;
-      case K_RNARROW: return 30;
       case K_RECON4: return 31;
       case K_RECON: return l.variant == 4 ? 40 : 41;
       case K_CHOL: return 42;

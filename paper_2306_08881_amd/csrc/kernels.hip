@@ -416,10 +416,11 @@ __device__ inline void narrow_recon(const KArgs& a, const Tile& t, const MatDesc
 
 // ---------------------------------------------------------------------------------------
 // Column mapping shared by the rank-4 streaming kernels.  The four waves of a workgroup split
-// a row of m4 = m / 4 float4 groups into four segments of 64 S groups; lane `lane` of wave w
-// owns groups w * 64 S + s * 64 + lane, s < S, for every row of the tile, so the factor rows
-// of those columns are loaded once per workgroup and kept in registers.  The waves work on the
-// same RB rows at a time (8 for S = 1, 2 for S = 2..4, 1 for S = 5).
+// a row of m4 = m / 4 float4 groups into four segments of 64 Se groups, Se = ceil(m4 / 256) <= S
+// (a launch of class S also carries rows of smaller classes); lane `lane` of wave w owns groups
+// w * 64 Se + s * 64 + lane, s < Se, for every row of the tile, so the factor rows of those
+// columns are loaded once per workgroup and kept in registers.  The waves work on the same RB
+// rows at a time (8 for S = 1, 2 for S = 2..4, 1 for S = 5).
 template <int S>
 struct Cols {
   static constexpr int RB = S == 1 ? 8 : (S <= 4 ? 2 : 1);
@@ -429,10 +430,11 @@ struct Cols {
   __device__ explicit Cols(int m4) {
     wave = tid() >> 6;
     lane = tid() & 63;
+    const int se = (m4 + 255) >> 8;
 #pragma unroll
     for (int s = 0; s < S; ++s) {
-      c4[s] = wave * 64 * S + s * 64 + lane;
-      ok[s] = c4[s] < m4;
+      c4[s] = wave * 64 * se + s * 64 + lane;
+      ok[s] = s < se && c4[s] < m4;
     }
   }
 };

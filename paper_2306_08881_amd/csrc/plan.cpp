@@ -26,6 +26,7 @@ constexpr int64_t kSmallTileElems = 2048;  // per tile of the general P-step E u
 constexpr int64_t kTargetTiles = 1024;     // workgroups a launch class aims for (4 per CU)
 constexpr int64_t kMinTileElems = 2048;    // smallest tile of a class that has few elements
 constexpr int64_t kPGroup = 8;            // P-step tiles whose rows interleave (rank 4)
+constexpr int64_t kMergeElems = int64_t(16) << 20;  // P-step classes below this share a launch
 constexpr int64_t kPMinRows = 8;          // fewest rows of a P-step tile (rank 4)
 constexpr int64_t kQGroup = 8;            // Q-step row chunks whose rows interleave (rank 4)
 constexpr int64_t kVecChunk = 4096;     // raw-vector elements per copy tile
@@ -157,6 +158,20 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     const auto it = class_elems.find(class_key(kernel, variant));
     const int64_t tot = it == class_elems.end() ? 0 : it->second;
     return std::max<int64_t>(kMinTileElems, std::min<int64_t>(base, tot / kTargetTiles));
+  };
+
+  // P-step launch classes: a class S >= 2 with fewer than kMergeElems elements in all runs in
+  // one launch with the other such classes, as the largest of them (pmerge; 0: none)
+  int32_t pmerge = 0;
+  for (int32_t S = 2; S <= 5; ++S) {
+    const auto it = class_elems.find(class_key(K_PFUSED, S));
+    if (it != class_elems.end() && it->second > 0 && it->second < kMergeElems) pmerge = S;
+  }
+  auto class_of_p = [&](int32_t S) -> int32_t {
+    if (S < 2 || pmerge == 0) return S;
+    const auto it = class_elems.find(class_key(K_PFUSED, S));
+    const int64_t tot = it == class_elems.end() ? 0 : it->second;
+    return tot < kMergeElems ? pmerge : S;
   };
 
   // ---- per-tensor device descriptors and state regions
@@ -445,20 +460,37 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       Launch l = sink.begin(K_APPLY, 1);
       apply_tiles(generic, true);
       sink.end(l, L);
+      // the classes S >= 2 with few elements in all (launch variant pmerge) share one launch
+      auto pfused_tiles = [&](int32_t S) {
+        // rows of 4 KB: 32K elements per tile; rows of 12 KB and more: 64K
+        const int64_t base = (S >= 4 ? 4 : 2) * kTileElems;
+        for (int32_t mi : of_class(S))
+          pstep_tiles(mi, rows_for(mi, std::max<int64_t>(kPMinRows * plan.mats[mi].m,
+                                                          class_tile(K_PFUSED, S, base))));
+      };
       for (int32_t S = 1; S <= 5; ++S) {
-        const std::vector<int32_t> cls = of_class(S);
-        if (cls.empty() && (S > 1 || narrow.empty())) continue;
+        const bool merged = S >= 2 && class_of_p(S) != S;
+        if (merged || (S == pmerge && S >= 2)) continue;  // the merged launch follows
+        if (of_class(S).empty() && (S > 1 || narrow.empty())) continue;
         l = sink.begin(K_PFUSED, S);
         if (S == 1)  // the narrow-row matrices' tiles ride in the S = 1 launch
           for (int32_t v : narrow_vars)
             for (int32_t mi : of_narrow(v)) row_tiles(mi, narrow_rows(mi, class_tile(K_PNARROW, v, 2 * kTileElems)));
-        // rows of 4 KB: 32K elements per tile; rows of 12 KB and more: 64K
-        const int64_t base = (S >= 4 ? 4 : 2) * kTileElems;
-        for (int32_t mi : cls)
-          pstep_tiles(mi, rows_for(mi, std::max<int64_t>(kPMinRows * plan.mats[mi].m,
-                                                          class_tile(K_PFUSED, S, base))));
+        pfused_tiles(S);
         if (!vec_done) vec_tiles(bk), vec_done = true;
         sink.end(l, L);
+      }
+      if (pmerge >= 2) {
+        bool any = false;
+        for (int32_t S = 2; S <= 5; ++S)
+          if (class_of_p(S) == pmerge && !of_class(S).empty()) any = true;
+        if (any) {
+          l = sink.begin(K_PFUSED, pmerge);
+          for (int32_t S = 2; S <= 5; ++S)
+            if (class_of_p(S) == pmerge) pfused_tiles(S);
+          if (!vec_done) vec_tiles(bk), vec_done = true;
+          sink.end(l, L);
+        }
       }
       if (!generic.empty()) {
         l = sink.begin(K_PROW, 0);

@@ -33,6 +33,8 @@ constexpr int kMaxTileRows = 256; // rows per tile of the rank-4 row kernels (fa
 // for up to 8 row chunks, 4 threads for up to 64, 16 threads beyond
 constexpr int qfin_entries(int32_t q_chunks) { return q_chunks <= 8 ? 1024 : (q_chunks <= 64 ? 64 : 16); }
 constexpr int64_t kMaxCols = int64_t(1) << 24;  // columns of a compressed matrix, at most
+constexpr int kSmallRows = 256;  // T_SMALL matrices: rows (their P rows sit in LDS)
+constexpr int kSmallCols = 512;  // T_SMALL matrices: columns (their Q rows sit in LDS)
 constexpr int kReconRows = 4;   // rows per tile of the rank-4 decompress
 constexpr int kQRows = 256;       // rows per Q-step row chunk (at most; the chunk's Ph rows sit in LDS)
 
@@ -86,9 +88,11 @@ struct VecDesc {
   int32_t bucket, pad;
 };
 
-enum TileKind : int32_t { T_ROWS = 0, T_FACT = 1, T_VEC = 2, T_QTILE = 3, T_SROWS = 4 };
+enum TileKind : int32_t { T_ROWS = 0, T_FACT = 1, T_VEC = 2, T_QTILE = 3, T_SROWS = 4, T_SMALL = 5 };
 
 // kind T_ROWS : idx = matrix, a = first row, b = row count
+// kind T_SMALL: idx = matrix, the whole matrix in one workgroup (rank 4, small matrices whose
+//               rows are not 16-byte aligned: n <= kSmallRows, m <= kSmallCols)
 // kind T_SROWS: idx = matrix, a = first row, b = cb | stride << 4 | count << 16: columns
 //               [1024 cb, 1024 cb + 1024) of rows a + k stride, k < count
 // kind T_FACT : idx = matrix, a = slice, b = slice count

@@ -100,6 +100,109 @@ __global__ __launch_bounds__(kBlock) void k_apply(KArgs a) {
 }
 
 // ---------------------------------------------------------------------------------------
+// Small rank-4 matrices whose rows are not 16-byte aligned (T_SMALL: n <= kSmallRows,
+// m <= kSmallCols): one workgroup takes the whole matrix with scalar column accesses, inside
+// the P-step, Q-step and decompress launches of the register-resident kernels.
+
+// P-step: Qh = Q W (stored), per row P = M' Qh with M' = M + E (or M + F - Ph_row Q_loc^T),
+// E = M' - P Qh^T, P to the factor buffer.  Shared memory: Wsh (16 doubles), qhs and qls
+// (kSmallCols float4 each).
+__device__ inline void small_pstep(const KArgs& a, const MatDesc& d, double* Wsh, float4* qhs, float4* qls) {
+  const int n = d.n, m = d.m;
+  const bool deferred = deferred_of(a, d.bucket);
+  if (tid() < 16) Wsh[tid()] = a.w[d.w_slot + tid()];
+  __syncthreads();
+  const float4* Q4 = reinterpret_cast<const float4*>(a.fac + d.q_slot);
+  const float4* Ql4 = reinterpret_cast<const float4*>(a.fac + d.ql_slot);
+  float4* Qh4 = reinterpret_cast<float4*>(a.fac + d.qh_slot);
+  for (int j = tid(); j < m; j += kBlock) {
+    const float4 q = apply_w4(Q4[j], Wsh);
+    qhs[j] = q;
+    Qh4[j] = q;
+    qls[j] = deferred ? Ql4[j] : zero4();
+  }
+  __syncthreads();
+  const float* G = src_of(a, d.bucket) + d.grad_off;
+  float* E = a.e + d.e_off;
+  const float4* Ph4 = reinterpret_cast<const float4*>(a.fac + d.ph_slot);
+  float* P = dst_of(a, d.bucket) + d.fac_off_p;
+  const int wave = tid() >> 6, lane = tid() & 63;
+  for (int row = wave; row < n; row += kBlock / kWave) {
+    const float4 ph = deferred ? Ph4[row] : zero4();
+    const int64_t base = static_cast<int64_t>(row) * m;
+    auto mprime = [&](int j) {
+      const float e = a.ef ? E[base + j] : 0.f;
+      return (G[base + j] + e) - dot4(ph, qls[j]);
+    };
+    float4 acc = zero4();
+    for (int j = lane; j < m; j += kWave) acc = fma4(mprime(j), qhs[j], acc);
+    const float4 pr = wave_sum_dpp(acc);
+    if (a.ef)
+      for (int j = lane; j < m; j += kWave) E[base + j] = mprime(j) - dot4(pr, qhs[j]);
+    if (lane < 4) P[static_cast<int64_t>(row) * 4 + lane] = lane == 0 ? pr.x : lane == 1 ? pr.y : lane == 2 ? pr.z : pr.w;
+  }
+}
+
+// Q-step: Ph = P W (stored), F = M + E written back, Q_loc = F^T Ph summed over the rows in
+// order, written to the factor buffer and the Ql slot (no row-chunk partials).  Shared memory:
+// Wsh (16 doubles), phs (kSmallRows float4).
+__device__ inline void small_qstep(const KArgs& a, const MatDesc& d, double* Wsh, float4* phs) {
+  const int n = d.n, m = d.m;
+  if (tid() < 16) Wsh[tid()] = a.w[d.w_slot + tid()];
+  __syncthreads();
+  const float4* P4 = reinterpret_cast<const float4*>(a.fac + d.p_slot);
+  float4* Ph4 = reinterpret_cast<float4*>(a.fac + d.ph_slot);
+  for (int i = tid(); i < n; i += kBlock) {
+    const float4 y = apply_w4(P4[i], Wsh);
+    phs[i] = y;
+    Ph4[i] = y;
+  }
+  __syncthreads();
+  const float* G = src_of(a, d.bucket) + d.grad_off;
+  float* E = a.e + d.e_off;
+  float* Q = dst_of(a, d.bucket) + d.fac_off_q;
+  float* Ql = a.fac + d.ql_slot;
+  for (int j = tid(); j < m; j += kBlock) {
+    float4 acc = zero4();
+    for (int row = 0; row < n; ++row) {
+      const int64_t idx = static_cast<int64_t>(row) * m + j;
+      float f = G[idx];
+      if (a.ef) {
+        f += E[idx];
+        E[idx] = f;
+      }
+      acc = fma4(f, phs[row], acc);
+    }
+    const float q[4] = {acc.x, acc.y, acc.z, acc.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      Q[static_cast<int64_t>(j) * 4 + k] = q[k];
+      Ql[static_cast<int64_t>(j) * 4 + k] = q[k];
+    }
+  }
+}
+
+// Decompress: M_hat = A B^T / p (odd step: A = P_agg, B = Qh; even step: A = Ph, B = Q_agg).
+// Shared memory: bs (kSmallCols float4).
+__device__ inline void small_recon(const KArgs& a, const MatDesc& d, float4* bs) {
+  const int n = d.n, m = d.m;
+  const bool odd = a.parity != 0;
+  const float* agg = src_of(a, d.bucket);
+  const float* A = odd ? agg + d.fac_off_p : a.fac + d.ph_slot;
+  const float* B = odd ? a.fac + d.qh_slot : agg + d.fac_off_q;
+  for (int j = tid(); j < m; j += kBlock)
+    bs[j] = make_float4(B[4 * j], B[4 * j + 1], B[4 * j + 2], B[4 * j + 3]);
+  __syncthreads();
+  float* O = dst_of(a, d.bucket) + d.grad_off;
+  const int wave = tid() >> 6, lane = tid() & 63;
+  for (int row = wave; row < n; row += kBlock / kWave) {
+    const float* ar = A + static_cast<int64_t>(row) * 4;
+    const float4 av = scale4(make_float4(ar[0], ar[1], ar[2], ar[3]), a.inv_p);
+    for (int j = lane; j < m; j += kWave) O[static_cast<int64_t>(row) * m + j] = dot4(av, bs[j]);
+  }
+}
+
+// ---------------------------------------------------------------------------------------
 // Narrow rows (r = 4, 16-byte aligned rows of at most 512 columns): L lanes per row (16, 32 or
 // 64), G float4 groups per lane (1 or 2).  A wave holds 64 / L whole rows at a time and the
 // workgroup 256 / L; lane l of row slot l / L owns groups (l % L) + L g, whose factor rows stay
@@ -462,6 +565,12 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
       narrow_pstep(a, t, d, Wn);
       return;
     }
+    if (t.kind == T_SMALL) {  // a small matrix, whole (the S = 1 launch carries them)
+      __shared__ double Ws[16];
+      __shared__ float4 qhs[kSmallCols], qls[kSmallCols];
+      small_pstep(a, d, Ws, qhs, qls);
+      return;
+    }
   }
   const int m4 = d.m >> 2;
   const Cols<S> cl(m4);
@@ -684,6 +793,11 @@ __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
   __shared__ double Wsh[16];
   __shared__ __align__(16) float phs[kQRows * RK];
   if constexpr (FUSED) {
+    static_assert(kSmallRows <= kQRows, "a small matrix's Ph rows use the chunk's Ph buffer");
+    if (t.kind == T_SMALL) {  // a small matrix, whole (the fused launch carries them)
+      small_qstep(a, d, Wsh, reinterpret_cast<float4*>(phs));
+      return;
+    }
     if (d.scls == 0) {  // a narrow-row matrix's chunk (the fused launch carries them)
       __shared__ float4 red[kNarrowRed];
       narrow_qstep(a, t, d, Wsh, reinterpret_cast<float4*>(phs), red);
@@ -957,6 +1071,11 @@ __global__ __launch_bounds__(kBlock) void k_recon4(KArgs a) {
   if (t.kind == T_ROWS) {  // a narrow-row matrix's tile
     __shared__ float4 asn[kMaxTileRows];
     narrow_recon(a, t, d, asn);
+    return;
+  }
+  if (t.kind == T_SMALL) {  // a small matrix, whole
+    __shared__ float4 bsm[kSmallCols];
+    small_recon(a, d, bsm);
     return;
   }
   const int cb = t.b & 15, stride = (t.b >> 4) & 0xfff, rows = t.b >> 16;

@@ -323,6 +323,11 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
                                   static_cast<int32_t>((g << 4) | (cdiv(rem - x, g) << 16))});
     }
   };
+  // rank-4 matrices that one workgroup takes whole (T_SMALL) when the row kernels cannot
+  auto is_small = [&](int32_t mi) {
+    const MatDesc& d = plan.mats[mi];
+    return r == 4 && d.n <= kSmallRows && d.m <= kSmallCols;
+  };
   auto is_vec4 = [&](int32_t mi) {
     const MatDesc& d = plan.mats[mi];
     return d.m % 4 == 0 && d.grad_off % 4 == 0;
@@ -346,6 +351,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     Launch l = sink.begin(K_QFIN, 0);
     for (int32_t mi : bk.mats) {
       const MatDesc& d = plan.mats[mi];
+      if (d.scls < 0) continue;  // T_SMALL: the Q-step writes Q_loc itself
       const int64_t nblk = cdiv(int64_t(d.m) * r, qfin_entries(d.q_chunks));
       for (int64_t eb = 0; eb < nblk; ++eb)
         plan.tiles.push_back(Tile{T_QTILE, mi, static_cast<int32_t>(eb), 0});
@@ -422,17 +428,25 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       wide_lists(bk);
       continue;
     }
-    // fast: rank-4 register-resident kernels; narrow: rows of at most 512 columns (scls 0)
-    std::vector<int32_t> fast, narrow, generic;
+    // fast: rank-4 register-resident kernels; narrow: rows of at most 512 columns (scls 0);
+    // small: rank-4 matrices of other rows, small enough for one workgroup (scls -1, T_SMALL
+    // tiles in the same launches); generic: the general kernels
+    std::vector<int32_t> fast, narrow, small, generic;
     for (int32_t mi : bk.mats) {
       if (is_fast(mi)) {
         const int64_t m4 = plan.mats[mi].m / 4;
         plan.mats[mi].scls = m4 <= 128 ? 0 : static_cast<int32_t>(cdiv(m4, 256));
         (m4 <= 128 ? narrow : fast).push_back(mi);
+      } else if (is_small(mi)) {
+        plan.mats[mi].scls = -1;
+        small.push_back(mi);
       } else {
         generic.push_back(mi);
       }
     }
+    auto small_tiles = [&]() {
+      for (int32_t mi : small) plan.tiles.push_back(Tile{T_SMALL, mi, 0, 0});
+    };
     auto of_narrow = [&](int32_t v) {
       std::vector<int32_t> out;
       for (int32_t mi : narrow)
@@ -471,11 +485,13 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       for (int32_t S = 1; S <= 5; ++S) {
         const bool merged = S >= 2 && class_of_p(S) != S;
         if (merged || (S == pmerge && S >= 2)) continue;  // the merged launch follows
-        if (of_class(S).empty() && (S > 1 || narrow.empty())) continue;
+        if (of_class(S).empty() && (S > 1 || (narrow.empty() && small.empty()))) continue;
         l = sink.begin(K_PFUSED, S);
-        if (S == 1)  // the narrow-row matrices' tiles ride in the S = 1 launch
+        if (S == 1) {  // the narrow-row and small matrices' tiles ride in the S = 1 launch
+          small_tiles();
           for (int32_t v : narrow_vars)
             for (int32_t mi : of_narrow(v)) row_tiles(mi, narrow_rows(mi, class_tile(K_PNARROW, v, 2 * kTileElems)));
+        }
         pfused_tiles(S);
         if (!vec_done) vec_tiles(bk), vec_done = true;
         sink.end(l, L);
@@ -526,11 +542,11 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       for (int32_t variant : {4 | kQFused, 4, 1}) {
         l = sink.begin(K_QSTEP, variant);
         bool any = false;
-        if (variant & kQFused)  // the narrow-row matrices' chunks ride in the fused launch
-          for (int32_t mi : narrow) {
-            qtiles(mi);
-            any = true;
-          }
+        if (variant & kQFused) {  // the small and narrow-row matrices ride in the fused launch
+          small_tiles();
+          for (int32_t mi : narrow) qtiles(mi);
+          any = !small.empty() || !narrow.empty();
+        }
         const std::vector<int32_t>& set = (variant & kQFused) ? fast : generic;
         for (int32_t mi : set) {
           if (!(variant & kQFused) && plan.mats[mi].q_cb != 4 * 64 * variant) continue;
@@ -558,9 +574,10 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         vec_tiles(bk);
         extra_done = true;
       };
-      if (!fast.empty() || !narrow.empty()) {
+      if (!fast.empty() || !narrow.empty() || !small.empty()) {
         Launch l = sink.begin(K_RECON4, 0);
         extra();
+        small_tiles();
         for (int32_t v : narrow_vars)
           for (int32_t mi : of_narrow(v)) row_tiles(mi, narrow_rows(mi, class_tile(K_RNARROW, v, kTileElems)));
         for (int32_t mi : fast) recon4_tiles(mi);
@@ -600,6 +617,11 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     if (t.kind == T_VEC) return 8.0 * t.b;
     const MatDesc& d = plan.mats[t.idx];
     const double n = d.n, m = d.m, rr = double(r);
+    if (t.kind == T_SMALL) {  // a whole small matrix: P-step, Q-step (with its finish), decompress
+      if (l.kernel == K_PFUSED) return n * m * eb + n * rr * 8.0 + m * rr * 12.0;
+      if (l.kernel == K_QSTEP) return n * m * eb + n * rr * 8.0 + m * rr * 8.0;
+      return n * m * 4.0 + n * rr * 4.0 + m * rr * 4.0;
+    }
     switch (l.kernel) {
       case K_PFUSED: {  // strided tiles, or a narrow-row matrix's block of rows
         const double rows = t.kind == T_SROWS ? double(t.b >> 16) : double(t.b);

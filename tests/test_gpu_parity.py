@@ -118,6 +118,20 @@ def test_narrow_rows(ef):
     _assert_ok(_custom(NARROW, 4, ef=ef))
 
 
+# rank-4 matrices whose rows or factor offsets are not 16-byte aligned and that fit one
+# workgroup (at most 256 rows and 512 columns: taken whole inside the row kernels' launches),
+# at the limits and just past them (the general kernels), behind a 3-element vector that
+# misaligns everything after it
+SMALL = [(3,), (5, 5), (256, 512), (256, 511), (257, 147), (64, 3, 7, 7), (200, 513), (9, 2, 2),
+         (255, 6), (6, 255)]
+
+
+@pytest.mark.parametrize("ef", [True, False])
+def test_small_unaligned_matrices(ef):
+    _require_gpu()
+    _assert_ok(_custom(SMALL, 4, ef=ef))
+
+
 def test_error_feedback_off():
     _require_gpu()
     _assert_ok(_custom(RAGGED[:6] + [(256, 64, 3, 3)], 4, ef=False))

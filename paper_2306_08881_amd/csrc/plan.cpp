@@ -238,9 +238,10 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       d.qpart = qpart;
       qpart += align_up(int64_t(d.q_chunks) * ncb * d.q_cb * r, kSlotAlign);
       d.bucket = b;
-      // factor rows per Gram slice: 2048 at r <= 8; at r >= 16 at least 256 and at most 32
-      // slices per factor (K_CHOL adds a factor's slice partials in one workgroup)
-      d.fact_rows = r <= 8 ? 2048
+      // factor rows per Gram slice: at r <= 8 up to 8192 (one slice, and no K_CHOL, for
+      // factors of at most 8192 rows); at r >= 16 at least 256 and at most 32 slices per factor
+      // (K_CHOL adds a factor's slice partials in one workgroup)
+      d.fact_rows = r <= 8 ? 8192
                            : static_cast<int32_t>(std::max<int64_t>(256, align_up(cdiv(std::max(t.n, t.m), 32), 64)));
       d.fact_slices_p = static_cast<int32_t>(cdiv(t.n, d.fact_rows));
       d.fact_slices_q = static_cast<int32_t>(cdiv(t.m, d.fact_rows));

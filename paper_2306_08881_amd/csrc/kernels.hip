@@ -1191,6 +1191,7 @@ hipError_t launch(const Launch& l, int32_t rank, const KArgs& args, hipStream_t 
     case 8: return launch_rank<8>(l, args, s);
     case 16: return launch_rank<16>(l, args, s);
     case 32: return launch_rank<32>(l, args, s);
+    case 64: return launch_rank<64>(l, args, s);
     default: return hipErrorInvalidValue;
   }
 }

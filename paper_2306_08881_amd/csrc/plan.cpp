@@ -36,7 +36,7 @@ constexpr int64_t kSlotAlign = 64;      // floats (256 bytes)
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 int64_t align_up(int64_t x, int64_t a) { return cdiv(x, a) * a; }
 
-bool rank_supported(int32_t r) { return r == 1 || r == 2 || r == 4 || r == 8 || r == 16 || r == 32; }
+bool rank_supported(int32_t r) { return r == 1 || r == 2 || r == 4 || r == 8 || r == 16 || r == 32 || r == 64; }
 
 struct TileSink {
   std::vector<Tile>& tiles;

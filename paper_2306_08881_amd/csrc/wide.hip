@@ -1,4 +1,4 @@
-// gfx950 MFMA kernels of the ACP-SGD compressor for ranks 8, 16 and 32 (arXiv 2306.08881,
+// gfx950 MFMA kernels of the ACP-SGD compressor for ranks 8 to 64 (arXiv 2306.08881,
 // Algorithm 2).  At these ranks a step costs 2r multiply-adds per gradient element against
 // 12 bytes of HBM traffic, more than the fp32 vector units sustain at full bandwidth, so the
 // rank-r contractions run on v_mfma_f32_32x32x2f32.
@@ -9,7 +9,9 @@
 //            P_loc = X Qh;  afterwards E = X - P_loc Qh^T is implied.
 //   Q-step:  F = M + E_arena (- Pl Qh^T when the arena holds X), F written to the arena,
 //            Q_loc = F^T Ph; afterwards E = F - Ph Q_loc^T is implied.
-// Each is one rank-r correction and one rank-r product per element.
+// Each is one rank-r correction and one rank-r product per element.  Rank 64 keeps two 32-rank
+// blocks of the product's output per wave; its compress kernels run one wave per SIMD (their
+// operands take every VGPR) instead of spilling.
 //
 // MFMA layout (one wave): D (32 x 32) += A (32 x 2) B (2 x 32).  Lane l supplies
 // A[l % 32][l / 32] and B[l / 32][l % 32]; register v of lane l holds D[drow(v, l / 32)][l % 32].
@@ -66,8 +68,9 @@ __device__ inline bool aligned16(const float* p) { return (reinterpret_cast<uint
 // [l % 32].  The next block's M, E and factor rows are requested before the current block's
 // MFMAs.
 template <int RK>
-__global__ __launch_bounds__(kWideBlock, 2) void k_wpstep(KArgs a) {
+__global__ __launch_bounds__(kWideBlock, RK > 32 ? 1 : 2) void k_wpstep(KArgs a) {
   constexpr int KH = RK / 2;
+  constexpr int NR = RK > 32 ? RK / 32 : 1;  // 32-rank blocks of P (one MFMA block each)
   constexpr int LD = 33;  // padded LDS row: the transposed reads hit 32 different banks
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
@@ -97,32 +100,39 @@ __global__ __launch_bounds__(kWideBlock, 2) void k_wpstep(KArgs a) {
       e[v] = bld1_nt(E, o);
     }
   };
-  // the block's factor operands: Ql rows (correction B) and Qh rows (product B)
-  auto load_ops = [&](int64_t c0, float* qa, float* qb) {
+  // the block's factor operands: Ql rows (correction B) and Qh rows (product B, rank block kb)
+  auto load_ops = [&](int64_t c0, float* qa, float (*qb)[16]) {
     const int64_t qcol = c0 + li;
     if (fform) load_run<KH>(Qlr, qcol < m ? u32(qcol * RK + KH * h) * 4u : kOut, ql4, qa);
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int64_t col = c0 + drow(v, h);
-      qb[v] = bld1(Qhr, (col < m && li < RK) ? u32(col * RK + li) * 4u : kOut);
-    }
+    for (int kb = 0; kb < NR; ++kb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int64_t col = c0 + drow(v, h);
+        const int rank = kb * 32 + li;
+        qb[kb][v] = bld1(Qhr, (col < m && rank < RK) ? u32(col * RK + rank) * 4u : kOut);
+      }
   };
   __shared__ float xt[2][32 * LD];
-  float g[16], e[16], qa[KH], qb[16];
+  float g[16], e[16], qa[KH], qb[NR][16];
   load_block(0, g, e);
   load_ops(0, qa, qb);
 
-  v16f p = zero16();
+  v16f p[NR];
+#pragma unroll
+  for (int kb = 0; kb < NR; ++kb) p[kb] = zero16();
   int buf = 0;
   for (int64_t c0 = 0; c0 < m; c0 += 32, buf ^= 1) {
     v16f x;
 #pragma unroll
     for (int v = 0; v < 16; ++v) x[v] = g[v] + e[v];
-    float ca[KH], cb[16];
+    float ca[KH], cb[NR][16];
 #pragma unroll
     for (int s = 0; s < KH; ++s) ca[s] = qa[s];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) cb[v] = qb[v];
+    for (int kb = 0; kb < NR; ++kb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) cb[kb][v] = qb[kb][v];
     const uint32_t coff = c0 + li < m ? u32(c0 + li) * 4u : kOut;
     load_block(c0 + 32, g, e);  // next block (past m: zeros, no traffic)
     load_ops(c0 + 32, qa, qb);
@@ -137,21 +147,28 @@ __global__ __launch_bounds__(kWideBlock, 2) void k_wpstep(KArgs a) {
     }
     __syncthreads();
 #pragma unroll
-    for (int v = 0; v < 16; ++v)  // P += X Qh: A = X (row, column), B = Qh (column, rank)
-      p = mfma(xt[buf][li * LD + drow(v, h)], cb[v], p);
+    for (int v = 0; v < 16; ++v) {  // P += X Qh: A = X (row, column), B = Qh (column, rank)
+      const float xa = xt[buf][li * LD + drow(v, h)];
+#pragma unroll
+      for (int kb = 0; kb < NR; ++kb) p[kb] = mfma(xa, cb[kb][v], p[kb]);
+    }
   }
 
   float* P = dst_of(a, d.bucket) + d.fac_off_p;
   float* Pl = a.fac + d.pl_slot;
-  if (li < RK)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int row = drow(v, h);
-      if (row < rows) {
-        P[(r0 + row) * RK + li] = p[v];
-        Pl[(r0 + row) * RK + li] = p[v];
+  for (int kb = 0; kb < NR; ++kb) {
+    const int rank = kb * 32 + li;
+    if (rank < RK)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = drow(v, h);
+        if (row < rows) {
+          P[(r0 + row) * RK + rank] = p[kb][v];
+          Pl[(r0 + row) * RK + rank] = p[kb][v];
+        }
       }
-    }
+  }
 }
 
 // Q-step over a tile (row chunk t.a of q_rows rows, column block t.b of 32 columns c0 ...
@@ -161,8 +178,9 @@ __global__ __launch_bounds__(kWideBlock, 2) void k_wpstep(KArgs a) {
 // Q += F^T Ph with the rows as K.  Lane l's partial Q of column c0 + drow(v, l / 32), rank
 // l % 32, goes to the chunk's partial block for K_QFIN.
 template <int RK>
-__global__ __launch_bounds__(kWideBlock, 2) void k_wqstep(KArgs a) {
+__global__ __launch_bounds__(kWideBlock, RK > 32 ? 1 : 2) void k_wqstep(KArgs a) {
   constexpr int KH = RK / 2;
+  constexpr int NR = RK > 32 ? RK / 32 : 1;  // 32-rank blocks of Q (one MFMA block each)
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
   const int lane = tid(), h = lane >> 5, li = lane & 31;
@@ -193,26 +211,34 @@ __global__ __launch_bounds__(kWideBlock, 2) void k_wqstep(KArgs a) {
       e[v] = bld1_nt(E, o);
     }
   };
-  // the block's factor operands: Pl rows (correction A) and Ph rows (product B)
-  auto load_ops = [&](int rb, float* pa, float* pb) {
+  // the block's factor operands: Pl rows (correction A) and Ph rows (product B, rank block kb)
+  auto load_ops = [&](int rb, float* pa, float (*pb)[16]) {
     if (xform) load_run<KH>(Plr, u32((rb + li) * RK + KH * h) * 4u, pl4, pa);
 #pragma unroll
-    for (int v = 0; v < 16; ++v)
-      pb[v] = bld1(Phr, li < RK ? u32((rb + drow(v, h)) * RK + li) * 4u : kOut);
+    for (int kb = 0; kb < NR; ++kb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int rank = kb * 32 + li;
+        pb[kb][v] = bld1(Phr, rank < RK ? u32((rb + drow(v, h)) * RK + rank) * 4u : kOut);
+      }
   };
-  float g[16], e[16], pa[KH], pb[16];
+  float g[16], e[16], pa[KH], pb[NR][16];
   load_block(0, g, e);
   load_ops(0, pa, pb);
-  v16f q = zero16();
+  v16f q[NR];
+#pragma unroll
+  for (int kb = 0; kb < NR; ++kb) q[kb] = zero16();
   for (int rb = 0; rb < rows; rb += 32) {
     v16f x;
 #pragma unroll
     for (int v = 0; v < 16; ++v) x[v] = g[v] + e[v];
-    float ca[KH], cb[16];
+    float ca[KH], cb[NR][16];
 #pragma unroll
     for (int s = 0; s < KH; ++s) ca[s] = pa[s];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) cb[v] = pb[v];
+    for (int kb = 0; kb < NR; ++kb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) cb[kb][v] = pb[kb][v];
     load_block(rb + 32, g, e);  // next block (past the chunk: zeros, no traffic)
     load_ops(rb + 32, pa, pb);
     if (xform) {  // F -= Pl Qh^T: A = -Pl (row, rank), B = Qh^T (rank, column)
@@ -223,14 +249,20 @@ __global__ __launch_bounds__(kWideBlock, 2) void k_wqstep(KArgs a) {
     for (int v = 0; v < 16; ++v)
       bst1_nt(E, coff == kOut ? kOut : u32(rb + drow(v, h)) * row_bytes + coff, x[v]);
 #pragma unroll
-    for (int v = 0; v < 16; ++v) q = mfma(x[v], cb[v], q);  // Q += F^T Ph: A = F^T, B = Ph
+    for (int v = 0; v < 16; ++v)  // Q += F^T Ph: A = F^T, B = Ph
+#pragma unroll
+      for (int kb = 0; kb < NR; ++kb) q[kb] = mfma(x[v], cb[kb][v], q[kb]);
   }
   const int64_t ncb = (m + d.q_cb - 1) / d.q_cb;
   const int64_t stride = ncb * d.q_cb * RK;  // one row chunk of partials
   float* part = a.qpart + d.qpart + static_cast<int64_t>(t.a) * stride + c0 * RK;
-  if (li < RK)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) part[drow(v, h) * RK + li] = q[v];
+  for (int kb = 0; kb < NR; ++kb) {
+    const int rank = kb * 32 + li;
+    if (rank < RK)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) part[drow(v, h) * RK + rank] = q[kb][v];
+  }
 }
 
 // Decompress: M_hat = A B^T / p over a tile (32-row block t.a, 1024-column group t.b), one wave
@@ -322,6 +354,7 @@ hipError_t launch_wide(const Launch& l, int32_t rank, const KArgs& args, hipStre
     case 8: return launch_wide_rank<8>(l, args, s);
     case 16: return launch_wide_rank<16>(l, args, s);
     case 32: return launch_wide_rank<32>(l, args, s);
+    case 64: return launch_wide_rank<64>(l, args, s);
     default: return hipErrorInvalidValue;
   }
 }

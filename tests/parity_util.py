@@ -68,8 +68,10 @@ class Report:
 class Runner:
     """One library context plus the device buffers of every bucket."""
 
-    def __init__(self, shapes, rank, seed=0, cap=25 << 20, world=1, ef=True, device="cuda:0"):
+    def __init__(self, shapes, rank, seed=0, cap=25 << 20, world=1, ef=True, device="cuda:0",
+                 grouped=False):
         self.dev = torch.device(device)
+        self.grouped = grouped  # step() through acp_compress_all / acp_decompress_all
         self.acp = Acp(shapes, rank, seed=seed, cap_bytes=cap, world_size=world, ef=ef, device=self.dev)
         self.nb = self.acp.num_buckets()
         self.info = [self.acp.bucket_info(b) for b in range(self.nb)]
@@ -99,6 +101,10 @@ class Runner:
         return bufs
 
     def step(self, t: int, gbufs: Sequence[torch.Tensor], buckets: Optional[Sequence[int]] = None):
+        if self.grouped and buckets is None:  # the launch configuration bench.py times
+            self.acp.compress_all(t, gbufs, self.fbuf)
+            self.acp.decompress_all(t, self.fbuf, self.out)
+            return
         for b in (range(self.nb) if buckets is None else buckets):
             self.acp.compress(t, b, gbufs[b], self.fbuf[b])
             self.acp.decompress(t, b, self.fbuf[b], self.out[b])
@@ -171,7 +177,7 @@ def read_state_into(run: Runner, orc: AcpOracle, t_done: int, tids: Sequence[int
 
 def run_parity(wl: sg.Workload, mode: str, steps: int, check: Sequence[int], tids: Sequence[int],
                ef: bool = True, tol: float = TOL, free: Optional[int] = None,
-               device="cuda:0") -> Report:
+               device="cuda:0", grouped: bool = False) -> Report:
     """Parity over ``steps`` steps, comparing the sampled tensors at the ``check`` steps.
 
     Steps 1..``free`` run free: the oracle carries its own fp64 state from step 1.  At a
@@ -184,7 +190,7 @@ def run_parity(wl: sg.Workload, mode: str, steps: int, check: Sequence[int], tid
     free = steps if free is None else free
     shapes = [p.shape for p in wl.params]
     t0 = time.time()
-    run = Runner(shapes, wl.rank, wl.seed, wl.cap_bytes, ef=ef, device=device)
+    run = Runner(shapes, wl.rank, wl.seed, wl.cap_bytes, ef=ef, device=device, grouped=grouped)
     orc = AcpOracle(shapes, wl.rank, seed=wl.seed, cap_bytes=wl.cap_bytes, ef=ef, tensor_ids=tids)
     rep = Report()
     cache: Dict[int, List[torch.Tensor]] = {}

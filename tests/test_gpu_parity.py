@@ -78,11 +78,12 @@ def test_bert_base_100_steps(name):
 
 @pytest.mark.parametrize("name", ["bert_large_r4", "bert_large_r32", "bert_large_r64"])
 def test_bert_large_100_steps(name):
+    """Sampled BERT-large tensors over 100 steps, through the all-bucket calls of bench.py."""
     _require_gpu()
     wl = sg.WORKLOADS[name]
     names = BERT_SAMPLE[:-1] + ["encoder.layer.23.attention.output.dense.weight",
                                 "encoder.layer.23.output.dense.weight"]
-    rep = PU.run_parity(wl, "pool3", 100, CHECK, PU.tids_by_name(wl, names), free=FREE)
+    rep = PU.run_parity(wl, "pool3", 100, CHECK, PU.tids_by_name(wl, names), free=FREE, grouped=True)
     _assert_ok(rep)
 
 

@@ -133,6 +133,7 @@ constexpr int32_t narrow_variant(int32_t m4) {
 }
 
 constexpr int32_t kWideRank = 8;   // ranks at or above this take the K_W* kernels
+constexpr int32_t kBlockedRank = 128;  // ranks whose W K_CHOL forms from Gram partials in global memory
 constexpr int kWideBlock = 64;     // threads per workgroup of K_WPSTEP, K_WQSTEP, K_WRECON: one wave
 constexpr int kWideQCols = 32;     // K_WQSTEP column block (one MFMA block)
 constexpr int kWideQRows = 512;    // K_WQSTEP rows per chunk (at most)

@@ -355,22 +355,95 @@ __device__ void cholesky_w(const double* G, double* w_out) {
   }
 }
 
+// Gram of rows [r0, r1) of X (row-major, RK >= kBlockedRank columns) into `out` (RK x RK
+// doubles, global memory): thread t owns the 4 x 4 blocks t + 256 q, q < QB, of the (RK / 4)^2
+// blocks, over every row of a chunk; the chunk's rows sit in LDS as doubles and the next chunk
+// is requested before the current one's products.  The rows are also copied to `copy` when set.
+template <int RK>
+__device__ void gram_blocked(const float* X, int64_t r0, int64_t r1, double* out, float* copy) {
+  constexpr int CH = 32;
+  constexpr int NB4 = RK / 4, QB = NB4 * NB4 / kBlock;
+  constexpr int PT = CH * RK / kBlock;  // chunk elements per thread
+  static_assert(QB * kBlock == NB4 * NB4, "blocks must spread evenly over the workgroup");
+  __shared__ __align__(16) double sh[CH * RK];
+  int bi[QB], bj[QB];
+  double acc[QB][4][4];
+#pragma unroll
+  for (int q = 0; q < QB; ++q) {
+    const int b = tid() + q * kBlock;
+    bi[q] = 4 * (b / NB4);
+    bj[q] = 4 * (b % NB4);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) acc[q][u][v] = 0.0;
+  }
+  const int64_t end = r1 * RK;
+  float nx[PT];
+  auto fetch = [&](int64_t c0) {
+#pragma unroll
+    for (int k = 0; k < PT; ++k) {
+      const int64_t e = c0 * RK + tid() + k * kBlock;
+      nx[k] = e < end ? X[e] : 0.f;
+    }
+  };
+  fetch(r0);
+  for (int64_t c0 = r0; c0 < r1; c0 += CH) {
+    const int cn = static_cast<int>((r1 - c0) < CH ? (r1 - c0) : CH);
+#pragma unroll
+    for (int k = 0; k < PT; ++k) {
+      const int e = tid() + k * kBlock;
+      sh[e] = static_cast<double>(nx[k]);
+      if (copy && c0 * RK + e < end) copy[c0 * RK + e] = nx[k];
+    }
+    __syncthreads();
+    fetch(c0 + CH);
+    for (int rr = 0; rr < cn; ++rr) {
+#pragma unroll
+      for (int q = 0; q < QB; ++q) {
+        double xi[4], xj[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          xi[u] = sh[rr * RK + bi[q] + u];
+          xj[u] = sh[rr * RK + bj[q] + u];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) acc[q][u][v] = fma(xi[u], xj[v], acc[q][u][v]);
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int q = 0; q < QB; ++q)
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) out[(bi[q] + u) * RK + bj[q] + v] = acc[q][u][v];
+}
+
 // Factor tile: slice t.a of the t.b slices of fact_rows rows of the factor `src` (rows x RK).
 // When `dst` is set the slice is also copied there (the aggregated factor becomes the next
-// step's reused factor).  A factor of one slice finishes W here; otherwise the slice's Gram
-// is stored as a partial and K_CHOL adds the partials and finishes W.
+// step's reused factor).  A factor of one slice finishes W here; otherwise (and always from
+// kBlockedRank on) the slice's Gram is stored as a partial and K_CHOL adds the partials and
+// finishes W.
 template <int RK>
 __device__ void fact_tile(const KArgs& a, const Tile& t, const float* src, float* dst, int64_t rows) {
   const MatDesc d = a.mats[t.idx];
-  __shared__ double G[RK * RK];
   const int64_t r0 = static_cast<int64_t>(t.a) * d.fact_rows;
   const int64_t r1 = r0 + d.fact_rows < rows ? r0 + d.fact_rows : rows;
-  gram_rows<RK>(src, r0, r1, G, dst);
-  if (t.b == 1) {
-    cholesky_w<RK>(G, a.w + d.w_slot);
+  if constexpr (RK >= kBlockedRank) {  // always a partial: K_CHOL forms W
+    gram_blocked<RK>(src, r0, r1, a.gpart + d.gpart + static_cast<int64_t>(t.a) * RK * RK, dst);
   } else {
-    double* part = a.gpart + d.gpart + static_cast<int64_t>(t.a) * RK * RK;
-    for (int e = tid(); e < RK * RK; e += kBlock) part[e] = G[e];
+    __shared__ double G[RK * RK];
+    gram_rows<RK>(src, r0, r1, G, dst);
+    if (t.b == 1) {
+      cholesky_w<RK>(G, a.w + d.w_slot);
+    } else {
+      double* part = a.gpart + d.gpart + static_cast<int64_t>(t.a) * RK * RK;
+      for (int e = tid(); e < RK * RK; e += kBlock) part[e] = G[e];
+    }
   }
 }
 

@@ -29,6 +29,61 @@ __global__ __launch_bounds__(kBlock) void k_fact(KArgs a) {
   fact_tile<RK>(a, t, a.fac + (q ? d.q_slot : d.p_slot), nullptr, q ? d.m : d.n);
 }
 
+// Cholesky and W = R^-1 of a Gram matrix in shared memory for ranks from kBlockedRank on, by the
+// whole workgroup: right-looking over the upper triangle (pivot k: its drop test on thread 0,
+// row k of R scaled in parallel, then the trailing update), with the subtractions in pivot
+// order as in cholesky_w; then column c of W by back substitution on thread c, kept transposed
+// in the strictly lower triangle (the diagonal of W apart).  Dropped pivots give zero rows and
+// columns of R and W.  G[] is overwritten.
+template <int RK>
+__device__ void cholesky_w_blocked(double* G, double* w_out) {
+  __shared__ double g0[RK], wdiag[RK];
+  __shared__ int drop[RK];
+  for (int i = tid(); i < RK; i += kBlock) g0[i] = G[i * RK + i];
+  __syncthreads();
+  for (int k = 0; k < RK; ++k) {
+    if (tid() == 0) {
+      const double dk = G[k * RK + k];
+      const bool keep = g0[k] > 0.0 && dk > kTau * kTau * g0[k];
+      drop[k] = keep ? 0 : 1;
+      G[k * RK + k] = keep ? sqrt(dk) : 0.0;
+    }
+    __syncthreads();
+    const bool keep = drop[k] == 0;
+    const double rkk = G[k * RK + k];
+    for (int j = k + 1 + tid(); j < RK; j += kBlock) G[k * RK + j] = keep ? G[k * RK + j] / rkk : 0.0;
+    __syncthreads();
+    if (keep) {
+      const int n1 = RK - k - 1;
+      for (int e = tid(); e < n1 * n1; e += kBlock) {
+        const int i = k + 1 + e / n1, j = k + 1 + e % n1;
+        if (j >= i) G[i * RK + j] -= G[k * RK + i] * G[k * RK + j];
+      }
+    }
+    __syncthreads();
+  }
+  if (tid() < RK) {
+    const int c = tid();
+    if (drop[c]) {
+      wdiag[c] = 0.0;
+      for (int i = 0; i < c; ++i) G[c * RK + i] = 0.0;
+    } else {
+      const double wc = 1.0 / G[c * RK + c];
+      wdiag[c] = wc;
+      for (int i = c - 1; i >= 0; --i) {  // W[i][c], kept at G[c][i]
+        if (drop[i]) {
+          G[c * RK + i] = 0.0;
+          continue;
+        }
+        double s = G[i * RK + c] * wc;
+        for (int l = i + 1; l < c; ++l) s += G[i * RK + l] * G[c * RK + l];
+        G[c * RK + i] = -s / G[i * RK + i];
+      }
+    }
+    for (int i = 0; i < RK; ++i) w_out[i * RK + c] = i == c ? wdiag[c] : (i < c ? G[c * RK + i] : 0.0);
+  }
+}
+
 // W from the Gram partials of a matrix's t.b slices, added in slice order.
 template <int RK>
 __global__ __launch_bounds__(kBlock) void k_chol(KArgs a) {
@@ -51,7 +106,47 @@ __global__ __launch_bounds__(kBlock) void k_chol(KArgs a) {
     G[e] = s;
   }
   __syncthreads();
-  cholesky_w<RK>(G, a.w + d.w_slot);
+  if constexpr (RK >= kBlockedRank)
+    cholesky_w_blocked<RK>(G, a.w + d.w_slot);
+  else
+    cholesky_w<RK>(G, a.w + d.w_slot);
+}
+
+// Xh = X W for rows [t.a, t.a + t.b) of the P (variant 0) or Q (variant 1) slot, from
+// kBlockedRank on: each thread forms 32 columns of two rows (W in shared memory), the sums over
+// the rank index in increasing order.
+template <int RK>
+__device__ void apply_blocked(const KArgs& a, const Tile& t, const MatDesc& d, const double* W) {
+  constexpr int TPR = RK / 32;            // threads per row
+  constexpr int RPP = 2 * kBlock / TPR;   // rows per pass
+  const int j = tid() % TPR, rp = tid() / TPR;
+  const bool q = a.variant == 1;
+  const float* X = a.fac + (q ? d.q_slot : d.p_slot);
+  float* Y = a.fac + (q ? d.qh_slot : d.ph_slot);
+  for (int base = 0; base < t.b; base += RPP) {
+    const int64_t r0 = static_cast<int64_t>(t.a) + base + 2 * rp;
+    const bool v0 = base + 2 * rp < t.b, v1 = base + 2 * rp + 1 < t.b;
+    double y0[32], y1[32];
+#pragma unroll
+    for (int k = 0; k < 32; ++k) y0[k] = y1[k] = 0.0;
+    for (int l = 0; l < 32 * j + 32; ++l) {
+      const double x0 = v0 ? static_cast<double>(X[r0 * RK + l]) : 0.0;
+      const double x1 = v1 ? static_cast<double>(X[(r0 + 1) * RK + l]) : 0.0;
+#pragma unroll
+      for (int k = 0; k < 32; ++k) {
+        if (32 * j + k >= l) {
+          const double w = W[l * RK + 32 * j + k];
+          y0[k] = fma(x0, w, y0[k]);
+          y1[k] = fma(x1, w, y1[k]);
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 32; ++k) {
+      if (v0) Y[r0 * RK + 32 * j + k] = static_cast<float>(y0[k]);
+      if (v1) Y[(r0 + 1) * RK + 32 * j + k] = static_cast<float>(y1[k]);
+    }
+  }
 }
 
 // Xh = X W for rows [t.a, t.a + t.b) of the P (variant 0) or Q (variant 1) slot.
@@ -62,40 +157,44 @@ __global__ __launch_bounds__(kBlock) void k_apply(KArgs a) {
   __shared__ double W[RK * RK];
   for (int e = tid(); e < RK * RK; e += kBlock) W[e] = a.w[d.w_slot + e];
   __syncthreads();
-  const int64_t row = static_cast<int64_t>(t.a) + tid();
-  if (tid() >= t.b) return;
-  const bool q = a.variant == 1;
-  const float* X = a.fac + (q ? d.q_slot : d.p_slot) + row * RK;
-  float* Y = a.fac + (q ? d.qh_slot : d.ph_slot) + row * RK;
-  double x[RK];
-  float y[RK];
-  if constexpr (RK % 4 == 0) {  // factor slots are 256-byte aligned: rows are 16-byte aligned
+  if constexpr (RK >= kBlockedRank) {
+    apply_blocked<RK>(a, t, d, W);
+  } else {
+    const int64_t row = static_cast<int64_t>(t.a) + tid();
+    if (tid() >= t.b) return;
+    const bool q = a.variant == 1;
+    const float* X = a.fac + (q ? d.q_slot : d.p_slot) + row * RK;
+    float* Y = a.fac + (q ? d.qh_slot : d.ph_slot) + row * RK;
+    double x[RK];
+    float y[RK];
+    if constexpr (RK % 4 == 0) {  // factor slots are 256-byte aligned: rows are 16-byte aligned
 #pragma unroll
-    for (int l = 0; l < RK; l += 4) {
-      const float4 v = *reinterpret_cast<const float4*>(X + l);
-      x[l] = v.x;
-      x[l + 1] = v.y;
-      x[l + 2] = v.z;
-      x[l + 3] = v.w;
+      for (int l = 0; l < RK; l += 4) {
+        const float4 v = *reinterpret_cast<const float4*>(X + l);
+        x[l] = v.x;
+        x[l + 1] = v.y;
+        x[l + 2] = v.z;
+        x[l + 3] = v.w;
+      }
+    } else {
+#pragma unroll
+      for (int l = 0; l < RK; ++l) x[l] = static_cast<double>(X[l]);
     }
-  } else {
 #pragma unroll
-    for (int l = 0; l < RK; ++l) x[l] = static_cast<double>(X[l]);
-  }
+    for (int k = 0; k < RK; ++k) {
+      double s = 0.0;
 #pragma unroll
-  for (int k = 0; k < RK; ++k) {
-    double s = 0.0;
+      for (int l = 0; l <= k; ++l) s = fma(x[l], W[l * RK + k], s);
+      y[k] = static_cast<float>(s);
+    }
+    if constexpr (RK % 4 == 0) {
 #pragma unroll
-    for (int l = 0; l <= k; ++l) s = fma(x[l], W[l * RK + k], s);
-    y[k] = static_cast<float>(s);
-  }
-  if constexpr (RK % 4 == 0) {
+      for (int k = 0; k < RK; k += 4)
+        *reinterpret_cast<float4*>(Y + k) = make_float4(y[k], y[k + 1], y[k + 2], y[k + 3]);
+    } else {
 #pragma unroll
-    for (int k = 0; k < RK; k += 4)
-      *reinterpret_cast<float4*>(Y + k) = make_float4(y[k], y[k + 1], y[k + 2], y[k + 3]);
-  } else {
-#pragma unroll
-    for (int k = 0; k < RK; ++k) Y[k] = y[k];
+      for (int k = 0; k < RK; ++k) Y[k] = y[k];
+    }
   }
 }
 
@@ -1118,64 +1217,77 @@ __global__ __launch_bounds__(kBlock) void k_vec(KArgs a) {
 template <int RK>
 hipError_t launch_rank(const Launch& l, const KArgs& args, hipStream_t s) {
   const dim3 grid(static_cast<unsigned>(l.ntiles)), block(kBlock);
-  switch (l.kernel) {
-    case K_APPLY: hipLaunchKernelGGL(k_apply<RK>, grid, block, 0, s, args); break;
-    case K_PROW: hipLaunchKernelGGL(k_prow<RK>, grid, block, 0, s, args); break;
-    case K_EUPD: hipLaunchKernelGGL(k_eupd<RK>, grid, block, 0, s, args); break;
-    case K_EMAT: hipLaunchKernelGGL(k_emat<RK>, grid, block, 0, s, args); break;
-    case K_FACT: hipLaunchKernelGGL(k_fact<RK>, grid, block, 0, s, args); break;
-    case K_CHOL: hipLaunchKernelGGL(k_chol<RK>, grid, block, 0, s, args); break;
-    case K_QFIN: hipLaunchKernelGGL(k_qfin<RK>, grid, block, 0, s, args); break;
-    case K_QSTEP:
-      if (l.variant == (4 | kQFused)) {
+  if constexpr (RK >= kBlockedRank) {  // only the kernels the r >= 8 launch lists use
+    switch (l.kernel) {
+      case K_APPLY: hipLaunchKernelGGL(k_apply<RK>, grid, block, 0, s, args); break;
+      case K_EMAT: hipLaunchKernelGGL(k_emat<RK>, grid, block, 0, s, args); break;
+      case K_FACT: hipLaunchKernelGGL(k_fact<RK>, grid, block, 0, s, args); break;
+      case K_CHOL: hipLaunchKernelGGL(k_chol<RK>, grid, block, 0, s, args); break;
+      case K_QFIN: hipLaunchKernelGGL(k_qfin<RK>, grid, block, 0, s, args); break;
+      case K_VEC: hipLaunchKernelGGL(k_vec, grid, block, 0, s, args); break;
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  } else {
+    switch (l.kernel) {
+      case K_APPLY: hipLaunchKernelGGL(k_apply<RK>, grid, block, 0, s, args); break;
+      case K_PROW: hipLaunchKernelGGL(k_prow<RK>, grid, block, 0, s, args); break;
+      case K_EUPD: hipLaunchKernelGGL(k_eupd<RK>, grid, block, 0, s, args); break;
+      case K_EMAT: hipLaunchKernelGGL(k_emat<RK>, grid, block, 0, s, args); break;
+      case K_FACT: hipLaunchKernelGGL(k_fact<RK>, grid, block, 0, s, args); break;
+      case K_CHOL: hipLaunchKernelGGL(k_chol<RK>, grid, block, 0, s, args); break;
+      case K_QFIN: hipLaunchKernelGGL(k_qfin<RK>, grid, block, 0, s, args); break;
+      case K_QSTEP:
+        if (l.variant == (4 | kQFused)) {
+          if constexpr (RK == 4) {
+            hipLaunchKernelGGL((k_qstep<4, 4, true>), grid, block, 0, s, args);
+          } else {
+            return hipErrorInvalidValue;
+          }
+        } else if (l.variant == 4) {
+          if constexpr (RK <= 8) {
+            hipLaunchKernelGGL((k_qstep<RK, 4, false>), grid, block, 0, s, args);
+          } else {
+            return hipErrorInvalidValue;
+          }
+        } else if (l.variant == 1) {
+          hipLaunchKernelGGL((k_qstep<RK, 1, false>), grid, block, 0, s, args);
+        } else {
+          return hipErrorInvalidValue;
+        }
+        break;
+      case K_RECON:
+        if (l.variant == 4)
+          hipLaunchKernelGGL((k_recon<RK, 4>), grid, block, 0, s, args);
+        else
+          hipLaunchKernelGGL((k_recon<RK, 1>), grid, block, 0, s, args);
+        break;
+      case K_PFUSED:
         if constexpr (RK == 4) {
-          hipLaunchKernelGGL((k_qstep<4, 4, true>), grid, block, 0, s, args);
+          switch (l.variant) {
+            case 1: hipLaunchKernelGGL(k_pfused<1>, grid, block, 0, s, args); break;
+            case 2: hipLaunchKernelGGL(k_pfused<2>, grid, block, 0, s, args); break;
+            case 3: hipLaunchKernelGGL(k_pfused<3>, grid, block, 0, s, args); break;
+            case 4: hipLaunchKernelGGL(k_pfused<4>, grid, block, 0, s, args); break;
+            case 5: hipLaunchKernelGGL(k_pfused<5>, grid, block, 0, s, args); break;
+            default: return hipErrorInvalidValue;
+          }
+          break;
         } else {
           return hipErrorInvalidValue;
         }
-      } else if (l.variant == 4) {
-        if constexpr (RK <= 8) {
-          hipLaunchKernelGGL((k_qstep<RK, 4, false>), grid, block, 0, s, args);
+      case K_RECON4:
+        if constexpr (RK == 4) {
+          hipLaunchKernelGGL(k_recon4, grid, block, 0, s, args);
+          break;
         } else {
           return hipErrorInvalidValue;
         }
-      } else if (l.variant == 1) {
-        hipLaunchKernelGGL((k_qstep<RK, 1, false>), grid, block, 0, s, args);
-      } else {
-        return hipErrorInvalidValue;
-      }
-      break;
-    case K_RECON:
-      if (l.variant == 4)
-        hipLaunchKernelGGL((k_recon<RK, 4>), grid, block, 0, s, args);
-      else
-        hipLaunchKernelGGL((k_recon<RK, 1>), grid, block, 0, s, args);
-      break;
-    case K_PFUSED:
-      if constexpr (RK == 4) {
-        switch (l.variant) {
-          case 1: hipLaunchKernelGGL(k_pfused<1>, grid, block, 0, s, args); break;
-          case 2: hipLaunchKernelGGL(k_pfused<2>, grid, block, 0, s, args); break;
-          case 3: hipLaunchKernelGGL(k_pfused<3>, grid, block, 0, s, args); break;
-          case 4: hipLaunchKernelGGL(k_pfused<4>, grid, block, 0, s, args); break;
-          case 5: hipLaunchKernelGGL(k_pfused<5>, grid, block, 0, s, args); break;
-          default: return hipErrorInvalidValue;
-        }
-        break;
-      } else {
-        return hipErrorInvalidValue;
-      }
-    case K_RECON4:
-      if constexpr (RK == 4) {
-        hipLaunchKernelGGL(k_recon4, grid, block, 0, s, args);
-        break;
-      } else {
-        return hipErrorInvalidValue;
-      }
-    case K_VEC: hipLaunchKernelGGL(k_vec, grid, block, 0, s, args); break;
-    default: return hipErrorInvalidValue;
+      case K_VEC: hipLaunchKernelGGL(k_vec, grid, block, 0, s, args); break;
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
   }
-  return hipGetLastError();
 }
 
 }  // namespace
@@ -1192,6 +1304,7 @@ hipError_t launch(const Launch& l, int32_t rank, const KArgs& args, hipStream_t 
     case 16: return launch_rank<16>(l, args, s);
     case 32: return launch_rank<32>(l, args, s);
     case 64: return launch_rank<64>(l, args, s);
+    case 128: return launch_rank<128>(l, args, s);
     default: return hipErrorInvalidValue;
   }
 }

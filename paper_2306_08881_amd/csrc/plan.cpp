@@ -36,7 +36,9 @@ constexpr int64_t kSlotAlign = 64;      // floats (256 bytes)
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 int64_t align_up(int64_t x, int64_t a) { return cdiv(x, a) * a; }
 
-bool rank_supported(int32_t r) { return r == 1 || r == 2 || r == 4 || r == 8 || r == 16 || r == 32 || r == 64; }
+bool rank_supported(int32_t r) {
+  return r == 1 || r == 2 || r == 4 || r == 8 || r == 16 || r == 32 || r == 64 || r == 128;
+}
 
 struct TileSink {
   std::vector<Tile>& tiles;
@@ -217,7 +219,8 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       // rows per chunk: kQRows (kWideQRows), fewer when a chunk's byte extent would pass 2^30
       // (the kernels address a tile with 32-bit offsets from the tile's first element)
       d.q_rows = static_cast<int32_t>(std::max<int64_t>(
-          1, std::min<int64_t>(wide ? kWideQRows : kQRows, (int64_t(1) << 30) / (t.m * 4))));
+          1, std::min<int64_t>(wide ? (r >= kBlockedRank ? 4 * kWideQRows : kWideQRows) : kQRows,
+                               (int64_t(1) << 30) / (t.m * 4))));
       // a small matrix the general kernels take is split into at least 4 chunks (16 rows or
       // more each), so its Q-step is not one workgroup's serial walk
       const bool fast = r == 4 && vec4 && d.fac_off_p % 4 == 0 && d.fac_off_q % 4 == 0 && t.m / 4 <= 1280;
@@ -248,7 +251,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       d.gpart = gpart;
       {
         const int64_t nsl = std::max(d.fact_slices_p, d.fact_slices_q);
-        if (nsl > 1) gpart += nsl * r * r;
+        if (nsl > 1 || r >= kBlockedRank) gpart += nsl * r * r;
       }
       d.w_slot = static_cast<int64_t>(plan.mats.size()) * r * r;
       t.mat = static_cast<int32_t>(plan.mats.size());
@@ -285,7 +288,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   auto chol_tiles = [&](int32_t mi, bool q) {
     const MatDesc& d = plan.mats[mi];
     const int32_t nsl = q ? d.fact_slices_q : d.fact_slices_p;
-    if (nsl > 1) plan.tiles.push_back(Tile{T_FACT, mi, 0, nsl});
+    if (nsl > 1 || r >= kBlockedRank) plan.tiles.push_back(Tile{T_FACT, mi, 0, nsl});
   };
   auto row_tiles = [&](int32_t mi, int64_t rows_per_tile) {
     const MatDesc& d = plan.mats[mi];

@@ -1,4 +1,4 @@
-// gfx950 MFMA kernels of the ACP-SGD compressor for ranks 8 to 64 (arXiv 2306.08881,
+// gfx950 MFMA kernels of the ACP-SGD compressor for ranks 8 to 128 (arXiv 2306.08881,
 // Algorithm 2).  At these ranks a step costs 2r multiply-adds per gradient element against
 // 12 bytes of HBM traffic, more than the fp32 vector units sustain at full bandwidth, so the
 // rank-r contractions run on v_mfma_f32_32x32x2f32.
@@ -9,9 +9,10 @@
 //            P_loc = X Qh;  afterwards E = X - P_loc Qh^T is implied.
 //   Q-step:  F = M + E_arena (- Pl Qh^T when the arena holds X), F written to the arena,
 //            Q_loc = F^T Ph; afterwards E = F - Ph Q_loc^T is implied.
-// Each is one rank-r correction and one rank-r product per element.  Rank 64 keeps two 32-rank
-// blocks of the product's output per wave; its compress kernels run one wave per SIMD (their
-// operands take every VGPR) instead of spilling.
+// Each is one rank-r correction and one rank-r product per element.  Ranks 64 and 128 keep
+// r / 32 blocks of the product's output per wave; their compress kernels run one wave per SIMD
+// (their operands take every VGPR) instead of spilling, and at rank 128 the operands the tile
+// reuses sit in LDS.
 //
 // MFMA layout (one wave): D (32 x 32) += A (32 x 2) B (2 x 32).  Lane l supplies
 // A[l % 32][l / 32] and B[l / 32][l % 32]; register v of lane l holds D[drow(v, l / 32)][l % 32].
@@ -86,10 +87,24 @@ __global__ __launch_bounds__(kWideBlock, RK > 32 ? 1 : 2) void k_wpstep(KArgs a)
   const Rsrc Qlr = tile_rsrc(a.fac + d.ql_slot, fform ? u32(m) * RK * 4u : 0u);
   const Rsrc Qhr = tile_rsrc(a.fac + d.qh_slot, u32(m) * RK * 4u);
   const bool ph4 = aligned16(a.fac + d.ph_slot), ql4 = aligned16(a.fac + d.ql_slot);
-  float pa[KH];  // correction A operand: -Ph[r0 + l % 32][KH h + s]
-  load_run<KH>(Phr, u32(li * RK + KH * h) * 4u, ph4, pa);
+  // from kBlockedRank on the tile's Ph rows sit in LDS (padded rows) and the block operands are
+  // loaded for the current block instead of one block ahead: the VGPRs hold P's accumulators
+  constexpr bool BIG = RK >= kBlockedRank;
+  constexpr int PL = RK + 1;
+  __shared__ float phs[BIG ? 32 * PL : 1];
+  float pa[BIG ? 1 : KH];  // correction A operand: -Ph[r0 + l % 32][KH h + s]
+  if constexpr (BIG) {
+    const float* Ph = a.fac + d.ph_slot + r0 * RK;
+    for (int e = lane; e < 32 * RK; e += kWideBlock) {
+      const int r = e / RK, k = e % RK;
+      phs[r * PL + k] = (fform && r < rows) ? -Ph[r * RK + k] : 0.f;
+    }
+    __syncthreads();
+  } else {
+    load_run<KH>(Phr, u32(li * RK + KH * h) * 4u, ph4, pa);
 #pragma unroll
-  for (int s = 0; s < KH; ++s) pa[s] = -pa[s];
+    for (int s = 0; s < KH; ++s) pa[s] = -pa[s];
+  }
 
   auto load_block = [&](int64_t c0, float* g, float* e) {
     const uint32_t coff = c0 + li < m ? u32(c0 + li) * 4u : kOut;
@@ -116,29 +131,37 @@ __global__ __launch_bounds__(kWideBlock, RK > 32 ? 1 : 2) void k_wpstep(KArgs a)
   __shared__ float xt[2][32 * LD];
   float g[16], e[16], qa[KH], qb[NR][16];
   load_block(0, g, e);
-  load_ops(0, qa, qb);
+  if constexpr (!BIG) load_ops(0, qa, qb);
 
   v16f p[NR];
 #pragma unroll
   for (int kb = 0; kb < NR; ++kb) p[kb] = zero16();
   int buf = 0;
   for (int64_t c0 = 0; c0 < m; c0 += 32, buf ^= 1) {
+    if constexpr (BIG) load_ops(c0, qa, qb);
     v16f x;
 #pragma unroll
     for (int v = 0; v < 16; ++v) x[v] = g[v] + e[v];
-    float ca[KH], cb[NR][16];
+    float ca[BIG ? 1 : KH], cb[BIG ? 1 : NR][16];
+    if constexpr (!BIG) {
 #pragma unroll
-    for (int s = 0; s < KH; ++s) ca[s] = qa[s];
+      for (int s = 0; s < KH; ++s) ca[s] = qa[s];
 #pragma unroll
-    for (int kb = 0; kb < NR; ++kb)
+      for (int kb = 0; kb < NR; ++kb)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) cb[kb][v] = qb[kb][v];
+        for (int v = 0; v < 16; ++v) cb[kb][v] = qb[kb][v];
+    }
     const uint32_t coff = c0 + li < m ? u32(c0 + li) * 4u : kOut;
     load_block(c0 + 32, g, e);  // next block (past m: zeros, no traffic)
-    load_ops(c0 + 32, qa, qb);
+    if constexpr (!BIG) load_ops(c0 + 32, qa, qb);
     if (fform) {  // X -= Ph Ql^T: A = -Ph (row, rank), B = Ql^T (rank, column)
 #pragma unroll
-      for (int s = 0; s < KH; ++s) x = mfma(pa[s], ca[s], x);
+      for (int s = 0; s < KH; ++s) {
+        if constexpr (BIG)
+          x = mfma(phs[li * PL + KH * h + s], qa[s], x);
+        else
+          x = mfma(pa[s], ca[s], x);
+      }
     }
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
@@ -150,7 +173,12 @@ __global__ __launch_bounds__(kWideBlock, RK > 32 ? 1 : 2) void k_wpstep(KArgs a)
     for (int v = 0; v < 16; ++v) {  // P += X Qh: A = X (row, column), B = Qh (column, rank)
       const float xa = xt[buf][li * LD + drow(v, h)];
 #pragma unroll
-      for (int kb = 0; kb < NR; ++kb) p[kb] = mfma(xa, cb[kb][v], p[kb]);
+      for (int kb = 0; kb < NR; ++kb) {
+        if constexpr (BIG)
+          p[kb] = mfma(xa, qb[kb][v], p[kb]);
+        else
+          p[kb] = mfma(xa, cb[kb][v], p[kb]);
+      }
     }
   }
 
@@ -197,9 +225,23 @@ __global__ __launch_bounds__(kWideBlock, RK > 32 ? 1 : 2) void k_wqstep(KArgs a)
   const Rsrc Qhr = tile_rsrc(a.fac + d.qh_slot + c0 * RK, xform ? u32(w) * RK * 4u : 0u);
   const Rsrc Plr = tile_rsrc(a.fac + d.pl_slot + r0 * RK, xform ? u32(rows) * RK * 4u : 0u);
   const Rsrc Phr = tile_rsrc(a.fac + d.ph_slot + r0 * RK, u32(rows) * RK * 4u);
-  float qv[KH];  // correction B operand: Qh[c0 + l % 32][KH h + s]
+  // from kBlockedRank on the block's Qh rows sit in LDS (padded rows) and the row blocks'
+  // operands are loaded for the current block instead of one block ahead
+  constexpr bool BIG = RK >= kBlockedRank;
+  constexpr int PL = RK + 1;
+  __shared__ float qvs[BIG ? 32 * PL : 1];
+  float qv[BIG ? 1 : KH];  // correction B operand: Qh[c0 + l % 32][KH h + s]
+  if constexpr (BIG) {
+    const float* Qh = a.fac + d.qh_slot + c0 * RK;
+    for (int e = lane; e < 32 * RK; e += kWideBlock) {
+      const int c = e / RK, k = e % RK;
+      qvs[c * PL + k] = (xform && c < w) ? Qh[c * RK + k] : 0.f;
+    }
+    __syncthreads();
+  } else {
 #pragma unroll
-  for (int s = 0; s < KH; ++s) qv[s] = bld1(Qhr, u32(li * RK + KH * h + s) * 4u);
+    for (int s = 0; s < KH; ++s) qv[s] = bld1(Qhr, u32(li * RK + KH * h + s) * 4u);
+  }
   const uint32_t coff = li < w ? u32(li) * 4u : kOut;
 
   const bool pl4 = aligned16(a.fac + d.pl_slot);
@@ -224,26 +266,34 @@ __global__ __launch_bounds__(kWideBlock, RK > 32 ? 1 : 2) void k_wqstep(KArgs a)
   };
   float g[16], e[16], pa[KH], pb[NR][16];
   load_block(0, g, e);
-  load_ops(0, pa, pb);
+  if constexpr (!BIG) load_ops(0, pa, pb);
   v16f q[NR];
 #pragma unroll
   for (int kb = 0; kb < NR; ++kb) q[kb] = zero16();
   for (int rb = 0; rb < rows; rb += 32) {
+    if constexpr (BIG) load_ops(rb, pa, pb);
     v16f x;
 #pragma unroll
     for (int v = 0; v < 16; ++v) x[v] = g[v] + e[v];
-    float ca[KH], cb[NR][16];
+    float ca[BIG ? 1 : KH], cb[BIG ? 1 : NR][16];
+    if constexpr (!BIG) {
 #pragma unroll
-    for (int s = 0; s < KH; ++s) ca[s] = pa[s];
+      for (int s = 0; s < KH; ++s) ca[s] = pa[s];
 #pragma unroll
-    for (int kb = 0; kb < NR; ++kb)
+      for (int kb = 0; kb < NR; ++kb)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) cb[kb][v] = pb[kb][v];
+        for (int v = 0; v < 16; ++v) cb[kb][v] = pb[kb][v];
+    }
     load_block(rb + 32, g, e);  // next block (past the chunk: zeros, no traffic)
-    load_ops(rb + 32, pa, pb);
+    if constexpr (!BIG) load_ops(rb + 32, pa, pb);
     if (xform) {  // F -= Pl Qh^T: A = -Pl (row, rank), B = Qh^T (rank, column)
 #pragma unroll
-      for (int s = 0; s < KH; ++s) x = mfma(-ca[s], qv[s], x);
+      for (int s = 0; s < KH; ++s) {
+        if constexpr (BIG)
+          x = mfma(-pa[s], qvs[li * PL + KH * h + s], x);
+        else
+          x = mfma(-ca[s], qv[s], x);
+      }
     }
 #pragma unroll
     for (int v = 0; v < 16; ++v)
@@ -251,7 +301,12 @@ __global__ __launch_bounds__(kWideBlock, RK > 32 ? 1 : 2) void k_wqstep(KArgs a)
 #pragma unroll
     for (int v = 0; v < 16; ++v)  // Q += F^T Ph: A = F^T, B = Ph
 #pragma unroll
-      for (int kb = 0; kb < NR; ++kb) q[kb] = mfma(x[v], cb[kb][v], q[kb]);
+      for (int kb = 0; kb < NR; ++kb) {
+        if constexpr (BIG)
+          q[kb] = mfma(x[v], pb[kb][v], q[kb]);
+        else
+          q[kb] = mfma(x[v], cb[kb][v], q[kb]);
+      }
   }
   const int64_t ncb = (m + d.q_cb - 1) / d.q_cb;
   const int64_t stride = ncb * d.q_cb * RK;  // one row chunk of partials
@@ -355,6 +410,7 @@ hipError_t launch_wide(const Launch& l, int32_t rank, const KArgs& args, hipStre
     case 16: return launch_wide_rank<16>(l, args, s);
     case 32: return launch_wide_rank<32>(l, args, s);
     case 64: return launch_wide_rank<64>(l, args, s);
+    case 128: return launch_wide_rank<128>(l, args, s);
     default: return hipErrorInvalidValue;
   }
 }

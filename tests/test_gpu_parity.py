@@ -76,7 +76,7 @@ def test_bert_base_100_steps(name):
     _assert_ok(rep)
 
 
-@pytest.mark.parametrize("name", ["bert_large_r4", "bert_large_r32", "bert_large_r64"])
+@pytest.mark.parametrize("name", ["bert_large_r4", "bert_large_r32", "bert_large_r64", "bert_large_r128"])
 def test_bert_large_100_steps(name):
     """Sampled BERT-large tensors over 100 steps, through the all-bucket calls of bench.py."""
     _require_gpu()
@@ -100,7 +100,7 @@ RAGGED = [(37, 3, 3), (5, 7), (129, 1030), (64,), (300, 147), (3,), (1000, 2048)
           (2, 900), (17, 4100), (260, 4608), (7, 5121)]
 
 
-@pytest.mark.parametrize("rank", [1, 2, 4, 8, 16, 32, 64])
+@pytest.mark.parametrize("rank", [1, 2, 4, 8, 16, 32, 64, 128])
 def test_ragged_shapes_all_ranks(rank):
     _require_gpu()
     _assert_ok(_custom(RAGGED, rank))

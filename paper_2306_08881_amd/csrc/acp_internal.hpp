@@ -95,7 +95,8 @@ enum TileKind : int32_t { T_ROWS = 0, T_FACT = 1, T_VEC = 2, T_QTILE = 3, T_SROW
 //               rows are not 16-byte aligned: n <= kSmallRows, m <= kSmallCols)
 // kind T_SROWS: idx = matrix, a = first row, b = cb | stride << 4 | count << 16: columns
 //               [1024 cb, 1024 cb + 1024) of rows a + k stride, k < count
-// kind T_FACT : idx = matrix, a = slice, b = slice count
+// kind T_FACT : idx = matrix, a = slice (+ 65536 x quarter of the Gram blocks from kBlockedRank
+//               on), b = slice count
 // kind T_VEC  : idx = vector, a = first element, b = element count
 // kind T_QTILE: idx = matrix, a = row chunk (K_QSTEP) or entry block (K_QFIN), b = column block
 struct Tile {
@@ -134,6 +135,7 @@ constexpr int32_t narrow_variant(int32_t m4) {
 
 constexpr int32_t kWideRank = 8;   // ranks at or above this take the K_W* kernels
 constexpr int32_t kBlockedRank = 128;  // ranks whose W K_CHOL forms from Gram partials in global memory
+constexpr int32_t kGramQuarters = 4;   // from kBlockedRank on a slice's Gram is split over 4 tiles
 constexpr int kWideBlock = 64;     // threads per workgroup of K_WPSTEP, K_WQSTEP, K_WRECON: one wave
 constexpr int kWideQCols = 32;     // K_WQSTEP column block (one MFMA block)
 constexpr int kWideQRows = 512;    // K_WQSTEP rows per chunk (at most)

@@ -30,57 +30,65 @@ __global__ __launch_bounds__(kBlock) void k_fact(KArgs a) {
 }
 
 // Cholesky and W = R^-1 of a Gram matrix in shared memory for ranks from kBlockedRank on, by the
-// whole workgroup: right-looking over the upper triangle (pivot k: its drop test on thread 0,
-// row k of R scaled in parallel, then the trailing update), with the subtractions in pivot
-// order as in cholesky_w; then column c of W by back substitution on thread c, kept transposed
-// in the strictly lower triangle (the diagonal of W apart).  Dropped pivots give zero rows and
-// columns of R and W.  G[] is overwritten.
+// whole workgroup: right-looking over the upper triangle, one barrier per pivot (every thread
+// takes pivot k's drop test; the trailing update, one row per wave at a time, subtracts
+// G_ki G_kj / d_k with the rows still unscaled, in pivot order); the rows of R are scaled once
+// at the end.  Then column c of W = R^-1 on thread c by
+// back substitution from the last row up.  W[i][c] (i < c) is kept in the strictly lower
+// triangle at G[RK-1-i][RK-1-c], where the threads of a row step touch adjacent words (and
+// every thread reads the same row of R), its diagonal apart.  Dropped pivots give zero rows
+// and columns of R and W.  G[] is overwritten.
 template <int RK>
 __device__ void cholesky_w_blocked(double* G, double* w_out) {
   __shared__ double g0[RK], wdiag[RK];
   __shared__ int drop[RK];
   for (int i = tid(); i < RK; i += kBlock) g0[i] = G[i * RK + i];
   __syncthreads();
+  const int wave = tid() / kWave, lane = tid() % kWave;
   for (int k = 0; k < RK; ++k) {
-    if (tid() == 0) {
-      const double dk = G[k * RK + k];
-      const bool keep = g0[k] > 0.0 && dk > kTau * kTau * g0[k];
-      drop[k] = keep ? 0 : 1;
-      G[k * RK + k] = keep ? sqrt(dk) : 0.0;
-    }
-    __syncthreads();
-    const bool keep = drop[k] == 0;
-    const double rkk = G[k * RK + k];
-    for (int j = k + 1 + tid(); j < RK; j += kBlock) G[k * RK + j] = keep ? G[k * RK + j] / rkk : 0.0;
-    __syncthreads();
+    const double dk = G[k * RK + k];
+    const bool keep = g0[k] > 0.0 && dk > kTau * kTau * g0[k];
+    if (tid() == 0) drop[k] = keep ? 0 : 1;
     if (keep) {
-      const int n1 = RK - k - 1;
-      for (int e = tid(); e < n1 * n1; e += kBlock) {
-        const int i = k + 1 + e / n1, j = k + 1 + e % n1;
-        if (j >= i) G[i * RK + j] -= G[k * RK + i] * G[k * RK + j];
+      const double inv = 1.0 / dk;
+      static_assert(RK % kWave == 0, "rows of whole waves");
+#pragma unroll 4
+      for (int i = k + 1 + wave; i < RK; i += kBlock / kWave) {
+        const double gki = G[k * RK + i] * inv;
+#pragma unroll
+        for (int jj = 0; jj < RK; jj += kWave) {
+          const int j = i + jj + lane;
+          if (j < RK) G[i * RK + j] -= gki * G[k * RK + j];
+        }
       }
     }
     __syncthreads();
   }
+  // R: row k = G_k / sqrt(d_k) (zero for a dropped pivot)
+  for (int k = wave; k < RK; k += kBlock / kWave) {
+    const bool keep = drop[k] == 0;
+    const double rkk = keep ? sqrt(G[k * RK + k]) : 0.0;
+    for (int j = k + 1 + lane; j < RK; j += kWave) G[k * RK + j] = keep ? G[k * RK + j] / rkk : 0.0;
+    if (lane == 0) G[k * RK + k] = rkk;
+  }
+  __syncthreads();
   if (tid() < RK) {
     const int c = tid();
-    if (drop[c]) {
-      wdiag[c] = 0.0;
-      for (int i = 0; i < c; ++i) G[c * RK + i] = 0.0;
-    } else {
-      const double wc = 1.0 / G[c * RK + c];
-      wdiag[c] = wc;
-      for (int i = c - 1; i >= 0; --i) {  // W[i][c], kept at G[c][i]
-        if (drop[i]) {
-          G[c * RK + i] = 0.0;
-          continue;
-        }
-        double s = G[i * RK + c] * wc;
-        for (int l = i + 1; l < c; ++l) s += G[i * RK + l] * G[c * RK + l];
-        G[c * RK + i] = -s / G[i * RK + i];
+    auto wt = [&](int i) -> double& { return G[(RK - 1 - i) * RK + (RK - 1 - c)]; };  // W[i][c], i < c
+    const bool kc = drop[c] == 0;
+    wdiag[c] = kc ? 1.0 / G[c * RK + c] : 0.0;
+    for (int i = RK - 1; i >= 0; --i) {
+      if (i >= c) continue;
+      double w = 0.0;
+      if (kc && drop[i] == 0) {
+        double s = G[i * RK + c] * wdiag[c];
+#pragma unroll 8
+        for (int l = i + 1; l < c; ++l) s += G[i * RK + l] * wt(l);
+        w = -s / G[i * RK + i];
       }
+      wt(i) = w;
     }
-    for (int i = 0; i < RK; ++i) w_out[i * RK + c] = i == c ? wdiag[c] : (i < c ? G[c * RK + i] : 0.0);
+    for (int i = 0; i < RK; ++i) w_out[i * RK + c] = i < c ? wt(i) : (i == c ? wdiag[c] : 0.0);
   }
 }
 
@@ -91,19 +99,34 @@ __global__ __launch_bounds__(kBlock) void k_chol(KArgs a) {
   const MatDesc d = a.mats[t.idx];
   __shared__ double G[RK * RK];
   const double* gp = a.gpart + d.gpart;
-  for (int e = tid(); e < RK * RK; e += kBlock) {
-    // eight slices' partials requested together, added in slice order
-    double s = 0.0;
+  // EU entries x eight slices' partials requested together, each entry added in slice order
+  constexpr int EU = RK >= kBlockedRank ? 4 : 1;
+  for (int e0 = tid(); e0 < RK * RK; e0 += EU * kBlock) {
+    double s[EU];
+#pragma unroll
+    for (int u = 0; u < EU; ++u) s[u] = 0.0;
     int sl = 0;
     for (; sl + 8 <= t.b; sl += 8) {
-      double v[8];
+      double v[EU][8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = gp[static_cast<int64_t>(sl + u) * RK * RK + e];
+      for (int u = 0; u < EU; ++u)
 #pragma unroll
-      for (int u = 0; u < 8; ++u) s += v[u];
+        for (int w = 0; w < 8; ++w) {
+          const int e = e0 + u * kBlock;
+          v[u][w] = e < RK * RK ? gp[static_cast<int64_t>(sl + w) * RK * RK + e] : 0.0;
+        }
+#pragma unroll
+      for (int u = 0; u < EU; ++u)
+#pragma unroll
+        for (int w = 0; w < 8; ++w) s[u] += v[u][w];
     }
-    for (; sl < t.b; ++sl) s += gp[static_cast<int64_t>(sl) * RK * RK + e];
-    G[e] = s;
+    for (; sl < t.b; ++sl)
+#pragma unroll
+      for (int u = 0; u < EU; ++u)
+        if (e0 + u * kBlock < RK * RK) s[u] += gp[static_cast<int64_t>(sl) * RK * RK + e0 + u * kBlock];
+#pragma unroll
+    for (int u = 0; u < EU; ++u)
+      if (e0 + u * kBlock < RK * RK) G[e0 + u * kBlock] = s[u];
   }
   __syncthreads();
   if constexpr (RK >= kBlockedRank)
@@ -113,38 +136,45 @@ __global__ __launch_bounds__(kBlock) void k_chol(KArgs a) {
 }
 
 // Xh = X W for rows [t.a, t.a + t.b) of the P (variant 0) or Q (variant 1) slot, from
-// kBlockedRank on: each thread forms 32 columns of two rows (W in shared memory), the sums over
-// the rank index in increasing order.
+// kBlockedRank on: passes of 32 rows staged in LDS (padded rows); thread t forms the 16 columns
+// 16 (t % 8) ... of row t / 8 of the pass, each a sum over the rank index in increasing order up
+// to the block's last column (W is upper triangular: its zeros below the diagonal add nothing).
+// W sits in LDS with column kk at kk + kk / 16 (the eight blocks a wave reads hit other banks).
+template <int RK>
+constexpr int apply_wl() { return RK + RK / 16; }
 template <int RK>
 __device__ void apply_blocked(const KArgs& a, const Tile& t, const MatDesc& d, const double* W) {
-  constexpr int TPR = RK / 32;            // threads per row
-  constexpr int RPP = 2 * kBlock / TPR;   // rows per pass
-  const int j = tid() % TPR, rp = tid() / TPR;
+  constexpr int WL = apply_wl<RK>();
+  constexpr int NJ = RK / 16;          // 16-column blocks
+  constexpr int RP = kBlock / NJ;      // rows per pass
+  constexpr int XL = RK + 1;           // padded X row (floats)
+  __shared__ float xs[RP * XL];
+  const int jb = tid() % NJ, rr = tid() / NJ;
   const bool q = a.variant == 1;
   const float* X = a.fac + (q ? d.q_slot : d.p_slot);
   float* Y = a.fac + (q ? d.qh_slot : d.ph_slot);
-  for (int base = 0; base < t.b; base += RPP) {
-    const int64_t r0 = static_cast<int64_t>(t.a) + base + 2 * rp;
-    const bool v0 = base + 2 * rp < t.b, v1 = base + 2 * rp + 1 < t.b;
-    double y0[32], y1[32];
-#pragma unroll
-    for (int k = 0; k < 32; ++k) y0[k] = y1[k] = 0.0;
-    for (int l = 0; l < 32 * j + 32; ++l) {
-      const double x0 = v0 ? static_cast<double>(X[r0 * RK + l]) : 0.0;
-      const double x1 = v1 ? static_cast<double>(X[(r0 + 1) * RK + l]) : 0.0;
-#pragma unroll
-      for (int k = 0; k < 32; ++k) {
-        if (32 * j + k >= l) {
-          const double w = W[l * RK + 32 * j + k];
-          y0[k] = fma(x0, w, y0[k]);
-          y1[k] = fma(x1, w, y1[k]);
-        }
-      }
+  for (int base = 0; base < t.b; base += RP) {
+    __syncthreads();  // the previous pass is done with xs
+    for (int e = tid(); e < RP * RK; e += kBlock) {
+      const int r = e / RK, l = e % RK;
+      xs[r * XL + l] = base + r < t.b ? X[(static_cast<int64_t>(t.a) + base + r) * RK + l] : 0.f;
     }
+    __syncthreads();
+    double y[16];
 #pragma unroll
-    for (int k = 0; k < 32; ++k) {
-      if (v0) Y[r0 * RK + 32 * j + k] = static_cast<float>(y0[k]);
-      if (v1) Y[(r0 + 1) * RK + 32 * j + k] = static_cast<float>(y1[k]);
+    for (int k = 0; k < 16; ++k) y[k] = 0.0;
+    const double* wb = W + 17 * jb;  // column 16 jb of row 0
+    for (int l = 0; l < 16 * jb + 16; ++l) {
+      const double xl = xs[rr * XL + l];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) y[k] = fma(xl, wb[l * WL + k], y[k]);
+    }
+    if (base + rr < t.b) {
+      float4* Y4 = reinterpret_cast<float4*>(Y + (static_cast<int64_t>(t.a) + base + rr) * RK + 16 * jb);
+#pragma unroll
+      for (int k = 0; k < 16; k += 4)
+        Y4[k / 4] = make_float4(static_cast<float>(y[k]), static_cast<float>(y[k + 1]),
+                                static_cast<float>(y[k + 2]), static_cast<float>(y[k + 3]));
     }
   }
 }
@@ -154,10 +184,18 @@ template <int RK>
 __global__ __launch_bounds__(kBlock) void k_apply(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
-  __shared__ double W[RK * RK];
-  for (int e = tid(); e < RK * RK; e += kBlock) W[e] = a.w[d.w_slot + e];
+  constexpr bool BIG = RK >= kBlockedRank;
+  __shared__ double W[BIG ? RK * apply_wl<RK>() : RK * RK];
+  for (int e = tid(); e < RK * RK; e += kBlock) {
+    if constexpr (BIG) {
+      const int l = e / RK, k = e % RK;
+      W[l * apply_wl<RK>() + k + k / 16] = a.w[d.w_slot + e];
+    } else {
+      W[e] = a.w[d.w_slot + e];
+    }
+  }
   __syncthreads();
-  if constexpr (RK >= kBlockedRank) {
+  if constexpr (BIG) {
     apply_blocked<RK>(a, t, d, W);
   } else {
     const int64_t row = static_cast<int64_t>(t.a) + tid();

@@ -243,9 +243,11 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       d.bucket = b;
       // factor rows per Gram slice: at r <= 8 up to 8192 (one slice, and no K_CHOL, for
       // factors of at most 8192 rows); at r >= 16 at least 256 and at most 32 slices per factor
-      // (K_CHOL adds a factor's slice partials in one workgroup)
+      // (K_CHOL adds a factor's slice partials in one workgroup), 16 from kBlockedRank on, where
+      // four tiles share a slice's Gram
       d.fact_rows = r <= 8 ? 8192
-                           : static_cast<int32_t>(std::max<int64_t>(256, align_up(cdiv(std::max(t.n, t.m), 32), 64)));
+                           : static_cast<int32_t>(std::max<int64_t>(
+                                 256, align_up(cdiv(std::max(t.n, t.m), r >= kBlockedRank ? 16 : 32), 64)));
       d.fact_slices_p = static_cast<int32_t>(cdiv(t.n, d.fact_rows));
       d.fact_slices_q = static_cast<int32_t>(cdiv(t.m, d.fact_rows));
       d.gpart = gpart;
@@ -282,7 +284,9 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   auto fact_tiles = [&](int32_t mi, bool q) {
     const MatDesc& d = plan.mats[mi];
     const int32_t nsl = q ? d.fact_slices_q : d.fact_slices_p;
-    for (int32_t s = 0; s < nsl; ++s) plan.tiles.push_back(Tile{T_FACT, mi, s, nsl});
+    const int32_t nq = r >= kBlockedRank ? kGramQuarters : 1;
+    for (int32_t s = 0; s < nsl; ++s)
+      for (int32_t q4 = 0; q4 < nq; ++q4) plan.tiles.push_back(Tile{T_FACT, mi, s + 65536 * q4, nsl});
   };
   // Gram finish of the factors of more than one slice
   auto chol_tiles = [&](int32_t mi, bool q) {
@@ -663,9 +667,10 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         const double cols = std::min<double>(d.q_cb, m - double(t.b) * d.q_cb);
         return rows * cols * eb + (t.b == 0 ? rows * rr * 8.0 : 0.0);
       }
-      case K_WFACT: {
+      case K_WFACT: {  // from kBlockedRank on, the first quarter's tile reads and copies the rows
         const double rows = odd ? n : m;
-        return std::min<double>(d.fact_rows, rows - double(t.a) * d.fact_rows) * rr * 8.0;
+        if (t.a >> 16) return 0.0;
+        return std::min<double>(d.fact_rows, rows - double(t.a & 0xffff) * d.fact_rows) * rr * 8.0;
       }
       case K_WRECON: {
         const double rows = std::min<double>(32.0, n - 32.0 * t.a);
@@ -675,7 +680,8 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       case K_APPLY:
         return t.b * rr * 8.0;
       case K_FACT:
-        return std::min<double>(d.fact_rows, (l.variant & 1 ? m : n) - double(t.a) * d.fact_rows) * rr * 4.0;
+        if (t.a >> 16) return 0.0;
+        return std::min<double>(d.fact_rows, (l.variant & 1 ? m : n) - double(t.a & 0xffff) * d.fact_rows) * rr * 4.0;
       case K_EMAT:
         return t.b * m * 8.0;
       default:

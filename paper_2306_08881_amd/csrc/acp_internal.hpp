@@ -143,6 +143,8 @@ constexpr int kWideRCols = 1024;   // K_WRECON columns per tile: 32 blocks of 32
 
 // K_QSTEP variants: column slots per lane | kQFused when the kernel also orthogonalises P
 constexpr int32_t kQFused = 16;
+// K_PFUSED variant bit: S = 1 on three waves, for rows of 516 to 768 columns
+constexpr int32_t kThreeWaves = 32;
 // K_FACT variants: bit 0 = Q (else P); the factor is read from its state slot
 
 struct Launch {

@@ -160,7 +160,7 @@ __device__ void vec_tile(const KArgs& a, const Tile& t, bool compress) {
   const int64_t foff = a.parity ? v.fac_off_p : v.fac_off_q;
   const float* src = src_of(a, v.bucket);
   float* dst = dst_of(a, v.bucket);
-  for (int i = tid(); i < t.b; i += kBlock) {
+  for (int i = tid(); i < t.b; i += static_cast<int>(blockDim.x)) {  // launches of 3 or 4 waves
     const int64_t k = static_cast<int64_t>(t.a) + i;
     if (compress)
       dst[foff + k] = src[v.grad_off + k];

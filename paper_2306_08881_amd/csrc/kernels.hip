@@ -655,13 +655,14 @@ __device__ inline void narrow_recon(const KArgs& a, const Tile& t, const MatDesc
 }
 
 // ---------------------------------------------------------------------------------------
-// Column mapping shared by the rank-4 streaming kernels.  The four waves of a workgroup split
-// a row of m4 = m / 4 float4 groups into four segments of 64 Se groups, Se = ceil(m4 / 256) <= S
+// Column mapping shared by the rank-4 streaming kernels.  The W waves of a workgroup (four, or
+// three for rows of at most 768 columns) split a row of m4 = m / 4 float4 groups into W
+// segments of 64 Se groups, Se = ceil(m4 / 64 W) <= S
 // (a launch of class S also carries rows of smaller classes); lane `lane` of wave w owns groups
 // w * 64 Se + s * 64 + lane, s < Se, for every row of the tile, so the factor rows of those
 // columns are loaded once per workgroup and kept in registers.  The waves work on the same RB
 // rows at a time (8 for S = 1, 2 for S = 2..4, 1 for S = 5).
-template <int S>
+template <int S, int W = 4>
 struct Cols {
   static constexpr int RB = S == 1 ? 8 : (S <= 4 ? 2 : 1);
   int wave, lane;
@@ -670,7 +671,7 @@ struct Cols {
   __device__ explicit Cols(int m4) {
     wave = tid() >> 6;
     lane = tid() & 63;
-    const int se = (m4 + 255) >> 8;
+    const int se = (m4 + 64 * W - 1) / (64 * W);
 #pragma unroll
     for (int s = 0; s < S; ++s) {
       c4[s] = wave * 64 * se + s * 64 + lane;
@@ -687,16 +688,16 @@ struct Cols {
 // order), E = M' - P Qh^T written back, P written to the factor buffer.  The next rows' M and
 // E are requested before the reduction; all streamed accesses are tile-relative buffer
 // accesses (E's resource is empty when error feedback is off).
-template <int S>
-__global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
-  constexpr int RB = Cols<S>::RB;
+template <int S, int W = 4>
+__global__ __launch_bounds__(64 * W) void k_pfused(KArgs a) {
+  constexpr int RB = Cols<S, W>::RB;
   const Tile t = a.tiles[blockIdx.x];
   if (t.kind == T_VEC) {
     vec_tile(a, t, true);
     return;
   }
   const MatDesc d = a.mats[t.idx];
-  if constexpr (S == 1) {
+  if constexpr (S == 1 && W == 4) {
     if (t.kind == T_ROWS) {  // a narrow-row matrix's tile (the S = 1 launch carries them)
       __shared__ double Wn[16];
       narrow_pstep(a, t, d, Wn);
@@ -710,7 +711,7 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
     }
   }
   const int m4 = d.m >> 2;
-  const Cols<S> cl(m4);
+  const Cols<S, W> cl(m4);
   const bool deferred = deferred_of(a, d.bucket);
   // tile rows t.a + k * stride, k < rows (T_SROWS)
   const int stride = (t.b >> 4) & 0xfff, rows = t.b >> 16;
@@ -741,12 +742,12 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
   load_rows(0);
 
   __shared__ double Wsh[16];
-  __shared__ float4 red[2][4][RB];
+  __shared__ float4 red[2][W][RB];
   __shared__ float4 phs[kMaxTileRows];  // the tile's rows of Ph (zero unless E is deferred)
   if (tid() < 16) Wsh[tid()] = a.w[d.w_slot + tid()];
-  if (tid() < rows)
-    phs[tid()] = deferred ? reinterpret_cast<const float4*>(a.fac + d.ph_slot)[t.a + static_cast<int64_t>(tid()) * stride]
-                          : zero4();
+  for (int i = tid(); i < rows; i += 64 * W)
+    phs[i] = deferred ? reinterpret_cast<const float4*>(a.fac + d.ph_slot)[t.a + static_cast<int64_t>(i) * stride]
+                      : zero4();
   __syncthreads();
 
   const float4* Q4 = reinterpret_cast<const float4*>(a.fac + d.q_slot);
@@ -799,7 +800,9 @@ __global__ __launch_bounds__(kBlock) void k_pfused(KArgs a) {
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
       const uint32_t roff = static_cast<uint32_t>(r0 + rb) * step_bytes;
-      const float4 Pr = ((red[buf][0][rb] + red[buf][1][rb]) + red[buf][2][rb]) + red[buf][3][rb];
+      float4 Pr = red[buf][0][rb];  // the waves' sums in wave order
+#pragma unroll
+      for (int w = 1; w < W; ++w) Pr = Pr + red[buf][w][rb];
 #pragma unroll
       for (int s = 0; s < S; ++s) {
         float4 r = mp[rb][s];
@@ -1304,6 +1307,9 @@ hipError_t launch_rank(const Launch& l, const KArgs& args, hipStream_t s) {
         if constexpr (RK == 4) {
           switch (l.variant) {
             case 1: hipLaunchKernelGGL(k_pfused<1>, grid, block, 0, s, args); break;
+            case 1 | kThreeWaves:
+              hipLaunchKernelGGL((k_pfused<1, 3>), grid, dim3(3 * kWave), 0, s, args);
+              break;
             case 2: hipLaunchKernelGGL(k_pfused<2>, grid, block, 0, s, args); break;
             case 3: hipLaunchKernelGGL(k_pfused<3>, grid, block, 0, s, args); break;
             case 4: hipLaunchKernelGGL(k_pfused<4>, grid, block, 0, s, args); break;

@@ -78,9 +78,9 @@ typedef enum {
  *   num_tensors      number of parameters, in registration (forward) order.
  *   ndims[i]         rank of parameter i (1..8); dims holds all dims flattened, each in
  *                    1..2^31.  A compressed matrix (ndims >= 2 and r < min(n, m), n = dim 0,
- *                    m = product of the others) may have at most 2^24 columns m; a longer
- *                    one returns ACP_E_INVALID.
- *   rank             r: 1, 2, 4, 8, 16, 32, 64 or 128.
+ *                    m = product of the others) may have at most min(2^24, (2^32 - 1) / (4 r))
+ *                    columns m; a longer one returns ACP_E_INVALID.
+ *   rank             r: 1, 2, 4, 8, 16, 32, 64, 128 or 256.
  *   seed             key of the initial-factor draw: element i (row-major) of P_0 (f = 0) or
  *                    Q_0 (f = 1) of tensor k is z = sqrt(-2 ln u1) cos(2 pi u2) rounded to fp32,
  *                    with s = mix(seed ^ mix(2k + f)), u1 = ((mix(s + (2i+1)g) >> 11) + 1) 2^-53,

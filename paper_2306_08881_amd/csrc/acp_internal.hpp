@@ -90,13 +90,14 @@ struct VecDesc {
 
 enum TileKind : int32_t { T_ROWS = 0, T_FACT = 1, T_VEC = 2, T_QTILE = 3, T_SROWS = 4, T_SMALL = 5 };
 
-// kind T_ROWS : idx = matrix, a = first row, b = row count
+// kind T_ROWS : idx = matrix, a = first row, b = row count (K_APPLY from kSplitRank on: + 65536 x
+//               the 64-column block of Xh)
 // kind T_SMALL: idx = matrix, the whole matrix in one workgroup (rank 4, small matrices whose
 //               rows are not 16-byte aligned: n <= kSmallRows, m <= kSmallCols)
 // kind T_SROWS: idx = matrix, a = first row, b = cb | stride << 4 | count << 16: columns
 //               [1024 cb, 1024 cb + 1024) of rows a + k stride, k < count
-// kind T_FACT : idx = matrix, a = slice (+ 65536 x quarter of the Gram blocks from kBlockedRank
-//               on), b = slice count
+// kind T_FACT : idx = matrix, a = slice (+ 65536 x part of the Gram blocks from kBlockedRank
+//               on: gram_parts(r) parts), b = slice count
 // kind T_VEC  : idx = vector, a = first element, b = element count
 // kind T_QTILE: idx = matrix, a = row chunk (K_QSTEP) or entry block (K_QFIN), b = column block
 struct Tile {
@@ -135,8 +136,13 @@ constexpr int32_t narrow_variant(int32_t m4) {
 
 constexpr int32_t kWideRank = 8;   // ranks at or above this take the K_W* kernels
 constexpr int32_t kBlockedRank = 128;  // ranks whose W K_CHOL forms from Gram partials in global memory
-constexpr int32_t kGramQuarters = 4;   // from kBlockedRank on a slice's Gram is split over 4 tiles
+// ranks whose MFMA kernels split the rank blocks over the four waves of a workgroup, whose W is
+// factored in 2 x 2 blocks and whose Xh = X W runs per 64-column block
+constexpr int32_t kSplitRank = 256;
+// tiles that share one slice's Gram: 4 from kBlockedRank on, 16 from kSplitRank on
+constexpr int32_t gram_parts(int32_t r) { return r >= kSplitRank ? 16 : (r >= kBlockedRank ? 4 : 1); }
 constexpr int kWideBlock = 64;     // threads per workgroup of K_WPSTEP, K_WQSTEP, K_WRECON: one wave
+constexpr int kSplitBlock = 256;   // the same from kSplitRank on: four waves
 constexpr int kWideQCols = 32;     // K_WQSTEP column block (one MFMA block)
 constexpr int kWideQRows = 512;    // K_WQSTEP rows per chunk (at most)
 constexpr int kWideRCols = 1024;   // K_WRECON columns per tile: 32 blocks of 32

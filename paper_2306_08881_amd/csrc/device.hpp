@@ -355,23 +355,24 @@ __device__ void cholesky_w(const double* G, double* w_out) {
   }
 }
 
-// Quarter `quarter` of the Gram of rows [r0, r1) of X (row-major, RK >= kBlockedRank columns)
-// into `out` (RK x RK doubles, global memory): of the (RK / 4)^2 blocks of 4 x 4 the quarter
-// holds a contiguous fourth, thread t owning blocks t + 256 q, q < QB, over every row of a
+// Part `part` of the Gram of rows [r0, r1) of X (row-major, RK >= kBlockedRank columns) into
+// `out` (RK x RK doubles, global memory): of the (RK / 4)^2 blocks of 4 x 4 the part holds a
+// contiguous 1 / gram_parts(RK), thread t owning blocks t + 256 q, q < QB, over every row of a
 // chunk; the chunk's rows sit in LDS as doubles and the next chunk is requested before the
 // current one's products.  The rows are also copied to `copy` when set.
 template <int RK>
-__device__ void gram_blocked(const float* X, int64_t r0, int64_t r1, double* out, float* copy, int quarter) {
+__device__ void gram_blocked(const float* X, int64_t r0, int64_t r1, double* out, float* copy, int part) {
   constexpr int CH = 32;
-  constexpr int NB4 = RK / 4, QB = NB4 * NB4 / (kBlock * kGramQuarters);
+  constexpr int NP = gram_parts(RK);
+  constexpr int NB4 = RK / 4, QB = NB4 * NB4 / (kBlock * NP);
   constexpr int PT = CH * RK / kBlock;  // chunk elements per thread
-  static_assert(QB * kBlock * kGramQuarters == NB4 * NB4, "blocks must spread evenly over the workgroups");
+  static_assert(QB >= 1 && QB * kBlock * NP == NB4 * NB4, "blocks must spread evenly over the workgroups");
   __shared__ __align__(16) double sh[CH * RK];
   int bi[QB], bj[QB];
   double acc[QB][4][4];
 #pragma unroll
   for (int q = 0; q < QB; ++q) {
-    const int b = quarter * QB * kBlock + tid() + q * kBlock;
+    const int b = part * QB * kBlock + tid() + q * kBlock;
     bi[q] = 4 * (b / NB4);
     bj[q] = 4 * (b % NB4);
 #pragma unroll
@@ -433,11 +434,11 @@ template <int RK>
 __device__ void fact_tile(const KArgs& a, const Tile& t, const float* src, float* dst, int64_t rows) {
   const MatDesc d = a.mats[t.idx];
   if constexpr (RK >= kBlockedRank) {  // always a partial: K_CHOL forms W
-    const int sl = t.a & 0xffff, quarter = t.a >> 16;
+    const int sl = t.a & 0xffff, part = t.a >> 16;
     const int64_t r0 = static_cast<int64_t>(sl) * d.fact_rows;
     const int64_t r1 = r0 + d.fact_rows < rows ? r0 + d.fact_rows : rows;
     gram_blocked<RK>(src, r0, r1, a.gpart + d.gpart + static_cast<int64_t>(sl) * RK * RK,
-                     quarter == 0 ? dst : nullptr, quarter);
+                     part == 0 ? dst : nullptr, part);
   } else {
     const int64_t r0 = static_cast<int64_t>(t.a) * d.fact_rows;
     const int64_t r1 = r0 + d.fact_rows < rows ? r0 + d.fact_rows : rows;

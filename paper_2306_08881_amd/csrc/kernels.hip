@@ -37,12 +37,15 @@ __global__ __launch_bounds__(kBlock) void k_fact(KArgs a) {
 // back substitution from the last row up.  W[i][c] (i < c) is kept in the strictly lower
 // triangle at G[RK-1-i][RK-1-c], where the threads of a row step touch adjacent words (and
 // every thread reads the same row of R), its diagonal apart.  Dropped pivots give zero rows
-// and columns of R and W.  G[] is overwritten.
+// and columns of R and W.  G[] is overwritten.  The drop test compares with the diagonal
+// gref[i * gstride] (G's own unless given: a trailing block of a larger Gram matrix is tested
+// against that matrix's diagonal); W goes to w_out with rows ldw apart.
 template <int RK>
-__device__ void cholesky_w_blocked(double* G, double* w_out) {
+__device__ void cholesky_w_blocked(double* G, double* w_out, int ldw = RK, const double* gref = nullptr,
+                                   int gstride = 0) {
   __shared__ double g0[RK], wdiag[RK];
   __shared__ int drop[RK];
-  for (int i = tid(); i < RK; i += kBlock) g0[i] = G[i * RK + i];
+  for (int i = tid(); i < RK; i += kBlock) g0[i] = gref ? gref[i * gstride] : G[i * RK + i];
   __syncthreads();
   const int wave = tid() / kWave, lane = tid() % kWave;
   for (int k = 0; k < RK; ++k) {
@@ -88,8 +91,65 @@ __device__ void cholesky_w_blocked(double* G, double* w_out) {
       }
       wt(i) = w;
     }
-    for (int i = 0; i < RK; ++i) w_out[i * RK + c] = i < c ? wt(i) : (i == c ? wdiag[c] : 0.0);
+    for (int i = 0; i < RK; ++i) w_out[i * ldw + c] = i < c ? wt(i) : (i == c ? wdiag[c] : 0.0);
   }
+}
+
+// C = A B for 128 x 128 fp64 blocks in global or shared memory, by the whole workgroup: thread t
+// forms the 8 x 8 block at rows 8 (t / 16), columns 8 (t % 16), each entry a sum over k < 128
+// in increasing order, with A[i][k] = A[i * ai + k * ak] and B[k][j] = B[k * bk + j];
+// store(i, j, value) takes the entries.
+template <typename Store>
+__device__ void mm128(const double* A, int ai, int ak, const double* B, int bk, Store store) {
+  static_assert(kBlock == 256, "16 x 16 threads of 8 x 8 entries");
+  const int i0 = 8 * (tid() / 16), j0 = 8 * (tid() % 16);
+  double c[8][8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u)
+#pragma unroll
+    for (int v = 0; v < 8; ++v) c[u][v] = 0.0;
+  for (int k = 0; k < 128; ++k) {
+    double x[8], y[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) x[u] = A[(i0 + u) * ai + k * ak];
+#pragma unroll
+    for (int v = 0; v < 8; ++v) y[v] = B[k * bk + j0 + v];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int v = 0; v < 8; ++v) c[u][v] = fma(x[u], y[v], c[u][v]);
+  }
+#pragma unroll
+  for (int u = 0; u < 8; ++u)
+#pragma unroll
+    for (int v = 0; v < 8; ++v) store(i0 + u, j0 + v, c[u][v]);
+}
+
+// W = R^-1 of a 256 x 256 Gram matrix G (global memory: the matrix's first Gram partial, which
+// holds the slices' sum) in 2 x 2 blocks of 128, from the factorisation
+//   G11 = R11^T R11,  R12 = R11^-T G12,  G22 - R12^T R12 = R22^T R22,
+//   W11 = R11^-1,  W22 = R22^-1,  W12 = -W11 R12 W22,  W21 = 0,
+// the same pivots in the same order as the unblocked form.  With dropped pivots R11^-T G12 is
+// W11^T G12 (W11's zero columns give R12's zero rows) and the pivots of the second block are
+// tested against G's own diagonal.  R12 (called Y) is kept in G's lower left block, which the
+// upper triangle makes redundant; the shared block S holds G11, then G22 - Y^T Y, then Y W22.
+__device__ void chol_split(double* G, double* W, double* S) {
+  constexpr int N = 256, H = 128;
+  for (int e = tid(); e < H * H; e += kBlock) S[e] = G[(e / H) * N + e % H];
+  __syncthreads();
+  cholesky_w_blocked<H>(S, W, N);  // W11
+  __syncthreads();
+  double* Y = G + H * N;  // Y[i][j] at Y[i * N + j]
+  mm128(W, 1, N, G + H, N, [&](int i, int j, double v) { Y[i * N + j] = v; });  // W11^T G12
+  __syncthreads();
+  mm128(Y, 1, N, Y, N, [&](int i, int j, double v) { S[i * H + j] = G[(H + i) * N + H + j] - v; });
+  __syncthreads();
+  cholesky_w_blocked<H>(S, W + H * N + H, N, G + H * N + H, N + 1);  // W22
+  __syncthreads();
+  mm128(Y, N, 1, W + H * N + H, N, [&](int i, int j, double v) { S[i * H + j] = v; });  // Y W22
+  __syncthreads();
+  mm128(W, N, 1, S, H, [&](int i, int j, double v) { W[i * N + H + j] = -v; });  // -W11 (Y W22)
+  for (int e = tid(); e < H * H; e += kBlock) W[(H + e / H) * N + e % H] = 0.0;
 }
 
 // W from the Gram partials of a matrix's t.b slices, added in slice order.
@@ -97,8 +157,11 @@ template <int RK>
 __global__ __launch_bounds__(kBlock) void k_chol(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
-  __shared__ double G[RK * RK];
-  const double* gp = a.gpart + d.gpart;
+  constexpr bool SPLIT = RK >= kSplitRank;
+  // the sum goes to LDS, or from kSplitRank on in place into the first partial
+  __shared__ double Gs[SPLIT ? 128 * 128 : RK * RK];
+  double* gp = a.gpart + d.gpart;
+  double* G = SPLIT ? gp : Gs;
   // EU entries x eight slices' partials requested together, each entry added in slice order
   constexpr int EU = RK >= kBlockedRank ? 4 : 1;
   for (int e0 = tid(); e0 < RK * RK; e0 += EU * kBlock) {
@@ -129,10 +192,14 @@ __global__ __launch_bounds__(kBlock) void k_chol(KArgs a) {
       if (e0 + u * kBlock < RK * RK) G[e0 + u * kBlock] = s[u];
   }
   __syncthreads();
-  if constexpr (RK >= kBlockedRank)
+  if constexpr (SPLIT) {
+    static_assert(RK == 256, "2 x 2 blocks of 128");
+    chol_split(G, a.w + d.w_slot, Gs);
+  } else if constexpr (RK >= kBlockedRank) {
     cholesky_w_blocked<RK>(G, a.w + d.w_slot);
-  else
+  } else {
     cholesky_w<RK>(G, a.w + d.w_slot);
+  }
 }
 
 // Xh = X W for rows [t.a, t.a + t.b) of the P (variant 0) or Q (variant 1) slot, from
@@ -179,59 +246,126 @@ __device__ void apply_blocked(const KArgs& a, const Tile& t, const MatDesc& d, c
   }
 }
 
+// Xh = X W from kSplitRank on, for rows [t.a, t.a + rows) and the 64 columns c0 = 64 cb ... of
+// Xh (t.b = rows | cb << 16): passes of 128 rows; per pass W's rows come in chunks of 64 up to
+// the block's last column (W is upper triangular), each chunk's 64 x 64 block of W and the
+// pass's rows of X for those ranks staged in LDS.  Thread t forms columns c0 + 8 (t % 8) ... + 7
+// of rows 4 (t / 8) ... + 3 of the pass, each entry a sum over the rank index in increasing order.
+// W sits in LDS with column k at k + k / 8.
+template <int RK>
+__device__ void apply_split(const KArgs& a, const Tile& t, const MatDesc& d) {
+  constexpr int CB = 64, KC = 64, NJ = CB / 8, RG = kBlock / NJ, RP = 4 * RG;
+  constexpr int WL = CB + CB / 8, XL = KC + 1;
+  __shared__ double ws[KC * WL];
+  __shared__ float xs[RP * XL];
+  const int rows = t.b & 0xffff, c0 = CB * (t.b >> 16);
+  const int jb = tid() % NJ, rg = tid() / NJ;
+  const bool q = a.variant == 1;
+  const float* X = a.fac + (q ? d.q_slot : d.p_slot);
+  float* Y = a.fac + (q ? d.qh_slot : d.ph_slot);
+  const double* W = a.w + d.w_slot;
+  for (int base = 0; base < rows; base += RP) {
+    double y[4][8];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int k = 0; k < 8; ++k) y[u][k] = 0.0;
+    for (int k0 = 0; k0 < c0 + CB; k0 += KC) {
+      __syncthreads();  // the previous chunk is done with ws and xs
+      for (int e = tid(); e < KC * CB; e += kBlock) {
+        const int l = e / CB, k = e % CB;
+        ws[l * WL + k + k / 8] = W[static_cast<int64_t>(k0 + l) * RK + c0 + k];
+      }
+      for (int e = tid(); e < RP * KC; e += kBlock) {
+        const int r = e / KC, l = e % KC;
+        xs[r * XL + l] = base + r < rows ? X[(static_cast<int64_t>(t.a) + base + r) * RK + k0 + l] : 0.f;
+      }
+      __syncthreads();
+      const int lend = min(KC, c0 + 8 * jb + 8 - k0);  // ranks past the block's last column add zero
+      const double* wb = ws + 9 * jb;
+      for (int l = 0; l < lend; ++l) {
+        double xl[4], wl[8];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) xl[u] = xs[(4 * rg + u) * XL + l];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) wl[k] = wb[l * WL + k];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int k = 0; k < 8; ++k) y[u][k] = fma(xl[u], wl[k], y[u][k]);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int r = base + 4 * rg + u;
+      if (r < rows) {
+        float4* Y4 = reinterpret_cast<float4*>(Y + (static_cast<int64_t>(t.a) + r) * RK + c0 + 8 * jb);
+        Y4[0] = make_float4(static_cast<float>(y[u][0]), static_cast<float>(y[u][1]),
+                            static_cast<float>(y[u][2]), static_cast<float>(y[u][3]));
+        Y4[1] = make_float4(static_cast<float>(y[u][4]), static_cast<float>(y[u][5]),
+                            static_cast<float>(y[u][6]), static_cast<float>(y[u][7]));
+      }
+    }
+  }
+}
+
 // Xh = X W for rows [t.a, t.a + t.b) of the P (variant 0) or Q (variant 1) slot.
 template <int RK>
 __global__ __launch_bounds__(kBlock) void k_apply(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
-  constexpr bool BIG = RK >= kBlockedRank;
-  __shared__ double W[BIG ? RK * apply_wl<RK>() : RK * RK];
-  for (int e = tid(); e < RK * RK; e += kBlock) {
-    if constexpr (BIG) {
-      const int l = e / RK, k = e % RK;
-      W[l * apply_wl<RK>() + k + k / 16] = a.w[d.w_slot + e];
-    } else {
-      W[e] = a.w[d.w_slot + e];
-    }
-  }
-  __syncthreads();
-  if constexpr (BIG) {
-    apply_blocked<RK>(a, t, d, W);
+  if constexpr (RK >= kSplitRank) {
+    apply_split<RK>(a, t, d);
   } else {
-    const int64_t row = static_cast<int64_t>(t.a) + tid();
-    if (tid() >= t.b) return;
-    const bool q = a.variant == 1;
-    const float* X = a.fac + (q ? d.q_slot : d.p_slot) + row * RK;
-    float* Y = a.fac + (q ? d.qh_slot : d.ph_slot) + row * RK;
-    double x[RK];
-    float y[RK];
-    if constexpr (RK % 4 == 0) {  // factor slots are 256-byte aligned: rows are 16-byte aligned
-#pragma unroll
-      for (int l = 0; l < RK; l += 4) {
-        const float4 v = *reinterpret_cast<const float4*>(X + l);
-        x[l] = v.x;
-        x[l + 1] = v.y;
-        x[l + 2] = v.z;
-        x[l + 3] = v.w;
+    constexpr bool BIG = RK >= kBlockedRank;
+    __shared__ double W[BIG ? RK * apply_wl<RK>() : RK * RK];
+    for (int e = tid(); e < RK * RK; e += kBlock) {
+      if constexpr (BIG) {
+        const int l = e / RK, k = e % RK;
+        W[l * apply_wl<RK>() + k + k / 16] = a.w[d.w_slot + e];
+      } else {
+        W[e] = a.w[d.w_slot + e];
       }
-    } else {
-#pragma unroll
-      for (int l = 0; l < RK; ++l) x[l] = static_cast<double>(X[l]);
     }
-#pragma unroll
-    for (int k = 0; k < RK; ++k) {
-      double s = 0.0;
-#pragma unroll
-      for (int l = 0; l <= k; ++l) s = fma(x[l], W[l * RK + k], s);
-      y[k] = static_cast<float>(s);
-    }
-    if constexpr (RK % 4 == 0) {
-#pragma unroll
-      for (int k = 0; k < RK; k += 4)
-        *reinterpret_cast<float4*>(Y + k) = make_float4(y[k], y[k + 1], y[k + 2], y[k + 3]);
+    __syncthreads();
+    if constexpr (BIG) {
+      apply_blocked<RK>(a, t, d, W);
     } else {
+      const int64_t row = static_cast<int64_t>(t.a) + tid();
+      if (tid() >= t.b) return;
+      const bool q = a.variant == 1;
+      const float* X = a.fac + (q ? d.q_slot : d.p_slot) + row * RK;
+      float* Y = a.fac + (q ? d.qh_slot : d.ph_slot) + row * RK;
+      double x[RK];
+      float y[RK];
+      if constexpr (RK % 4 == 0) {  // factor slots are 256-byte aligned: rows are 16-byte aligned
 #pragma unroll
-      for (int k = 0; k < RK; ++k) Y[k] = y[k];
+        for (int l = 0; l < RK; l += 4) {
+          const float4 v = *reinterpret_cast<const float4*>(X + l);
+          x[l] = v.x;
+          x[l + 1] = v.y;
+          x[l + 2] = v.z;
+          x[l + 3] = v.w;
+        }
+      } else {
+#pragma unroll
+        for (int l = 0; l < RK; ++l) x[l] = static_cast<double>(X[l]);
+      }
+#pragma unroll
+      for (int k = 0; k < RK; ++k) {
+        double s = 0.0;
+#pragma unroll
+        for (int l = 0; l <= k; ++l) s = fma(x[l], W[l * RK + k], s);
+        y[k] = static_cast<float>(s);
+      }
+      if constexpr (RK % 4 == 0) {
+#pragma unroll
+        for (int k = 0; k < RK; k += 4)
+          *reinterpret_cast<float4*>(Y + k) = make_float4(y[k], y[k + 1], y[k + 2], y[k + 3]);
+      } else {
+#pragma unroll
+        for (int k = 0; k < RK; ++k) Y[k] = y[k];
+      }
     }
   }
 }
@@ -1349,6 +1483,7 @@ hipError_t launch(const Launch& l, int32_t rank, const KArgs& args, hipStream_t 
     case 32: return launch_rank<32>(l, args, s);
     case 64: return launch_rank<64>(l, args, s);
     case 128: return launch_rank<128>(l, args, s);
+    case 256: return launch_rank<256>(l, args, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -37,7 +37,7 @@ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 int64_t align_up(int64_t x, int64_t a) { return cdiv(x, a) * a; }
 
 bool rank_supported(int32_t r) {
-  return r == 1 || r == 2 || r == 4 || r == 8 || r == 16 || r == 32 || r == 64 || r == 128;
+  return r == 1 || r == 2 || r == 4 || r == 8 || r == 16 || r == 32 || r == 64 || r == 128 || r == 256;
 }
 
 struct TileSink {
@@ -61,7 +61,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
                        int32_t rank, int64_t cap_bytes, bool ef) {
   if (num_tensors <= 0) return "num_tensors must be positive";
   if (!ndims || !dims) return "ndims and dims must not be NULL";
-  if (!rank_supported(rank)) return "rank must be one of 1, 2, 4, 8, 16, 32";
+  if (!rank_supported(rank)) return "rank must be one of 1, 2, 4, 8, 16, 32, 64, 128, 256";
   if (cap_bytes <= 0) return "bucket_cap_bytes must be positive";
   plan = Plan{};
   plan.rank = rank;
@@ -89,8 +89,10 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     if (nd >= 2) {
       const int64_t n = t.shape[0], m = numel / n;
       if (r < std::min(n, m)) {
-        if (m > kMaxCols)
-          return "tensor " + std::to_string(i) + ": compressed matrices may have at most 2^24 columns";
+        // the kernels address a factor of m rows of r floats with 32-bit byte offsets
+        if (m > std::min<int64_t>(kMaxCols, ((int64_t(1) << 32) - 1) / (4 * r)))
+          return "tensor " + std::to_string(i) +
+                 ": compressed matrices may have at most min(2^24, (2^32 - 1) / (4 r)) columns";
         t.compressed = true;
         t.n = n;
         t.m = m;
@@ -274,19 +276,23 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
                                   static_cast<int32_t>(std::min(kVecChunk, n - s))});
     }
   };
+  // orthogonalisation tiles of kApplyRows factor rows; from kSplitRank on one per 64-column
+  // block of Xh as well (b = rows | block << 16)
   auto apply_tiles = [&](const std::vector<int32_t>& mats, bool q) {
+    const int32_t ncb = r >= kSplitRank ? static_cast<int32_t>(r / 64) : 1;
     for (int32_t mi : mats) {
       const int64_t rows = q ? plan.mats[mi].m : plan.mats[mi].n;
       for (int64_t s = 0; s < rows; s += kApplyRows)
-        plan.tiles.push_back(Tile{T_ROWS, mi, static_cast<int32_t>(s),
-                                  static_cast<int32_t>(std::min(kApplyRows, rows - s))});
+        for (int32_t cb = 0; cb < ncb; ++cb)
+          plan.tiles.push_back(Tile{T_ROWS, mi, static_cast<int32_t>(s),
+                                    static_cast<int32_t>(std::min(kApplyRows, rows - s)) | (cb << 16)});
     }
   };
   // factor tiles: one per slice of fact_rows factor rows
   auto fact_tiles = [&](int32_t mi, bool q) {
     const MatDesc& d = plan.mats[mi];
     const int32_t nsl = q ? d.fact_slices_q : d.fact_slices_p;
-    const int32_t nq = r >= kBlockedRank ? kGramQuarters : 1;
+    const int32_t nq = gram_parts(static_cast<int32_t>(r));
     for (int32_t s = 0; s < nsl; ++s)
       for (int32_t q4 = 0; q4 < nq; ++q4) plan.tiles.push_back(Tile{T_FACT, mi, s + 65536 * q4, nsl});
   };
@@ -681,7 +687,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         const double cols = std::min<double>(d.q_cb, m - double(t.b) * d.q_cb);
         return rows * cols * eb + (t.b == 0 ? rows * rr * 8.0 : 0.0);
       }
-      case K_WFACT: {  // from kBlockedRank on, the first quarter's tile reads and copies the rows
+      case K_WFACT: {  // from kBlockedRank on, the first part's tile reads and copies the rows
         const double rows = odd ? n : m;
         if (t.a >> 16) return 0.0;
         return std::min<double>(d.fact_rows, rows - double(t.a & 0xffff) * d.fact_rows) * rr * 8.0;
@@ -691,8 +697,8 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         const double cols = std::min<double>(kWideRCols, m - double(kWideRCols) * t.b);
         return rows * cols * 4.0 + (t.b == 0 ? rows * rr * 4.0 : 0.0) + (t.a == 0 ? cols * rr * 4.0 : 0.0);
       }
-      case K_APPLY:
-        return t.b * rr * 8.0;
+      case K_APPLY:  // from kSplitRank on a tile covers one of r / 64 column blocks
+        return (t.b & 0xffff) * rr * 8.0 / (r >= kSplitRank ? rr / 64.0 : 1.0);
       case K_FACT:
         if (t.a >> 16) return 0.0;
         return std::min<double>(d.fact_rows, (l.variant & 1 ? m : n) - double(t.a & 0xffff) * d.fact_rows) * rr * 4.0;

@@ -1,4 +1,4 @@
-// gfx950 MFMA kernels of the ACP-SGD compressor for ranks 8 to 128 (arXiv 2306.08881,
+// gfx950 MFMA kernels of the ACP-SGD compressor for ranks 8 to 256 (arXiv 2306.08881,
 // Algorithm 2).  At these ranks a step costs 2r multiply-adds per gradient element against
 // 12 bytes of HBM traffic, more than the fp32 vector units sustain at full bandwidth, so the
 // rank-r contractions run on v_mfma_f32_32x32x2f32.
@@ -12,7 +12,8 @@
 // Each is one rank-r correction and one rank-r product per element.  Ranks 64 and 128 keep
 // r / 32 blocks of the product's output per wave; their compress kernels run one wave per SIMD
 // (their operands take every VGPR) instead of spilling, and at rank 128 the operands the tile
-// reuses sit in LDS.
+// reuses sit in LDS.  At rank 256 the four waves of a workgroup split the rank (k_spstep,
+// k_sqstep, k_srecon).
 //
 // MFMA layout (one wave): D (32 x 32) += A (32 x 2) B (2 x 32).  Lane l supplies
 // A[l % 32][l / 32] and B[l / 32][l % 32]; register v of lane l holds D[drow(v, l / 32)][l % 32].
@@ -372,6 +373,298 @@ __global__ __launch_bounds__(kWideBlock) void k_wrecon(KArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------------------
+// From kSplitRank on one wave cannot hold the operands of every rank, so the four waves of a
+// 256-thread workgroup split the rank: wave w takes ranks rk0 = 64 w ... rk0 + 63 of each
+// rank-r term (r / 128 K steps per lane half, two 32-rank output blocks), with the operand
+// layout of the kernels above.  A correction (or a decompressed block) is a sum over all ranks,
+// so each wave writes its partial 32 x 32 block to LDS and wave w adds the four partials, in wave
+// order, for its entries v = 4 w + j (j < 4) of the MFMA layout: rows 8 w + 4 (l / 32) + j of the
+// block (drow(4 w + j, h) = 8 w + 4 h + j).  Wave w also loads M and E for those entries only.
+// LDS buffers alternate between blocks, so one barrier per use suffices.
+constexpr int kSplitWaves = kSplitBlock / kWave;
+
+// P-step over a 32-row tile, the 32-column blocks in order: partial corrections -Ph Ql^T (F
+// form) -> X = M + E + their sum for the wave's entries, stored to the arena and to the
+// transposing tile -> P += X Qh over the wave's ranks.  The next block's M, E and factor rows are
+// requested before the current block's MFMAs.
+template <int RK>
+__global__ __launch_bounds__(kSplitBlock, 2) void k_spstep(KArgs a) {
+  constexpr int RS = RK / kSplitWaves, KH = RS / 2, NR = RS / 32;
+  constexpr int LD = 33;
+  const Tile t = a.tiles[blockIdx.x];
+  const MatDesc d = a.mats[t.idx];
+  const int wave = tid() >> 6, lane = tid() & 63, h = lane >> 5, li = lane & 31;
+  const int rk0 = wave * RS;
+  const int64_t m = d.m, r0 = t.a;
+  const int rows = t.b;
+  const bool fform = deferred_of(a, d.bucket);
+  const uint32_t row_bytes = u32(m) * 4u;
+  const uint32_t ext = u32(rows) * row_bytes;
+  const Rsrc G = tile_rsrc(src_of(a, d.bucket) + d.grad_off + r0 * m, ext);
+  const Rsrc E = tile_rsrc(a.e + d.e_off + r0 * m, a.ef ? ext : 0u);
+  const Rsrc Phr = tile_rsrc(a.fac + d.ph_slot + r0 * RK, fform ? u32(rows) * RK * 4u : 0u);
+  const Rsrc Qlr = tile_rsrc(a.fac + d.ql_slot, fform ? u32(m) * RK * 4u : 0u);
+  const Rsrc Qhr = tile_rsrc(a.fac + d.qh_slot, u32(m) * RK * 4u);
+  const bool ph4 = aligned16(a.fac + d.ph_slot), ql4 = aligned16(a.fac + d.ql_slot);
+  float pa[KH];  // correction A operand: -Ph[r0 + l % 32][rk0 + KH h + s]
+  load_run<KH>(Phr, u32(li * RK + rk0 + KH * h) * 4u, ph4, pa);
+#pragma unroll
+  for (int s = 0; s < KH; ++s) pa[s] = -pa[s];
+
+  auto load_block = [&](int64_t c0, float* g, float* e) {  // the wave's four entries
+    const uint32_t coff = c0 + li < m ? u32(c0 + li) * 4u : kOut;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t o = coff == kOut ? kOut : u32(8 * wave + 4 * h + j) * row_bytes + coff;
+      g[j] = bld1_nt(G, o);
+      e[j] = bld1_nt(E, o);
+    }
+  };
+  auto load_ql = [&](int64_t c0, float* qa) {  // correction B operand: Ql rows
+    const int64_t qcol = c0 + li;
+    load_run<KH>(Qlr, qcol < m ? u32(qcol * RK + rk0 + KH * h) * 4u : kOut, ql4, qa);
+  };
+  auto load_qh = [&](int64_t c0, float (*qb)[16]) {  // product B operand: Qh rows
+#pragma unroll
+    for (int kb = 0; kb < NR; ++kb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int64_t col = c0 + drow(v, h);
+        qb[kb][v] = bld1(Qhr, col < m ? u32(col * RK + rk0 + kb * 32 + li) * 4u : kOut);
+      }
+  };
+  __shared__ float red[2][kSplitWaves][16 * kWave];
+  __shared__ float xt[2][32 * LD];
+  float g[4], e[4], qa[KH], qb[NR][16];
+  load_block(0, g, e);
+  if (fform) load_ql(0, qa);
+  load_qh(0, qb);
+  v16f p[NR];
+#pragma unroll
+  for (int kb = 0; kb < NR; ++kb) p[kb] = zero16();
+  int buf = 0;
+  for (int64_t c0 = 0; c0 < m; c0 += 32, buf ^= 1) {
+    // each operand's registers take the next block's values once this block has used them
+    if (fform) {  // the wave's share of -Ph Ql^T: A = -Ph (row, rank), B = Ql^T (rank, column)
+      v16f x = zero16();
+#pragma unroll
+      for (int s = 0; s < KH; ++s) x = mfma(pa[s], qa[s], x);
+      load_ql(c0 + 32, qa);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) red[buf][wave][v * kWave + lane] = x[v];
+      __syncthreads();
+    }
+    float cg[4], ce[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      cg[j] = g[j];
+      ce[j] = e[j];
+    }
+    load_block(c0 + 32, g, e);  // next block (past m: zeros, no traffic)
+    const uint32_t coff = c0 + li < m ? u32(c0 + li) * 4u : kOut;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int v = 4 * wave + j, row = 8 * wave + 4 * h + j;
+      float xv = cg[j] + ce[j];
+      if (fform) {
+        float c = red[buf][0][v * kWave + lane];
+#pragma unroll
+        for (int w = 1; w < kSplitWaves; ++w) c += red[buf][w][v * kWave + lane];
+        xv += c;
+      }
+      bst1_nt(E, coff == kOut ? kOut : u32(row) * row_bytes + coff, xv);
+      xt[buf][row * LD + li] = xv;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {  // P += X Qh: A = X (row, column), B = Qh (column, rank)
+      const float xa = xt[buf][li * LD + drow(v, h)];
+#pragma unroll
+      for (int kb = 0; kb < NR; ++kb) p[kb] = mfma(xa, qb[kb][v], p[kb]);
+    }
+    load_qh(c0 + 32, qb);
+  }
+
+  float* P = dst_of(a, d.bucket) + d.fac_off_p;
+  float* Pl = a.fac + d.pl_slot;
+#pragma unroll
+  for (int kb = 0; kb < NR; ++kb) {
+    const int rank = rk0 + kb * 32 + li;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int row = drow(v, h);
+      if (row < rows) {
+        P[(r0 + row) * RK + rank] = p[kb][v];
+        Pl[(r0 + row) * RK + rank] = p[kb][v];
+      }
+    }
+  }
+}
+
+// Q-step over a tile (row chunk t.a, 32-column block t.b), the 32-row blocks in order: partial
+// corrections -Pl Qh^T (X form) -> F = M + E + their sum for the wave's entries, stored to the
+// arena and shared through LDS -> Q += F^T Ph over the wave's ranks, into the chunk's partials.
+template <int RK>
+__global__ __launch_bounds__(kSplitBlock, 2) void k_sqstep(KArgs a) {
+  constexpr int RS = RK / kSplitWaves, KH = RS / 2, NR = RS / 32;
+  const Tile t = a.tiles[blockIdx.x];
+  const MatDesc d = a.mats[t.idx];
+  const int wave = tid() >> 6, lane = tid() & 63, h = lane >> 5, li = lane & 31;
+  const int rk0 = wave * RS;
+  const int64_t n = d.n, m = d.m;
+  const int64_t r0 = static_cast<int64_t>(t.a) * d.q_rows;
+  const int rows = static_cast<int>((r0 + d.q_rows < n) ? d.q_rows : n - r0);
+  const int64_t c0 = static_cast<int64_t>(t.b) * d.q_cb;
+  const int64_t w = (m - c0) < 32 ? (m - c0) : 32;  // valid columns of the block
+  const bool xform = deferred_p_of(a, d.bucket);
+  const uint32_t row_bytes = u32(m) * 4u;
+  const uint32_t ext = u32(rows - 1) * row_bytes + u32(w) * 4u;
+  const Rsrc G = tile_rsrc(src_of(a, d.bucket) + d.grad_off + r0 * m + c0, ext);
+  const Rsrc E = tile_rsrc(a.e + d.e_off + r0 * m + c0, a.ef ? ext : 0u);
+  const Rsrc Qhr = tile_rsrc(a.fac + d.qh_slot + c0 * RK, xform ? u32(w) * RK * 4u : 0u);
+  const Rsrc Plr = tile_rsrc(a.fac + d.pl_slot + r0 * RK, xform ? u32(rows) * RK * 4u : 0u);
+  const Rsrc Phr = tile_rsrc(a.fac + d.ph_slot + r0 * RK, u32(rows) * RK * 4u);
+  const bool qh4 = aligned16(a.fac + d.qh_slot), pl4 = aligned16(a.fac + d.pl_slot);
+  float qv[KH];  // correction B operand: Qh[c0 + l % 32][rk0 + KH h + s]
+  load_run<KH>(Qhr, u32(li * RK + rk0 + KH * h) * 4u, qh4, qv);
+  const uint32_t coff = li < w ? u32(li) * 4u : kOut;
+
+  auto load_block = [&](int rb, float* g, float* e) {  // the wave's four entries
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t o = coff == kOut ? kOut : u32(rb + 8 * wave + 4 * h + j) * row_bytes + coff;
+      g[j] = bld1_nt(G, o);
+      e[j] = bld1_nt(E, o);
+    }
+  };
+  auto load_ops = [&](int rb, float* pa, float (*pb)[16]) {
+    if (xform) load_run<KH>(Plr, u32((rb + li) * RK + rk0 + KH * h) * 4u, pl4, pa);
+#pragma unroll
+    for (int kb = 0; kb < NR; ++kb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        pb[kb][v] = bld1(Phr, u32((rb + drow(v, h)) * RK + rk0 + kb * 32 + li) * 4u);
+  };
+  __shared__ float red[2][kSplitWaves][16 * kWave];
+  __shared__ float fs[2][16 * kWave];
+  float g[4], e[4], pa[KH], pb[NR][16];
+  load_block(0, g, e);
+  load_ops(0, pa, pb);
+  v16f q[NR];
+#pragma unroll
+  for (int kb = 0; kb < NR; ++kb) q[kb] = zero16();
+  int buf = 0;
+  for (int rb = 0; rb < rows; rb += 32, buf ^= 1) {
+    float cg[4], ce[4], ca[KH], cb[NR][16];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      cg[j] = g[j];
+      ce[j] = e[j];
+    }
+#pragma unroll
+    for (int s = 0; s < KH; ++s) ca[s] = pa[s];
+#pragma unroll
+    for (int kb = 0; kb < NR; ++kb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) cb[kb][v] = pb[kb][v];
+    load_block(rb + 32, g, e);  // next block (past the chunk: zeros, no traffic)
+    load_ops(rb + 32, pa, pb);
+    if (xform) {  // the wave's share of -Pl Qh^T: A = -Pl (row, rank), B = Qh^T (rank, column)
+      v16f x = zero16();
+#pragma unroll
+      for (int s = 0; s < KH; ++s) x = mfma(-ca[s], qv[s], x);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) red[buf][wave][v * kWave + lane] = x[v];
+      __syncthreads();
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int v = 4 * wave + j;
+      float f = cg[j] + ce[j];
+      if (xform) {
+        float c = red[buf][0][v * kWave + lane];
+#pragma unroll
+        for (int w2 = 1; w2 < kSplitWaves; ++w2) c += red[buf][w2][v * kWave + lane];
+        f += c;
+      }
+      bst1_nt(E, coff == kOut ? kOut : u32(rb + 8 * wave + 4 * h + j) * row_bytes + coff, f);
+      fs[buf][v * kWave + lane] = f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {  // Q += F^T Ph: A = F^T, B = Ph
+      const float fv = fs[buf][v * kWave + lane];
+#pragma unroll
+      for (int kb = 0; kb < NR; ++kb) q[kb] = mfma(fv, cb[kb][v], q[kb]);
+    }
+  }
+  const int64_t ncb = (m + d.q_cb - 1) / d.q_cb;
+  const int64_t stride = ncb * d.q_cb * RK;  // one row chunk of partials
+  float* part = a.qpart + d.qpart + static_cast<int64_t>(t.a) * stride + c0 * RK;
+#pragma unroll
+  for (int kb = 0; kb < NR; ++kb)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) part[drow(v, h) * RK + rk0 + kb * 32 + li] = q[kb][v];
+}
+
+// Decompress over a tile (32-row block t.a, 1024-column group t.b): per 32-column block the
+// wave's share of A B^T / p, the shares added in wave order for the wave's entries and stored
+// with nontemporal stores.  The next block's B rows are requested before the current MFMAs.
+template <int RK>
+__global__ __launch_bounds__(kSplitBlock, 2) void k_srecon(KArgs a) {
+  constexpr int RS = RK / kSplitWaves, KH = RS / 2;
+  const Tile t = a.tiles[blockIdx.x];
+  const bool odd = a.parity != 0;
+  const MatDesc d = a.mats[t.idx];
+  const int wave = tid() >> 6, lane = tid() & 63, h = lane >> 5, li = lane & 31;
+  const int rk0 = wave * RS;
+  const int64_t n = d.n, m = d.m;
+  const int64_t r0 = static_cast<int64_t>(t.a) * 32;
+  const int rows = static_cast<int>((r0 + 32 < n) ? 32 : n - r0);
+  const float* agg = src_of(a, d.bucket);
+  const float* A = odd ? agg + d.fac_off_p : a.fac + d.ph_slot;
+  const float* B = odd ? a.fac + d.qh_slot : agg + d.fac_off_q;
+  const Rsrc Ar = tile_rsrc(A + r0 * RK, u32(rows) * RK * 4u);
+  const Rsrc Br = tile_rsrc(B, u32(m) * RK * 4u);
+  const bool a4 = aligned16(A), b4 = aligned16(B);
+  float av[KH];  // A operand: A[r0 + l % 32][rk0 + KH h + s] / p
+  load_run<KH>(Ar, u32(li * RK + rk0 + KH * h) * 4u, a4, av);
+#pragma unroll
+  for (int s = 0; s < KH; ++s) av[s] *= a.inv_p;
+  float* O = dst_of(a, d.bucket) + d.grad_off + r0 * m;
+  const uint32_t row_bytes = u32(m) * 4u;
+  constexpr int NB = kWideRCols / 32;  // column blocks per tile
+  auto bcol = [&](int j) { return static_cast<int64_t>(t.b) * kWideRCols + j * 32; };
+  auto boff = [&](int64_t c) { return c + li < m ? u32((c + li) * RK + rk0 + KH * h) * 4u : kOut; };
+  __shared__ float red[2][kSplitWaves][16 * kWave];
+  float bv[2][KH];  // B operand: B[c0 + l % 32][rk0 + KH h + s], this block and the next
+  load_run<KH>(Br, boff(bcol(0)), b4, bv[0]);
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int64_t c0 = bcol(j);
+    if (c0 >= m) break;
+    if (j + 1 < NB) load_run<KH>(Br, boff(bcol(j + 1)), b4, bv[(j + 1) & 1]);
+    v16f o = zero16();
+#pragma unroll
+    for (int s = 0; s < KH; ++s) o = mfma(av[s], bv[j & 1][s], o);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) red[j & 1][wave][v * kWave + lane] = o[v];
+    __syncthreads();
+    const int64_t w = (m - c0) < 32 ? (m - c0) : 32;
+    const Rsrc Or = tile_rsrc(O + c0, u32(rows - 1) * row_bytes + u32(w) * 4u);
+    const uint32_t coff = li < w ? u32(li) * 4u : kOut;
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const int v = 4 * wave + jj;
+      float s = red[j & 1][0][v * kWave + lane];
+#pragma unroll
+      for (int w2 = 1; w2 < kSplitWaves; ++w2) s += red[j & 1][w2][v * kWave + lane];
+      bst1_nt(Or, coff == kOut ? kOut : u32(8 * wave + 4 * h + jj) * row_bytes + coff, s);
+    }
+  }
+}
+
 // Decompress companions of K_WRECON (whole workgroups): factor tiles keep the aggregated
 // factor as the next step's reused factor and build its W; vector tiles unpack sum / p.
 template <int RK>
@@ -390,13 +683,25 @@ __global__ __launch_bounds__(kBlock) void k_wfact(KArgs a) {
 
 template <int RK>
 hipError_t launch_wide_rank(const Launch& l, const KArgs& args, hipStream_t s) {
-  const dim3 grid(static_cast<unsigned>(l.ntiles)), block(kWideBlock);
-  switch (l.kernel) {
-    case K_WFACT: hipLaunchKernelGGL(k_wfact<RK>, grid, dim3(kBlock), 0, s, args); break;
-    case K_WPSTEP: hipLaunchKernelGGL(k_wpstep<RK>, grid, block, 0, s, args); break;
-    case K_WQSTEP: hipLaunchKernelGGL(k_wqstep<RK>, grid, block, 0, s, args); break;
-    case K_WRECON: hipLaunchKernelGGL(k_wrecon<RK>, grid, block, 0, s, args); break;
-    default: return hipErrorInvalidValue;
+  const dim3 grid(static_cast<unsigned>(l.ntiles));
+  if constexpr (RK >= kSplitRank) {
+    const dim3 block(kSplitBlock);
+    switch (l.kernel) {
+      case K_WFACT: hipLaunchKernelGGL(k_wfact<RK>, grid, dim3(kBlock), 0, s, args); break;
+      case K_WPSTEP: hipLaunchKernelGGL(k_spstep<RK>, grid, block, 0, s, args); break;
+      case K_WQSTEP: hipLaunchKernelGGL(k_sqstep<RK>, grid, block, 0, s, args); break;
+      case K_WRECON: hipLaunchKernelGGL(k_srecon<RK>, grid, block, 0, s, args); break;
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    const dim3 block(kWideBlock);
+    switch (l.kernel) {
+      case K_WFACT: hipLaunchKernelGGL(k_wfact<RK>, grid, dim3(kBlock), 0, s, args); break;
+      case K_WPSTEP: hipLaunchKernelGGL(k_wpstep<RK>, grid, block, 0, s, args); break;
+      case K_WQSTEP: hipLaunchKernelGGL(k_wqstep<RK>, grid, block, 0, s, args); break;
+      case K_WRECON: hipLaunchKernelGGL(k_wrecon<RK>, grid, block, 0, s, args); break;
+      default: return hipErrorInvalidValue;
+    }
   }
   return hipGetLastError();
 }
@@ -411,6 +716,7 @@ hipError_t launch_wide(const Launch& l, int32_t rank, const KArgs& args, hipStre
     case 32: return launch_wide_rank<32>(l, args, s);
     case 64: return launch_wide_rank<64>(l, args, s);
     case 128: return launch_wide_rank<128>(l, args, s);
+    case 256: return launch_wide_rank<256>(l, args, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -72,8 +72,8 @@ def _make() -> Dict[str, Workload]:
     for r in (4, 32):
         w[f"bert_base_r{r}"] = Workload(f"bert_base_r{r}", S.bert_base(), r, 100, _sigma_const(0.02))
         w[f"bert_large_r{r}"] = Workload(f"bert_large_r{r}", S.bert_large(), r, 100, _sigma_const(0.02))
-    # the rank sweep on the BERT-large shapes continues at r = 64 and 128
-    for r in (64, 128):
+    # the rank sweep on the BERT-large shapes continues at r = 64, 128 and 256
+    for r in (64, 128, 256):
         w[f"bert_large_r{r}"] = Workload(f"bert_large_r{r}", S.bert_large(), r, 100, _sigma_const(0.02))
     return w
 

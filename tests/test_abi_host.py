@@ -134,7 +134,10 @@ def test_init_factors_bit_exact(lib, name, tids):
 
 def test_init_errors(lib):
     assert _ctx(lib, [(4, 4)], 3)[0] == L.ACP_E_INVALID          # unsupported rank
-    assert _ctx(lib, [(4, 4)], 256)[0] == L.ACP_E_INVALID
+    assert _ctx(lib, [(4, 4)], 512)[0] == L.ACP_E_INVALID
+    # a factor of m rows of r floats must stay within 32-bit byte offsets
+    assert _ctx(lib, [(300, 1 << 22)], 256)[0] == L.ACP_E_INVALID
+    assert _ctx(lib, [(300, 1 << 24)], 64)[0] == L.ACP_E_INVALID
     assert _ctx(lib, [(4, 4)], 0)[0] == L.ACP_E_INVALID
     assert _ctx(lib, [(4, 4)], 4, cap=0)[0] == L.ACP_E_INVALID
     assert _ctx(lib, [(4, 4)], 4, world=0)[0] == L.ACP_E_INVALID

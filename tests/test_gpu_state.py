@@ -89,7 +89,8 @@ def test_checkpoint_rejects_other_context():
     assert e.value.status == L.ACP_E_STATE
 
 
-@pytest.mark.parametrize("name", ["bert_large_r4", "bert_large_r32", "bert_large_r64", "bert_large_r128"])
+@pytest.mark.parametrize("name", ["bert_large_r4", "bert_large_r32", "bert_large_r64", "bert_large_r128",
+                                  "bert_large_r256"])
 def test_full_size_residual_identity(name):
     wl = sg.WORKLOADS[name]
     shapes = [p.shape for p in wl.params]

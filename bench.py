@@ -81,14 +81,21 @@ def cpu_baseline(wl, seconds: float = 12.0):
 
 def kernel_families(rank: int):
     """(label, ACP_KERNEL_* family, kernel symbol prefix) of the timed kernel families: the rank-4
-    register-resident kernels, or the MFMA kernels of ranks 8 to 64."""
+    register-resident kernels, the one-wave MFMA kernels of ranks 8 to 128 or the rank-split
+    MFMA kernels of rank 256, and the separate orthogonalisation kernels."""
     from paper_2306_08881_amd import _lib as L
-    wide = rank >= 8
-    p, q, d = ("k_wpstep", "k_wqstep", "k_wrecon") if wide else ("k_pfused", "k_qstep", "k_recon")
+    if rank >= 256:
+        p, q, d = "k_spstep", "k_sqstep", "k_srecon"
+    elif rank >= 8:
+        p, q, d = "k_wpstep", "k_wqstep", "k_wrecon"
+    else:
+        p, q, d = "k_pfused", "k_qstep", "k_recon4"
+    orth = "k_apply, k_wfact, k_chol" if rank >= 8 else "k_chol"
     return [(f"P-step compress ({p})", L.ACP_KERNEL_P_STEP, p),
             (f"Q-step compress ({q})", L.ACP_KERNEL_Q_STEP, q),
             ("Q-step finish (k_qfin)", L.ACP_KERNEL_Q_FINISH, "k_qfin"),
-            (f"decompress ({d if wide else 'k_recon4'})", L.ACP_KERNEL_RECONSTRUCT, d)]
+            (f"decompress ({d})", L.ACP_KERNEL_RECONSTRUCT, d),
+            (f"orthogonalisation ({orth})", L.ACP_KERNEL_ORTH, orth)]
 
 
 WORKLOAD_KIND = {"conv": "one 256x64x3x3 convolution gradient", "resnet50": "ResNet-50-shaped gradients",
@@ -154,7 +161,7 @@ def measured_traffic(workload: str, family: str, launches: int):
         return None
     if t.get("source_hash") != kernel_source_hash() or t.get("workload") not in (None, workload):
         return None
-    sym = next((k[2] for k in kernel_families(4) + kernel_families(8) if k[0] == family), None)
+    sym = next((k[2] for k in kernel_families(4) + kernel_families(8) + kernel_families(256) if k[0] == family), None)
     ks = [v for k, v in t["kernels"].items() if sym and k.startswith(sym)]
     if not ks:
         return None

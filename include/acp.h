@@ -216,6 +216,8 @@ acp_status acp_set_state(acp_ctx *ctx, const void *host_buf, int64_t bytes);
 #define ACP_KERNEL_Q_FINISH 3     /* Q-step partial-sum finish */
 #define ACP_KERNEL_RECONSTRUCT 4  /* decompress kernels */
 #define ACP_KERNEL_ORTH 5         /* separate orthogonalisation kernels (general path, r > 8) */
+/* Raw-vector launches of their own (ranks 8 and up) belong to no family; at rank 4 the vectors
+ * ride in the P-step, Q-step and decompress launches. */
 acp_status acp_profile_start(acp_ctx *ctx, int32_t kernel_family, int32_t max_launches);
 acp_status acp_profile_stop(acp_ctx *ctx, int64_t *launches, double *seconds, double *alg_bytes);
 

@@ -97,7 +97,8 @@ enum TileKind : int32_t { T_ROWS = 0, T_FACT = 1, T_VEC = 2, T_QTILE = 3, T_SROW
 // kind T_SROWS: idx = matrix, a = first row, b = cb | stride << 4 | count << 16: columns
 //               [1024 cb, 1024 cb + 1024) of rows a + k stride, k < count
 // kind T_FACT : idx = matrix, a = slice (+ 65536 x part of the Gram blocks from kBlockedRank
-//               on: gram_parts(r) parts), b = slice count
+//               on: gram_parts(r) parts), b = slice count; K_GSUM: a = entry block of
+//               kGsumEntries, b = slice count
 // kind T_VEC  : idx = vector, a = first element, b = element count
 // kind T_QTILE: idx = matrix, a = row chunk (K_QSTEP) or entry block (K_QFIN), b = column block
 struct Tile {
@@ -126,6 +127,7 @@ enum KernelId : int32_t {
   K_PNARROW,
   K_QNARROW,
   K_RNARROW,
+  K_GSUM,        // from kBlockedRank on: a factor's Gram partials summed (and mirrored) into the first
 };
 
 // Narrow rows (r = 4, m / 4 = m4 <= 128 float4 groups): L lanes per row (16, 32 or 64), G float4
@@ -139,8 +141,12 @@ constexpr int32_t kBlockedRank = 128;  // ranks whose W K_CHOL forms from Gram p
 // ranks whose MFMA kernels split the rank blocks over the four waves of a workgroup, whose W is
 // factored in 2 x 2 blocks and whose Xh = X W runs per 64-column block
 constexpr int32_t kSplitRank = 256;
-// tiles that share one slice's Gram: 4 from kBlockedRank on, 16 from kSplitRank on
-constexpr int32_t gram_parts(int32_t r) { return r >= kSplitRank ? 16 : (r >= kBlockedRank ? 4 : 1); }
+// tiles that share one slice's Gram from kBlockedRank on: the (r / 4)(r / 4 + 1) / 2 blocks of 4 x 4
+// on and above the diagonal, one per thread of a 256-thread tile
+constexpr int32_t gram_parts(int32_t r) {
+  return r >= kBlockedRank ? ((r / 4) * (r / 4 + 1) / 2 + 255) / 256 : 1;
+}
+constexpr int32_t kGsumEntries = 4096;  // Gram entries per K_GSUM tile
 constexpr int kWideBlock = 64;     // threads per workgroup of K_WPSTEP, K_WQSTEP, K_WRECON: one wave
 constexpr int kSplitBlock = 256;   // the same from kSplitRank on: four waves
 constexpr int kWideQCols = 32;     // K_WQSTEP column block (one MFMA block)

@@ -356,30 +356,32 @@ __device__ void cholesky_w(const double* G, double* w_out) {
 }
 
 // Part `part` of the Gram of rows [r0, r1) of X (row-major, RK >= kBlockedRank columns) into
-// `out` (RK x RK doubles, global memory): of the (RK / 4)^2 blocks of 4 x 4 the part holds a
-// contiguous 1 / gram_parts(RK), thread t owning blocks t + 256 q, q < QB, over every row of a
-// chunk; the chunk's rows sit in LDS as doubles and the next chunk is requested before the
-// current one's products.  The rows are also copied to `copy` when set.
+// `out` (RK x RK doubles, global memory): G is symmetric, so only its 4 x 4 blocks on and above
+// the diagonal are formed (K_GSUM mirrors them); of those, numbered row by row, thread t of part
+// p owns block 256 p + t over every row of a chunk.  The chunk's rows sit in LDS as doubles and
+// the next chunk is requested before the current one's products.  The rows are also copied to
+// `copy` when set.
 template <int RK>
 __device__ void gram_blocked(const float* X, int64_t r0, int64_t r1, double* out, float* copy, int part) {
   constexpr int CH = 32;
-  constexpr int NP = gram_parts(RK);
-  constexpr int NB4 = RK / 4, QB = NB4 * NB4 / (kBlock * NP);
+  constexpr int NB4 = RK / 4, NU = NB4 * (NB4 + 1) / 2;
   constexpr int PT = CH * RK / kBlock;  // chunk elements per thread
-  static_assert(QB >= 1 && QB * kBlock * NP == NB4 * NB4, "blocks must spread evenly over the workgroups");
+  static_assert(gram_parts(RK) * kBlock >= NU, "every upper block needs a thread");
   __shared__ __align__(16) double sh[CH * RK];
-  int bi[QB], bj[QB];
-  double acc[QB][4][4];
-#pragma unroll
-  for (int q = 0; q < QB; ++q) {
-    const int b = part * QB * kBlock + tid() + q * kBlock;
-    bi[q] = 4 * (b / NB4);
-    bj[q] = 4 * (b % NB4);
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) acc[q][u][v] = 0.0;
+  const int b = part * kBlock + tid();
+  const bool own = b < NU;
+  int bi = 0, bj = 0;
+  {
+    int rem = own ? b : 0, i = 0;
+    while (rem >= NB4 - i) rem -= NB4 - i, ++i;
+    bi = 4 * i;
+    bj = 4 * (i + rem);
   }
+  double acc[4][4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) acc[u][v] = 0.0;
   const int64_t end = r1 * RK;
   float nx[PT];
   auto fetch = [&](int64_t c0) {
@@ -400,36 +402,34 @@ __device__ void gram_blocked(const float* X, int64_t r0, int64_t r1, double* out
     }
     __syncthreads();
     fetch(c0 + CH);
-    for (int rr = 0; rr < cn; ++rr) {
-#pragma unroll
-      for (int q = 0; q < QB; ++q) {
+    if (own)
+      for (int rr = 0; rr < cn; ++rr) {
         double xi[4], xj[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          xi[u] = sh[rr * RK + bi[q] + u];
-          xj[u] = sh[rr * RK + bj[q] + u];
+          xi[u] = sh[rr * RK + bi + u];
+          xj[u] = sh[rr * RK + bj + u];
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u)
 #pragma unroll
-          for (int v = 0; v < 4; ++v) acc[q][u][v] = fma(xi[u], xj[v], acc[q][u][v]);
+          for (int v = 0; v < 4; ++v) acc[u][v] = fma(xi[u], xj[v], acc[u][v]);
       }
-    }
     __syncthreads();
   }
-#pragma unroll
-  for (int q = 0; q < QB; ++q)
+  if (own)
 #pragma unroll
     for (int u = 0; u < 4; ++u)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) out[(bi[q] + u) * RK + bj[q] + v] = acc[q][u][v];
+      for (int v = 0; v < 4; ++v) out[(bi + u) * RK + bj + v] = acc[u][v];
 }
 
 // Factor tile: slice t.a of the t.b slices of fact_rows rows of the factor `src` (rows x RK).
 // When `dst` is set the slice is also copied there (the aggregated factor becomes the next
-// step's reused factor).  A factor of one slice finishes W here; otherwise (and always from
-// kBlockedRank on) the slice's Gram is stored as a partial and K_CHOL adds the partials and
-// finishes W.
+// step's reused factor).  A factor of one slice finishes W here; otherwise the slice's Gram is
+// stored as a partial and K_CHOL adds the partials and finishes W.  From kBlockedRank on the
+// Gram always goes to a partial (its blocks on and above the diagonal), K_GSUM adds and mirrors
+// the partials and K_CHOL finishes W.
 template <int RK>
 __device__ void fact_tile(const KArgs& a, const Tile& t, const float* src, float* dst, int64_t rows) {
   const MatDesc d = a.mats[t.idx];

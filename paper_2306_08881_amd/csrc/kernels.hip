@@ -152,53 +152,77 @@ __device__ void chol_split(double* G, double* W, double* S) {
   for (int e = tid(); e < H * H; e += kBlock) W[(H + e / H) * N + e % H] = 0.0;
 }
 
-// W from the Gram partials of a matrix's t.b slices, added in slice order.
+// From kBlockedRank on: entries [t.a kGsumEntries, ...) of a matrix's Gram, the sum of its t.b
+// slices' partials in slice order, into the first partial.  The partials hold the 4 x 4 blocks
+// on and above the diagonal; the thread of an entry of a block above the diagonal also writes
+// its mirror, so every entry is read and written by one thread only.
+template <int RK>
+__global__ __launch_bounds__(kBlock) void k_gsum(KArgs a) {
+  const Tile t = a.tiles[blockIdx.x];
+  const MatDesc d = a.mats[t.idx];
+  double* gp = a.gpart + d.gpart;
+  constexpr int EPT = kGsumEntries / kBlock;  // entries per thread, 256 apart
+  static_assert(kGsumEntries % kBlock == 0 && (RK * RK) % kGsumEntries == 0, "whole tiles");
+  int64_t e[EPT];
+  bool up[EPT];
+  double s[EPT];
+#pragma unroll
+  for (int k = 0; k < EPT; ++k) {
+    e[k] = static_cast<int64_t>(t.a) * kGsumEntries + tid() + k * kBlock;
+    up[k] = (e[k] / RK) / 4 <= (e[k] % RK) / 4;
+    s[k] = 0.0;
+  }
+  for (int sl = 0; sl < t.b; ++sl) {
+    double v[EPT];
+#pragma unroll
+    for (int k = 0; k < EPT; ++k) v[k] = up[k] ? gp[static_cast<int64_t>(sl) * RK * RK + e[k]] : 0.0;
+#pragma unroll
+    for (int k = 0; k < EPT; ++k) s[k] += v[k];
+  }
+#pragma unroll
+  for (int k = 0; k < EPT; ++k) {
+    if (!up[k]) continue;
+    const int i = static_cast<int>(e[k] / RK), j = static_cast<int>(e[k] % RK);
+    gp[e[k]] = s[k];
+    if (i / 4 < j / 4) gp[j * RK + i] = s[k];
+  }
+}
+
+// W from the Gram partials of a matrix's t.b slices, added in slice order (from kBlockedRank on
+// K_GSUM has added them into the first).
 template <int RK>
 __global__ __launch_bounds__(kBlock) void k_chol(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
   constexpr bool SPLIT = RK >= kSplitRank;
-  // the sum goes to LDS, or from kSplitRank on in place into the first partial
   __shared__ double Gs[SPLIT ? 128 * 128 : RK * RK];
   double* gp = a.gpart + d.gpart;
-  double* G = SPLIT ? gp : Gs;
-  // EU entries x eight slices' partials requested together, each entry added in slice order
-  constexpr int EU = RK >= kBlockedRank ? 4 : 1;
-  for (int e0 = tid(); e0 < RK * RK; e0 += EU * kBlock) {
-    double s[EU];
-#pragma unroll
-    for (int u = 0; u < EU; ++u) s[u] = 0.0;
-    int sl = 0;
-    for (; sl + 8 <= t.b; sl += 8) {
-      double v[EU][8];
-#pragma unroll
-      for (int u = 0; u < EU; ++u)
-#pragma unroll
-        for (int w = 0; w < 8; ++w) {
-          const int e = e0 + u * kBlock;
-          v[u][w] = e < RK * RK ? gp[static_cast<int64_t>(sl + w) * RK * RK + e] : 0.0;
-        }
-#pragma unroll
-      for (int u = 0; u < EU; ++u)
-#pragma unroll
-        for (int w = 0; w < 8; ++w) s[u] += v[u][w];
+  if constexpr (RK >= kBlockedRank) {
+    if constexpr (SPLIT) {
+      static_assert(RK == 256, "2 x 2 blocks of 128");
+      chol_split(gp, a.w + d.w_slot, Gs);
+    } else {
+      for (int e = tid(); e < RK * RK; e += kBlock) Gs[e] = gp[e];
+      __syncthreads();
+      cholesky_w_blocked<RK>(Gs, a.w + d.w_slot);
     }
-    for (; sl < t.b; ++sl)
-#pragma unroll
-      for (int u = 0; u < EU; ++u)
-        if (e0 + u * kBlock < RK * RK) s[u] += gp[static_cast<int64_t>(sl) * RK * RK + e0 + u * kBlock];
-#pragma unroll
-    for (int u = 0; u < EU; ++u)
-      if (e0 + u * kBlock < RK * RK) G[e0 + u * kBlock] = s[u];
-  }
-  __syncthreads();
-  if constexpr (SPLIT) {
-    static_assert(RK == 256, "2 x 2 blocks of 128");
-    chol_split(G, a.w + d.w_slot, Gs);
-  } else if constexpr (RK >= kBlockedRank) {
-    cholesky_w_blocked<RK>(G, a.w + d.w_slot);
   } else {
-    cholesky_w<RK>(G, a.w + d.w_slot);
+    // eight slices' partials requested together, each entry added in slice order
+    for (int e = tid(); e < RK * RK; e += kBlock) {
+      double s = 0.0;
+      int sl = 0;
+      for (; sl + 8 <= t.b; sl += 8) {
+        double v[8];
+#pragma unroll
+        for (int w = 0; w < 8; ++w) v[w] = gp[static_cast<int64_t>(sl + w) * RK * RK + e];
+#pragma unroll
+        for (int w = 0; w < 8; ++w) s += v[w];
+      }
+      for (; sl < t.b; ++sl) s += gp[static_cast<int64_t>(sl) * RK * RK + e];
+      Gs[e] = s;
+    }
+    __syncthreads();
+    cholesky_w<RK>(Gs, a.w + d.w_slot);
   }
 }
 
@@ -1398,6 +1422,7 @@ hipError_t launch_rank(const Launch& l, const KArgs& args, hipStream_t s) {
       case K_EMAT: hipLaunchKernelGGL(k_emat<RK>, grid, block, 0, s, args); break;
       case K_FACT: hipLaunchKernelGGL(k_fact<RK>, grid, block, 0, s, args); break;
       case K_CHOL: hipLaunchKernelGGL(k_chol<RK>, grid, block, 0, s, args); break;
+      case K_GSUM: hipLaunchKernelGGL(k_gsum<RK>, grid, block, 0, s, args); break;
       case K_QFIN: hipLaunchKernelGGL(k_qfin<RK>, grid, block, 0, s, args); break;
       case K_VEC: hipLaunchKernelGGL(k_vec, grid, block, 0, s, args); break;
       default: return hipErrorInvalidValue;

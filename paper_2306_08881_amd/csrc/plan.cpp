@@ -302,6 +302,24 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     const int32_t nsl = q ? d.fact_slices_q : d.fact_slices_p;
     if (nsl > 1 || r >= kBlockedRank) plan.tiles.push_back(Tile{T_FACT, mi, 0, nsl});
   };
+  // from kBlockedRank on: the partials' sum, kGsumEntries Gram entries per tile
+  auto gsum_tiles = [&](int32_t mi, bool q) {
+    const MatDesc& d = plan.mats[mi];
+    const int32_t nsl = q ? d.fact_slices_q : d.fact_slices_p;
+    for (int32_t e = 0; e < static_cast<int32_t>(r * r / kGsumEntries); ++e)
+      plan.tiles.push_back(Tile{T_FACT, mi, e, nsl});
+  };
+  // the Gram finish after the factor tiles: K_GSUM from kBlockedRank on, then K_CHOL
+  auto chol_launches = [&](const std::vector<int32_t>& mats, bool q, std::vector<Launch>& L) {
+    if (r >= kBlockedRank) {
+      Launch l = sink.begin(K_GSUM, 0);
+      for (int32_t mi : mats) gsum_tiles(mi, q);
+      sink.end(l, L);
+    }
+    Launch l = sink.begin(K_CHOL, 0);
+    for (int32_t mi : mats) chol_tiles(mi, q);
+    sink.end(l, L);
+  };
   auto row_tiles = [&](int32_t mi, int64_t rows_per_tile) {
     const MatDesc& d = plan.mats[mi];
     for (int64_t s = 0; s < d.n; s += rows_per_tile)
@@ -432,9 +450,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       for (int32_t mi : bk.mats) fact_tiles(mi, q);
       vec_tiles(bk);
       sink.end(l, L);
-      l = sink.begin(K_CHOL, 0);
-      for (int32_t mi : bk.mats) chol_tiles(mi, q);
-      sink.end(l, L);
+      chol_launches(bk.mats, q, L);
     }
     emat_launch(bk);
   };
@@ -634,9 +650,9 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     Launch l = sink.begin(K_FACT, 1);
     for (int32_t mi = 0; mi < static_cast<int32_t>(plan.mats.size()); ++mi) fact_tiles(mi, true);
     sink.end(l, plan.gram_init);
-    l = sink.begin(K_CHOL, 0);
-    for (int32_t mi = 0; mi < static_cast<int32_t>(plan.mats.size()); ++mi) chol_tiles(mi, true);
-    sink.end(l, plan.gram_init);
+    std::vector<int32_t> all(plan.mats.size());
+    for (int32_t mi = 0; mi < static_cast<int32_t>(plan.mats.size()); ++mi) all[mi] = mi;
+    chol_launches(all, true, plan.gram_init);
   }
 
   // ---- launch families and algorithmic bytes (host-side profiling)
@@ -704,6 +720,8 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         return std::min<double>(d.fact_rows, (l.variant & 1 ? m : n) - double(t.a & 0xffff) * d.fact_rows) * rr * 4.0;
       case K_EMAT:
         return t.b * m * 8.0;
+      case K_GSUM:  // the slices' partials read, the sum written
+        return (t.b + 1.0) * kGsumEntries * 8.0;
       default:
         return 0.0;
     }
@@ -718,9 +736,8 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       case K_RECON: case K_RECON4: case K_WRECON:
         return 4;  // ACP_KERNEL_RECONSTRUCT
       case K_WFACT: return 5;                                              // ACP_KERNEL_ORTH
-      case K_APPLY: case K_FACT: case K_CHOL: return 5;     // ACP_KERNEL_ORTH
-      case K_VEC: return odd ? 1 : 2;
-      default: return 0;
+      case K_APPLY: case K_FACT: case K_CHOL: case K_GSUM: return 5;  // ACP_KERNEL_ORTH
+      default: return 0;  // K_VEC (raw-vector launches of their own) and K_EMAT: no family
     }
   };
   auto annotate = [&](std::vector<Launch>& list, bool odd) {
@@ -755,7 +772,8 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       case K_QFIN: return 23;
       case K_RECON4: return 31;
       case K_RECON: return l.variant == 4 ? 40 : 41;
-      case K_CHOL: return 42;
+      case K_GSUM: return 42;
+      case K_CHOL: return 43;
       case K_VEC: return 50;
       default: return 60;
     }

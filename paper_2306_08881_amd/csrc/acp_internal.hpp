@@ -90,7 +90,7 @@ struct VecDesc {
 
 enum TileKind : int32_t { T_ROWS = 0, T_FACT = 1, T_VEC = 2, T_QTILE = 3, T_SROWS = 4, T_SMALL = 5 };
 
-// kind T_ROWS : idx = matrix, a = first row, b = row count (K_APPLY from kSplitRank on: + 65536 x
+// kind T_ROWS : idx = matrix, a = first row, b = row count (K_APPLY from kBlockedRank on: + 65536 x
 //               the 64-column block of Xh)
 // kind T_SMALL: idx = matrix, the whole matrix in one workgroup (rank 4, small matrices whose
 //               rows are not 16-byte aligned: n <= kSmallRows, m <= kSmallCols)
@@ -138,8 +138,8 @@ constexpr int32_t narrow_variant(int32_t m4) {
 
 constexpr int32_t kWideRank = 8;   // ranks at or above this take the K_W* kernels
 constexpr int32_t kBlockedRank = 128;  // ranks whose W K_CHOL forms from Gram partials in global memory
-// ranks whose MFMA kernels split the rank blocks over the four waves of a workgroup, whose W is
-// factored in 2 x 2 blocks and whose Xh = X W runs per 64-column block
+// ranks whose MFMA kernels split the rank blocks over the four waves of a workgroup and whose W
+// is factored in 2 x 2 blocks
 constexpr int32_t kSplitRank = 256;
 // tiles that share one slice's Gram from kBlockedRank on: the (r / 4)(r / 4 + 1) / 2 blocks of 4 x 4
 // on and above the diagonal, one per thread of a 256-thread tile

@@ -29,69 +29,143 @@ __global__ __launch_bounds__(kBlock) void k_fact(KArgs a) {
   fact_tile<RK>(a, t, a.fac + (q ? d.q_slot : d.p_slot), nullptr, q ? d.m : d.n);
 }
 
-// Cholesky and W = R^-1 of a Gram matrix in shared memory for ranks from kBlockedRank on, by the
-// whole workgroup: right-looking over the upper triangle, one barrier per pivot (every thread
-// takes pivot k's drop test; the trailing update, one row per wave at a time, subtracts
-// G_ki G_kj / d_k with the rows still unscaled, in pivot order); the rows of R are scaled once
-// at the end.  Then column c of W = R^-1 on thread c by
-// back substitution from the last row up.  W[i][c] (i < c) is kept in the strictly lower
-// triangle at G[RK-1-i][RK-1-c], where the threads of a row step touch adjacent words (and
-// every thread reads the same row of R), its diagonal apart.  Dropped pivots give zero rows
-// and columns of R and W.  G[] is overwritten.  The drop test compares with the diagonal
-// gref[i * gstride] (G's own unless given: a trailing block of a larger Gram matrix is tested
-// against that matrix's diagonal); W goes to w_out with rows ldw apart.
+// Cholesky G = R^T R and W = R^-1 of a Gram matrix in shared memory (RK = 128, row-major; only
+// the upper triangle is read) for ranks from kBlockedRank on, by the whole workgroup, in blocks
+// of 32.  For each diagonal block K in order:
+//   (i)   one wave factors the block (lane j keeps column j in registers; at pivot p every lane
+//         takes the drop test, forms R[p][j] and updates its column with R[p][i] read from lane
+//         i) and forms W_KK = R_KK^-1 by columns (lane j solves R_KK w = e_j from the bottom up);
+//   (ii)  the block row right of it: R_KJ = W_KK^T G_KJ (with dropped pivots W_KK's zero columns
+//         give R's zero rows, as forward substitution over the kept pivots would);
+//   (iii) the trailing upper triangle: G_IJ -= R_KI^T R_KJ.
+// These are the pivots of the unblocked right-looking form, in the same order.  Then block column
+// J of W (J = 1, 2, 3) from the earlier ones: W_IJ = -(sum_{I <= L < J} W_IL R_LJ) W_JJ.  W[i][c]
+// (i < c) is kept in the strictly lower triangle at G[RK-1-i][RK-1-c] and its diagonal apart.
+// Dropped pivots give zero rows and columns of R and W.  G[] is overwritten.  The drop test
+// compares with the diagonal gref[i * gstride] (G's own unless given: a trailing block of a
+// larger Gram matrix is tested against that matrix's diagonal); W goes to w_out with rows ldw
+// apart.
 template <int RK>
 __device__ void cholesky_w_blocked(double* G, double* w_out, int ldw = RK, const double* gref = nullptr,
                                    int gstride = 0) {
+  static_assert(RK == 128 && kBlock == 256, "4 x 4 blocks of 32 on 256 threads");
+  constexpr int B = 32, NBK = RK / B;
   __shared__ double g0[RK], wdiag[RK];
-  __shared__ int drop[RK];
+  __shared__ double T[(RK - B) * B];  // one block column's W[0:k0][.] R[.][block] products
+  auto wl = [&](int i, int c) -> double& { return G[(RK - 1 - i) * RK + (RK - 1 - c)]; };  // W[i][c], i < c
   for (int i = tid(); i < RK; i += kBlock) g0[i] = gref ? gref[i * gstride] : G[i * RK + i];
   __syncthreads();
-  const int wave = tid() / kWave, lane = tid() % kWave;
-  for (int k = 0; k < RK; ++k) {
-    const double dk = G[k * RK + k];
-    const bool keep = g0[k] > 0.0 && dk > kTau * kTau * g0[k];
-    if (tid() == 0) drop[k] = keep ? 0 : 1;
-    if (keep) {
-      const double inv = 1.0 / dk;
-      static_assert(RK % kWave == 0, "rows of whole waves");
-#pragma unroll 4
-      for (int i = k + 1 + wave; i < RK; i += kBlock / kWave) {
-        const double gki = G[k * RK + i] * inv;
+  const int lane = tid() & 63;
+  for (int K = 0; K < NBK; ++K) {
+    const int k0 = K * B, nc = RK - k0 - B;  // columns right of the block
+    // (i) the diagonal block on the first wave
+    if (tid() < B) {
+      const int j = lane;
+      double g[B];
 #pragma unroll
-        for (int jj = 0; jj < RK; jj += kWave) {
-          const int j = i + jj + lane;
-          if (j < RK) G[i * RK + j] -= gki * G[k * RK + j];
-        }
+      for (int a = 0; a < B; ++a) g[a] = a <= j ? G[(k0 + a) * RK + k0 + j] : 0.0;
+#pragma unroll
+      for (int p = 0; p < B; ++p) {
+        asm volatile("" ::: "memory");  // one pivot at a time
+        const double dk = readlane_d(g[p], p);
+        const double ref = g0[k0 + p];
+        const bool keep = ref > 0.0 && dk > kTau * kTau * ref;
+        const double rkk = keep ? sqrt(dk) : 0.0, rinv = keep ? 1.0 / rkk : 0.0;
+        const double rpj = j > p ? g[p] * rinv : (j == p ? rkk : 0.0);
+        g[p] = rpj;  // row p of R
+        if (j == 0) wdiag[k0 + p] = rinv;  // W's diagonal: 1 / R[p][p], zero when dropped
+        if (keep)
+#pragma unroll
+          for (int a = p + 1; a < B; ++a) g[a] -= readlane_d(rpj, a) * rpj;
       }
+#pragma unroll
+      for (int a = 0; a < B; ++a)
+        if (a <= j) G[(k0 + a) * RK + k0 + j] = g[a];
+      // W_KK row a = j: W[a][c] = -(sum_{l < c} W[a][l] R[l][c]) / R[c][c] for c > a (zero for
+      // l < a), read back from LDS one column of R at a time
+      const double* R = G + k0 * RK + k0;
+      double w[B];
+#pragma unroll
+      for (int c = 0; c < B; ++c) {
+        asm volatile("" ::: "memory");  // this column's loads only
+        double s = 0.0;
+#pragma unroll
+        for (int l = 0; l < c; ++l) s += w[l] * R[l * RK + c];
+        const double rinv = wdiag[k0 + c];
+        w[c] = c < j ? 0.0 : (c == j ? rinv : -s * rinv);
+      }
+#pragma unroll
+      for (int c = 0; c < B; ++c)
+        if (c > j) wl(k0 + j, k0 + c) = w[c];
+    }
+    __syncthreads();
+    if (nc == 0) break;
+    // (ii) R_KJ = W_KK^T G_KJ: entry (k0 + a, k0 + B + c), a sum over b <= a
+    {
+      constexpr int QN = B * (RK - B) / kBlock;
+      double res[QN];
+#pragma unroll
+      for (int q = 0; q < QN; ++q) {
+        const int e = tid() + q * kBlock, a = e / nc, c = e % nc;
+        double v = 0.0;
+        if (e < B * nc) {
+          const int j = k0 + B + c;
+          double s2[2] = {wdiag[k0 + a] * G[(k0 + a) * RK + j], 0.0};
+          for (int b = 0; b < a; ++b) s2[b & 1] += wl(k0 + b, k0 + a) * G[(k0 + b) * RK + j];
+          v = s2[0] + s2[1];
+        }
+        res[q] = v;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int q = 0; q < QN; ++q) {
+        const int e = tid() + q * kBlock;
+        if (e < B * nc) G[(k0 + e / nc) * RK + k0 + B + e % nc] = res[q];
+      }
+      __syncthreads();
+    }
+    // (iii) the trailing upper triangle: G[i][j] -= sum_a R[k0 + a][i] R[k0 + a][j], i <= j
+    for (int e = tid(); e < nc * nc; e += kBlock) {
+      const int i = k0 + B + e / nc, j = k0 + B + e % nc;
+      if (i > j) continue;
+      double s[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+      for (int a = 0; a < B; ++a) s[a & 3] += G[(k0 + a) * RK + i] * G[(k0 + a) * RK + j];
+      G[i * RK + j] -= (s[0] + s[1]) + (s[2] + s[3]);
     }
     __syncthreads();
   }
-  // R: row k = G_k / sqrt(d_k) (zero for a dropped pivot)
-  for (int k = wave; k < RK; k += kBlock / kWave) {
-    const bool keep = drop[k] == 0;
-    const double rkk = keep ? sqrt(G[k * RK + k]) : 0.0;
-    for (int j = k + 1 + lane; j < RK; j += kWave) G[k * RK + j] = keep ? G[k * RK + j] / rkk : 0.0;
-    if (lane == 0) G[k * RK + k] = rkk;
-  }
-  __syncthreads();
-  if (tid() < RK) {
-    const int c = tid();
-    auto wt = [&](int i) -> double& { return G[(RK - 1 - i) * RK + (RK - 1 - c)]; };  // W[i][c], i < c
-    const bool kc = drop[c] == 0;
-    wdiag[c] = kc ? 1.0 / G[c * RK + c] : 0.0;
-    for (int i = RK - 1; i >= 0; --i) {
-      if (i >= c) continue;
-      double w = 0.0;
-      if (kc && drop[i] == 0) {
-        double s = G[i * RK + c] * wdiag[c];
-#pragma unroll 8
-        for (int l = i + 1; l < c; ++l) s += G[i * RK + l] * wt(l);
-        w = -s / G[i * RK + i];
-      }
-      wt(i) = w;
+  // block columns of W: T = W[0:k0][0:k0] R[0:k0][block], then W[0:k0][block] = -T W_JJ
+  for (int J = 1; J < NBK; ++J) {
+    const int k0 = J * B;
+    for (int e = tid(); e < k0 * B; e += kBlock) {
+      const int i = e / B, c = e % B;
+      double s[4] = {0.0, 0.0, 0.0, 0.0};
+      int l = i;
+      s[0] = wdiag[i] * G[i * RK + k0 + c];
+      for (++l; l + 4 <= k0; l += 4)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) s[u] += wl(i, l + u) * G[(l + u) * RK + k0 + c];
+      for (; l < k0; ++l) s[0] += wl(i, l) * G[l * RK + k0 + c];
+      T[e] = (s[0] + s[1]) + (s[2] + s[3]);
     }
-    for (int i = 0; i < RK; ++i) w_out[i * ldw + c] = i < c ? wt(i) : (i == c ? wdiag[c] : 0.0);
+    __syncthreads();
+    for (int e = tid(); e < k0 * B; e += kBlock) {
+      const int i = e / B, jj = e % B;
+      double s[4] = {0.0, 0.0, 0.0, 0.0};
+      int c = 0;
+      for (; c + 4 <= jj; c += 4)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) s[u] += T[i * B + c + u] * wl(k0 + c + u, k0 + jj);
+      for (; c < jj; ++c) s[0] += T[i * B + c] * wl(k0 + c, k0 + jj);
+      s[1] += T[i * B + jj] * wdiag[k0 + jj];
+      wl(i, k0 + jj) = -((s[0] + s[1]) + (s[2] + s[3]));
+    }
+    __syncthreads();
+  }
+  for (int e = tid(); e < RK * RK; e += kBlock) {
+    const int i = e / RK, c = e % RK;
+    w_out[i * ldw + c] = i < c ? wl(i, c) : (i == c ? wdiag[c] : 0.0);
   }
 }
 
@@ -108,16 +182,26 @@ __device__ void mm128(const double* A, int ai, int ak, const double* B, int bk, 
   for (int u = 0; u < 8; ++u)
 #pragma unroll
     for (int v = 0; v < 8; ++v) c[u][v] = 0.0;
-  for (int k = 0; k < 128; ++k) {
-    double x[8], y[8];
+  // the operands of steps k + 1 and k + 2 are requested before step k's products
+  double x[3][8], y[3][8];
+  auto load = [&](int k, double* xs, double* ys) {
 #pragma unroll
-    for (int u = 0; u < 8; ++u) x[u] = A[(i0 + u) * ai + k * ak];
+    for (int u = 0; u < 8; ++u) xs[u] = A[(i0 + u) * ai + k * ak];
 #pragma unroll
-    for (int v = 0; v < 8; ++v) y[v] = B[k * bk + j0 + v];
+    for (int v = 0; v < 8; ++v) ys[v] = B[k * bk + j0 + v];
+  };
+  load(0, x[0], y[0]);
+  load(1, x[1], y[1]);
+  for (int k = 0; k < 128; k += 3) {
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
+    for (int st = 0; st < 3; ++st) {
+      if (k + st >= 128) break;
+      if (k + st + 2 < 128) load(k + st + 2, x[(st + 2) % 3], y[(st + 2) % 3]);
 #pragma unroll
-      for (int v = 0; v < 8; ++v) c[u][v] = fma(x[u], y[v], c[u][v]);
+      for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int v = 0; v < 8; ++v) c[u][v] = fma(x[st][u], y[st][v], c[u][v]);
+    }
   }
 #pragma unroll
   for (int u = 0; u < 8; ++u)
@@ -226,62 +310,19 @@ __global__ __launch_bounds__(kBlock) void k_chol(KArgs a) {
   }
 }
 
-// Xh = X W for rows [t.a, t.a + t.b) of the P (variant 0) or Q (variant 1) slot, from
-// kBlockedRank on: passes of 32 rows staged in LDS (padded rows); thread t forms the 16 columns
-// 16 (t % 8) ... of row t / 8 of the pass, each a sum over the rank index in increasing order up
-// to the block's last column (W is upper triangular: its zeros below the diagonal add nothing).
-// W sits in LDS with column kk at kk + kk / 16 (the eight blocks a wave reads hit other banks).
-template <int RK>
-constexpr int apply_wl() { return RK + RK / 16; }
-template <int RK>
-__device__ void apply_blocked(const KArgs& a, const Tile& t, const MatDesc& d, const double* W) {
-  constexpr int WL = apply_wl<RK>();
-  constexpr int NJ = RK / 16;          // 16-column blocks
-  constexpr int RP = kBlock / NJ;      // rows per pass
-  constexpr int XL = RK + 1;           // padded X row (floats)
-  __shared__ float xs[RP * XL];
-  const int jb = tid() % NJ, rr = tid() / NJ;
-  const bool q = a.variant == 1;
-  const float* X = a.fac + (q ? d.q_slot : d.p_slot);
-  float* Y = a.fac + (q ? d.qh_slot : d.ph_slot);
-  for (int base = 0; base < t.b; base += RP) {
-    __syncthreads();  // the previous pass is done with xs
-    for (int e = tid(); e < RP * RK; e += kBlock) {
-      const int r = e / RK, l = e % RK;
-      xs[r * XL + l] = base + r < t.b ? X[(static_cast<int64_t>(t.a) + base + r) * RK + l] : 0.f;
-    }
-    __syncthreads();
-    double y[16];
-#pragma unroll
-    for (int k = 0; k < 16; ++k) y[k] = 0.0;
-    const double* wb = W + 17 * jb;  // column 16 jb of row 0
-    for (int l = 0; l < 16 * jb + 16; ++l) {
-      const double xl = xs[rr * XL + l];
-#pragma unroll
-      for (int k = 0; k < 16; ++k) y[k] = fma(xl, wb[l * WL + k], y[k]);
-    }
-    if (base + rr < t.b) {
-      float4* Y4 = reinterpret_cast<float4*>(Y + (static_cast<int64_t>(t.a) + base + rr) * RK + 16 * jb);
-#pragma unroll
-      for (int k = 0; k < 16; k += 4)
-        Y4[k / 4] = make_float4(static_cast<float>(y[k]), static_cast<float>(y[k + 1]),
-                                static_cast<float>(y[k + 2]), static_cast<float>(y[k + 3]));
-    }
-  }
-}
-
-// Xh = X W from kSplitRank on, for rows [t.a, t.a + rows) and the 64 columns c0 = 64 cb ... of
+// Xh = X W from kBlockedRank on, for rows [t.a, t.a + rows) and the 64 columns c0 = 64 cb ... of
 // Xh (t.b = rows | cb << 16): passes of 128 rows; per pass W's rows come in chunks of 64 up to
 // the block's last column (W is upper triangular), each chunk's 64 x 64 block of W and the
 // pass's rows of X for those ranks staged in LDS.  Thread t forms columns c0 + 8 (t % 8) ... + 7
-// of rows 4 (t / 8) ... + 3 of the pass, each entry a sum over the rank index in increasing order.
-// W sits in LDS with column k at k + k / 8.
+// of rows 4 (t / 8) ... + 3 of the pass, each entry a sum over the rank index in increasing order;
+// per rank it reads its four X values (X sits transposed in LDS) and its eight W values (column k
+// at k + 2 (k / 8)) as 16-byte words.
 template <int RK>
 __device__ void apply_split(const KArgs& a, const Tile& t, const MatDesc& d) {
   constexpr int CB = 64, KC = 64, NJ = CB / 8, RG = kBlock / NJ, RP = 4 * RG;
-  constexpr int WL = CB + CB / 8, XL = KC + 1;
-  __shared__ double ws[KC * WL];
-  __shared__ float xs[RP * XL];
+  constexpr int WL = CB + 2 * (CB / 8), XT = RP + 4;
+  __shared__ __align__(16) double ws[KC * WL];
+  __shared__ __align__(16) float xt[KC * XT];
   const int rows = t.b & 0xffff, c0 = CB * (t.b >> 16);
   const int jb = tid() % NJ, rg = tid() / NJ;
   const bool q = a.variant == 1;
@@ -295,24 +336,28 @@ __device__ void apply_split(const KArgs& a, const Tile& t, const MatDesc& d) {
 #pragma unroll
       for (int k = 0; k < 8; ++k) y[u][k] = 0.0;
     for (int k0 = 0; k0 < c0 + CB; k0 += KC) {
-      __syncthreads();  // the previous chunk is done with ws and xs
+      __syncthreads();  // the previous chunk is done with ws and xt
       for (int e = tid(); e < KC * CB; e += kBlock) {
         const int l = e / CB, k = e % CB;
-        ws[l * WL + k + k / 8] = W[static_cast<int64_t>(k0 + l) * RK + c0 + k];
+        ws[l * WL + k + 2 * (k / 8)] = W[static_cast<int64_t>(k0 + l) * RK + c0 + k];
       }
       for (int e = tid(); e < RP * KC; e += kBlock) {
         const int r = e / KC, l = e % KC;
-        xs[r * XL + l] = base + r < rows ? X[(static_cast<int64_t>(t.a) + base + r) * RK + k0 + l] : 0.f;
+        xt[l * XT + r] = base + r < rows ? X[(static_cast<int64_t>(t.a) + base + r) * RK + k0 + l] : 0.f;
       }
       __syncthreads();
       const int lend = min(KC, c0 + 8 * jb + 8 - k0);  // ranks past the block's last column add zero
-      const double* wb = ws + 9 * jb;
       for (int l = 0; l < lend; ++l) {
-        double xl[4], wl[8];
+        const float4 xv = *reinterpret_cast<const float4*>(&xt[l * XT + 4 * rg]);
+        const double2* w2 = reinterpret_cast<const double2*>(&ws[l * WL + 10 * jb]);
+        const double xl[4] = {xv.x, xv.y, xv.z, xv.w};
+        double wl[8];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) xl[u] = xs[(4 * rg + u) * XL + l];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) wl[k] = wb[l * WL + k];
+        for (int k = 0; k < 4; ++k) {
+          const double2 p = w2[k];
+          wl[2 * k] = p.x;
+          wl[2 * k + 1] = p.y;
+        }
 #pragma unroll
         for (int u = 0; u < 4; ++u)
 #pragma unroll
@@ -338,23 +383,13 @@ template <int RK>
 __global__ __launch_bounds__(kBlock) void k_apply(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
-  if constexpr (RK >= kSplitRank) {
+  if constexpr (RK >= kBlockedRank) {
     apply_split<RK>(a, t, d);
   } else {
-    constexpr bool BIG = RK >= kBlockedRank;
-    __shared__ double W[BIG ? RK * apply_wl<RK>() : RK * RK];
-    for (int e = tid(); e < RK * RK; e += kBlock) {
-      if constexpr (BIG) {
-        const int l = e / RK, k = e % RK;
-        W[l * apply_wl<RK>() + k + k / 16] = a.w[d.w_slot + e];
-      } else {
-        W[e] = a.w[d.w_slot + e];
-      }
-    }
+    __shared__ double W[RK * RK];
+    for (int e = tid(); e < RK * RK; e += kBlock) W[e] = a.w[d.w_slot + e];
     __syncthreads();
-    if constexpr (BIG) {
-      apply_blocked<RK>(a, t, d, W);
-    } else {
+    {
       const int64_t row = static_cast<int64_t>(t.a) + tid();
       if (tid() >= t.b) return;
       const bool q = a.variant == 1;

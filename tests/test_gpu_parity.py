@@ -195,6 +195,49 @@ def test_zero_gradient_then_nonzero():
         assert PU.rel_err(run.error_slice(0), orc.error(0)) <= PU.TOL
 
 
+@pytest.mark.parametrize("rank,k", [(128, 40), (256, 100)])
+def test_rank_deficient_high_rank(rank, k):
+    """Gradients of exact rank k < r: from step 2 on the orthogonalisation drops r - k columns of
+    the reused factor (kept and dropped pivots in the first 32-column block of the blocked
+    Cholesky, dropped ones only in the others), on both sides alike.  The kept columns'
+    Gram-Schmidt is as ill-conditioned as a random k x k matrix, which scales the fp32 rounding
+    difference from the fp64 oracle and makes it compound from step to step, so the oracle is
+    re-synced from the device state before every step after the first: each step's arithmetic
+    is checked on its own."""
+    _require_gpu()
+    shapes = [(300, 520)]
+    run = PU.Runner(shapes, rank)
+    orc = AcpOracle(shapes, rank)
+    rng = np.random.default_rng(5)
+    a = rng.standard_normal((300, k))
+    b = rng.standard_normal((520, k))
+    for t in range(1, 7):
+        g = (a @ rng.standard_normal((k, k)) @ b.T / k).astype(np.float32)
+        if t > 1:
+            PU.read_state_into(run, orc, t - 1, [0])
+        run.step(t, run.pack({0: g}))
+        emit = orc.compress_tensor(t, 0, g)
+        out = orc.decompress_tensor(t, 0, emit)
+        torch.cuda.synchronize()
+        st = orc.state[0]
+        errs = {"emitted factor": PU.rel_err(run.factor_slice(t, 0), emit),
+                "orthonormal factor": PU.rel_err(run.ortho(t, 0), st.ortho),
+                "M_hat": PU.rel_err(run.out_slice(0), out),
+                # after a Q-step E is zero up to rounding (the kept columns span M'), so its
+                # error is measured against the gradient's norm
+                "E": float(np.linalg.norm(run.error_slice(0) - orc.error(0).reshape(-1))
+                           / max(np.linalg.norm(orc.error(0)), np.linalg.norm(g)))}
+        PU.log(f"  rank {rank}, gradient rank {k}, t={t}: " + ", ".join(f"{n} {v:.2e}" for n, v in errs.items()))
+        assert all(v <= PU.TOL for v in errs.values()), (t, errs)
+        # the dropped columns are zero on both sides, the kept ones orthonormal
+        f = run.ortho(t, 0).reshape(-1, rank).astype(np.float64)
+        dropped = np.all(f == 0, axis=0)
+        assert np.array_equal(dropped, np.all(st.ortho.reshape(-1, rank) == 0, axis=0)), t
+        assert t == 1 or dropped.sum() == rank - k, (t, dropped.sum())
+        kept = f[:, ~dropped]
+        assert np.allclose(kept.T @ kept, np.eye(kept.shape[1]), atol=1e-5), t
+
+
 def test_three_workers_loopback():
     """p = 3 workers on one GPU; the caller's all-reduce is a sum of their factor buffers."""
     _require_gpu()

@@ -313,7 +313,8 @@ __global__ __launch_bounds__(kBlock) void k_chol(KArgs a) {
 // Xh = X W from kBlockedRank on, for rows [t.a, t.a + rows) and the 64 columns c0 = 64 cb ... of
 // Xh (t.b = rows | cb << 16): passes of 128 rows; per pass W's rows come in chunks of 64 up to
 // the block's last column (W is upper triangular), each chunk's 64 x 64 block of W and the
-// pass's rows of X for those ranks staged in LDS.  Thread t forms columns c0 + 8 (t % 8) ... + 7
+// pass's rows of X for those ranks staged in LDS (requested during the previous chunk's
+// products).  Thread t forms columns c0 + 8 (t % 8) ... + 7
 // of rows 4 (t / 8) ... + 3 of the pass, each entry a sum over the rank index in increasing order;
 // per rank it reads its four X values (X sits transposed in LDS) and its eight W values (column k
 // at k + 2 (k / 8)) as 16-byte words.
@@ -321,6 +322,7 @@ template <int RK>
 __device__ void apply_split(const KArgs& a, const Tile& t, const MatDesc& d) {
   constexpr int CB = 64, KC = 64, NJ = CB / 8, RG = kBlock / NJ, RP = 4 * RG;
   constexpr int WL = CB + 2 * (CB / 8), XT = RP + 4;
+  constexpr int NW = KC * CB / kBlock, NX = RP * KC / kBlock;  // staged words per thread
   __shared__ __align__(16) double ws[KC * WL];
   __shared__ __align__(16) float xt[KC * XT];
   const int rows = t.b & 0xffff, c0 = CB * (t.b >> 16);
@@ -329,58 +331,78 @@ __device__ void apply_split(const KArgs& a, const Tile& t, const MatDesc& d) {
   const float* X = a.fac + (q ? d.q_slot : d.p_slot);
   float* Y = a.fac + (q ? d.qh_slot : d.ph_slot);
   const double* W = a.w + d.w_slot;
-  for (int base = 0; base < rows; base += RP) {
-    double y[4][8];
+  // steps (pass of RP rows, chunk of KC ranks); a step's W block and X rows are requested into
+  // registers during the previous step's products and stored to LDS at its start
+  const int nchunk = c0 / KC + 1, nstep = ((rows + RP - 1) / RP) * nchunk;
+  // thread t stages column t % 64 of rows t / 64 + 4 u of both blocks (W: rank rows, X: factor
+  // rows), so that every word it moves is a constant offset from one address
+  static_assert(CB == 64 && KC == 64 && kBlock == 256, "four rows of 64 per pass of the workgroup");
+  const int sr = tid() / 64, sc = tid() % 64;
+  double wv[NW];
+  float xv[NX];
+  auto fetch = [&](int st) {
+    const int base = (st / nchunk) * RP, k0 = (st % nchunk) * KC;
+    const double* wsrc = W + static_cast<int64_t>(k0 + sr) * RK + c0 + sc;
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < NW; ++u) wv[u] = wsrc[4 * u * RK];
+    const float* xsrc = X + (static_cast<int64_t>(t.a) + base + sr) * RK + k0 + sc;
 #pragma unroll
-      for (int k = 0; k < 8; ++k) y[u][k] = 0.0;
-    for (int k0 = 0; k0 < c0 + CB; k0 += KC) {
-      __syncthreads();  // the previous chunk is done with ws and xt
-      for (int e = tid(); e < KC * CB; e += kBlock) {
-        const int l = e / CB, k = e % CB;
-        ws[l * WL + k + 2 * (k / 8)] = W[static_cast<int64_t>(k0 + l) * RK + c0 + k];
+    for (int u = 0; u < NX; ++u) xv[u] = base + sr + 4 * u < rows ? xsrc[4 * u * RK] : 0.f;
+  };
+  double* wdst = ws + sr * WL + sc + 2 * (sc / 8);
+  float* xdst = xt + sc * XT + sr;
+  fetch(0);
+  double y[4][8];
+  for (int st = 0; st < nstep; ++st) {
+    const int base = (st / nchunk) * RP, ch = st % nchunk, k0 = ch * KC;
+    if (ch == 0)
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int k = 0; k < 8; ++k) y[u][k] = 0.0;
+    __syncthreads();  // the previous step is done with ws and xt
+#pragma unroll
+    for (int u = 0; u < NW; ++u) wdst[4 * u * WL] = wv[u];
+#pragma unroll
+    for (int u = 0; u < NX; ++u) xdst[4 * u] = xv[u];
+    __syncthreads();
+    if (st + 1 < nstep) fetch(st + 1);
+    const int lend = min(KC, c0 + 8 * jb + 8 - k0);  // ranks past the block's last column add zero
+#pragma unroll 2
+    for (int l = 0; l < lend; ++l) {
+      const float4 x4 = *reinterpret_cast<const float4*>(&xt[l * XT + 4 * rg]);
+      const double2* w2 = reinterpret_cast<const double2*>(&ws[l * WL + 10 * jb]);
+      const double xl[4] = {x4.x, x4.y, x4.z, x4.w};
+      double wl[8];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const double2 p = w2[k];
+        wl[2 * k] = p.x;
+        wl[2 * k + 1] = p.y;
       }
-      for (int e = tid(); e < RP * KC; e += kBlock) {
-        const int r = e / KC, l = e % KC;
-        xt[l * XT + r] = base + r < rows ? X[(static_cast<int64_t>(t.a) + base + r) * RK + k0 + l] : 0.f;
-      }
-      __syncthreads();
-      const int lend = min(KC, c0 + 8 * jb + 8 - k0);  // ranks past the block's last column add zero
-      for (int l = 0; l < lend; ++l) {
-        const float4 xv = *reinterpret_cast<const float4*>(&xt[l * XT + 4 * rg]);
-        const double2* w2 = reinterpret_cast<const double2*>(&ws[l * WL + 10 * jb]);
-        const double xl[4] = {xv.x, xv.y, xv.z, xv.w};
-        double wl[8];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const double2 p = w2[k];
-          wl[2 * k] = p.x;
-          wl[2 * k + 1] = p.y;
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int k = 0; k < 8; ++k) y[u][k] = fma(xl[u], wl[k], y[u][k]);
+    }
+    if (ch == nchunk - 1)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int r = base + 4 * rg + u;
+        if (r < rows) {
+          float4* Y4 = reinterpret_cast<float4*>(Y + (static_cast<int64_t>(t.a) + r) * RK + c0 + 8 * jb);
+          Y4[0] = make_float4(static_cast<float>(y[u][0]), static_cast<float>(y[u][1]),
+                              static_cast<float>(y[u][2]), static_cast<float>(y[u][3]));
+          Y4[1] = make_float4(static_cast<float>(y[u][4]), static_cast<float>(y[u][5]),
+                              static_cast<float>(y[u][6]), static_cast<float>(y[u][7]));
         }
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-          for (int k = 0; k < 8; ++k) y[u][k] = fma(xl[u], wl[k], y[u][k]);
       }
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int r = base + 4 * rg + u;
-      if (r < rows) {
-        float4* Y4 = reinterpret_cast<float4*>(Y + (static_cast<int64_t>(t.a) + r) * RK + c0 + 8 * jb);
-        Y4[0] = make_float4(static_cast<float>(y[u][0]), static_cast<float>(y[u][1]),
-                            static_cast<float>(y[u][2]), static_cast<float>(y[u][3]));
-        Y4[1] = make_float4(static_cast<float>(y[u][4]), static_cast<float>(y[u][5]),
-                            static_cast<float>(y[u][6]), static_cast<float>(y[u][7]));
-      }
-    }
   }
 }
 
 // Xh = X W for rows [t.a, t.a + t.b) of the P (variant 0) or Q (variant 1) slot.
 template <int RK>
-__global__ __launch_bounds__(kBlock) void k_apply(KArgs a) {
+__global__ __launch_bounds__(kBlock, RK >= kBlockedRank ? 2 : 1) void k_apply(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
   if constexpr (RK >= kBlockedRank) {

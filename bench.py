@@ -90,7 +90,7 @@ def kernel_families(rank: int):
         p, q, d = "k_wpstep", "k_wqstep", "k_wrecon"
     else:
         p, q, d = "k_pfused", "k_qstep", "k_recon4"
-    orth = "k_apply, k_wfact, k_chol" if rank >= 8 else "k_chol"
+    orth = ("k_apply, k_wfact, k_gsum, k_chol" if rank >= 128 else "k_apply, k_wfact, k_chol") if rank >= 8 else "k_chol"
     return [(f"P-step compress ({p})", L.ACP_KERNEL_P_STEP, p),
             (f"Q-step compress ({q})", L.ACP_KERNEL_Q_STEP, q),
             ("Q-step finish (k_qfin)", L.ACP_KERNEL_Q_FINISH, "k_qfin"),

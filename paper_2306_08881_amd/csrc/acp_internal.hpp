@@ -138,9 +138,12 @@ constexpr int32_t narrow_variant(int32_t m4) {
 
 constexpr int32_t kWideRank = 8;   // ranks at or above this take the K_W* kernels
 constexpr int32_t kBlockedRank = 128;  // ranks whose W K_CHOL forms from Gram partials in global memory
-// ranks whose MFMA kernels split the rank blocks over the four waves of a workgroup and whose W
-// is factored in 2 x 2 blocks
-constexpr int32_t kSplitRank = 256;
+// ranks whose MFMA compress kernels split the rank over the four waves of a workgroup
+// (kSplitRank), whose decompress kernel does (kSplitReconRank), and whose W is factored in
+// 2 x 2 blocks of 128 (kCholBlockRank)
+constexpr int32_t kSplitRank = 128;
+constexpr int32_t kSplitReconRank = 256;
+constexpr int32_t kCholBlockRank = 256;
 // tiles that share one slice's Gram from kBlockedRank on: the (r / 4)(r / 4 + 1) / 2 blocks of 4 x 4
 // on and above the diagonal, one per thread of a 256-thread tile
 constexpr int32_t gram_parts(int32_t r) {
@@ -148,7 +151,6 @@ constexpr int32_t gram_parts(int32_t r) {
 }
 constexpr int32_t kGsumEntries = 4096;  // Gram entries per K_GSUM tile
 constexpr int kWideBlock = 64;     // threads per workgroup of K_WPSTEP, K_WQSTEP, K_WRECON: one wave
-constexpr int kSplitBlock = 256;   // the same from kSplitRank on: four waves
 constexpr int kWideQCols = 32;     // K_WQSTEP column block (one MFMA block)
 constexpr int kWideQRows = 512;    // K_WQSTEP rows per chunk (at most)
 constexpr int kWideRCols = 1024;   // K_WRECON columns per tile: 32 blocks of 32

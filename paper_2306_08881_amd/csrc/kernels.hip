@@ -278,7 +278,7 @@ template <int RK>
 __global__ __launch_bounds__(kBlock) void k_chol(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
-  constexpr bool SPLIT = RK >= kSplitRank;
+  constexpr bool SPLIT = RK >= kCholBlockRank;
   __shared__ double Gs[SPLIT ? 128 * 128 : RK * RK];
   double* gp = a.gpart + d.gpart;
   if constexpr (RK >= kBlockedRank) {

@@ -9,11 +9,11 @@
 //            P_loc = X Qh;  afterwards E = X - P_loc Qh^T is implied.
 //   Q-step:  F = M + E_arena (- Pl Qh^T when the arena holds X), F written to the arena,
 //            Q_loc = F^T Ph; afterwards E = F - Ph Q_loc^T is implied.
-// Each is one rank-r correction and one rank-r product per element.  Ranks 64 and 128 keep
-// r / 32 blocks of the product's output per wave; their compress kernels run one wave per SIMD
-// (their operands take every VGPR) instead of spilling, and at rank 128 the operands the tile
-// reuses sit in LDS.  At rank 256 the four waves of a workgroup split the rank (k_spstep,
-// k_sqstep, k_srecon).
+// Each is one rank-r correction and one rank-r product per element.  Rank 64 keeps two blocks
+// of the product's output per wave; its compress kernels run one wave per SIMD (their operands
+// take every VGPR) instead of spilling.  From rank 128 the four waves of a workgroup split the
+// rank in the compress kernels (k_spstep, k_sqstep), at rank 256 in the decompress kernel too
+// (k_srecon).
 //
 // MFMA layout (one wave): D (32 x 32) += A (32 x 2) B (2 x 32).  Lane l supplies
 // A[l % 32][l / 32] and B[l / 32][l % 32]; register v of lane l holds D[drow(v, l / 32)][l % 32].
@@ -88,24 +88,11 @@ __global__ __launch_bounds__(kWideBlock, RK > 32 ? 1 : 2) void k_wpstep(KArgs a)
   const Rsrc Qlr = tile_rsrc(a.fac + d.ql_slot, fform ? u32(m) * RK * 4u : 0u);
   const Rsrc Qhr = tile_rsrc(a.fac + d.qh_slot, u32(m) * RK * 4u);
   const bool ph4 = aligned16(a.fac + d.ph_slot), ql4 = aligned16(a.fac + d.ql_slot);
-  // from kBlockedRank on the tile's Ph rows sit in LDS (padded rows) and the block operands are
-  // loaded for the current block instead of one block ahead: the VGPRs hold P's accumulators
-  constexpr bool BIG = RK >= kBlockedRank;
-  constexpr int PL = RK + 1;
-  __shared__ float phs[BIG ? 32 * PL : 1];
-  float pa[BIG ? 1 : KH];  // correction A operand: -Ph[r0 + l % 32][KH h + s]
-  if constexpr (BIG) {
-    const float* Ph = a.fac + d.ph_slot + r0 * RK;
-    for (int e = lane; e < 32 * RK; e += kWideBlock) {
-      const int r = e / RK, k = e % RK;
-      phs[r * PL + k] = (fform && r < rows) ? -Ph[r * RK + k] : 0.f;
-    }
-    __syncthreads();
-  } else {
-    load_run<KH>(Phr, u32(li * RK + KH * h) * 4u, ph4, pa);
+  static_assert(RK < kSplitRank, "from kSplitRank on the rank-split kernel takes the P-step");
+  float pa[KH];  // correction A operand: -Ph[r0 + l % 32][KH h + s]
+  load_run<KH>(Phr, u32(li * RK + KH * h) * 4u, ph4, pa);
 #pragma unroll
-    for (int s = 0; s < KH; ++s) pa[s] = -pa[s];
-  }
+  for (int s = 0; s < KH; ++s) pa[s] = -pa[s];
 
   auto load_block = [&](int64_t c0, float* g, float* e) {
     const uint32_t coff = c0 + li < m ? u32(c0 + li) * 4u : kOut;
@@ -132,37 +119,29 @@ __global__ __launch_bounds__(kWideBlock, RK > 32 ? 1 : 2) void k_wpstep(KArgs a)
   __shared__ float xt[2][32 * LD];
   float g[16], e[16], qa[KH], qb[NR][16];
   load_block(0, g, e);
-  if constexpr (!BIG) load_ops(0, qa, qb);
+  load_ops(0, qa, qb);
 
   v16f p[NR];
 #pragma unroll
   for (int kb = 0; kb < NR; ++kb) p[kb] = zero16();
   int buf = 0;
   for (int64_t c0 = 0; c0 < m; c0 += 32, buf ^= 1) {
-    if constexpr (BIG) load_ops(c0, qa, qb);
     v16f x;
 #pragma unroll
     for (int v = 0; v < 16; ++v) x[v] = g[v] + e[v];
-    float ca[BIG ? 1 : KH], cb[BIG ? 1 : NR][16];
-    if constexpr (!BIG) {
+    float ca[KH], cb[NR][16];
 #pragma unroll
-      for (int s = 0; s < KH; ++s) ca[s] = qa[s];
+    for (int s = 0; s < KH; ++s) ca[s] = qa[s];
 #pragma unroll
-      for (int kb = 0; kb < NR; ++kb)
+    for (int kb = 0; kb < NR; ++kb)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) cb[kb][v] = qb[kb][v];
-    }
+      for (int v = 0; v < 16; ++v) cb[kb][v] = qb[kb][v];
     const uint32_t coff = c0 + li < m ? u32(c0 + li) * 4u : kOut;
     load_block(c0 + 32, g, e);  // next block (past m: zeros, no traffic)
-    if constexpr (!BIG) load_ops(c0 + 32, qa, qb);
+    load_ops(c0 + 32, qa, qb);
     if (fform) {  // X -= Ph Ql^T: A = -Ph (row, rank), B = Ql^T (rank, column)
 #pragma unroll
-      for (int s = 0; s < KH; ++s) {
-        if constexpr (BIG)
-          x = mfma(phs[li * PL + KH * h + s], qa[s], x);
-        else
-          x = mfma(pa[s], ca[s], x);
-      }
+      for (int s = 0; s < KH; ++s) x = mfma(pa[s], ca[s], x);
     }
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
@@ -174,12 +153,7 @@ __global__ __launch_bounds__(kWideBlock, RK > 32 ? 1 : 2) void k_wpstep(KArgs a)
     for (int v = 0; v < 16; ++v) {  // P += X Qh: A = X (row, column), B = Qh (column, rank)
       const float xa = xt[buf][li * LD + drow(v, h)];
 #pragma unroll
-      for (int kb = 0; kb < NR; ++kb) {
-        if constexpr (BIG)
-          p[kb] = mfma(xa, qb[kb][v], p[kb]);
-        else
-          p[kb] = mfma(xa, cb[kb][v], p[kb]);
-      }
+      for (int kb = 0; kb < NR; ++kb) p[kb] = mfma(xa, cb[kb][v], p[kb]);
     }
   }
 
@@ -226,23 +200,10 @@ __global__ __launch_bounds__(kWideBlock, RK > 32 ? 1 : 2) void k_wqstep(KArgs a)
   const Rsrc Qhr = tile_rsrc(a.fac + d.qh_slot + c0 * RK, xform ? u32(w) * RK * 4u : 0u);
   const Rsrc Plr = tile_rsrc(a.fac + d.pl_slot + r0 * RK, xform ? u32(rows) * RK * 4u : 0u);
   const Rsrc Phr = tile_rsrc(a.fac + d.ph_slot + r0 * RK, u32(rows) * RK * 4u);
-  // from kBlockedRank on the block's Qh rows sit in LDS (padded rows) and the row blocks'
-  // operands are loaded for the current block instead of one block ahead
-  constexpr bool BIG = RK >= kBlockedRank;
-  constexpr int PL = RK + 1;
-  __shared__ float qvs[BIG ? 32 * PL : 1];
-  float qv[BIG ? 1 : KH];  // correction B operand: Qh[c0 + l % 32][KH h + s]
-  if constexpr (BIG) {
-    const float* Qh = a.fac + d.qh_slot + c0 * RK;
-    for (int e = lane; e < 32 * RK; e += kWideBlock) {
-      const int c = e / RK, k = e % RK;
-      qvs[c * PL + k] = (xform && c < w) ? Qh[c * RK + k] : 0.f;
-    }
-    __syncthreads();
-  } else {
+  static_assert(RK < kSplitRank, "from kSplitRank on the rank-split kernel takes the Q-step");
+  float qv[KH];  // correction B operand: Qh[c0 + l % 32][KH h + s]
 #pragma unroll
-    for (int s = 0; s < KH; ++s) qv[s] = bld1(Qhr, u32(li * RK + KH * h + s) * 4u);
-  }
+  for (int s = 0; s < KH; ++s) qv[s] = bld1(Qhr, u32(li * RK + KH * h + s) * 4u);
   const uint32_t coff = li < w ? u32(li) * 4u : kOut;
 
   const bool pl4 = aligned16(a.fac + d.pl_slot);
@@ -267,34 +228,26 @@ __global__ __launch_bounds__(kWideBlock, RK > 32 ? 1 : 2) void k_wqstep(KArgs a)
   };
   float g[16], e[16], pa[KH], pb[NR][16];
   load_block(0, g, e);
-  if constexpr (!BIG) load_ops(0, pa, pb);
+  load_ops(0, pa, pb);
   v16f q[NR];
 #pragma unroll
   for (int kb = 0; kb < NR; ++kb) q[kb] = zero16();
   for (int rb = 0; rb < rows; rb += 32) {
-    if constexpr (BIG) load_ops(rb, pa, pb);
     v16f x;
 #pragma unroll
     for (int v = 0; v < 16; ++v) x[v] = g[v] + e[v];
-    float ca[BIG ? 1 : KH], cb[BIG ? 1 : NR][16];
-    if constexpr (!BIG) {
+    float ca[KH], cb[NR][16];
 #pragma unroll
-      for (int s = 0; s < KH; ++s) ca[s] = pa[s];
+    for (int s = 0; s < KH; ++s) ca[s] = pa[s];
 #pragma unroll
-      for (int kb = 0; kb < NR; ++kb)
+    for (int kb = 0; kb < NR; ++kb)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) cb[kb][v] = pb[kb][v];
-    }
+      for (int v = 0; v < 16; ++v) cb[kb][v] = pb[kb][v];
     load_block(rb + 32, g, e);  // next block (past the chunk: zeros, no traffic)
-    if constexpr (!BIG) load_ops(rb + 32, pa, pb);
+    load_ops(rb + 32, pa, pb);
     if (xform) {  // F -= Pl Qh^T: A = -Pl (row, rank), B = Qh^T (rank, column)
 #pragma unroll
-      for (int s = 0; s < KH; ++s) {
-        if constexpr (BIG)
-          x = mfma(-pa[s], qvs[li * PL + KH * h + s], x);
-        else
-          x = mfma(-ca[s], qv[s], x);
-      }
+      for (int s = 0; s < KH; ++s) x = mfma(-ca[s], qv[s], x);
     }
 #pragma unroll
     for (int v = 0; v < 16; ++v)
@@ -302,12 +255,7 @@ __global__ __launch_bounds__(kWideBlock, RK > 32 ? 1 : 2) void k_wqstep(KArgs a)
 #pragma unroll
     for (int v = 0; v < 16; ++v)  // Q += F^T Ph: A = F^T, B = Ph
 #pragma unroll
-      for (int kb = 0; kb < NR; ++kb) {
-        if constexpr (BIG)
-          q[kb] = mfma(x[v], pb[kb][v], q[kb]);
-        else
-          q[kb] = mfma(x[v], cb[kb][v], q[kb]);
-      }
+      for (int kb = 0; kb < NR; ++kb) q[kb] = mfma(x[v], cb[kb][v], q[kb]);
   }
   const int64_t ncb = (m + d.q_cb - 1) / d.q_cb;
   const int64_t stride = ncb * d.q_cb * RK;  // one row chunk of partials
@@ -374,15 +322,16 @@ __global__ __launch_bounds__(kWideBlock) void k_wrecon(KArgs a) {
 }
 
 // ---------------------------------------------------------------------------------------
-// From kSplitRank on one wave cannot hold the operands of every rank, so the four waves of a
-// 256-thread workgroup split the rank: wave w takes ranks rk0 = 64 w ... rk0 + 63 of each
-// rank-r term (r / 128 K steps per lane half, two 32-rank output blocks), with the operand
-// layout of the kernels above.  A correction (or a decompressed block) is a sum over all ranks,
-// so each wave writes its partial 32 x 32 block to LDS and wave w adds the four partials, in wave
-// order, for its entries v = 4 w + j (j < 4) of the MFMA layout: rows 8 w + 4 (l / 32) + j of the
-// block (drow(4 w + j, h) = 8 w + 4 h + j).  Wave w also loads M and E for those entries only.
-// LDS buffers alternate between blocks, so one barrier per use suffices.
-constexpr int kSplitWaves = kSplitBlock / kWave;
+// From kSplitRank on one wave cannot hold the operands of every rank, so the SW = 4 waves of a
+// 256-thread workgroup split the rank: wave w takes ranks rk0 = w r / 4 ... of each rank-r term
+// (r / 8 K steps per lane half, r / 128 32-rank output blocks), with the operand layout of the
+// kernels above.  A correction (or a decompressed block) is a sum over all ranks, so each wave
+// writes its partial 32 x 32 block to LDS and wave w adds the SW partials, in wave order, for its
+// EPW = 16 / SW entries v = EPW w + j (j < EPW) of the MFMA layout, rows drow(v, l / 32) of the
+// block.  Wave w also loads M and E for those entries only.  LDS buffers alternate between
+// blocks, so one barrier per use suffices.
+constexpr int kSplitWaves = 4;
+constexpr int kSplitBlock = kSplitWaves * kWave;
 
 // P-step over a 32-row tile, the 32-column blocks in order: partial corrections -Ph Ql^T (F
 // form) -> X = M + E + their sum for the wave's entries, stored to the arena and to the
@@ -390,7 +339,8 @@ constexpr int kSplitWaves = kSplitBlock / kWave;
 // requested before the current block's MFMAs.
 template <int RK>
 __global__ __launch_bounds__(kSplitBlock, 2) void k_spstep(KArgs a) {
-  constexpr int RS = RK / kSplitWaves, KH = RS / 2, NR = RS / 32;
+  constexpr int SW = kSplitWaves, EPW = 16 / SW, RS = RK / SW, KH = RS / 2, NR = RS / 32;
+  static_assert(RS % 32 == 0 && EPW * SW == 16, "whole 32-rank blocks and entries per wave");
   constexpr int LD = 33;
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
@@ -412,11 +362,11 @@ __global__ __launch_bounds__(kSplitBlock, 2) void k_spstep(KArgs a) {
 #pragma unroll
   for (int s = 0; s < KH; ++s) pa[s] = -pa[s];
 
-  auto load_block = [&](int64_t c0, float* g, float* e) {  // the wave's four entries
+  auto load_block = [&](int64_t c0, float* g, float* e) {  // the wave's entries
     const uint32_t coff = c0 + li < m ? u32(c0 + li) * 4u : kOut;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint32_t o = coff == kOut ? kOut : u32(8 * wave + 4 * h + j) * row_bytes + coff;
+    for (int j = 0; j < EPW; ++j) {
+      const uint32_t o = coff == kOut ? kOut : u32(drow(EPW * wave + j, h)) * row_bytes + coff;
       g[j] = bld1_nt(G, o);
       e[j] = bld1_nt(E, o);
     }
@@ -434,9 +384,9 @@ __global__ __launch_bounds__(kSplitBlock, 2) void k_spstep(KArgs a) {
         qb[kb][v] = bld1(Qhr, col < m ? u32(col * RK + rk0 + kb * 32 + li) * 4u : kOut);
       }
   };
-  __shared__ float red[2][kSplitWaves][16 * kWave];
+  __shared__ float red[2][SW][16 * kWave];
   __shared__ float xt[2][32 * LD];
-  float g[4], e[4], qa[KH], qb[NR][16];
+  float g[EPW], e[EPW], qa[KH], qb[NR][16];
   load_block(0, g, e);
   if (fform) load_ql(0, qa);
   load_qh(0, qb);
@@ -455,22 +405,22 @@ __global__ __launch_bounds__(kSplitBlock, 2) void k_spstep(KArgs a) {
       for (int v = 0; v < 16; ++v) red[buf][wave][v * kWave + lane] = x[v];
       __syncthreads();
     }
-    float cg[4], ce[4];
+    float cg[EPW], ce[EPW];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < EPW; ++j) {
       cg[j] = g[j];
       ce[j] = e[j];
     }
     load_block(c0 + 32, g, e);  // next block (past m: zeros, no traffic)
     const uint32_t coff = c0 + li < m ? u32(c0 + li) * 4u : kOut;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int v = 4 * wave + j, row = 8 * wave + 4 * h + j;
+    for (int j = 0; j < EPW; ++j) {
+      const int v = EPW * wave + j, row = drow(v, h);
       float xv = cg[j] + ce[j];
       if (fform) {
         float c = red[buf][0][v * kWave + lane];
 #pragma unroll
-        for (int w = 1; w < kSplitWaves; ++w) c += red[buf][w][v * kWave + lane];
+        for (int w = 1; w < SW; ++w) c += red[buf][w][v * kWave + lane];
         xv += c;
       }
       bst1_nt(E, coff == kOut ? kOut : u32(row) * row_bytes + coff, xv);
@@ -507,7 +457,8 @@ __global__ __launch_bounds__(kSplitBlock, 2) void k_spstep(KArgs a) {
 // arena and shared through LDS -> Q += F^T Ph over the wave's ranks, into the chunk's partials.
 template <int RK>
 __global__ __launch_bounds__(kSplitBlock, 2) void k_sqstep(KArgs a) {
-  constexpr int RS = RK / kSplitWaves, KH = RS / 2, NR = RS / 32;
+  constexpr int SW = kSplitWaves, EPW = 16 / SW, RS = RK / SW, KH = RS / 2, NR = RS / 32;
+  static_assert(RS % 32 == 0 && EPW * SW == 16, "whole 32-rank blocks and entries per wave");
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
   const int wave = tid() >> 6, lane = tid() & 63, h = lane >> 5, li = lane & 31;
@@ -530,10 +481,10 @@ __global__ __launch_bounds__(kSplitBlock, 2) void k_sqstep(KArgs a) {
   load_run<KH>(Qhr, u32(li * RK + rk0 + KH * h) * 4u, qh4, qv);
   const uint32_t coff = li < w ? u32(li) * 4u : kOut;
 
-  auto load_block = [&](int rb, float* g, float* e) {  // the wave's four entries
+  auto load_block = [&](int rb, float* g, float* e) {  // the wave's entries
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint32_t o = coff == kOut ? kOut : u32(rb + 8 * wave + 4 * h + j) * row_bytes + coff;
+    for (int j = 0; j < EPW; ++j) {
+      const uint32_t o = coff == kOut ? kOut : u32(rb + drow(EPW * wave + j, h)) * row_bytes + coff;
       g[j] = bld1_nt(G, o);
       e[j] = bld1_nt(E, o);
     }
@@ -546,9 +497,9 @@ __global__ __launch_bounds__(kSplitBlock, 2) void k_sqstep(KArgs a) {
       for (int v = 0; v < 16; ++v)
         pb[kb][v] = bld1(Phr, u32((rb + drow(v, h)) * RK + rk0 + kb * 32 + li) * 4u);
   };
-  __shared__ float red[2][kSplitWaves][16 * kWave];
+  __shared__ float red[2][SW][16 * kWave];
   __shared__ float fs[2][16 * kWave];
-  float g[4], e[4], pa[KH], pb[NR][16];
+  float g[EPW], e[EPW], pa[KH], pb[NR][16];
   load_block(0, g, e);
   load_ops(0, pa, pb);
   v16f q[NR];
@@ -556,9 +507,9 @@ __global__ __launch_bounds__(kSplitBlock, 2) void k_sqstep(KArgs a) {
   for (int kb = 0; kb < NR; ++kb) q[kb] = zero16();
   int buf = 0;
   for (int rb = 0; rb < rows; rb += 32, buf ^= 1) {
-    float cg[4], ce[4], ca[KH], cb[NR][16];
+    float cg[EPW], ce[EPW], ca[KH], cb[NR][16];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < EPW; ++j) {
       cg[j] = g[j];
       ce[j] = e[j];
     }
@@ -579,16 +530,16 @@ __global__ __launch_bounds__(kSplitBlock, 2) void k_sqstep(KArgs a) {
       __syncthreads();
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int v = 4 * wave + j;
+    for (int j = 0; j < EPW; ++j) {
+      const int v = EPW * wave + j;
       float f = cg[j] + ce[j];
       if (xform) {
         float c = red[buf][0][v * kWave + lane];
 #pragma unroll
-        for (int w2 = 1; w2 < kSplitWaves; ++w2) c += red[buf][w2][v * kWave + lane];
+        for (int w2 = 1; w2 < SW; ++w2) c += red[buf][w2][v * kWave + lane];
         f += c;
       }
-      bst1_nt(E, coff == kOut ? kOut : u32(rb + 8 * wave + 4 * h + j) * row_bytes + coff, f);
+      bst1_nt(E, coff == kOut ? kOut : u32(rb + drow(v, h)) * row_bytes + coff, f);
       fs[buf][v * kWave + lane] = f;
     }
     __syncthreads();
@@ -613,7 +564,8 @@ __global__ __launch_bounds__(kSplitBlock, 2) void k_sqstep(KArgs a) {
 // with nontemporal stores.  The next block's B rows are requested before the current MFMAs.
 template <int RK>
 __global__ __launch_bounds__(kSplitBlock, 2) void k_srecon(KArgs a) {
-  constexpr int RS = RK / kSplitWaves, KH = RS / 2;
+  constexpr int SW = kSplitWaves, EPW = 16 / SW, RS = RK / SW, KH = RS / 2;
+  static_assert(RS % 32 == 0 && EPW * SW == 16, "whole 32-rank blocks and entries per wave");
   const Tile t = a.tiles[blockIdx.x];
   const bool odd = a.parity != 0;
   const MatDesc d = a.mats[t.idx];
@@ -637,7 +589,7 @@ __global__ __launch_bounds__(kSplitBlock, 2) void k_srecon(KArgs a) {
   constexpr int NB = kWideRCols / 32;  // column blocks per tile
   auto bcol = [&](int j) { return static_cast<int64_t>(t.b) * kWideRCols + j * 32; };
   auto boff = [&](int64_t c) { return c + li < m ? u32((c + li) * RK + rk0 + KH * h) * 4u : kOut; };
-  __shared__ float red[2][kSplitWaves][16 * kWave];
+  __shared__ float red[2][SW][16 * kWave];
   float bv[2][KH];  // B operand: B[c0 + l % 32][rk0 + KH h + s], this block and the next
   load_run<KH>(Br, boff(bcol(0)), b4, bv[0]);
 #pragma unroll
@@ -655,12 +607,12 @@ __global__ __launch_bounds__(kSplitBlock, 2) void k_srecon(KArgs a) {
     const Rsrc Or = tile_rsrc(O + c0, u32(rows - 1) * row_bytes + u32(w) * 4u);
     const uint32_t coff = li < w ? u32(li) * 4u : kOut;
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-      const int v = 4 * wave + jj;
+    for (int jj = 0; jj < EPW; ++jj) {
+      const int v = EPW * wave + jj;
       float s = red[j & 1][0][v * kWave + lane];
 #pragma unroll
-      for (int w2 = 1; w2 < kSplitWaves; ++w2) s += red[j & 1][w2][v * kWave + lane];
-      bst1_nt(Or, coff == kOut ? kOut : u32(8 * wave + 4 * h + jj) * row_bytes + coff, s);
+      for (int w2 = 1; w2 < SW; ++w2) s += red[j & 1][w2][v * kWave + lane];
+      bst1_nt(Or, coff == kOut ? kOut : u32(drow(v, h)) * row_bytes + coff, s);
     }
   }
 }
@@ -690,7 +642,12 @@ hipError_t launch_wide_rank(const Launch& l, const KArgs& args, hipStream_t s) {
       case K_WFACT: hipLaunchKernelGGL(k_wfact<RK>, grid, dim3(kBlock), 0, s, args); break;
       case K_WPSTEP: hipLaunchKernelGGL(k_spstep<RK>, grid, block, 0, s, args); break;
       case K_WQSTEP: hipLaunchKernelGGL(k_sqstep<RK>, grid, block, 0, s, args); break;
-      case K_WRECON: hipLaunchKernelGGL(k_srecon<RK>, grid, block, 0, s, args); break;
+      case K_WRECON:
+        if constexpr (RK >= kSplitReconRank)
+          hipLaunchKernelGGL(k_srecon<RK>, grid, block, 0, s, args);
+        else
+          hipLaunchKernelGGL(k_wrecon<RK>, grid, dim3(kWideBlock), 0, s, args);
+        break;
       default: return hipErrorInvalidValue;
     }
   } else {

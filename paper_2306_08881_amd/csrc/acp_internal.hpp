@@ -141,7 +141,7 @@ constexpr int32_t kBlockedRank = 128;  // ranks whose W K_CHOL forms from Gram p
 // ranks whose MFMA compress kernels split the rank over the four waves of a workgroup
 // (kSplitRank), whose decompress kernel does (kSplitReconRank), and whose W is factored in
 // 2 x 2 blocks of 128 (kCholBlockRank)
-constexpr int32_t kSplitRank = 128;
+constexpr int32_t kSplitRank = 64;
 constexpr int32_t kSplitReconRank = 256;
 constexpr int32_t kCholBlockRank = 256;
 // tiles that share one slice's Gram from kBlockedRank on: the (r / 4)(r / 4 + 1) / 2 blocks of 4 x 4

@@ -9,11 +9,9 @@
 //            P_loc = X Qh;  afterwards E = X - P_loc Qh^T is implied.
 //   Q-step:  F = M + E_arena (- Pl Qh^T when the arena holds X), F written to the arena,
 //            Q_loc = F^T Ph; afterwards E = F - Ph Q_loc^T is implied.
-// Each is one rank-r correction and one rank-r product per element.  Rank 64 keeps two blocks
-// of the product's output per wave; its compress kernels run one wave per SIMD (their operands
-// take every VGPR) instead of spilling.  From rank 128 the four waves of a workgroup split the
-// rank in the compress kernels (k_spstep, k_sqstep), at rank 256 in the decompress kernel too
-// (k_srecon).
+// Each is one rank-r correction and one rank-r product per element.  From rank 64 the waves of
+// a workgroup split the rank in the compress kernels (k_spstep, k_sqstep), at rank 256 in the
+// decompress kernel too (k_srecon); the one-wave decompress keeps r / 32 output blocks per wave.
 //
 // MFMA layout (one wave): D (32 x 32) += A (32 x 2) B (2 x 32).  Lane l supplies
 // A[l % 32][l / 32] and B[l / 32][l % 32]; register v of lane l holds D[drow(v, l / 32)][l % 32].
@@ -322,24 +320,23 @@ __global__ __launch_bounds__(kWideBlock) void k_wrecon(KArgs a) {
 }
 
 // ---------------------------------------------------------------------------------------
-// From kSplitRank on one wave cannot hold the operands of every rank, so the SW = 4 waves of a
-// 256-thread workgroup split the rank: wave w takes ranks rk0 = w r / 4 ... of each rank-r term
-// (r / 8 K steps per lane half, r / 128 32-rank output blocks), with the operand layout of the
-// kernels above.  A correction (or a decompressed block) is a sum over all ranks, so each wave
+// From kSplitRank on one wave cannot hold the operands of every rank, so the SW waves of a
+// workgroup (split_waves: 2 at rank 64, 4 from rank 128) split the rank: wave w takes ranks
+// rk0 = w r / SW ... of each rank-r term (r / 2 SW K steps per lane half, r / 32 SW 32-rank
+// output blocks), with the operand layout of the kernels above.  A correction (or a decompressed block) is a sum over all ranks, so each wave
 // writes its partial 32 x 32 block to LDS and wave w adds the SW partials, in wave order, for its
 // EPW = 16 / SW entries v = EPW w + j (j < EPW) of the MFMA layout, rows drow(v, l / 32) of the
 // block.  Wave w also loads M and E for those entries only.  LDS buffers alternate between
 // blocks, so one barrier per use suffices.
-constexpr int kSplitWaves = 4;
-constexpr int kSplitBlock = kSplitWaves * kWave;
+constexpr int split_waves(int r) { return r >= 128 ? 4 : 2; }
 
 // P-step over a 32-row tile, the 32-column blocks in order: partial corrections -Ph Ql^T (F
 // form) -> X = M + E + their sum for the wave's entries, stored to the arena and to the
 // transposing tile -> P += X Qh over the wave's ranks.  The next block's M, E and factor rows are
 // requested before the current block's MFMAs.
 template <int RK>
-__global__ __launch_bounds__(kSplitBlock, 2) void k_spstep(KArgs a) {
-  constexpr int SW = kSplitWaves, EPW = 16 / SW, RS = RK / SW, KH = RS / 2, NR = RS / 32;
+__global__ __launch_bounds__(kWave * split_waves(RK), 2) void k_spstep(KArgs a) {
+  constexpr int SW = split_waves(RK), EPW = 16 / SW, RS = RK / SW, KH = RS / 2, NR = RS / 32;
   static_assert(RS % 32 == 0 && EPW * SW == 16, "whole 32-rank blocks and entries per wave");
   constexpr int LD = 33;
   const Tile t = a.tiles[blockIdx.x];
@@ -456,8 +453,8 @@ __global__ __launch_bounds__(kSplitBlock, 2) void k_spstep(KArgs a) {
 // corrections -Pl Qh^T (X form) -> F = M + E + their sum for the wave's entries, stored to the
 // arena and shared through LDS -> Q += F^T Ph over the wave's ranks, into the chunk's partials.
 template <int RK>
-__global__ __launch_bounds__(kSplitBlock, 2) void k_sqstep(KArgs a) {
-  constexpr int SW = kSplitWaves, EPW = 16 / SW, RS = RK / SW, KH = RS / 2, NR = RS / 32;
+__global__ __launch_bounds__(kWave * split_waves(RK), 2) void k_sqstep(KArgs a) {
+  constexpr int SW = split_waves(RK), EPW = 16 / SW, RS = RK / SW, KH = RS / 2, NR = RS / 32;
   static_assert(RS % 32 == 0 && EPW * SW == 16, "whole 32-rank blocks and entries per wave");
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
@@ -563,8 +560,8 @@ __global__ __launch_bounds__(kSplitBlock, 2) void k_sqstep(KArgs a) {
 // wave's share of A B^T / p, the shares added in wave order for the wave's entries and stored
 // with nontemporal stores.  The next block's B rows are requested before the current MFMAs.
 template <int RK>
-__global__ __launch_bounds__(kSplitBlock, 2) void k_srecon(KArgs a) {
-  constexpr int SW = kSplitWaves, EPW = 16 / SW, RS = RK / SW, KH = RS / 2;
+__global__ __launch_bounds__(kWave * split_waves(RK), 2) void k_srecon(KArgs a) {
+  constexpr int SW = split_waves(RK), EPW = 16 / SW, RS = RK / SW, KH = RS / 2;
   static_assert(RS % 32 == 0 && EPW * SW == 16, "whole 32-rank blocks and entries per wave");
   const Tile t = a.tiles[blockIdx.x];
   const bool odd = a.parity != 0;
@@ -637,7 +634,7 @@ template <int RK>
 hipError_t launch_wide_rank(const Launch& l, const KArgs& args, hipStream_t s) {
   const dim3 grid(static_cast<unsigned>(l.ntiles));
   if constexpr (RK >= kSplitRank) {
-    const dim3 block(kSplitBlock);
+    const dim3 block(kWave * split_waves(RK));
     switch (l.kernel) {
       case K_WFACT: hipLaunchKernelGGL(k_wfact<RK>, grid, dim3(kBlock), 0, s, args); break;
       case K_WPSTEP: hipLaunchKernelGGL(k_spstep<RK>, grid, block, 0, s, args); break;

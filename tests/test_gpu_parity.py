@@ -167,6 +167,14 @@ def test_error_feedback_off():
     _assert_ok(_custom(RAGGED[:6] + [(256, 64, 3, 3)], 4, ef=False))
 
 
+@pytest.mark.parametrize("rank", [8, 64, 128])
+def test_error_feedback_off_mfma_ranks(rank):
+    """Without error feedback the MFMA kernels read no E and write none (one-wave and
+    rank-split kernels)."""
+    _require_gpu()
+    _assert_ok(_custom([(300, 1030), (64,), (129, 2048), (1000, 520)], rank, ef=False))
+
+
 def test_single_bucket_of_vectors_and_tiny_cap():
     _require_gpu()
     _assert_ok(_custom([(10,), (20,), (8, 8), (30,)], 2, cap=16))
@@ -195,15 +203,15 @@ def test_zero_gradient_then_nonzero():
         assert PU.rel_err(run.error_slice(0), orc.error(0)) <= PU.TOL
 
 
-@pytest.mark.parametrize("rank,k", [(128, 40), (256, 100)])
+@pytest.mark.parametrize("rank,k", [(8, 3), (32, 10), (64, 20), (128, 40), (256, 100)])
 def test_rank_deficient_high_rank(rank, k):
     """Gradients of exact rank k < r: from step 2 on the orthogonalisation drops r - k columns of
-    the reused factor (kept and dropped pivots in the first 32-column block of the blocked
-    Cholesky, dropped ones only in the others), on both sides alike.  The kept columns'
-    Gram-Schmidt is as ill-conditioned as a random k x k matrix, which scales the fp32 rounding
-    difference from the fp64 oracle and makes it compound from step to step, so the oracle is
-    re-synced from the device state before every step after the first: each step's arithmetic
-    is checked on its own."""
+    the reused factor (r <= 64: the one-wave Cholesky; r = 128 and 256: kept and dropped pivots
+    in the blocked Cholesky's first blocks, dropped ones only after them), on both sides alike.
+    The kept columns' Gram-Schmidt is as ill-conditioned as a random k x k matrix, which scales
+    the fp32 rounding difference from the fp64 oracle and makes it compound from step to step,
+    so the oracle is re-synced from the device state before every step after the first: each
+    step's arithmetic is checked on its own."""
     _require_gpu()
     shapes = [(300, 520)]
     run = PU.Runner(shapes, rank)

@@ -68,7 +68,7 @@ __device__ inline bool aligned16(const float* p) { return (reinterpret_cast<uint
 // [l % 32].  The next block's M, E and factor rows are requested before the current block's
 // MFMAs.
 template <int RK>
-__global__ __launch_bounds__(kWideBlock, RK > 32 ? 1 : 2) void k_wpstep(KArgs a) {
+__global__ __launch_bounds__(kWideBlock, 2) void k_wpstep(KArgs a) {
   constexpr int KH = RK / 2;
   constexpr int NR = RK > 32 ? RK / 32 : 1;  // 32-rank blocks of P (one MFMA block each)
   constexpr int LD = 33;  // padded LDS row: the transposed reads hit 32 different banks
@@ -179,7 +179,7 @@ __global__ __launch_bounds__(kWideBlock, RK > 32 ? 1 : 2) void k_wpstep(KArgs a)
 // Q += F^T Ph with the rows as K.  Lane l's partial Q of column c0 + drow(v, l / 32), rank
 // l % 32, goes to the chunk's partial block for K_QFIN.
 template <int RK>
-__global__ __launch_bounds__(kWideBlock, RK > 32 ? 1 : 2) void k_wqstep(KArgs a) {
+__global__ __launch_bounds__(kWideBlock, 2) void k_wqstep(KArgs a) {
   constexpr int KH = RK / 2;
   constexpr int NR = RK > 32 ? RK / 32 : 1;  // 32-rank blocks of Q (one MFMA block each)
   const Tile t = a.tiles[blockIdx.x];

@@ -323,11 +323,12 @@ __global__ __launch_bounds__(kWideBlock) void k_wrecon(KArgs a) {
 // From kSplitRank on one wave cannot hold the operands of every rank, so the SW waves of a
 // workgroup (split_waves: 2 at rank 64, 4 from rank 128) split the rank: wave w takes ranks
 // rk0 = w r / SW ... of each rank-r term (r / 2 SW K steps per lane half, r / 32 SW 32-rank
-// output blocks), with the operand layout of the kernels above.  A correction (or a decompressed block) is a sum over all ranks, so each wave
-// writes its partial 32 x 32 block to LDS and wave w adds the SW partials, in wave order, for its
-// EPW = 16 / SW entries v = EPW w + j (j < EPW) of the MFMA layout, rows drow(v, l / 32) of the
-// block.  Wave w also loads M and E for those entries only.  LDS buffers alternate between
-// blocks, so one barrier per use suffices.
+// output blocks), with the operand layout of the kernels above.  A correction (or a
+// decompressed block) is a sum over all ranks, so each wave writes its partial 32 x 32 block to
+// LDS and wave w adds the SW partials, in wave order, for its EPW = 16 / SW entries
+// v = EPW w + j (j < EPW) of the MFMA layout, rows drow(v, l / 32) of the block.  Wave w also
+// loads M and E for those entries only.  LDS buffers alternate between blocks, so one barrier
+// per use suffices.
 constexpr int split_waves(int r) { return r >= 128 ? 4 : 2; }
 
 // P-step over a 32-row tile, the 32-column blocks in order: partial corrections -Ph Ql^T (F

@@ -39,19 +39,23 @@ def _resnet_inputs(run, wl, t):
 
 
 WIDE_SHAPES = [(96, 80), (33, 5, 7), (40,), (70, 130), (17,), (64, 64), (200, 36)]
+# rank-split kernels, Gram partials over several slices, the blocked Cholesky
+SPLIT_SHAPES = [(300, 520), (40,), (2100, 300), (270, 1000)]
 
 
-@pytest.mark.parametrize("case", ["resnet50_r4", "wide_r16_after_p", "wide_r32_after_q"])
+@pytest.mark.parametrize("case", ["resnet50_r4", "wide_r16_after_p", "wide_r32_after_q",
+                                  "split_r128_after_p", "split_r256_after_q"])
 def test_bitwise_repeatable_and_resume(case):
     """Repeat runs agree bitwise; resuming from a checkpoint continues bitwise.  The wide cases
     checkpoint a rank-16 context after a P-step (its arena holds X) and a rank-32 context after
-    a Q-step (its arena holds F)."""
+    a Q-step (its arena holds F); the split cases do the same at ranks 128 and 256."""
     if case == "resnet50_r4":
         wl = sg.WORKLOADS["resnet50_r4"]
         shapes, rank, cap, at = [p.shape for p in wl.params], 4, 25 << 20, 3
     else:
-        rank, at = (16, 3) if case == "wide_r16_after_p" else (32, 4)
-        shapes, cap = WIDE_SHAPES, 1 << 15
+        rank, at = {"wide_r16_after_p": (16, 3), "wide_r32_after_q": (32, 4),
+                    "split_r128_after_p": (128, 3), "split_r256_after_q": (256, 4)}[case]
+        shapes, cap = (WIDE_SHAPES, 1 << 15) if case.startswith("wide") else (SPLIT_SHAPES, 1 << 20)
         wl = sg.Workload(case, [sg.Param(f"t{i}", s) for i, s in enumerate(shapes)], rank, 8,
                          lambda p: 0.05, seed=11)
     inputs = {}

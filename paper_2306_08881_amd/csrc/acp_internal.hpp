@@ -157,8 +157,10 @@ constexpr int kWideRCols = 1024;   // K_WRECON columns per tile: 32 blocks of 32
 
 // K_QSTEP variants: column slots per lane | kQFused when the kernel also orthogonalises P
 constexpr int32_t kQFused = 16;
-// K_PFUSED variant bit: S = 1 on three waves, for rows of 516 to 768 columns
+// K_PFUSED variant bits: S = 1 on three waves, for rows of 516 to 768 columns; S = 2 on eight
+// waves, for rows of 3076 to 4096 columns
 constexpr int32_t kThreeWaves = 32;
+constexpr int32_t kEightWaves = 64;
 // K_FACT variants: bit 0 = Q (else P); the factor is read from its state slot
 
 struct Launch {

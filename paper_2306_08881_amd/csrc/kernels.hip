@@ -1526,6 +1526,9 @@ hipError_t launch_rank(const Launch& l, const KArgs& args, hipStream_t s) {
             case 1 | kThreeWaves:
               hipLaunchKernelGGL((k_pfused<1, 3>), grid, dim3(3 * kWave), 0, s, args);
               break;
+            case 2 | kEightWaves:
+              hipLaunchKernelGGL((k_pfused<2, 8>), grid, dim3(8 * kWave), 0, s, args);
+              break;
             case 2: hipLaunchKernelGGL(k_pfused<2>, grid, block, 0, s, args); break;
             case 3: hipLaunchKernelGGL(k_pfused<3>, grid, block, 0, s, args); break;
             case 4: hipLaunchKernelGGL(k_pfused<4>, grid, block, 0, s, args); break;

@@ -146,6 +146,8 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       c = {{{K_PNARROW, v}, {K_QNARROW, v}, {K_RNARROW, v}}};
     } else if (m / 4 <= 192) {  // three waves cover a row of the P-step
       c = {{{K_PFUSED, 1 | kThreeWaves}, {K_QSTEP, 4 | kQFused}, {K_RECON4, 0}}};
+    } else if (m / 4 > 768 && m / 4 <= 1024) {  // eight waves of two groups cover a row
+      c = {{{K_PFUSED, 2 | kEightWaves}, {K_QSTEP, 4 | kQFused}, {K_RECON4, 0}}};
     } else {
       const int32_t S = static_cast<int32_t>(cdiv(m / 4, 256));
       c = {{{K_PFUSED, S}, {K_QSTEP, 4 | kQFused}, {K_RECON4, 0}}};
@@ -464,12 +466,13 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     // small: rank-4 matrices of other rows, small enough for one workgroup (scls -1, T_SMALL
     // tiles in the same launches); generic: the general kernels
     // three: fast rows of 516-768 columns (three-wave P-step launch)
-    std::vector<int32_t> fast, narrow, small, generic, three;
+    // eight: fast rows of 3076-4096 columns (eight-wave P-step launch)
+    std::vector<int32_t> fast, narrow, small, generic, three, eight;
     for (int32_t mi : bk.mats) {
       if (is_fast(mi)) {
         const int64_t m4 = plan.mats[mi].m / 4;
         plan.mats[mi].scls = m4 <= 128 ? 0 : static_cast<int32_t>(cdiv(m4, 256));
-        (m4 <= 128 ? narrow : (m4 <= 192 ? three : fast)).push_back(mi);
+        (m4 <= 128 ? narrow : (m4 <= 192 ? three : (m4 > 768 && m4 <= 1024 ? eight : fast))).push_back(mi);
       } else if (is_small(mi)) {
         plan.mats[mi].scls = -1;
         small.push_back(mi);
@@ -537,6 +540,14 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         if (!vec_done) vec_tiles(bk), vec_done = true;
         sink.end(l, L);
       }
+      if (!eight.empty()) {
+        l = sink.begin(K_PFUSED, 2 | kEightWaves);
+        for (int32_t mi : eight)
+          pstep_tiles(mi, rows_for(mi, std::max<int64_t>(kPMinRows * plan.mats[mi].m,
+                                                          class_tile(K_PFUSED, 2 | kEightWaves, 4 * kTileElems))));
+        if (!vec_done) vec_tiles(bk), vec_done = true;
+        sink.end(l, L);
+      }
       if (pmerge >= 2) {
         bool any = false;
         for (int32_t S = 2; S <= 5; ++S)
@@ -589,8 +600,10 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
           any = !small.empty() || !narrow.empty();
         }
         const std::vector<int32_t>& set = (variant & kQFused) ? fast : generic;
-        if (variant & kQFused)  // the three-wave P-step's matrices too
+        if (variant & kQFused) {  // the three- and eight-wave P-step's matrices too
           for (int32_t mi : three) qtiles(mi), any = true;
+          for (int32_t mi : eight) qtiles(mi), any = true;
+        }
         for (int32_t mi : set) {
           if (!(variant & kQFused) && plan.mats[mi].q_cb != 4 * 64 * variant) continue;
           qtiles(mi);
@@ -617,7 +630,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         vec_tiles(bk);
         extra_done = true;
       };
-      if (!fast.empty() || !narrow.empty() || !small.empty() || !three.empty()) {
+      if (!fast.empty() || !narrow.empty() || !small.empty() || !three.empty() || !eight.empty()) {
         Launch l = sink.begin(K_RECON4, 0);
         extra();
         small_tiles();
@@ -625,6 +638,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
           for (int32_t mi : of_narrow(v)) row_tiles(mi, narrow_rows(mi, class_tile(K_RNARROW, v, kTileElems)));
         for (int32_t mi : fast) recon4_tiles(mi);
         for (int32_t mi : three) recon4_tiles(mi);
+        for (int32_t mi : eight) recon4_tiles(mi);
         sink.end(l, L);
       }
       for (int32_t vw : {4, 1}) {
@@ -761,7 +775,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   auto order_of = [](const Launch& l) -> int32_t {
     switch (l.kernel) {
       case K_APPLY: return 0;
-      case K_PFUSED: return (l.variant & kThreeWaves) ? 7 : 1 + l.variant;  // 2..7
+      case K_PFUSED: return (l.variant & kEightWaves) ? 8 : (l.variant & kThreeWaves) ? 7 : 1 + l.variant;  // 2..8
       case K_PROW: return 10;
       case K_EUPD: return 11;
       case K_WPSTEP: return 12;

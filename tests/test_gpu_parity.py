@@ -143,11 +143,11 @@ SMALL = [(3,), (5, 5), (256, 512), (256, 511), (257, 147), (64, 3, 7, 7), (200, 
          (255, 6), (6, 255)]
 
 
-# rank-4 rows of 516 to 768 columns (three-wave P-step and Q-step launches): at both ends of
-# that range and just past them, ragged row counts, beside a 1024-column matrix of the four-wave
-# launches and a vector
+# rank-4 rows of 516 to 768 columns (three-wave P-step launch) and of 3076 to 4096 columns
+# (eight-wave P-step launch): at both ends of those ranges and just past them, ragged row counts,
+# beside a 1024-column matrix of the four-wave launches and a vector
 THREE_WAVE = [(300, 516), (9, 768), (1000, 768), (129, 640), (64,), (37, 772), (260, 1024),
-              (2, 512), (4100, 700)]
+              (2, 512), (4100, 700), (37, 3076), (300, 4096), (5, 4000), (70, 3072), (33, 4100)]
 
 
 @pytest.mark.parametrize("ef", [True, False])

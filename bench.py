@@ -81,11 +81,12 @@ def cpu_baseline(wl, seconds: float = 12.0):
 
 def kernel_families(rank: int):
     """(label, ACP_KERNEL_* family, kernel symbol prefix) of the timed kernel families: the rank-4
-    register-resident kernels, the one-wave MFMA kernels of ranks 8 to 128 or the rank-split
-    MFMA kernels of rank 256, and the separate orthogonalisation kernels."""
+    register-resident kernels; the one-wave MFMA kernels of ranks 8 to 32; from rank 64 the
+    rank-split MFMA compress kernels, with the one-wave decompress up to rank 128 and the
+    rank-split one at 256; and the separate orthogonalisation kernels."""
     from paper_2306_08881_amd import _lib as L
-    if rank >= 256:
-        p, q, d = "k_spstep", "k_sqstep", "k_srecon"
+    if rank >= 64:
+        p, q, d = "k_spstep", "k_sqstep", "k_srecon" if rank >= 256 else "k_wrecon"
     elif rank >= 8:
         p, q, d = "k_wpstep", "k_wqstep", "k_wrecon"
     else:
@@ -161,7 +162,7 @@ def measured_traffic(workload: str, family: str, launches: int):
         return None
     if t.get("source_hash") != kernel_source_hash() or t.get("workload") not in (None, workload):
         return None
-    sym = next((k[2] for k in kernel_families(4) + kernel_families(8) + kernel_families(256) if k[0] == family), None)
+    sym = next((k[2] for k in kernel_families(4) + kernel_families(8) + kernel_families(64) + kernel_families(256) if k[0] == family), None)
     ks = [v for k, v in t["kernels"].items() if sym and k.startswith(sym)]
     if not ks:
         return None

@@ -144,10 +144,10 @@ constexpr int32_t kBlockedRank = 128;  // ranks whose W K_CHOL forms from Gram p
 constexpr int32_t kSplitRank = 64;
 constexpr int32_t kSplitReconRank = 256;
 constexpr int32_t kCholBlockRank = 256;
-// tiles that share one slice's Gram from kBlockedRank on: the (r / 4)(r / 4 + 1) / 2 blocks of 4 x 4
-// on and above the diagonal, one per thread of a 256-thread tile
+// tiles that share one slice's Gram from kBlockedRank on: the (r / 64)(r / 64 + 1) / 2 blocks of
+// 64 x 64 on and above the diagonal, one per wave of a four-wave tile
 constexpr int32_t gram_parts(int32_t r) {
-  return r >= kBlockedRank ? ((r / 4) * (r / 4 + 1) / 2 + 255) / 256 : 1;
+  return r >= kBlockedRank ? ((r / 64) * (r / 64 + 1) / 2 + 3) / 4 : 1;
 }
 constexpr int32_t kGsumEntries = 4096;  // Gram entries per K_GSUM tile
 constexpr int kWideBlock = 64;     // threads per workgroup of K_WPSTEP, K_WQSTEP, K_WRECON: one wave

@@ -356,72 +356,109 @@ __device__ void cholesky_w(const double* G, double* w_out) {
 }
 
 // Part `part` of the Gram of rows [r0, r1) of X (row-major, RK >= kBlockedRank columns) into
-// `out` (RK x RK doubles, global memory): G is symmetric, so only its 4 x 4 blocks on and above
-// the diagonal are formed (K_GSUM mirrors them); of those, numbered row by row, thread t of part
-// p owns block 256 p + t over every row of a chunk.  The chunk's rows sit in LDS as doubles and
-// the next chunk is requested before the current one's products.  The rows are also copied to
-// `copy` when set.
-template <int RK>
-__device__ void gram_blocked(const float* X, int64_t r0, int64_t r1, double* out, float* copy, int part) {
-  constexpr int CH = 32;
-  constexpr int NB4 = RK / 4, NU = NB4 * (NB4 + 1) / 2;
-  constexpr int PT = CH * RK / kBlock;  // chunk elements per thread
-  static_assert(gram_parts(RK) * kBlock >= NU, "every upper block needs a thread");
-  __shared__ __align__(16) double sh[CH * RK];
-  const int b = part * kBlock + tid();
-  const bool own = b < NU;
-  int bi = 0, bj = 0;
-  {
-    int rem = own ? b : 0, i = 0;
-    while (rem >= NB4 - i) rem -= NB4 - i, ++i;
-    bi = 4 * i;
-    bj = 4 * (i + rem);
-  }
-  double acc[4][4];
+// `out` (RK x RK doubles, global memory), on the fp64 matrix cores.  G is symmetric: of its
+// 64-column bands only the blocks G_IJ = X_I^T X_J with I <= J are formed, numbered row by row;
+// wave w of part p takes block 4 p + w.  A block is 4 x 4 products of 16 x 16
+// (v_mfma_f64_16x16x4f64, four rows of X each; operand entry [i][k] on lane i + 16 k, result
+// entry [4 v + l / 16][l % 16] in item v of lane l), product (a, b) for the columns 16 a ... and
+// 16 b ... of the two bands; a diagonal block skips its products a > b, whose entries lie below
+// the diagonal (K_GSUM mirrors the entries of the 4 x 4 blocks above it).  Each product adds the
+// rows in increasing groups of four; the next 16 rows are requested before the current ones'
+// products.  The diagonal blocks also copy their band of the rows to `copy` when set.
+typedef double v4d __attribute__((ext_vector_type(4)));
+
+template <int RK, bool DIAG>
+__device__ void gram_band(const float* X, int64_t r0, int64_t r1, double* out, float* copy, int I, int J) {
+  constexpr int G = 4;  // groups of four rows per step
+  const int lane = tid() % kWave, i = lane % 16, k = lane / 16;
+  const float* xa = X + 64 * I + i;
+  const float* xb = X + 64 * J + i;
+  v4d acc[4][4];
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
+  for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) acc[u][v] = 0.0;
-  const int64_t end = r1 * RK;
-  float nx[PT];
-  auto fetch = [&](int64_t c0) {
+    for (int b = 0; b < 4; ++b) acc[a][b] = v4d{0.0, 0.0, 0.0, 0.0};
+  // rows past the slice read its last row (no branch around the loads, so the wait for a step's
+  // rows leaves the next step's requests in flight); the A operand of those rows is zeroed
+  auto row_of = [&](int64_t g0, int s) {
+    const int64_t row = g0 + 4 * s + k;
+    return row < r1 ? row : r1 - 1;
+  };
+  // two register buffers of G groups, filled and consumed in turn
+  typedef float Buf[G][4];
+  auto fetch = [&](int64_t g0, Buf& ba, Buf& bb) {
 #pragma unroll
-    for (int k = 0; k < PT; ++k) {
-      const int64_t e = c0 * RK + tid() + k * kBlock;
-      nx[k] = e < end ? X[e] : 0.f;
+    for (int s = 0; s < G; ++s) {
+      const float* pa = xa + row_of(g0, s) * RK;
+      const float* pb = xb + row_of(g0, s) * RK;
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        ba[s][a] = pa[16 * a];
+        if (!DIAG) bb[s][a] = pb[16 * a];
+      }
     }
   };
-  fetch(r0);
-  for (int64_t c0 = r0; c0 < r1; c0 += CH) {
-    const int cn = static_cast<int>((r1 - c0) < CH ? (r1 - c0) : CH);
+  auto step = [&](int64_t g0, Buf& ba, Buf& bb) {
+    // the conversions stay behind the other buffer's requests, issued just before
 #pragma unroll
-    for (int k = 0; k < PT; ++k) {
-      const int e = tid() + k * kBlock;
-      sh[e] = static_cast<double>(nx[k]);
-      if (copy && c0 * RK + e < end) copy[c0 * RK + e] = nx[k];
-    }
-    __syncthreads();
-    fetch(c0 + CH);
-    if (own)
-      for (int rr = 0; rr < cn; ++rr) {
-        double xi[4], xj[4];
+    for (int s = 0; s < G; ++s)
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          xi[u] = sh[rr * RK + bi + u];
-          xj[u] = sh[rr * RK + bj + u];
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-          for (int v = 0; v < 4; ++v) acc[u][v] = fma(xi[u], xj[v], acc[u][v]);
+      for (int a = 0; a < 4; ++a) {
+        asm volatile("" : "+v"(ba[s][a]));
+        if (!DIAG) asm volatile("" : "+v"(bb[s][a]));
       }
-    __syncthreads();
+    // a row past the slice stores its clamped row's own values again
+    if (DIAG && copy)
+#pragma unroll
+      for (int s = 0; s < G; ++s)
+#pragma unroll
+        for (int a = 0; a < 4; ++a) copy[row_of(g0, s) * RK + 64 * I + 16 * a + i] = ba[s][a];
+#pragma unroll
+    for (int s = 0; s < G; ++s) {
+      const bool in = g0 + 4 * s + k < r1;
+      double xa4[4], xb4[4];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        xa4[a] = in ? static_cast<double>(ba[s][a]) : 0.0;
+        xb4[a] = static_cast<double>(DIAG ? ba[s][a] : bb[s][a]);
+      }
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+          if (!DIAG || a <= b) acc[a][b] = __builtin_amdgcn_mfma_f64_16x16x4f64(xa4[a], xb4[b], acc[a][b], 0, 0, 0);
+    }
+  };
+  Buf a0, b0, a1, b1;
+  fetch(r0, a0, b0);
+  for (int64_t g0 = r0; g0 < r1; g0 += 8 * G) {  // a second step past the slice adds zeros
+    fetch(g0 + 4 * G, a1, b1);
+    step(g0, a0, b0);
+    fetch(g0 + 8 * G, a0, b0);
+    step(g0 + 4 * G, a1, b1);
   }
-  if (own)
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+  for (int a = 0; a < 4; ++a)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) out[(bi + u) * RK + bj + v] = acc[u][v];
+    for (int b = 0; b < 4; ++b)
+      if (!DIAG || a <= b)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          out[(64 * I + 16 * a + 4 * v + k) * RK + 64 * J + 16 * b + i] = acc[a][b][v];
+}
+
+template <int RK>
+__device__ void gram_blocked(const float* X, int64_t r0, int64_t r1, double* out, float* copy, int part) {
+  constexpr int NB = RK / 64, NP = NB * (NB + 1) / 2;
+  static_assert(gram_parts(RK) * (kBlock / kWave) >= NP, "every band block needs a wave");
+  const int pr = part * (kBlock / kWave) + tid() / kWave;
+  if (pr >= NP) return;
+  int I = 0, rem = pr;
+  while (rem >= NB - I) rem -= NB - I, ++I;
+  if (rem == 0)
+    gram_band<RK, true>(X, r0, r1, out, copy, I, I);
+  else
+    gram_band<RK, false>(X, r0, r1, out, copy, I, I + rem);
 }
 
 // Factor tile: slice t.a of the t.b slices of fact_rows rows of the factor `src` (rows x RK).
@@ -437,8 +474,7 @@ __device__ void fact_tile(const KArgs& a, const Tile& t, const float* src, float
     const int sl = t.a & 0xffff, part = t.a >> 16;
     const int64_t r0 = static_cast<int64_t>(sl) * d.fact_rows;
     const int64_t r1 = r0 + d.fact_rows < rows ? r0 + d.fact_rows : rows;
-    gram_blocked<RK>(src, r0, r1, a.gpart + d.gpart + static_cast<int64_t>(sl) * RK * RK,
-                     part == 0 ? dst : nullptr, part);
+    gram_blocked<RK>(src, r0, r1, a.gpart + d.gpart + static_cast<int64_t>(sl) * RK * RK, dst, part);
   } else {
     const int64_t r0 = static_cast<int64_t>(t.a) * d.fact_rows;
     const int64_t r1 = r0 + d.fact_rows < rows ? r0 + d.fact_rows : rows;

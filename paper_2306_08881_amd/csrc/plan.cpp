@@ -719,7 +719,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         const double cols = std::min<double>(d.q_cb, m - double(t.b) * d.q_cb);
         return rows * cols * eb + (t.b == 0 ? rows * rr * 8.0 : 0.0);
       }
-      case K_WFACT: {  // from kBlockedRank on, the first part's tile reads and copies the rows
+      case K_WFACT: {  // from kBlockedRank on a slice's rows are read and copied once, counted on its first part
         const double rows = odd ? n : m;
         if (t.a >> 16) return 0.0;
         return std::min<double>(d.fact_rows, rows - double(t.a & 0xffff) * d.fact_rows) * rr * 8.0;

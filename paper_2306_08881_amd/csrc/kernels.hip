@@ -311,102 +311,103 @@ __global__ __launch_bounds__(kBlock) void k_chol(KArgs a) {
 }
 
 // Xh = X W from kBlockedRank on, for rows [t.a, t.a + rows) and the 64 columns c0 = 64 cb ... of
-// Xh (t.b = rows | cb << 16): passes of 128 rows; per pass W's rows come in chunks of 64 up to
-// the block's last column (W is upper triangular), each chunk's 64 x 64 block of W and the
-// pass's rows of X for those ranks staged in LDS (requested during the previous chunk's
-// products).  Thread t forms columns c0 + 8 (t % 8) ... + 7
-// of rows 4 (t / 8) ... + 3 of the pass, each entry a sum over the rank index in increasing order;
-// per rank it reads its four X values (X sits transposed in LDS) and its eight W values (column k
-// at k + 2 (k / 8)) as 16-byte words.
+// Xh (t.b = rows | cb << 16), on the fp64 matrix cores: wave w forms rows 64 w ... + 63 as 4 x 4
+// products of 16 x 16 (v_mfma_f64_16x16x4f64; operand entry [i][k] on lane i + 16 k, result
+// entry [4 v + l / 16][l % 16] in item v of lane l), over the ranks 0 ... c0 + 63 in steps of
+// 16.  W is upper triangular: later ranks add zero, and so do the ranks from c0 + 16 (b + 1) on
+// for the columns c0 + 16 b ... + 15, whose products are skipped.  Within a step, lane i + 16 k
+// holds the four ranks 4 k ... + 3 of its row as one 16-byte word, and product s of the step
+// takes rank 4 k + s from lane i + 16 k in both operands, so every rank enters once.  The next
+// step's rows of X are requested before the current step's products.
 template <int RK>
-__device__ void apply_split(const KArgs& a, const Tile& t, const MatDesc& d) {
-  constexpr int CB = 64, KC = 64, NJ = CB / 8, RG = kBlock / NJ, RP = 4 * RG;
-  constexpr int WL = CB + 2 * (CB / 8), XT = RP + 4;
-  constexpr int NW = KC * CB / kBlock, NX = RP * KC / kBlock;  // staged words per thread
-  __shared__ __align__(16) double ws[KC * WL];
-  __shared__ __align__(16) float xt[KC * XT];
-  const int rows = t.b & 0xffff, c0 = CB * (t.b >> 16);
-  const int jb = tid() % NJ, rg = tid() / NJ;
+__device__ void apply_mfma(const KArgs& a, const Tile& t, const MatDesc& d) {
+  const int rows = t.b & 0xffff, c0 = 64 * (t.b >> 16);
+  const int lane = tid() % kWave, i = lane % 16, k = lane / 16;
+  const int rb = 64 * (tid() / kWave);
+  if (rb >= rows) return;
   const bool q = a.variant == 1;
   const float* X = a.fac + (q ? d.q_slot : d.p_slot);
   float* Y = a.fac + (q ? d.qh_slot : d.ph_slot);
   const double* W = a.w + d.w_slot;
-  // steps (pass of RP rows, chunk of KC ranks); a step's W block and X rows are requested into
-  // registers during the previous step's products and stored to LDS at its start
-  const int nchunk = c0 / KC + 1, nstep = ((rows + RP - 1) / RP) * nchunk;
-  // thread t stages column t % 64 of rows t / 64 + 4 u of both blocks (W: rank rows, X: factor
-  // rows), so that every word it moves is a constant offset from one address
-  static_assert(CB == 64 && KC == 64 && kBlock == 256, "four rows of 64 per pass of the workgroup");
-  const int sr = tid() / 64, sc = tid() % 64;
-  double wv[NW];
-  float xv[NX];
-  auto fetch = [&](int st) {
-    const int base = (st / nchunk) * RP, k0 = (st % nchunk) * KC;
-    const double* wsrc = W + static_cast<int64_t>(k0 + sr) * RK + c0 + sc;
+  // rows past the tile read its last row (no branch around the loads); they are not stored
+  const float* xr[4];
 #pragma unroll
-    for (int u = 0; u < NW; ++u) wv[u] = wsrc[4 * u * RK];
-    const float* xsrc = X + (static_cast<int64_t>(t.a) + base + sr) * RK + k0 + sc;
-#pragma unroll
-    for (int u = 0; u < NX; ++u) xv[u] = base + sr + 4 * u < rows ? xsrc[4 * u * RK] : 0.f;
-  };
-  double* wdst = ws + sr * WL + sc + 2 * (sc / 8);
-  float* xdst = xt + sc * XT + sr;
-  fetch(0);
-  double y[4][8];
-  for (int st = 0; st < nstep; ++st) {
-    const int base = (st / nchunk) * RP, ch = st % nchunk, k0 = ch * KC;
-    if (ch == 0)
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int k = 0; k < 8; ++k) y[u][k] = 0.0;
-    __syncthreads();  // the previous step is done with ws and xt
-#pragma unroll
-    for (int u = 0; u < NW; ++u) wdst[4 * u * WL] = wv[u];
-#pragma unroll
-    for (int u = 0; u < NX; ++u) xdst[4 * u] = xv[u];
-    __syncthreads();
-    if (st + 1 < nstep) fetch(st + 1);
-    const int lend = min(KC, c0 + 8 * jb + 8 - k0);  // ranks past the block's last column add zero
-#pragma unroll 2
-    for (int l = 0; l < lend; ++l) {
-      const float4 x4 = *reinterpret_cast<const float4*>(&xt[l * XT + 4 * rg]);
-      const double2* w2 = reinterpret_cast<const double2*>(&ws[l * WL + 10 * jb]);
-      const double xl[4] = {x4.x, x4.y, x4.z, x4.w};
-      double wl[8];
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const double2 p = w2[k];
-        wl[2 * k] = p.x;
-        wl[2 * k + 1] = p.y;
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int k = 0; k < 8; ++k) y[u][k] = fma(xl[u], wl[k], y[u][k]);
-    }
-    if (ch == nchunk - 1)
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int r = base + 4 * rg + u;
-        if (r < rows) {
-          float4* Y4 = reinterpret_cast<float4*>(Y + (static_cast<int64_t>(t.a) + r) * RK + c0 + 8 * jb);
-          Y4[0] = make_float4(static_cast<float>(y[u][0]), static_cast<float>(y[u][1]),
-                              static_cast<float>(y[u][2]), static_cast<float>(y[u][3]));
-          Y4[1] = make_float4(static_cast<float>(y[u][4]), static_cast<float>(y[u][5]),
-                              static_cast<float>(y[u][6]), static_cast<float>(y[u][7]));
-        }
-      }
+  for (int ra = 0; ra < 4; ++ra) {
+    const int r = rb + 16 * ra + i;
+    xr[ra] = X + (static_cast<int64_t>(t.a) + (r < rows ? r : rows - 1)) * RK + 4 * k;
   }
+  const double* wr = W + static_cast<int64_t>(4 * k) * RK + c0 + i;
+  v4d acc[4][4];
+#pragma unroll
+  for (int ra = 0; ra < 4; ++ra)
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) acc[ra][cb] = v4d{0.0, 0.0, 0.0, 0.0};
+  // per step the W rows (from L2, where every tile of the matrix reads them) are requested
+  // first, then the next step's X rows (from HBM), so that the wait for the former leaves the
+  // latter in flight
+  typedef float4 XBuf[4];
+  auto fetch_x = [&](int k0, XBuf& b) {
+#pragma unroll
+    for (int ra = 0; ra < 4; ++ra) b[ra] = *reinterpret_cast<const float4*>(xr[ra] + k0);
+  };
+  auto step = [&](int k0, XBuf& b, int k1, XBuf& nb) {
+    // column group cb of the block takes ranks up to c0 + 16 cb + 15 only (W is upper triangular)
+    const int kz = k0 - c0;
+    double w[4][4];  // [s][cb]
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) w[s][cb] = wr[static_cast<int64_t>(k0 + s) * RK + 16 * cb];
+    __builtin_amdgcn_sched_barrier(0);  // in this order
+    fetch_x(k1, nb);
+    __builtin_amdgcn_sched_barrier(0);
+    // the conversions stay behind those requests
+#pragma unroll
+    for (int ra = 0; ra < 4; ++ra)
+      asm volatile("" : "+v"(b[ra].x), "+v"(b[ra].y), "+v"(b[ra].z), "+v"(b[ra].w));
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      double xa[4];
+#pragma unroll
+      for (int ra = 0; ra < 4; ++ra) {
+        const float4 v = b[ra];
+        xa[ra] = static_cast<double>(s == 0 ? v.x : s == 1 ? v.y : s == 2 ? v.z : v.w);
+      }
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb)
+        if (kz <= 16 * cb)
+#pragma unroll
+          for (int ra = 0; ra < 4; ++ra)
+            acc[ra][cb] = __builtin_amdgcn_mfma_f64_16x16x4f64(xa[ra], w[s][cb], acc[ra][cb], 0, 0, 0);
+    }
+  };
+  // c0 + 64 ranks: an even number of 16-rank steps, taken in pairs; past the last pair the X
+  // request repeats the last step's ranks, unused (no branch around it)
+  const int kend = c0 + 64;
+  XBuf x0, x1;
+  fetch_x(0, x0);
+  for (int k0 = 0; k0 < kend; k0 += 32) {
+    step(k0, x0, k0 + 16, x1);
+    step(k0 + 16, x1, min(k0 + 32, kend - 16), x0);
+  }
+#pragma unroll
+  for (int ra = 0; ra < 4; ++ra)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int r = rb + 16 * ra + 4 * v + k;
+      if (r < rows)
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb)
+          Y[(static_cast<int64_t>(t.a) + r) * RK + c0 + 16 * cb + i] = static_cast<float>(acc[ra][cb][v]);
+    }
 }
 
-// Xh = X W for rows [t.a, t.a + t.b) of the P (variant 0) or Q (variant 1) slot.
 template <int RK>
 __global__ __launch_bounds__(kBlock, RK >= kBlockedRank ? 2 : 1) void k_apply(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
   if constexpr (RK >= kBlockedRank) {
-    apply_split<RK>(a, t, d);
+    apply_mfma<RK>(a, t, d);
   } else {
     __shared__ double W[RK * RK];
     for (int e = tid(); e < RK * RK; e += kBlock) W[e] = a.w[d.w_slot + e];

@@ -169,44 +169,63 @@ __device__ void cholesky_w_blocked(double* G, double* w_out, int ldw = RK, const
   }
 }
 
-// C = A B for 128 x 128 fp64 blocks in global or shared memory, by the whole workgroup: thread t
-// forms the 8 x 8 block at rows 8 (t / 16), columns 8 (t % 16), each entry a sum over k < 128
-// in increasing order, with A[i][k] = A[i * ai + k * ak] and B[k][j] = B[k * bk + j];
-// store(i, j, value) takes the entries.
+// C = C0 + sg A B for 128 x 128 fp64 blocks in global or shared memory (sg = +1 or -1; C0 = 0
+// when c0 is null, else C0[i][j] = c0[i * ldc + j]), by the whole workgroup on the fp64 matrix
+// cores: wave w forms the 64 x 64 quadrant at rows 64 (w / 2), columns 64 (w % 2) as 4 x 4
+// products of 16 x 16 (v_mfma_f64_16x16x4f64; operand entry [i][k] on lane i + 16 k, result
+// entry [4 v + l / 16][l % 16] in item v of lane l), each entry C0 plus a sum over k < 128 in
+// increasing groups of four, with A[i][k] = A[i * ai + k * ak] and B[k][j] = B[k * bk + j];
+// store(i, j, value) takes the entries.  The next group's operands are requested before the
+// current group's products.
 template <typename Store>
-__device__ void mm128(const double* A, int ai, int ak, const double* B, int bk, Store store) {
-  static_assert(kBlock == 256, "16 x 16 threads of 8 x 8 entries");
-  const int i0 = 8 * (tid() / 16), j0 = 8 * (tid() % 16);
-  double c[8][8];
+__device__ void mm128(const double* A, int ai, int ak, const double* B, int bk, const double* c0, int ldc,
+                      double sg, Store store) {
+  static_assert(kBlock == 4 * kWave, "one 64 x 64 quadrant per wave");
+  const int lane = tid() % kWave, i = lane % 16, k = lane / 16;
+  const int i0 = 64 * (tid() / kWave / 2), j0 = 64 * (tid() / kWave % 2);
+  v4d acc[4][4];
 #pragma unroll
-  for (int u = 0; u < 8; ++u)
+  for (int ra = 0; ra < 4; ++ra)
 #pragma unroll
-    for (int v = 0; v < 8; ++v) c[u][v] = 0.0;
-  // the operands of steps k + 1 and k + 2 are requested before step k's products
-  double x[3][8], y[3][8];
-  auto load = [&](int k, double* xs, double* ys) {
+    for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
-    for (int u = 0; u < 8; ++u) xs[u] = A[(i0 + u) * ai + k * ak];
-#pragma unroll
-    for (int v = 0; v < 8; ++v) ys[v] = B[k * bk + j0 + v];
+      for (int v = 0; v < 4; ++v)
+        acc[ra][cb][v] = c0 ? c0[(i0 + 16 * ra + 4 * v + k) * ldc + j0 + 16 * cb + i] : 0.0;
+  struct Ops {
+    double a[4], b[4];
   };
-  load(0, x[0], y[0]);
-  load(1, x[1], y[1]);
-  for (int k = 0; k < 128; k += 3) {
+  auto fetch = [&](int k0, Ops& o) {
 #pragma unroll
-    for (int st = 0; st < 3; ++st) {
-      if (k + st >= 128) break;
-      if (k + st + 2 < 128) load(k + st + 2, x[(st + 2) % 3], y[(st + 2) % 3]);
+    for (int ra = 0; ra < 4; ++ra) o.a[ra] = A[(i0 + 16 * ra + i) * ai + (k0 + k) * ak];
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
+    for (int cb = 0; cb < 4; ++cb) o.b[cb] = B[(k0 + k) * bk + j0 + 16 * cb + i];
+  };
+  auto step = [&](const Ops& o) {
 #pragma unroll
-        for (int v = 0; v < 8; ++v) c[u][v] = fma(x[st][u], y[st][v], c[u][v]);
-    }
+    for (int ra = 0; ra < 4; ++ra)
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb)
+        acc[ra][cb] = __builtin_amdgcn_mfma_f64_16x16x4f64(sg * o.a[ra], o.b[cb], acc[ra][cb], 0, 0, 0);
+  };
+  // 32 groups of four, taken in pairs; past the last pair the request repeats the last group
+  Ops o0, o1;
+  fetch(0, o0);
+  for (int k0 = 0; k0 < 128; k0 += 8) {
+    fetch(k0 + 4, o1);
+    __builtin_amdgcn_sched_barrier(0);  // requests ahead of the products that do not need them
+    step(o0);
+    __builtin_amdgcn_sched_barrier(0);
+    fetch(k0 + 8 < 128 ? k0 + 8 : 124, o0);
+    __builtin_amdgcn_sched_barrier(0);
+    step(o1);
+    __builtin_amdgcn_sched_barrier(0);
   }
 #pragma unroll
-  for (int u = 0; u < 8; ++u)
+  for (int ra = 0; ra < 4; ++ra)
 #pragma unroll
-    for (int v = 0; v < 8; ++v) store(i0 + u, j0 + v, c[u][v]);
+    for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) store(i0 + 16 * ra + 4 * v + k, j0 + 16 * cb + i, acc[ra][cb][v]);
 }
 
 // W = R^-1 of a 256 x 256 Gram matrix G (global memory: the matrix's first Gram partial, which
@@ -224,15 +243,19 @@ __device__ void chol_split(double* G, double* W, double* S) {
   cholesky_w_blocked<H>(S, W, N);  // W11
   __syncthreads();
   double* Y = G + H * N;  // Y[i][j] at Y[i * N + j]
-  mm128(W, 1, N, G + H, N, [&](int i, int j, double v) { Y[i * N + j] = v; });  // W11^T G12
+  // Y = W11^T G12
+  mm128(W, 1, N, G + H, N, nullptr, 0, 1.0, [&](int i, int j, double v) { Y[i * N + j] = v; });
   __syncthreads();
-  mm128(Y, 1, N, Y, N, [&](int i, int j, double v) { S[i * H + j] = G[(H + i) * N + H + j] - v; });
+  // S = G22 - Y^T Y
+  mm128(Y, 1, N, Y, N, G + H * N + H, N, -1.0, [&](int i, int j, double v) { S[i * H + j] = v; });
   __syncthreads();
   cholesky_w_blocked<H>(S, W + H * N + H, N, G + H * N + H, N + 1);  // W22
   __syncthreads();
-  mm128(Y, N, 1, W + H * N + H, N, [&](int i, int j, double v) { S[i * H + j] = v; });  // Y W22
+  // S = Y W22
+  mm128(Y, N, 1, W + H * N + H, N, nullptr, 0, 1.0, [&](int i, int j, double v) { S[i * H + j] = v; });
   __syncthreads();
-  mm128(W, N, 1, S, H, [&](int i, int j, double v) { W[i * N + H + j] = -v; });  // -W11 (Y W22)
+  // W12 = -W11 (Y W22)
+  mm128(W, N, 1, S, H, nullptr, 0, -1.0, [&](int i, int j, double v) { W[i * N + H + j] = v; });
   for (int e = tid(); e < H * H; e += kBlock) W[(H + e / H) * N + e % H] = 0.0;
 }
 

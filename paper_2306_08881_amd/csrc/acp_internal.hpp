@@ -90,7 +90,7 @@ struct VecDesc {
 
 enum TileKind : int32_t { T_ROWS = 0, T_FACT = 1, T_VEC = 2, T_QTILE = 3, T_SROWS = 4, T_SMALL = 5 };
 
-// kind T_ROWS : idx = matrix, a = first row, b = row count (K_APPLY from kBlockedRank on: + 65536 x
+// kind T_ROWS : idx = matrix, a = first row, b = row count (K_APPLY from kApplyMfmaRank on: + 65536 x
 //               the 64-column block of Xh)
 // kind T_SMALL: idx = matrix, the whole matrix in one workgroup (rank 4, small matrices whose
 //               rows are not 16-byte aligned: n <= kSmallRows, m <= kSmallCols)
@@ -144,6 +144,9 @@ constexpr int32_t kBlockedRank = 128;  // ranks whose W K_CHOL forms from Gram p
 constexpr int32_t kSplitRank = 64;
 constexpr int32_t kSplitReconRank = 256;
 constexpr int32_t kCholBlockRank = 256;
+// ranks whose orthogonal factor X W is formed on the fp64 matrix cores (one 64-column block per
+// tile; below kBlockedRank a factor has one such block)
+constexpr int32_t kApplyMfmaRank = 64;
 // tiles that share one slice's Gram from kBlockedRank on: the (r / 64)(r / 64 + 1) / 2 blocks of
 // 64 x 64 on and above the diagonal, one per wave of a four-wave tile
 constexpr int32_t gram_parts(int32_t r) {

@@ -228,6 +228,26 @@ __device__ void mm128(const double* A, int ai, int ak, const double* B, int bk, 
       for (int v = 0; v < 4; ++v) store(i0 + 16 * ra + 4 * v + k, j0 + 16 * cb + i, acc[ra][cb][v]);
 }
 
+// Dst[e] = Src[(e / C) * lds + e % C] for e < R * C (R x C doubles from global memory into shared
+// memory), by the whole workgroup; each thread requests 16 entries before it stores them (one
+// request in flight at a time costs a memory latency per entry).
+template <int R, int C>
+__device__ void rows_to_lds(double* Dst, const double* Src, int lds) {
+  constexpr int PT = R * C / kBlock, U = 16;
+  static_assert(PT % U == 0, "whole batches");
+#pragma unroll 1
+  for (int c = 0; c < PT; c += U) {
+    double v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int e = tid() + (c + u) * kBlock;
+      v[u] = Src[(e / C) * lds + e % C];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) Dst[tid() + (c + u) * kBlock] = v[u];
+  }
+}
+
 // W = R^-1 of a 256 x 256 Gram matrix G (global memory: the matrix's first Gram partial, which
 // holds the slices' sum) in 2 x 2 blocks of 128, from the factorisation
 //   G11 = R11^T R11,  R12 = R11^-T G12,  G22 - R12^T R12 = R22^T R22,
@@ -238,7 +258,7 @@ __device__ void mm128(const double* A, int ai, int ak, const double* B, int bk, 
 // upper triangle makes redundant; the shared block S holds G11, then G22 - Y^T Y, then Y W22.
 __device__ void chol_split(double* G, double* W, double* S) {
   constexpr int N = 256, H = 128;
-  for (int e = tid(); e < H * H; e += kBlock) S[e] = G[(e / H) * N + e % H];
+  rows_to_lds<H, H>(S, G, N);
   __syncthreads();
   cholesky_w_blocked<H>(S, W, N);  // W11
   __syncthreads();
@@ -309,7 +329,7 @@ __global__ __launch_bounds__(kBlock) void k_chol(KArgs a) {
       static_assert(RK == 256, "2 x 2 blocks of 128");
       chol_split(gp, a.w + d.w_slot, Gs);
     } else {
-      for (int e = tid(); e < RK * RK; e += kBlock) Gs[e] = gp[e];
+      rows_to_lds<RK, RK>(Gs, gp, RK);
       __syncthreads();
       cholesky_w_blocked<RK>(Gs, a.w + d.w_slot);
     }
@@ -333,7 +353,7 @@ __global__ __launch_bounds__(kBlock) void k_chol(KArgs a) {
   }
 }
 
-// Xh = X W from kBlockedRank on, for rows [t.a, t.a + rows) and the 64 columns c0 = 64 cb ... of
+// Xh = X W from kApplyMfmaRank on, for rows [t.a, t.a + rows) and the 64 columns c0 = 64 cb ... of
 // Xh (t.b = rows | cb << 16), on the fp64 matrix cores: wave w forms rows 64 w ... + 63 as 4 x 4
 // products of 16 x 16 (v_mfma_f64_16x16x4f64; operand entry [i][k] on lane i + 16 k, result
 // entry [4 v + l / 16][l % 16] in item v of lane l), over the ranks 0 ... c0 + 63 in steps of
@@ -426,10 +446,10 @@ __device__ void apply_mfma(const KArgs& a, const Tile& t, const MatDesc& d) {
 }
 
 template <int RK>
-__global__ __launch_bounds__(kBlock, RK >= kBlockedRank ? 2 : 1) void k_apply(KArgs a) {
+__global__ __launch_bounds__(kBlock, RK >= kApplyMfmaRank ? 2 : 1) void k_apply(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
-  if constexpr (RK >= kBlockedRank) {
+  if constexpr (RK >= kApplyMfmaRank) {
     apply_mfma<RK>(a, t, d);
   } else {
     __shared__ double W[RK * RK];

@@ -177,6 +177,11 @@ __device__ void vec_tile(const KArgs& a, const Tile& t, bool compress) {
 // G_jj = 0 or its residual d_j = G_jj - sum_{i<j} R_ij^2 is at most tau^2 G_jj, i.e. when the
 // residual norm is at most tau times the column norm.
 
+typedef double v4d __attribute__((ext_vector_type(4)));
+template <int RK, bool DIAG>
+__device__ void gram_band(const float* X, int64_t r0, int64_t r1, float* copy, int I, int J, int nw, int w,
+                          v4d (&acc)[4][4]);
+
 // Gram of rows [r0, r1) of X (row-major, RK columns) into shared G (RK x RK), by the whole
 // workgroup, in a fixed order; the rows are also copied to `copy` when it is set.
 template <int RK>
@@ -229,6 +234,31 @@ __device__ void gram_rows(const float* X, int64_t r0, int64_t r1, double* G, flo
       const double s = ((red[0][e] + red[1][e]) + red[2][e]) + red[3][e];
       G[i * RK + j] = s;
       G[j * RK + i] = s;
+    }
+    __syncthreads();
+  } else if constexpr (RK == 64) {
+    // on the fp64 matrix cores (gram_band): the four waves take interleaved steps of 16 rows,
+    // each forming the products a <= b of the one band block; their sums are added into G in
+    // wave order, then the blocks a > b mirrored
+    const int w = tid() / kWave, lane = tid() % kWave, i = lane % 16, k = lane / 16;
+    v4d acc[4][4];
+    gram_band<RK, true>(X, r0, r1, copy, 0, 0, kBlock / kWave, w, acc);
+    for (int q = 0; q < kBlock / kWave; ++q) {
+      if (w == q)
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+          for (int b = a; b < 4; ++b)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              double& g = G[(16 * a + 4 * v + k) * RK + 16 * b + i];
+              g = q == 0 ? acc[a][b][v] : g + acc[a][b][v];
+            }
+      __syncthreads();
+    }
+    for (int e = tid(); e < RK * RK; e += kBlock) {
+      const int r = e / RK, c = e % RK;
+      if (r / 16 > c / 16) G[e] = G[c * RK + r];
     }
     __syncthreads();
   } else {
@@ -355,25 +385,21 @@ __device__ void cholesky_w(const double* G, double* w_out) {
   }
 }
 
-// Part `part` of the Gram of rows [r0, r1) of X (row-major, RK >= kBlockedRank columns) into
-// `out` (RK x RK doubles, global memory), on the fp64 matrix cores.  G is symmetric: of its
-// 64-column bands only the blocks G_IJ = X_I^T X_J with I <= J are formed, numbered row by row;
-// wave w of part p takes block 4 p + w.  A block is 4 x 4 products of 16 x 16
-// (v_mfma_f64_16x16x4f64, four rows of X each; operand entry [i][k] on lane i + 16 k, result
-// entry [4 v + l / 16][l % 16] in item v of lane l), product (a, b) for the columns 16 a ... and
-// 16 b ... of the two bands; a diagonal block skips its products a > b, whose entries lie below
-// the diagonal (K_GSUM mirrors the entries of the 4 x 4 blocks above it).  Each product adds the
-// rows in increasing groups of four; the next 16 rows are requested before the current ones'
-// products.  The diagonal blocks also copy their band of the rows to `copy` when set.
-typedef double v4d __attribute__((ext_vector_type(4)));
-
+// Band block X_I^T X_J of rows [r0, r1) of X (row-major, RK columns; 64-column bands I <= J)
+// into acc, on the fp64 matrix cores: 4 x 4 products of 16 x 16 (v_mfma_f64_16x16x4f64, four rows
+// of X each; operand entry [i][k] on lane i + 16 k, result entry [4 v + l / 16][l % 16] in item v
+// of lane l), product (a, b) for the columns 16 a ... and 16 b ... of the two bands; a diagonal
+// block (DIAG) skips its products a > b, whose entries lie below the diagonal.  The rows go in
+// steps of 16, of which the wave takes steps w, w + nw, ...; each product adds them in increasing
+// groups of four, and the wave's next step is requested before the current one's products.  A
+// diagonal block also copies its steps' rows of the band to `copy` when set.
 template <int RK, bool DIAG>
-__device__ void gram_band(const float* X, int64_t r0, int64_t r1, double* out, float* copy, int I, int J) {
+__device__ void gram_band(const float* X, int64_t r0, int64_t r1, float* copy, int I, int J, int nw, int w,
+                          v4d (&acc)[4][4]) {
   constexpr int G = 4;  // groups of four rows per step
   const int lane = tid() % kWave, i = lane % 16, k = lane / 16;
   const float* xa = X + 64 * I + i;
   const float* xb = X + 64 * J + i;
-  v4d acc[4][4];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
@@ -429,24 +455,22 @@ __device__ void gram_band(const float* X, int64_t r0, int64_t r1, double* out, f
           if (!DIAG || a <= b) acc[a][b] = __builtin_amdgcn_mfma_f64_16x16x4f64(xa4[a], xb4[b], acc[a][b], 0, 0, 0);
     }
   };
+  // steps of 4 G rows: this wave takes steps w, w + nw, ... of the slice
+  const int64_t sd = 4 * G * nw;
   Buf a0, b0, a1, b1;
-  fetch(r0, a0, b0);
-  for (int64_t g0 = r0; g0 < r1; g0 += 8 * G) {  // a second step past the slice adds zeros
-    fetch(g0 + 4 * G, a1, b1);
+  fetch(r0 + 4 * G * w, a0, b0);
+  for (int64_t g0 = r0 + 4 * G * w; g0 < r1; g0 += 2 * sd) {  // a second step past the slice adds zeros
+    fetch(g0 + sd, a1, b1);
     step(g0, a0, b0);
-    fetch(g0 + 8 * G, a0, b0);
-    step(g0 + 4 * G, a1, b1);
+    fetch(g0 + 2 * sd, a0, b0);
+    step(g0 + sd, a1, b1);
   }
-#pragma unroll
-  for (int a = 0; a < 4; ++a)
-#pragma unroll
-    for (int b = 0; b < 4; ++b)
-      if (!DIAG || a <= b)
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-          out[(64 * I + 16 * a + 4 * v + k) * RK + 64 * J + 16 * b + i] = acc[a][b][v];
 }
 
+// Part `part` of the Gram of rows [r0, r1) of X (RK >= kBlockedRank columns) into `out` (RK x RK
+// doubles, global memory): G is symmetric, so only its band blocks with I <= J are formed
+// (gram_band), numbered row by row; wave w of part p takes block 4 p + w over all the rows.
+// K_GSUM mirrors the entries of the 4 x 4 blocks above the diagonal.
 template <int RK>
 __device__ void gram_blocked(const float* X, int64_t r0, int64_t r1, double* out, float* copy, int part) {
   constexpr int NB = RK / 64, NP = NB * (NB + 1) / 2;
@@ -455,10 +479,19 @@ __device__ void gram_blocked(const float* X, int64_t r0, int64_t r1, double* out
   if (pr >= NP) return;
   int I = 0, rem = pr;
   while (rem >= NB - I) rem -= NB - I, ++I;
+  const int J = I + rem, lane = tid() % kWave, i = lane % 16, k = lane / 16;
+  v4d acc[4][4];
   if (rem == 0)
-    gram_band<RK, true>(X, r0, r1, out, copy, I, I);
+    gram_band<RK, true>(X, r0, r1, copy, I, I, 1, 0, acc);
   else
-    gram_band<RK, false>(X, r0, r1, out, copy, I, I + rem);
+    gram_band<RK, false>(X, r0, r1, copy, I, J, 1, 0, acc);
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+      if (rem != 0 || a <= b)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) out[(64 * I + 16 * a + 4 * v + k) * RK + 64 * J + 16 * b + i] = acc[a][b][v];
 }
 
 // Factor tile: slice t.a of the t.b slices of fact_rows rows of the factor `src` (rows x RK).

@@ -250,11 +250,11 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       // factor rows per Gram slice: at r <= 8 up to 8192 (one slice, and no K_CHOL, for
       // factors of at most 8192 rows); at r >= 16 at least 256 and at most 32 slices per factor
       // (K_CHOL adds a factor's slice partials in one workgroup); from kBlockedRank on at least
-      // 1024 and at most 16, since several tiles share a slice's Gram and every slice adds an
-      // r x r partial for K_GSUM to read (1024 measured faster than 256, 512, 2048 and 4096)
+      // 1024, since every slice adds an r x r partial for K_GSUM to read (1024 measured faster
+      // than 256, 512, 2048 and 4096), and again at most 32, so that no slice is much longer
       d.fact_rows = r <= 8 ? 8192
                     : r >= kBlockedRank
-                        ? static_cast<int32_t>(std::max<int64_t>(1024, align_up(cdiv(std::max(t.n, t.m), 16), 64)))
+                        ? static_cast<int32_t>(std::max<int64_t>(1024, align_up(cdiv(std::max(t.n, t.m), 32), 64)))
                         : static_cast<int32_t>(std::max<int64_t>(256, align_up(cdiv(std::max(t.n, t.m), 32), 64)));
       d.fact_slices_p = static_cast<int32_t>(cdiv(t.n, d.fact_rows));
       d.fact_slices_q = static_cast<int32_t>(cdiv(t.m, d.fact_rows));

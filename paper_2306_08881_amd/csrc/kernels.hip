@@ -124,14 +124,28 @@ __device__ void cholesky_w_blocked(double* G, double* w_out, int ldw = RK, const
       }
       __syncthreads();
     }
-    // (iii) the trailing upper triangle: G[i][j] -= sum_a R[k0 + a][i] R[k0 + a][j], i <= j
-    for (int e = tid(); e < nc * nc; e += kBlock) {
-      const int i = k0 + B + e / nc, j = k0 + B + e % nc;
-      if (i > j) continue;
-      double s[4] = {0.0, 0.0, 0.0, 0.0};
+    // (iii) the trailing upper triangle: G[i][j] -= sum_a R[k0 + a][i] R[k0 + a][j], i <= j, on
+    // the fp64 matrix cores in 16 x 16 tiles (tiles ti <= tj, tile t on wave t % 4; one
+    // v_mfma_f64_16x16x4f64 per four rows a); entries below the diagonal of a diagonal tile are
+    // not written (that triangle keeps W)
+    {
+      const int nt = nc / 16, w = tid() / kWave, li = lane % 16, lk = lane / 16, c0 = k0 + B;
+      int t = 0;
+      for (int ti = 0; ti < nt; ++ti)
+        for (int tj = ti; tj < nt; ++tj, ++t) {
+          if (t % (kBlock / kWave) != w) continue;
+          v4d acc = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-      for (int a = 0; a < B; ++a) s[a & 3] += G[(k0 + a) * RK + i] * G[(k0 + a) * RK + j];
-      G[i * RK + j] -= (s[0] + s[1]) + (s[2] + s[3]);
+          for (int s4 = 0; s4 < B / 4; ++s4) {
+            const double* r = G + (k0 + 4 * s4 + lk) * RK + c0 + li;
+            acc = __builtin_amdgcn_mfma_f64_16x16x4f64(r[16 * ti], r[16 * tj], acc, 0, 0, 0);
+          }
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int i = c0 + 16 * ti + 4 * v + lk, j = c0 + 16 * tj + li;
+            if (i <= j) G[i * RK + j] -= acc[v];
+          }
+        }
     }
     __syncthreads();
   }

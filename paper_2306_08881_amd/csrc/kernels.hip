@@ -33,8 +33,8 @@ __global__ __launch_bounds__(kBlock) void k_fact(KArgs a) {
 // the upper triangle is read) for ranks from kBlockedRank on, by the whole workgroup, in blocks
 // of 32.  For each diagonal block K in order:
 //   (i)   one wave factors the block (lane j keeps column j in registers; at pivot p every lane
-//         takes the drop test, forms R[p][j] and updates its column with R[p][i] read from lane
-//         i) and forms W_KK = R_KK^-1 by columns (lane j solves R_KK w = e_j from the bottom up);
+//         takes the drop test, forms R[p][j] and updates its column with row p of R, which the
+//         lanes pass through LDS) and forms W_KK = R_KK^-1 by rows (lane j, row j);
 //   (ii)  the block row right of it: R_KJ = W_KK^T G_KJ (with dropped pivots W_KK's zero columns
 //         give R's zero rows, as forward substitution over the kept pivots would);
 //   (iii) the trailing upper triangle: G_IJ -= R_KI^T R_KJ.
@@ -50,7 +50,7 @@ __device__ void cholesky_w_blocked(double* G, double* w_out, int ldw = RK, const
                                    int gstride = 0) {
   static_assert(RK == 128 && kBlock == 256, "4 x 4 blocks of 32 on 256 threads");
   constexpr int B = 32, NBK = RK / B;
-  __shared__ double g0[RK], wdiag[RK];
+  __shared__ double g0[RK], wdiag[RK], rowb[B];
   __shared__ double T[(RK - B) * B];  // one block column's W[0:k0][.] R[.][block] products
   auto wl = [&](int i, int c) -> double& { return G[(RK - 1 - i) * RK + (RK - 1 - c)]; };  // W[i][c], i < c
   for (int i = tid(); i < RK; i += kBlock) g0[i] = gref ? gref[i * gstride] : G[i * RK + i];
@@ -64,19 +64,24 @@ __device__ void cholesky_w_blocked(double* G, double* w_out, int ldw = RK, const
       double g[B];
 #pragma unroll
       for (int a = 0; a < B; ++a) g[a] = a <= j ? G[(k0 + a) * RK + k0 + j] : 0.0;
+      const double refl = g0[k0 + j];  // pivot j's reference diagonal, read by lane
 #pragma unroll
       for (int p = 0; p < B; ++p) {
         asm volatile("" ::: "memory");  // one pivot at a time
         const double dk = readlane_d(g[p], p);
-        const double ref = g0[k0 + p];
+        const double ref = readlane_d(refl, p);
         const bool keep = ref > 0.0 && dk > kTau * kTau * ref;
         const double rkk = keep ? sqrt(dk) : 0.0, rinv = keep ? 1.0 / rkk : 0.0;
         const double rpj = j > p ? g[p] * rinv : (j == p ? rkk : 0.0);
         g[p] = rpj;  // row p of R
         if (j == 0) wdiag[k0 + p] = rinv;  // W's diagonal: 1 / R[p][p], zero when dropped
-        if (keep)
+        if (keep) {
+          // row p goes to every lane through LDS (one wave: its LDS accesses keep their order)
+          rowb[j] = rpj;
+          asm volatile("" ::: "memory");
 #pragma unroll
-          for (int a = p + 1; a < B; ++a) g[a] -= readlane_d(rpj, a) * rpj;
+          for (int a = p + 1; a < B; ++a) g[a] -= rowb[a] * rpj;
+        }
       }
 #pragma unroll
       for (int a = 0; a < B; ++a)
@@ -149,33 +154,37 @@ __device__ void cholesky_w_blocked(double* G, double* w_out, int ldw = RK, const
     }
     __syncthreads();
   }
-  // block columns of W: T = W[0:k0][0:k0] R[0:k0][block], then W[0:k0][block] = -T W_JJ
-  for (int J = 1; J < NBK; ++J) {
-    const int k0 = J * B;
-    for (int e = tid(); e < k0 * B; e += kBlock) {
-      const int i = e / B, c = e % B;
-      double s[4] = {0.0, 0.0, 0.0, 0.0};
-      int l = i;
-      s[0] = wdiag[i] * G[i * RK + k0 + c];
-      for (++l; l + 4 <= k0; l += 4)
+  // block columns of W: T = W[0:k0][0:k0] R[0:k0][block], then W[0:k0][block] = -T W_JJ, both
+  // on the fp64 matrix cores in 16 x 16 tiles (tile t of the k0 / 16 x 2 on wave t % 4; one
+  // v_mfma_f64_16x16x4f64 per four ranks, the operands of W taken from its triangle: zero below
+  // the diagonal, wdiag on it)
+  {
+    const int w = tid() / kWave, li = lane % 16, lk = lane / 16;
+    auto wv = [&](int r, int c) { return c > r ? wl(r, c) : (c == r ? wdiag[r] : 0.0); };  // W[r][c]
+    for (int J = 1; J < NBK; ++J) {
+      const int k0 = J * B, nt = 2 * (k0 / 16);
+      for (int t = w; t < nt; t += kBlock / kWave) {
+        const int i0 = 16 * (t / 2), c0 = 16 * (t % 2);
+        v4d acc = {0.0, 0.0, 0.0, 0.0};
+        for (int l0 = i0; l0 < k0; l0 += 4)  // W[i][l] is zero for l < i
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(wv(i0 + li, l0 + lk), G[(l0 + lk) * RK + k0 + c0 + li],
+                                                     acc, 0, 0, 0);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) s[u] += wl(i, l + u) * G[(l + u) * RK + k0 + c];
-      for (; l < k0; ++l) s[0] += wl(i, l) * G[l * RK + k0 + c];
-      T[e] = (s[0] + s[1]) + (s[2] + s[3]);
-    }
-    __syncthreads();
-    for (int e = tid(); e < k0 * B; e += kBlock) {
-      const int i = e / B, jj = e % B;
-      double s[4] = {0.0, 0.0, 0.0, 0.0};
-      int c = 0;
-      for (; c + 4 <= jj; c += 4)
+        for (int v = 0; v < 4; ++v) T[(i0 + 4 * v + lk) * B + c0 + li] = acc[v];
+      }
+      __syncthreads();
+      for (int t = w; t < nt; t += kBlock / kWave) {
+        const int i0 = 16 * (t / 2), c0 = 16 * (t % 2);
+        v4d acc = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-        for (int u = 0; u < 4; ++u) s[u] += T[i * B + c + u] * wl(k0 + c + u, k0 + jj);
-      for (; c < jj; ++c) s[0] += T[i * B + c] * wl(k0 + c, k0 + jj);
-      s[1] += T[i * B + jj] * wdiag[k0 + jj];
-      wl(i, k0 + jj) = -((s[0] + s[1]) + (s[2] + s[3]));
+        for (int q0 = 0; q0 < B; q0 += 4)
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(T[(i0 + li) * B + q0 + lk], wv(k0 + q0 + lk, k0 + c0 + li),
+                                                     acc, 0, 0, 0);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) wl(i0 + 4 * v + lk, k0 + c0 + li) = -acc[v];
+      }
+      __syncthreads();
     }
-    __syncthreads();
   }
   for (int e = tid(); e < RK * RK; e += kBlock) {
     const int i = e / RK, c = e % RK;

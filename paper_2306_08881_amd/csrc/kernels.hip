@@ -46,8 +46,8 @@ __global__ __launch_bounds__(kBlock) void k_fact(KArgs a) {
 // larger Gram matrix is tested against that matrix's diagonal); W goes to w_out with rows ldw
 // apart.
 template <int RK>
-__device__ void cholesky_w_blocked(double* G, double* w_out, int ldw = RK, const double* gref = nullptr,
-                                   int gstride = 0) {
+__device__ __attribute__((always_inline)) void cholesky_w_blocked(double* G, double* w_out, int ldw = RK,
+                                                                const double* gref = nullptr, int gstride = 0) {
   static_assert(RK == 128 && kBlock == 256, "4 x 4 blocks of 32 on 256 threads");
   constexpr int B = 32, NBK = RK / B;
   __shared__ double g0[RK], wdiag[RK], rowb[B];

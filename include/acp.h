@@ -154,6 +154,22 @@ acp_status acp_compress(acp_ctx *ctx, int64_t step, int32_t b, const float *grad
                         void *stream);
 
 /*
+ * acp_compress_noalloc - acp_compress for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).  Same checks, same
+ * kernels, bitwise the same results and state changes as acp_compress, except that the bucket's
+ * Q-step partial sums (the per-row-chunk products that a second kernel adds) go to a static
+ * device array of the library instead of the state block: 32 MiB, one copy per GPU, held until
+ * the process ends, its address looked up once per device in acp_bind_state.  Nothing is
+ * allocated by this call.  A bucket whose partials need more than 32 MiB returns
+ * ACP_E_UNSUPPORTED (acp_compress takes it); ACP_E_DEVICE if the array's address could not be
+ * looked up.  Every call on one GPU shares that GPU's array and the partials of one call are
+ * dead once it is done, so nothing is cleared between calls; calls that overlap on one GPU (on
+ * other streams, contexts or threads) race on the array and must be ordered by the caller.
+ */
+acp_status acp_compress_noalloc(acp_ctx *ctx, int64_t step, int32_t b, const float *grad,
+                                float *factor_buf, void *stream);
+
+/*
  * acp_decompress - finish step `step` of bucket b: from the aggregated (summed) factor buffer
  * `agg_factor` (device), write M_hat = P_t Q_t^T / p for every compressed tensor and raw/p for
  * every vector into `out` (device, grad_elems(b) floats; may alias the gradient bucket but not

@@ -48,6 +48,7 @@ SIGNATURES = {
     "acp_fusion_groups": (_i32, [_p, _i32, _pi32, _pi32]),
     "acp_init_factor": (_i32, [_p, _i32, _i32, _pf, _i64]),
     "acp_compress": (_i32, [_p, _i64, _i32, _pf, _pf, _p]),
+    "acp_compress_noalloc": (_i32, [_p, _i64, _i32, _pf, _pf, _p]),
     "acp_decompress": (_i32, [_p, _i64, _i32, _pf, _pf, _p]),
     "acp_compress_all": (_i32, [_p, _i64, _p, _p, _p]),
     "acp_decompress_all": (_i32, [_p, _i64, _p, _p, _p]),

@@ -123,6 +123,11 @@ class Acp:
         _check(self.lib.acp_compress(self.ctx, step, b, _fptr(grad), _fptr(factor_buf), _stream_ptr(stream)),
                self.lib, self.ctx, "acp_compress")
 
+    def compress_noalloc(self, step: int, b: int, grad, factor_buf, stream=None):
+        _check(self.lib.acp_compress_noalloc(self.ctx, step, b, _fptr(grad), _fptr(factor_buf),
+                                             _stream_ptr(stream)),
+               self.lib, self.ctx, "acp_compress_noalloc")
+
     def decompress(self, step: int, b: int, agg_factor, out, stream=None):
         _check(self.lib.acp_decompress(self.ctx, step, b, _fptr(agg_factor), _fptr(out), _stream_ptr(stream)),
                self.lib, self.ctx, "acp_decompress")

@@ -37,6 +37,9 @@ constexpr int kSmallRows = 256;  // T_SMALL matrices: rows (their P rows sit in 
 constexpr int kSmallCols = 512;  // T_SMALL matrices: columns (their Q rows sit in LDS)
 constexpr int kReconRows = 4;   // rows per tile of the rank-4 decompress
 constexpr int kQRows = 256;       // rows per Q-step row chunk (at most; the chunk's Ph rows sit in LDS)
+// Size of the static device array that holds one bucket's Q-step partials for the compress entry
+// point that allocates nothing (acp_compress_noalloc); a bucket that needs more is refused.
+constexpr int64_t kScratchBytes = int64_t(32) << 20;
 
 struct MatDesc {
   int64_t grad_off;   // offset of the matrix in its gradient bucket (floats)

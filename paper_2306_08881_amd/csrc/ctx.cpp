@@ -11,6 +11,8 @@
 
 namespace acp {
 hipError_t launch(const Launch& l, int32_t rank, const KArgs& args, hipStream_t s);
+// address of the static Q-step scratch on `device`, which must be the current device
+hipError_t scratch_address(int device, float** out);
 }
 
 struct acp_ctx {
@@ -24,6 +26,8 @@ struct acp_ctx {
   uint8_t* dev = nullptr;       // bound state block
   int64_t dev_bytes = 0;
   int device = -1;
+  float* scratch = nullptr;     // the bound device's static Q-step scratch (acp_compress_noalloc)
+  std::string scratch_err;      // why it is null after a bind
   std::vector<int64_t> last_step;   // per bucket: last completed step
   std::vector<int64_t> pending;     // per bucket: compressed step awaiting decompress (0 = none)
   std::vector<uint8_t> deferred;    // per bucket: E form of the arena (kExplicit, kHoldsF, kHoldsX)
@@ -124,6 +128,45 @@ struct CkptHeader {
   int64_t e_floats, fac_floats, w_doubles;
 };
 
+// acp_compress and acp_compress_noalloc: checks, then the bucket's compress launches.  `qpart`,
+// when not null, replaces the state block's Q-step partial region as the kernels' base.
+acp_status compress_bucket(acp_ctx* c, int64_t step, int32_t b, const float* grad, float* factor_buf,
+                           void* stream, float* qpart) {
+  if (!c) return ACP_E_INVALID;
+  if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
+  if (b < 0 || b >= static_cast<int32_t>(c->plan.buckets.size()))
+    return fail(c, ACP_E_INVALID, "bucket index out of range");
+  if (!grad || !factor_buf) return fail(c, ACP_E_INVALID, "null buffer");
+  if (!aligned16(grad) || !aligned16(factor_buf)) return fail(c, ACP_E_INVALID, "buffers must be 16-byte aligned");
+  if (c->pending[b] != 0)
+    return fail(c, ACP_E_STEP, "compress called twice without decompress");
+  if (step != c->last_step[b] + 1)
+    return fail(c, ACP_E_STEP, "step " + std::to_string(step) + " out of order (expected " +
+                                   std::to_string(c->last_step[b] + 1) + ")");
+  const acp::BucketPlan& bk = c->plan.buckets[b];
+  {
+    const char* g0 = reinterpret_cast<const char*>(grad);
+    const char* f0 = reinterpret_cast<const char*>(factor_buf);
+    const int64_t fe = (step & 1) ? bk.fac_elems_p : bk.fac_elems_q;
+    if (g0 < f0 + fe * 4 && f0 < g0 + bk.grad_elems * 4)
+      return fail(c, ACP_E_INVALID, "factor_buf overlaps grad");
+  }
+  const acp_status ds = check_device(c);
+  if (ds != ACP_OK) return ds;
+  acp::KArgs a = base_args(c);
+  if (qpart) a.qpart = qpart;
+  a.base = b;
+  a.src[0] = grad;
+  a.dst[0] = factor_buf;
+  a.parity = static_cast<int32_t>(step & 1);
+  set_form(a, 0, c->deferred[b]);
+  const acp_status st = run(c, bk.compress[step & 1], a, static_cast<hipStream_t>(stream));
+  if (st != ACP_OK) return st;
+  c->pending[b] = step;
+  c->deferred[b] = form_after_compress(c, step);
+  return ACP_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -211,6 +254,14 @@ acp_status acp_bind_state(acp_ctx* c, void* device_ptr, int64_t bytes, void* str
   std::fill(c->last_step.begin(), c->last_step.end(), 0);
   std::fill(c->pending.begin(), c->pending.end(), 0);
   std::fill(c->deferred.begin(), c->deferred.end(), 0);
+  // the static scratch of acp_compress_noalloc: looked up once per device, with it current
+  c->scratch = nullptr;
+  c->scratch_err.clear();
+  e = acp::scratch_address(dev, &c->scratch);
+  if (e != hipSuccess) {
+    c->scratch = nullptr;
+    c->scratch_err = std::string("hipGetSymbolAddress of the static scratch failed: ") + hipGetErrorString(e);
+  }
   c->err.clear();
   return ACP_OK;
 }
@@ -309,38 +360,27 @@ acp_status acp_init_factor(const acp_ctx* c, int32_t tensor_id, int32_t which, f
 
 acp_status acp_compress(acp_ctx* c, int64_t step, int32_t b, const float* grad, float* factor_buf,
                         void* stream) {
+  return compress_bucket(c, step, b, grad, factor_buf, stream, nullptr);
+}
+
+acp_status acp_compress_noalloc(acp_ctx* c, int64_t step, int32_t b, const float* grad, float* factor_buf,
+                                void* stream) {
   if (!c) return ACP_E_INVALID;
-  if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
   if (b < 0 || b >= static_cast<int32_t>(c->plan.buckets.size()))
     return fail(c, ACP_E_INVALID, "bucket index out of range");
-  if (!grad || !factor_buf) return fail(c, ACP_E_INVALID, "null buffer");
-  if (!aligned16(grad) || !aligned16(factor_buf)) return fail(c, ACP_E_INVALID, "buffers must be 16-byte aligned");
-  if (c->pending[b] != 0)
-    return fail(c, ACP_E_STEP, "compress called twice without decompress");
-  if (step != c->last_step[b] + 1)
-    return fail(c, ACP_E_STEP, "step " + std::to_string(step) + " out of order (expected " +
-                                   std::to_string(c->last_step[b] + 1) + ")");
   const acp::BucketPlan& bk = c->plan.buckets[b];
-  {
-    const char* g0 = reinterpret_cast<const char*>(grad);
-    const char* f0 = reinterpret_cast<const char*>(factor_buf);
-    const int64_t fe = (step & 1) ? bk.fac_elems_p : bk.fac_elems_q;
-    if (g0 < f0 + fe * 4 && f0 < g0 + bk.grad_elems * 4)
-      return fail(c, ACP_E_INVALID, "factor_buf overlaps grad");
-  }
-  const acp_status ds = check_device(c);
-  if (ds != ACP_OK) return ds;
-  acp::KArgs a = base_args(c);
-  a.base = b;
-  a.src[0] = grad;
-  a.dst[0] = factor_buf;
-  a.parity = static_cast<int32_t>(step & 1);
-  set_form(a, 0, c->deferred[b]);
-  const acp_status st = run(c, bk.compress[step & 1], a, static_cast<hipStream_t>(stream));
-  if (st != ACP_OK) return st;
-  c->pending[b] = step;
-  c->deferred[b] = form_after_compress(c, step);
-  return ACP_OK;
+  if (bk.qpart_floats * 4 > acp::kScratchBytes)
+    return fail(c, ACP_E_UNSUPPORTED, "bucket " + std::to_string(b) + " needs " +
+                                          std::to_string(bk.qpart_floats * 4) +
+                                          " bytes of Q-step scratch; the static scratch holds " +
+                                          std::to_string(acp::kScratchBytes));
+  if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
+  if (!c->scratch) return fail(c, ACP_E_DEVICE, c->scratch_err);
+  // the kernels address partial k of a matrix as qpart + MatDesc::qpart + k; the bucket's
+  // partials start at qpart_base, so this base puts them at the start of the scratch
+  float* base = reinterpret_cast<float*>(reinterpret_cast<uintptr_t>(c->scratch) -
+                                         static_cast<uintptr_t>(bk.qpart_base) * sizeof(float));
+  return compress_bucket(c, step, b, grad, factor_buf, stream, base);
 }
 
 acp_status acp_decompress(acp_ctx* c, int64_t step, int32_t b, const float* agg_factor, float* out,

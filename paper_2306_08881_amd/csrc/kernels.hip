@@ -15,6 +15,9 @@
 // P_hat Q_loc^T while it streams F, so each step reads M and E once and writes E once.
 #include "device.hpp"
 
+#include <mutex>
+#include <vector>
+
 namespace acp {
 
 hipError_t launch_wide(const Launch& l, int32_t rank, const KArgs& args, hipStream_t s);
@@ -1638,6 +1641,28 @@ hipError_t launch(const Launch& l, int32_t rank, const KArgs& args, hipStream_t 
     case 256: return launch_rank<256>(l, args, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+// Q-step partials of acp_compress_noalloc: a file-scope device array, one copy on every GPU the
+// library runs on, kept until the process ends.  In host code its name is only a symbol, not a
+// device address: scratch_address() looks up the current device's copy once with
+// hipGetSymbolAddress and keeps that address per device; every launch takes the address.
+static __device__ __align__(256) float scratch[kScratchBytes / 4];
+
+hipError_t scratch_address(int device, float** out) {
+  static std::mutex mu;
+  static std::vector<float*> addr;  // per device; null until looked up
+  std::lock_guard<std::mutex> lock(mu);
+  if (device < 0) return hipErrorInvalidDevice;
+  if (addr.size() <= static_cast<size_t>(device)) addr.resize(static_cast<size_t>(device) + 1, nullptr);
+  if (!addr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[device] = static_cast<float*>(p);
+  }
+  *out = addr[device];
+  return hipSuccess;
 }
 
 }  // namespace acp

@@ -245,7 +245,9 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       d.q_chunks = static_cast<int32_t>(cdiv(t.n, d.q_rows));
       const int64_t ncb = cdiv(t.m, d.q_cb);
       d.qpart = qpart;
+      if (bk.mats.empty()) bk.qpart_base = qpart;
       qpart += align_up(int64_t(d.q_chunks) * ncb * d.q_cb * r, kSlotAlign);
+      bk.qpart_floats = qpart - bk.qpart_base;
       d.bucket = b;
       // factor rows per Gram slice: at r <= 8 up to 8192 (one slice, and no K_CHOL, for
       // factors of at most 8192 rows); at r >= 16 at least 256 and at most 32 slices per factor

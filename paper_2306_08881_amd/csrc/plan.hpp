@@ -27,6 +27,8 @@ struct BucketPlan {
   std::vector<int64_t> grad_off, fac_off_p, fac_off_q;
   int64_t grad_elems = 0, fac_elems_p = 0, fac_elems_q = 0;
   int64_t e_base = 0;                 // E arena offset of the bucket (floats)
+  int64_t qpart_base = 0;             // first Q-step partial of the bucket's matrices (floats)
+  int64_t qpart_floats = 0;           // Q-step partials of the bucket's matrices (floats)
   std::vector<int32_t> mats, vecs;    // members by kind
   std::vector<Launch> compress[2];    // [0] even step (Q-step), [1] odd step (P-step)
   std::vector<Launch> decompress[2];

@@ -267,3 +267,23 @@ def test_fusion_groups_errors(lib):
         assert lib.acp_fusion_groups(ctx, L.ACP_FACTOR_P, None, C.byref(ng)) == 0 and ng.value == 1
     finally:
         lib.acp_destroy(ctx)
+
+
+def test_noalloc_refuses_buckets_past_the_static_scratch(lib):
+    """acp_compress_noalloc refuses, before touching anything, a bucket whose Q-step partial sums
+    exceed its 32 MiB static array (69632 x 1024 at rank 256: 34 row chunks of 2048 rows x 1024
+    columns x 256 floats = 34 MiB), and an unbound context otherwise."""
+    st, ctx = _ctx(lib, [(69632, 1024)], 256)
+    assert st == L.ACP_OK
+    try:
+        assert lib.acp_compress_noalloc(ctx, 1, 0, 256, 256, None) == L.ACP_E_UNSUPPORTED
+        assert b"static scratch" in lib.acp_last_error(ctx)
+        assert lib.acp_compress_noalloc(ctx, 1, 1, 256, 256, None) == L.ACP_E_INVALID
+    finally:
+        lib.acp_destroy(ctx)
+    st, ctx = _ctx(lib, [(2048, 1024)], 256)
+    assert st == L.ACP_OK
+    try:
+        assert lib.acp_compress_noalloc(ctx, 1, 0, 256, 256, None) == L.ACP_E_STATE
+    finally:
+        lib.acp_destroy(ctx)

@@ -22,7 +22,8 @@ Readings taken where the paper is silent (each listed in the design notes):
 * E_0 = 0 and P0, Q0 come from ``oracle.rng``.
 * without error feedback (ablation, Section V-B) M' = M and no E is kept;
   without reuse the reused factor is replaced by a fresh standard normal draw
-  every step (numpy Philox keyed by seed, tensor, step and factor).
+  every step: the initial factors' counter-based generator keyed by the step
+  as well (``rng.fresh_factor``), so that the device can draw the same values.
 """
 
 from __future__ import annotations
@@ -69,6 +70,27 @@ def decompress_matrix(t: int, agg: np.ndarray, ortho: np.ndarray, world_size: in
     else:
         P, Q = ortho, agg
     return (P @ Q.T) / world_size, P, Q
+
+
+def powersgd_p(M: np.ndarray, E: Optional[np.ndarray], Q_prev: np.ndarray):
+    """First half of a Power-SGD step (Algorithm 1, left) for one matrix, with error feedback.
+
+    M' = M_t + E_{t-1} (M_t without error feedback) and the local P_t = M' Q_{t-1}, which the
+    workers all-reduce before the second half.  Returns (P_t, M').
+    """
+    Mp = np.asarray(M, dtype=np.float64)
+    if E is not None:
+        Mp = Mp + E
+    return Mp @ Q_prev, Mp
+
+
+def powersgd_q(Mp: np.ndarray, P_agg: np.ndarray, ef: bool):
+    """Second half: P_t = orth(all-reduced P_t); the local Q_t = M'^T P_t, all-reduced next;
+    with error feedback E_t = M' - P_t Q_t^T with the local Q_t (before the all-reduce, where
+    Algorithm 2 updates E).  Returns (Q_t, P_t, E_t or None)."""
+    p = gram_schmidt(P_agg)
+    q = Mp.T @ p
+    return q, p, (Mp - p @ q.T if ef else None)
 
 
 def powersgd_matrix(Ms: Sequence[np.ndarray], Q_prev: np.ndarray):
@@ -125,9 +147,7 @@ class AcpOracle:
             self.state[tid] = st
 
     def _fresh(self, tid: int, t: int, which: str, rows: int) -> np.ndarray:
-        f = 0 if which == "P" else 1
-        g = np.random.Generator(np.random.Philox(np.random.SeedSequence([self.seed, tid, t, f])))
-        return g.standard_normal((rows, self.rank))
+        return rng.fresh_factor(self.seed, tid, which, rows, self.rank, t).astype(np.float64)
 
     def compress_tensor(self, t: int, tid: int, grad: np.ndarray) -> np.ndarray:
         """Local message of one tensor at step t, flattened (a factor or the raw vector)."""
@@ -204,3 +224,88 @@ class LoopbackOracle:
         emits = [w.compress_tensor(t, tid, g) for w, g in zip(self.workers, grads)]
         agg = sum(emits)
         return [w.decompress_tensor(t, tid, agg) for w in self.workers], agg
+
+
+@dataclass
+class PsgdTensorState:
+    plan: L.TensorPlan
+    Q: Optional[np.ndarray] = None       # Q_{t-1}: the all-reduced Q of the last step (Q0 first)
+    E: Optional[np.ndarray] = None
+    Mp: Optional[np.ndarray] = None      # M' between the two halves of a step
+    P: Optional[np.ndarray] = None       # orthonormal P_t of the last second half
+    step: int = 0
+    phase: int = 0                       # 0: idle, 1: P sent, 2: Q sent
+    emit_p: Optional[np.ndarray] = None
+    emit_q: Optional[np.ndarray] = None
+
+
+class PowerSgdOracle:
+    """Power-SGD with error feedback (Algorithm 1, left) over a model's tensors, one worker.
+
+    Per step t and compressed tensor, in three calls with an all-reduce after each of the first
+    two: ``compress_p_tensor`` (M' = M + E, local P = M' Q_{t-1}), ``compress_q_tensor`` (P =
+    orth(all-reduced P), local Q = M'^T P, E = M' - P Q^T), ``decompress_tensor`` (M_hat = P
+    Q_agg^T / p; Q_agg is reused at t + 1).  Q_0 is the same draw as ACP-SGD's (``rng``).
+    Vectors are sent raw in both halves; the returned vector is the second all-reduce / p.
+    """
+
+    def __init__(self, shapes: Sequence[Sequence[int]], rank: int, seed: int = 0,
+                 cap_bytes: int = L.DEFAULT_CAP_BYTES, world_size: int = 1, ef: bool = True,
+                 tensor_ids: Optional[Sequence[int]] = None):
+        self.layout = L.plan(shapes, rank, cap_bytes)
+        self.rank, self.seed, self.world_size, self.ef = rank, seed, world_size, ef
+        ids = range(len(shapes)) if tensor_ids is None else tensor_ids
+        self.state: Dict[int, PsgdTensorState] = {}
+        for tid in ids:
+            pl = self.layout.tensors[tid]
+            st = PsgdTensorState(pl)
+            if pl.compressed:
+                st.Q = rng.init_factor(seed, tid, "Q", pl.m, rank).astype(np.float64)
+                if ef:
+                    st.E = np.zeros((pl.n, pl.m), dtype=np.float64)
+            self.state[tid] = st
+
+    def compress_p_tensor(self, t: int, tid: int, grad: np.ndarray) -> np.ndarray:
+        st = self.state[tid]
+        if t != st.step + 1 or st.phase != 0:
+            raise ValueError(f"tensor {tid}: first half of step {t} out of order")
+        g = np.asarray(grad, dtype=np.float64)
+        if st.plan.compressed:
+            p, st.Mp = powersgd_p(g.reshape(st.plan.n, st.plan.m), st.E, st.Q)
+            st.emit_p = p.reshape(-1).copy()
+        else:
+            st.Mp = g.reshape(-1).copy()
+            st.emit_p = st.Mp.copy()
+        st.phase = 1
+        return st.emit_p
+
+    def compress_q_tensor(self, t: int, tid: int, p_agg: np.ndarray) -> np.ndarray:
+        st = self.state[tid]
+        if t != st.step + 1 or st.phase != 1:
+            raise ValueError(f"tensor {tid}: second half of step {t} out of order")
+        if st.plan.compressed:
+            P_agg = np.asarray(p_agg, dtype=np.float64).reshape(st.plan.n, self.rank)
+            q, st.P, E_new = powersgd_q(st.Mp, P_agg, self.ef)
+            st.E = E_new
+            st.emit_q = q.reshape(-1).copy()
+        else:
+            st.emit_q = st.Mp.copy()
+        st.Mp = None
+        st.phase = 2
+        return st.emit_q
+
+    def decompress_tensor(self, t: int, tid: int, q_agg: np.ndarray) -> np.ndarray:
+        st = self.state[tid]
+        if t != st.step + 1 or st.phase != 2:
+            raise ValueError(f"tensor {tid}: decompress({t}) before both halves")
+        agg = np.asarray(q_agg, dtype=np.float64)
+        if st.plan.compressed:
+            st.Q = agg.reshape(st.plan.m, self.rank)
+            out = ((st.P @ st.Q.T) / self.world_size).reshape(st.plan.shape)
+        else:
+            out = (agg / self.world_size).reshape(st.plan.shape)
+        st.phase, st.step = 0, t
+        return out
+
+    def error(self, tid: int) -> Optional[np.ndarray]:
+        return self.state[tid].E

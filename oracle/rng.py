@@ -15,6 +15,10 @@ element) and independent of bucket layout:
   gamma) as its k-th output (k = 1, 2, ...).
 * stream key: s = mix(seed XOR mix(2 * tensor_id + f)), f = 0 for P0 and 1
   for Q0.
+* fresh factors of the no-reuse ablation (Section V-B: ACP-SGD "without
+  reuse" draws the factor it would have reused anew at every step): the same
+  generator with the step t >= 1 in the high half of the key,
+  s = mix(seed XOR mix(t 2^32 + 2 * tensor_id + f)); t = 0 is P0 / Q0.
 * element i (row-major): a = mix(s + (2i + 1) gamma), b = mix(s + (2i + 2) gamma),
   u1 = ((a >> 11) + 1) 2^-53 in (0, 1], u2 = (b >> 11) 2^-53 in [0, 1).
 * Box-Muller (Box and Muller, 1958): z = sqrt(-2 ln u1) cos(2 pi u2) in
@@ -58,13 +62,13 @@ def _mix_vec(z: np.ndarray) -> np.ndarray:
     return z
 
 
-def stream_key(seed: int, tensor_id: int, factor: int) -> int:
-    return mix((seed & MASK64) ^ mix(2 * tensor_id + factor))
+def stream_key(seed: int, tensor_id: int, factor: int, step: int = 0) -> int:
+    return mix((seed & MASK64) ^ mix((step << 32) + 2 * tensor_id + factor))
 
 
-def uniforms(seed: int, tensor_id: int, factor: int, count: int):
+def uniforms(seed: int, tensor_id: int, factor: int, count: int, step: int = 0):
     """(u1, u2) float64 arrays of the Box-Muller inputs for elements 0..count-1."""
-    s = np.uint64(stream_key(seed, tensor_id, factor))
+    s = np.uint64(stream_key(seed, tensor_id, factor, step))
     i = np.arange(count, dtype=np.uint64)
     g = np.uint64(GAMMA)
     with np.errstate(over="ignore"):
@@ -79,9 +83,9 @@ _log = np.frompyfunc(math.log, 1, 1)
 _cos = np.frompyfunc(math.cos, 1, 1)
 
 
-def normals(seed: int, tensor_id: int, factor: int, count: int) -> np.ndarray:
+def normals(seed: int, tensor_id: int, factor: int, count: int, step: int = 0) -> np.ndarray:
     """float32 standard normals of one factor, element by element."""
-    u1, u2 = uniforms(seed, tensor_id, factor, count)
+    u1, u2 = uniforms(seed, tensor_id, factor, count, step)
     rad = np.sqrt(-2.0 * _log(u1).astype(np.float64))
     ang = _cos(TWO_PI * u2).astype(np.float64)
     return (rad * ang).astype(np.float32)
@@ -91,3 +95,9 @@ def init_factor(seed: int, tensor_id: int, which: str, rows: int, r: int) -> np.
     """P0 (``which='P'``, rows = n) or Q0 (``which='Q'``, rows = m) as a float32 rows x r array."""
     f = 0 if which == "P" else 1
     return normals(seed, tensor_id, f, rows * r).reshape(rows, r)
+
+
+def fresh_factor(seed: int, tensor_id: int, which: str, rows: int, r: int, step: int) -> np.ndarray:
+    """The factor drawn anew at step ``step`` >= 1 without reuse, float32 rows x r."""
+    f = 0 if which == "P" else 1
+    return normals(seed, tensor_id, f, rows * r, step).reshape(rows, r)

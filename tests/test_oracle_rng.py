@@ -57,3 +57,23 @@ def test_init_factor_shape():
     q = rng.init_factor(0, 0, "Q", 576, 4)
     assert q.shape == (576, 4) and q.dtype == np.float32
     assert np.array_equal(q.reshape(-1), rng.normals(0, 0, 1, 576 * 4))
+
+
+def test_step_keyed_stream_extends_the_initial_draw():
+    """Step 0 of the step-keyed stream is the initial factor itself (the key's high half is
+    zero); later steps give other, standard-normal streams, each a pure function of the step."""
+    q0 = rng.init_factor(3, 7, "Q", 100, 8)
+    assert np.array_equal(rng.fresh_factor(3, 7, "Q", 100, 8, 0), q0)
+    assert rng.stream_key(3, 7, 1, 0) == rng.mix(3 ^ rng.mix(2 * 7 + 1))
+    assert rng.stream_key(3, 7, 1, 5) == rng.mix(3 ^ rng.mix((5 << 32) + 2 * 7 + 1))
+    f1 = rng.fresh_factor(3, 7, "Q", 100, 8, 1)
+    f2 = rng.fresh_factor(3, 7, "Q", 100, 8, 2)
+    assert not np.array_equal(f1, q0) and not np.array_equal(f1, f2)
+    assert np.array_equal(f1, rng.fresh_factor(3, 7, "Q", 100, 8, 1))
+    # (tensor, factor) pairs and steps never share a key: the low half holds 2 * tensor + f
+    keys = {rng.stream_key(0, k, f, t) for k in range(4) for f in (0, 1) for t in range(4)}
+    assert len(keys) == 32
+    z = rng.normals(0, 11, 1, 200000, step=9).astype(np.float64)
+    assert abs(z.mean()) < 5 / math.sqrt(z.size)
+    assert abs(z.var() - 1) < 5 * math.sqrt(2 / z.size)
+    assert stats.kstest(z, "norm").pvalue > 1e-4

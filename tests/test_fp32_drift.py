@@ -11,33 +11,18 @@ import numpy as np
 
 import synthgrad as sg
 from oracle.acp import AcpOracle
-from oracle import rng
+from tests.fp32_ref import Fp32Tensor
 
 
 def _fp32_run(wl, tid, steps, key_of):
-    pl_n, pl_m = wl.params[tid].shape[0], int(np.prod(wl.params[tid].shape[1:]))
-    P = rng.init_factor(wl.seed, tid, "P", pl_n, wl.rank)
-    Q = rng.init_factor(wl.seed, tid, "Q", pl_m, wl.rank)
-    E = np.zeros((pl_n, pl_m), np.float32)
+    n, m = wl.params[tid].shape[0], int(np.prod(wl.params[tid].shape[1:]))
+    f32 = Fp32Tensor(wl.seed, tid, n, m, wl.rank)
     orc = AcpOracle([p.shape for p in wl.params], wl.rank, seed=wl.seed, tensor_ids=[tid])
-
-    def orth32(A):
-        q, r = np.linalg.qr(A.astype(np.float32))
-        return (q * np.sign(np.diag(r))).astype(np.float32)
-
     errs = {}
     for t in range(1, steps + 1):
         g = sg.gradient(wl, tid, key_of(t))
         ref = orc.decompress_tensor(t, tid, orc.compress_tensor(t, tid, g))
-        Mp = g.reshape(pl_n, pl_m) + E
-        if t % 2:
-            Q = orth32(Q)
-            P = (Mp @ Q).astype(np.float32)
-        else:
-            P = orth32(P)
-            Q = (Mp.T @ P).astype(np.float32)
-        E = (Mp - P @ Q.T).astype(np.float32)
-        out = P @ Q.T
+        out = f32.step(t, g)
         errs[t] = np.linalg.norm(out.reshape(ref.shape) - ref) / np.linalg.norm(ref)
     return errs
 

@@ -1,12 +1,12 @@
 """GPU parity of libacp.so against the fp64 oracle (per layer, relative Frobenius <= 1e-4).
 
-Compared per sampled layer: the emitted (local) factor, the orthonormal factor, M_hat and E;
-raw vectors must be bit-exact.  Small cases compare every element at every step; the
-full-size workloads run all buckets on the GPU exactly as the benchmark does and compare
-sampled layers (each layer's arithmetic depends only on its own inputs, so the oracle runs
-only those layers) at steps 1, 2, 3, 4, 10, 50, 99 and 100: free-running up to step 10, and
-re-synced at 50, 99 and 100 (the oracle starts those steps from the device state after the
-previous step; see parity_util.run_parity for why).
+Compared per layer: the emitted (local) factor, the orthonormal factor, M_hat and E; raw vectors
+must be bit-exact.  Small cases compare every tensor at every step.  The five full-size workloads
+(ResNet-50, ResNet-152, BERT-base r = 4 and 32, BERT-large r = 4 and 32) run all buckets through
+the all-bucket calls, as the benchmark does, and compare every tensor at steps 1-4 (free-running)
+and 50, 99, 100 (re-synced), plus tracked tensors free-running over all 100 steps against an fp32
+drift envelope (tests/full_parity.py).  The rank sweep (r = 64, 128, 256) compares sampled tensors
+at steps 1, 2, 3, 4, 10 (free-running), 50, 99 and 100 (re-synced).
 """
 
 import numpy as np
@@ -15,6 +15,7 @@ import torch
 
 import synthgrad as sg
 from oracle.acp import AcpOracle, LoopbackOracle
+from tests import full_parity as FP
 from tests import parity_util as PU
 
 pytestmark = pytest.mark.gpu
@@ -41,54 +42,63 @@ def test_single_conv_every_step(mode):
     _assert_ok(rep)
 
 
-RESNET50_SAMPLE = ["conv1.weight", "bn1.weight", "layer1.0.conv1.weight", "layer1.0.conv2.weight",
-                   "layer1.0.downsample.0.weight", "layer3.2.conv3.weight", "layer4.2.conv2.weight",
-                   "fc.weight", "fc.bias"]
+# tensors tracked over all 100 steps (fresh gradient every step, free-running fp64 oracle and
+# fp32 re-implementation beside the device): ResNets
+RESNET_TRACKED = ["layer1.0.conv1.weight", "layer1.0.conv2.weight", "layer3.2.conv3.weight",
+                  "layer4.2.conv2.weight", "fc.weight", "fc.bias"]
+RESNET152_TRACKED = ["layer2.7.conv2.weight", "layer3.35.conv3.weight", "layer4.0.downsample.0.weight",
+                     "fc.weight", "layer3.20.bn2.bias"]
+BERT_TRACKED = ["embeddings.position_embeddings.weight", "encoder.layer.0.attention.self.query.weight",
+                "encoder.layer.0.attention.self.query.bias", "encoder.layer.5.intermediate.dense.weight",
+                "encoder.layer.5.output.dense.weight"]
 
 
-def test_resnet50_fresh_100_steps():
+def _assert_full(rep, drift_rows):
+    PU.log("  worst: " + rep.summary())
+    bad = rep.failures + FP.drift_failures(drift_rows)
+    assert not bad, "\n".join(bad[:20])
+
+
+@pytest.mark.parametrize("name,tracked", [("resnet50_r4", RESNET_TRACKED), ("resnet152_r4", RESNET152_TRACKED),
+                                          ("bert_base_r4", BERT_TRACKED), ("bert_base_r32", BERT_TRACKED),
+                                          ("bert_large_r4", BERT_TRACKED), ("bert_large_r32", BERT_TRACKED)])
+def test_every_tensor_100_steps(name, tracked):
+    """Every tensor compared with the oracle at t = 1-4 (free-running, fresh gradients) and at
+    t = 50, 99, 100 (re-synced, fresh gradients); tracked tensors free-running for 100 steps."""
     _require_gpu()
-    wl = sg.WORKLOADS["resnet50_r4"]
-    rep = PU.run_parity(wl, "fresh", 100, CHECK, PU.tids_by_name(wl, RESNET50_SAMPLE), free=FREE)
-    _assert_ok(rep)
-
-
-def test_resnet152_100_steps():
-    _require_gpu()
-    wl = sg.WORKLOADS["resnet152_r4"]
-    names = ["conv1.weight", "layer2.7.conv2.weight", "layer3.35.conv3.weight", "layer4.0.downsample.0.weight",
-             "layer4.2.conv2.weight", "fc.weight", "layer3.20.bn2.bias"]
-    rep = PU.run_parity(wl, "pool3", 100, CHECK, PU.tids_by_name(wl, names), free=FREE)
-    _assert_ok(rep)
+    rep, drift_rows = FP.run_full_parity(sg.WORKLOADS[name], tracked)
+    _assert_full(rep, drift_rows)
 
 
 BERT_SAMPLE = ["embeddings.word_embeddings.weight", "embeddings.position_embeddings.weight",
                "embeddings.LayerNorm.weight", "encoder.layer.0.attention.self.query.weight",
                "encoder.layer.0.attention.self.query.bias", "encoder.layer.5.intermediate.dense.weight",
-               "encoder.layer.5.output.dense.weight", "encoder.layer.11.attention.output.dense.weight"]
+               "encoder.layer.5.output.dense.weight", "encoder.layer.11.attention.output.dense.weight",
+               "encoder.layer.23.attention.output.dense.weight", "encoder.layer.23.output.dense.weight"]
 
 
-@pytest.mark.parametrize("name", ["bert_base_r4", "bert_base_r32"])
-def test_bert_base_100_steps(name):
+@pytest.mark.parametrize("name", ["bert_large_r64", "bert_large_r128", "bert_large_r256"])
+def test_bert_large_rank_sweep_100_steps(name):
+    """Rank sweep: sampled BERT-large tensors over 100 steps, through the all-bucket calls (the
+    oracle's Gram-Schmidt takes seconds per factor at these ranks, so not every tensor)."""
     _require_gpu()
     wl = sg.WORKLOADS[name]
-    rep = PU.run_parity(wl, "pool3", 100, CHECK, PU.tids_by_name(wl, BERT_SAMPLE), free=FREE)
+    names = list(BERT_SAMPLE)
+    if wl.rank >= 256:
+        # the oracle's Gram-Schmidt of the 30522 x 256 embedding factor takes about 20 s per
+        # even step; test_bert_large_r256_embedding compares that matrix at steps 1 and 2
+        names.remove("embeddings.word_embeddings.weight")
+    rep = PU.run_parity(wl, "pool3", 100, CHECK, PU.tids_by_name(wl, names), free=FREE, grouped=True)
     _assert_ok(rep)
 
 
-@pytest.mark.parametrize("name", ["bert_large_r4", "bert_large_r32", "bert_large_r64", "bert_large_r128",
-                                  "bert_large_r256"])
-def test_bert_large_100_steps(name):
-    """Sampled BERT-large tensors over 100 steps, through the all-bucket calls of bench.py."""
+def test_bert_large_r256_embedding():
+    """The 30522 x 1024 token embedding at rank 256 (30 Gram slices of its P factor, the blocked
+    Cholesky of the 2 x 2 split) at steps 1 and 2, every element compared, all buckets running."""
     _require_gpu()
-    wl = sg.WORKLOADS[name]
-    names = BERT_SAMPLE[:-1] + ["encoder.layer.23.attention.output.dense.weight",
-                                "encoder.layer.23.output.dense.weight"]
-    if wl.rank >= 256:
-        # the oracle's Gram-Schmidt of the 30522 x 256 embedding factor takes about 20 s per step
-        # here; test_full_size_residual_identity covers that matrix at this rank
-        names.remove("embeddings.word_embeddings.weight")
-    rep = PU.run_parity(wl, "pool3", 100, CHECK, PU.tids_by_name(wl, names), free=FREE, grouped=True)
+    wl = sg.WORKLOADS["bert_large_r256"]
+    rep = PU.run_parity(wl, "fresh", 2, (1, 2), PU.tids_by_name(wl, ["embeddings.word_embeddings.weight"]),
+                        grouped=True)
     _assert_ok(rep)
 
 

@@ -59,7 +59,7 @@ struct MatDesc {
   int32_t bucket;     // bucket index
   int32_t fact_slices_p, fact_slices_q;  // Gram slices of the P / Q factor rows
   int32_t q_grp;      // Q-step row chunks whose rows interleave (see q_chunk_rows)
-  int32_t pad;
+  int32_t tid;        // registration index of the tensor (keys the no-reuse draws)
 };
 
 // the planner (host compiler) and the kernels (hipcc) share the chunk geometry below
@@ -88,6 +88,7 @@ ACP_HOST_DEVICE inline ChunkRows q_chunk_rows(const MatDesc& d, int64_t c) {
 
 struct VecDesc {
   int64_t grad_off, fac_off_p, fac_off_q, numel;
+  int64_t e_off;      // its slot in the E arena (Power-SGD's image of M' holds the raw vector there)
   int32_t bucket, pad;
 };
 
@@ -103,7 +104,10 @@ enum TileKind : int32_t { T_ROWS = 0, T_FACT = 1, T_VEC = 2, T_QTILE = 3, T_SROW
 //               on: gram_parts(r) parts), b = slice count; K_GSUM: a = entry block of
 //               kGsumEntries, b = slice count
 // kind T_VEC  : idx = vector, a = first element, b = element count
-// kind T_QTILE: idx = matrix, a = row chunk (K_QSTEP) or entry block (K_QFIN), b = column block
+// kind T_QTILE: idx = matrix, a = row chunk (K_QSTEP) or entry block (K_QFIN), b = column block;
+//               K_IMAGE: a = first row, b = column block | row count << 16 (kImageCols columns)
+// K_DRAW      : T_ROWS, idx = matrix, a = first factor row, b = row count
+// K_IMAGE     : T_FACT, idx = matrix (W = I); T_VEC as for the vector copies
 struct Tile {
   int32_t kind, idx, a, b;
 };
@@ -131,6 +135,8 @@ enum KernelId : int32_t {
   K_QNARROW,
   K_RNARROW,
   K_GSUM,        // from kBlockedRank on: a factor's Gram partials summed (and mirrored) into the first
+  K_DRAW,        // no reuse: a fresh standard normal factor into the P (variant 0) or Q (1) slot
+  K_IMAGE,       // Power-SGD: M' = M + E into the E arena (raw vectors too), W = I
 };
 
 // Narrow rows (r = 4, m / 4 = m4 <= 128 float4 groups): L lanes per row (16, 32 or 64), G float4
@@ -160,6 +166,10 @@ constexpr int kWideBlock = 64;     // threads per workgroup of K_WPSTEP, K_WQSTE
 constexpr int kWideQCols = 32;     // K_WQSTEP column block (one MFMA block)
 constexpr int kWideQRows = 512;    // K_WQSTEP rows per chunk (at most)
 constexpr int kWideRCols = 1024;   // K_WRECON columns per tile: 32 blocks of 32
+constexpr int kImageCols = 256;    // K_IMAGE columns per tile: one per thread
+constexpr int kDrawRows = 256;     // K_DRAW factor rows per tile
+// K_IMAGE rows per tile: their row-factor rows sit in LDS (at most 16 KB)
+constexpr int image_rows(int32_t r) { return r <= 64 ? 64 : 4096 / r; }
 
 // K_QSTEP variants: column slots per lane | kQFused when the kernel also orthogonalises P
 constexpr int32_t kQFused = 16;
@@ -167,7 +177,9 @@ constexpr int32_t kQFused = 16;
 // waves, for rows of 3076 to 4096 columns
 constexpr int32_t kThreeWaves = 32;
 constexpr int32_t kEightWaves = 64;
-// K_FACT variants: bit 0 = Q (else P); the factor is read from its state slot
+// K_FACT variants: bit 0 = Q (else P); bit 1 (kFactFromBuffer): the factor is read from the
+// aggregated factor buffer (src) and copied into its slot, else read from its slot
+constexpr int32_t kFactFromBuffer = 2;
 
 struct Launch {
   int32_t kernel;
@@ -206,6 +218,9 @@ struct KArgs {
   int32_t ef;           // error feedback on
   float inv_p;          // 1 / world size
   int32_t parity;       // 1 on odd (P-) steps, 0 on even (Q-) steps
+  int32_t copy_only;    // factor tiles copy the aggregated factor but build no W (Power-SGD)
+  uint64_t seed;        // K_DRAW: the context's seed
+  int64_t step;         // K_DRAW: the step whose factors are drawn
 };
 
 }  // namespace acp

@@ -66,7 +66,8 @@ typedef enum {
 
 /* flags of acp_init */
 #define ACP_FLAG_EF 1u            /* error feedback (Algorithm 2); off = Algorithm 1's ACP branch */
-#define ACP_FLAG_REUSE 2u         /* reuse the previous factor (always on in this build) */
+#define ACP_FLAG_REUSE 2u         /* reuse the previous factor; off = draw it anew every step */
+#define ACP_FLAG_POWERSGD 4u      /* Power-SGD (Algorithm 1, left) through acp_powersgd_* */
 #define ACP_FLAGS_DEFAULT 3u
 
 /* which factor for acp_factor / acp_init_factor */
@@ -74,7 +75,12 @@ typedef enum {
 #define ACP_FACTOR_Q 1
 
 /*
- * acp_init - plan the layout and draw P_0, Q_0 on the host.  No device work.
+ * acp_init - plan the layout and draw P_0, Q_0 on the host.  No device work (Section IV-B and
+ * IV-C for the layout; Section IV-A, "Error-feedback", for E_0 = 0 and P_0, Q_0).  Layout rules:
+ * whole tensors in reverse registration order, a bucket closing once its bytes reach the cap;
+ * vectors and matrices with r >= min(n, m) pass through raw.  Errors: ACP_E_INVALID for a bad
+ * argument (shape, rank, cap, world size, unknown flag), ACP_E_UNSUPPORTED for Power-SGD without
+ * reuse.
  *   num_tensors      number of parameters, in registration (forward) order.
  *   ndims[i]         rank of parameter i (1..8); dims holds all dims flattened, each in
  *                    1..2^31.  A compressed matrix (ndims >= 2 and r < min(n, m), n = dim 0,
@@ -88,14 +94,25 @@ typedef enum {
  *                    g = 0x9E3779B97F4A7C15.
  *   bucket_cap_bytes fusion cap (> 0); 26214400 is PyTorch-DDP's 25 MiB default.
  *   world_size       p >= 1; decompress divides the aggregated sum by p.
- *   flags            ACP_FLAG_* ; clearing ACP_FLAG_REUSE returns ACP_E_UNSUPPORTED.
+ *   flags            ACP_FLAG_*.  Without ACP_FLAG_REUSE (the ablation of Section V-B) every
+ *                    step orthogonalises a fresh draw instead of the previous factor: at step t
+ *                    the factor is the draw above with the key mix(seed ^ mix(t 2^32 + 2k + f))
+ *                    (t = 0 gives P_0, Q_0), made on the device.  ACP_FLAG_POWERSGD selects
+ *                    Power-SGD (needs ACP_FLAG_REUSE): such a context takes acp_powersgd_* and
+ *                    refuses acp_compress / acp_decompress (ACP_E_UNSUPPORTED), and vice versa.
  * On success *out owns host memory only; free it with acp_destroy.
  */
 acp_status acp_init(acp_ctx **out, int32_t num_tensors, const int32_t *ndims, const int64_t *dims,
                     int32_t rank, uint64_t seed, int64_t bucket_cap_bytes, int32_t world_size,
                     uint32_t flags);
 
-/* Size in bytes of the device state block the caller must allocate (256-byte aligned). */
+/*
+ * acp_state_bytes - size in bytes of the device state block the caller must allocate (256-byte
+ * aligned): the error E of Algorithm 2 (one fp32 slot per bucket element, Section IV-A
+ * "Error-feedback"), the factors P and Q kept from step to step (Section IV-A, "query reuse"),
+ * the orthogonalisation transforms, the Q-step and Gram partial sums and the launch tables.
+ * ACP_E_INVALID for a NULL argument.
+ */
 acp_status acp_state_bytes(const acp_ctx *ctx, int64_t *bytes);
 
 /*
@@ -106,17 +123,27 @@ acp_status acp_state_bytes(const acp_ctx *ctx, int64_t *bytes);
  */
 acp_status acp_bind_state(acp_ctx *ctx, void *device_ptr, int64_t bytes, void *stream);
 
+/* Number of gradient buckets (Section IV-B, "Buffer Size"), or -1 for a NULL context. */
 int32_t acp_num_buckets(const acp_ctx *ctx);
 
-/* Bucket sizes in elements: tensors, gradient/output bucket, P-step and Q-step factor buffers. */
+/*
+ * acp_bucket_info - bucket b's sizes in elements (any output pointer may be NULL): its tensors,
+ * the gradient / output bucket, and the factor buffer of a P-step (each compressed tensor's P,
+ * n x r, and every raw vector) and of a Q-step (Q, m x r, and the vectors): what one all-reduce
+ * of that bucket carries (Section IV-B, compressed tensors copied into one buffer per bucket).
+ * ACP_E_INVALID for a NULL context or b out of range.
+ */
 acp_status acp_bucket_info(const acp_ctx *ctx, int32_t b, int32_t *num_tensors, int64_t *grad_elems,
                            int64_t *factor_elems_p, int64_t *factor_elems_q);
 
 /*
  * acp_layout - bucket b's metadata, one entry per tensor in bucket order (arrays of
- * num_tensors from acp_bucket_info; any pointer may be NULL to skip it): registration index,
- * element offsets in the gradient bucket and in the P-step / Q-step factor buffers, and
- * whether the tensor is compressed.
+ * num_tensors from acp_bucket_info, owned by the caller; any pointer may be NULL to skip it):
+ * registration index, element offsets in the gradient bucket and in the P-step / Q-step factor
+ * buffers (packed, no padding), and whether the tensor is compressed.  The layout is the one of
+ * Section IV-B ("Buffer Size": whole tensors in backward order, closing at the cap) and IV-C
+ * (vectors raw, other tensors reshaped to dim 0 x the rest).  ACP_E_INVALID for a NULL context
+ * or b out of range.
  */
 acp_status acp_layout(const acp_ctx *ctx, int32_t b, int32_t *tensor_ids, int64_t *grad_off,
                       int64_t *fac_off_p, int64_t *fac_off_q, int32_t *compressed);
@@ -170,10 +197,12 @@ acp_status acp_compress_noalloc(acp_ctx *ctx, int64_t step, int32_t b, const flo
                                 float *factor_buf, void *stream);
 
 /*
- * acp_decompress - finish step `step` of bucket b: from the aggregated (summed) factor buffer
- * `agg_factor` (device), write M_hat = P_t Q_t^T / p for every compressed tensor and raw/p for
- * every vector into `out` (device, grad_elems(b) floats; may alias the gradient bucket but not
- * agg_factor), and keep the aggregated factor as the next step's reused factor.
+ * acp_decompress - finish step `step` of bucket b (Algorithm 2, the returned P_t Q_t^T after the
+ * all-reduce): from the aggregated (summed) factor buffer `agg_factor` (device), write
+ * M_hat = P_t Q_t^T / p for every compressed tensor and raw/p for every vector into `out`
+ * (device, grad_elems(b) floats; may alias the gradient bucket but not agg_factor), and keep the
+ * aggregated factor as the next step's reused factor (Section IV-A, "query reuse").
+ * ACP_E_STEP unless compress(step) of this bucket came last; ACP_E_INVALID for bad buffers.
  */
 acp_status acp_decompress(acp_ctx *ctx, int64_t step, int32_t b, const float *agg_factor, float *out,
                           void *stream);
@@ -190,6 +219,41 @@ acp_status acp_compress_all(acp_ctx *ctx, int64_t step, const float *const *grad
                             float *const *factor_bufs, void *stream);
 acp_status acp_decompress_all(acp_ctx *ctx, int64_t step, const float *const *agg_factors,
                               float *const *outs, void *stream);
+
+/*
+ * Power-SGD (Algorithm 1, left) on a context made with ACP_FLAG_POWERSGD, with error feedback
+ * applied as Algorithm 2 applies it when ACP_FLAG_EF is set.  Step t of bucket b takes three
+ * calls, the caller all-reducing (summing) the buffer the first two write:
+ *   acp_powersgd_p          M' = M_t + E_{t-1} (kept in the state for the second half);
+ *                           P_t = M' Q_{t-1} into p_buf (P-step layout, factor_elems_p(b)
+ *                           floats; raw vectors too).
+ *   acp_powersgd_q          P_t = orth(p_agg's P), the all-reduced P; Q_t = M'^T P_t into q_buf
+ *                           (Q-step layout, factor_elems_q(b) floats; raw vectors too);
+ *                           E_t = M' - P_t Q_t^T with this local Q_t.  `grad` is the same
+ *                           gradient bucket as in acp_powersgd_p (read again without error
+ *                           feedback).
+ *   acp_powersgd_decompress M_hat = P_t Q_agg^T / p into `out`, raw vectors as q_agg / p; Q_agg
+ *                           is kept as Q_t, which step t + 1 multiplies by as it is.
+ * Q_0 is the same draw as ACP-SGD's.  The calls reuse ACP-SGD's product, orthogonalisation and
+ * decompress kernels.  Buffers are device memory, 16-byte aligned; p_buf must not overlap grad,
+ * q_buf neither grad nor p_agg, out not q_agg.  Out-of-order calls return ACP_E_STEP; on an
+ * ACP-SGD context ACP_E_UNSUPPORTED.  After decompress, acp_factor returns P_t (ACP_FACTOR_P) and
+ * Q_agg (ACP_FACTOR_Q), and acp_error E_t; between the first and second half acp_error returns
+ * ACP_E_STEP.  The _all forms take host arrays of acp_num_buckets() device pointers and run every
+ * bucket in one launch per kernel kind.
+ */
+acp_status acp_powersgd_p(acp_ctx *ctx, int64_t step, int32_t b, const float *grad, float *p_buf,
+                          void *stream);
+acp_status acp_powersgd_q(acp_ctx *ctx, int64_t step, int32_t b, const float *grad, const float *p_agg,
+                          float *q_buf, void *stream);
+acp_status acp_powersgd_decompress(acp_ctx *ctx, int64_t step, int32_t b, const float *q_agg, float *out,
+                                   void *stream);
+acp_status acp_powersgd_p_all(acp_ctx *ctx, int64_t step, const float *const *grads,
+                              float *const *p_bufs, void *stream);
+acp_status acp_powersgd_q_all(acp_ctx *ctx, int64_t step, const float *const *grads,
+                              const float *const *p_aggs, float *const *q_bufs, void *stream);
+acp_status acp_powersgd_decompress_all(acp_ctx *ctx, int64_t step, const float *const *q_aggs,
+                                       float *const *outs, void *stream);
 
 /*
  * acp_error - write the current error E of bucket b's compressed tensors into `e_out` (device,

@@ -22,6 +22,7 @@ STATUS_NAMES = {0: "ACP_OK", -1: "ACP_E_INVALID", -2: "ACP_E_STEP", -3: "ACP_E_S
 
 ACP_FLAG_EF = 1
 ACP_FLAG_REUSE = 2
+ACP_FLAG_POWERSGD = 4
 ACP_FLAGS_DEFAULT = 3
 ACP_FACTOR_P = 0
 ACP_FACTOR_Q = 1
@@ -52,6 +53,12 @@ SIGNATURES = {
     "acp_decompress": (_i32, [_p, _i64, _i32, _pf, _pf, _p]),
     "acp_compress_all": (_i32, [_p, _i64, _p, _p, _p]),
     "acp_decompress_all": (_i32, [_p, _i64, _p, _p, _p]),
+    "acp_powersgd_p": (_i32, [_p, _i64, _i32, _pf, _pf, _p]),
+    "acp_powersgd_q": (_i32, [_p, _i64, _i32, _pf, _pf, _pf, _p]),
+    "acp_powersgd_decompress": (_i32, [_p, _i64, _i32, _pf, _pf, _p]),
+    "acp_powersgd_p_all": (_i32, [_p, _i64, _p, _p, _p]),
+    "acp_powersgd_q_all": (_i32, [_p, _i64, _p, _p, _p, _p]),
+    "acp_powersgd_decompress_all": (_i32, [_p, _i64, _p, _p, _p]),
     "acp_error": (_i32, [_p, _i32, _pf, _p]),
     "acp_factor": (_i32, [_p, _i32, _i32, _pf, _p]),
     "acp_checkpoint_bytes": (_i32, [_p, _pi64]),

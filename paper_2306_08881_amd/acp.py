@@ -40,13 +40,14 @@ class Acp:
 
     def __init__(self, shapes: Sequence[Sequence[int]], rank: int, seed: int = 0,
                  cap_bytes: int = 25 * 1024 * 1024, world_size: int = 1, ef: bool = True,
-                 device=None, bind: bool = True):
+                 device=None, bind: bool = True, reuse: bool = True, powersgd: bool = False):
         self.lib = L.load()
         self.shapes = [tuple(int(d) for d in s) for s in shapes]
         ndims = (C.c_int32 * len(self.shapes))(*[len(s) for s in self.shapes])
         flat = [d for s in self.shapes for d in s]
         dims = (C.c_int64 * len(flat))(*flat)
-        flags = L.ACP_FLAG_REUSE | (L.ACP_FLAG_EF if ef else 0)
+        flags = ((L.ACP_FLAG_REUSE if reuse else 0) | (L.ACP_FLAG_EF if ef else 0) |
+                 (L.ACP_FLAG_POWERSGD if powersgd else 0))
         ctx = C.c_void_p()
         st = self.lib.acp_init(C.byref(ctx), len(self.shapes), ndims, dims, rank, seed, cap_bytes,
                                world_size, flags)
@@ -54,6 +55,7 @@ class Acp:
             raise L.AcpError(st, "acp_init")
         self.ctx = ctx
         self.rank, self.world_size, self.ef = rank, world_size, ef
+        self.reuse, self.powersgd = reuse, powersgd
         self.state = None
         if bind:
             self.bind_state(device)
@@ -132,18 +134,49 @@ class Acp:
         _check(self.lib.acp_decompress(self.ctx, step, b, _fptr(agg_factor), _fptr(out), _stream_ptr(stream)),
                self.lib, self.ctx, "acp_decompress")
 
+    def _ptrs(self, tensors):
+        """Host array of one device pointer per bucket (the library reads acp_num_buckets() of them)."""
+        if len(tensors) != self.num_buckets():
+            raise ValueError(f"expected {self.num_buckets()} buffers (one per bucket), got {len(tensors)}")
+        return (C.c_void_p * len(tensors))(*[_fptr(x) for x in tensors])
+
     def compress_all(self, step: int, grads, factor_bufs, stream=None):
         """One step for every bucket: ``grads`` / ``factor_bufs`` are lists of device tensors."""
-        g = (C.c_void_p * len(grads))(*[_fptr(x) for x in grads])
-        f = (C.c_void_p * len(factor_bufs))(*[_fptr(x) for x in factor_bufs])
+        g, f = self._ptrs(grads), self._ptrs(factor_bufs)
         _check(self.lib.acp_compress_all(self.ctx, step, g, f, _stream_ptr(stream)), self.lib, self.ctx,
                "acp_compress_all")
 
     def decompress_all(self, step: int, aggs, outs, stream=None):
-        a = (C.c_void_p * len(aggs))(*[_fptr(x) for x in aggs])
-        o = (C.c_void_p * len(outs))(*[_fptr(x) for x in outs])
+        a, o = self._ptrs(aggs), self._ptrs(outs)
         _check(self.lib.acp_decompress_all(self.ctx, step, a, o, _stream_ptr(stream)), self.lib, self.ctx,
                "acp_decompress_all")
+
+    # ---- Power-SGD (a context made with powersgd=True)
+    def powersgd_p(self, step: int, b: int, grad, p_buf, stream=None):
+        _check(self.lib.acp_powersgd_p(self.ctx, step, b, _fptr(grad), _fptr(p_buf), _stream_ptr(stream)),
+               self.lib, self.ctx, "acp_powersgd_p")
+
+    def powersgd_q(self, step: int, b: int, grad, p_agg, q_buf, stream=None):
+        _check(self.lib.acp_powersgd_q(self.ctx, step, b, _fptr(grad), _fptr(p_agg), _fptr(q_buf),
+                                       _stream_ptr(stream)), self.lib, self.ctx, "acp_powersgd_q")
+
+    def powersgd_decompress(self, step: int, b: int, q_agg, out, stream=None):
+        _check(self.lib.acp_powersgd_decompress(self.ctx, step, b, _fptr(q_agg), _fptr(out), _stream_ptr(stream)),
+               self.lib, self.ctx, "acp_powersgd_decompress")
+
+    def powersgd_p_all(self, step: int, grads, p_bufs, stream=None):
+        _check(self.lib.acp_powersgd_p_all(self.ctx, step, self._ptrs(grads), self._ptrs(p_bufs),
+                                           _stream_ptr(stream)), self.lib, self.ctx, "acp_powersgd_p_all")
+
+    def powersgd_q_all(self, step: int, grads, p_aggs, q_bufs, stream=None):
+        _check(self.lib.acp_powersgd_q_all(self.ctx, step, self._ptrs(grads), self._ptrs(p_aggs),
+                                           self._ptrs(q_bufs), _stream_ptr(stream)),
+               self.lib, self.ctx, "acp_powersgd_q_all")
+
+    def powersgd_decompress_all(self, step: int, q_aggs, outs, stream=None):
+        _check(self.lib.acp_powersgd_decompress_all(self.ctx, step, self._ptrs(q_aggs), self._ptrs(outs),
+                                                    _stream_ptr(stream)),
+               self.lib, self.ctx, "acp_powersgd_decompress_all")
 
     # ---- inspection and checkpoint
     def error(self, b: int, e_out, stream=None):

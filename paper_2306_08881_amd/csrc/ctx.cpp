@@ -31,6 +31,7 @@ struct acp_ctx {
   std::vector<int64_t> last_step;   // per bucket: last completed step
   std::vector<int64_t> pending;     // per bucket: compressed step awaiting decompress (0 = none)
   std::vector<uint8_t> deferred;    // per bucket: E form of the arena (kExplicit, kHoldsF, kHoldsX)
+  std::vector<uint8_t> phase;       // per bucket, Power-SGD: 1 after the first half, 2 after the second
   mutable std::string err;
 
   // kernel timing (acp_profile_start / acp_profile_stop)
@@ -89,14 +90,24 @@ acp::KArgs base_args(const acp_ctx* c) {
   a.vecs = reinterpret_cast<const acp::VecDesc*>(d + p.off_vecs);
   a.ef = p.ef ? 1 : 0;
   a.inv_p = 1.0f / static_cast<float>(c->world);
+  a.seed = c->seed;
   return a;
 }
 
+bool overlaps(const void* x, int64_t x_floats, const void* y, int64_t y_floats) {
+  const char* a = static_cast<const char*>(x);
+  const char* b = static_cast<const char*>(y);
+  return a < b + y_floats * 4 && b < a + x_floats * 4;
+}
+
+// Enqueues `launches` on s; skip_chol leaves out the Gram finish (K_GSUM, K_CHOL), which factor
+// tiles that only copy (KArgs::copy_only) do not need.
 acp_status run(const acp_ctx* c, const std::vector<acp::Launch>& launches, acp::KArgs a,
-               hipStream_t s) {
+               hipStream_t s, bool skip_chol = false) {
   const acp::Tile* tiles = reinterpret_cast<const acp::Tile*>(c->dev + c->plan.off_tiles);
   acp_ctx* mc = const_cast<acp_ctx*>(c);
   for (const acp::Launch& l : launches) {
+    if (skip_chol && (l.kernel == acp::K_GSUM || l.kernel == acp::K_CHOL)) continue;
     a.tiles = tiles + l.tile_off;
     a.ntiles = l.ntiles;
     a.variant = l.variant;
@@ -133,6 +144,7 @@ struct CkptHeader {
 acp_status compress_bucket(acp_ctx* c, int64_t step, int32_t b, const float* grad, float* factor_buf,
                            void* stream, float* qpart) {
   if (!c) return ACP_E_INVALID;
+  if (c->plan.psgd) return fail(c, ACP_E_UNSUPPORTED, "this context runs Power-SGD (acp_powersgd_*)");
   if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
   if (b < 0 || b >= static_cast<int32_t>(c->plan.buckets.size()))
     return fail(c, ACP_E_INVALID, "bucket index out of range");
@@ -159,12 +171,76 @@ acp_status compress_bucket(acp_ctx* c, int64_t step, int32_t b, const float* gra
   a.src[0] = grad;
   a.dst[0] = factor_buf;
   a.parity = static_cast<int32_t>(step & 1);
+  a.step = step;
   set_form(a, 0, c->deferred[b]);
+  if (!c->plan.reuse) {
+    const acp_status sd = run(c, bk.draw[step & 1], a, static_cast<hipStream_t>(stream));
+    if (sd != ACP_OK) return sd;
+  }
   const acp_status st = run(c, bk.compress[step & 1], a, static_cast<hipStream_t>(stream));
   if (st != ACP_OK) return st;
   c->pending[b] = step;
   c->deferred[b] = form_after_compress(c, step);
   return ACP_OK;
+}
+
+// Power-SGD: the bucket's image of M' in the E arena (the source of both products with error
+// feedback), else the gradient itself
+const float* psgd_source(const acp_ctx* c, int32_t b, const float* grad) {
+  if (!c->plan.ef) return grad;
+  return reinterpret_cast<const float*>(c->dev + c->plan.off_e) + c->plan.buckets[b].e_base;
+}
+
+// checks shared by the Power-SGD calls: context, bucket, phase of the step
+acp_status psgd_ready(const acp_ctx* c, int64_t step, int32_t b, int32_t phase) {
+  if (!c->plan.psgd) return fail(c, ACP_E_UNSUPPORTED, "this context runs ACP-SGD (acp_compress)");
+  if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
+  if (b < 0 || b >= static_cast<int32_t>(c->plan.buckets.size()))
+    return fail(c, ACP_E_INVALID, "bucket index out of range");
+  const bool ok = phase == 0 ? (c->pending[b] == 0 && step == c->last_step[b] + 1)
+                             : (c->pending[b] == step && c->phase[b] == phase);
+  if (!ok) {
+    static const char* what[3] = {"acp_powersgd_p", "acp_powersgd_q", "acp_powersgd_decompress"};
+    return fail(c, ACP_E_STEP, std::string(what[phase]) + "(" + std::to_string(step) + ") on bucket " +
+                                   std::to_string(b) + " out of order");
+  }
+  return ACP_OK;
+}
+
+acp_status psgd_p_bucket(acp_ctx* c, int64_t step, int32_t b, const float* grad, float* p_buf, hipStream_t s) {
+  const acp::BucketPlan& bk = c->plan.buckets[b];
+  acp::KArgs a = base_args(c);
+  a.base = b;
+  a.src[0] = grad;
+  a.parity = 1;
+  set_form(a, 0, c->deferred[b]);
+  acp_status st = run(c, bk.psgd_image, a, s);
+  if (st != ACP_OK) return st;
+  acp::KArgs m = base_args(c);
+  m.ef = 0;
+  m.base = b;
+  m.src[0] = psgd_source(c, b, grad);
+  m.dst[0] = p_buf;
+  m.parity = 1;
+  return run(c, bk.compress[1], m, s);
+}
+
+acp_status psgd_q_bucket(acp_ctx* c, int32_t b, const float* grad, const float* p_agg, float* q_buf,
+                         hipStream_t s) {
+  const acp::BucketPlan& bk = c->plan.buckets[b];
+  acp::KArgs a = base_args(c);
+  a.base = b;
+  a.src[0] = p_agg;
+  a.parity = 0;
+  acp_status st = run(c, bk.psgd_fact, a, s);
+  if (st != ACP_OK) return st;
+  acp::KArgs m = base_args(c);
+  m.ef = 0;
+  m.base = b;
+  m.src[0] = psgd_source(c, b, grad);
+  m.dst[0] = q_buf;
+  m.parity = 0;
+  return run(c, bk.compress[0], m, s);
 }
 
 }  // namespace
@@ -177,11 +253,12 @@ acp_status acp_init(acp_ctx** out, int32_t num_tensors, const int32_t* ndims, co
   if (!out) return ACP_E_INVALID;
   *out = nullptr;
   if (world_size < 1) return ACP_E_INVALID;
-  if (flags & ~ACP_FLAGS_DEFAULT) return ACP_E_INVALID;
-  if (!(flags & ACP_FLAG_REUSE)) return ACP_E_UNSUPPORTED;
+  if (flags & ~(ACP_FLAG_EF | ACP_FLAG_REUSE | ACP_FLAG_POWERSGD)) return ACP_E_INVALID;
+  const bool reuse = (flags & ACP_FLAG_REUSE) != 0, psgd = (flags & ACP_FLAG_POWERSGD) != 0;
+  if (psgd && !reuse) return ACP_E_UNSUPPORTED;
   acp_ctx* c = new acp_ctx();
   const std::string msg = acp::build_plan(c->plan, num_tensors, ndims, dims, rank, bucket_cap_bytes,
-                                          (flags & ACP_FLAG_EF) != 0);
+                                          (flags & ACP_FLAG_EF) != 0, reuse, psgd);
   if (!msg.empty()) {
     delete c;
     return ACP_E_INVALID;
@@ -202,6 +279,7 @@ acp_status acp_init(acp_ctx** out, int32_t num_tensors, const int32_t* ndims, co
   c->last_step.assign(nb, 0);
   c->pending.assign(nb, 0);
   c->deferred.assign(nb, 0);
+  c->phase.assign(nb, 0);
   *out = c;
   return ACP_OK;
 }
@@ -254,6 +332,7 @@ acp_status acp_bind_state(acp_ctx* c, void* device_ptr, int64_t bytes, void* str
   std::fill(c->last_step.begin(), c->last_step.end(), 0);
   std::fill(c->pending.begin(), c->pending.end(), 0);
   std::fill(c->deferred.begin(), c->deferred.end(), 0);
+  std::fill(c->phase.begin(), c->phase.end(), 0);
   // the static scratch of acp_compress_noalloc: looked up once per device, with it current
   c->scratch = nullptr;
   c->scratch_err.clear();
@@ -386,6 +465,7 @@ acp_status acp_compress_noalloc(acp_ctx* c, int64_t step, int32_t b, const float
 acp_status acp_decompress(acp_ctx* c, int64_t step, int32_t b, const float* agg_factor, float* out,
                           void* stream) {
   if (!c) return ACP_E_INVALID;
+  if (c->plan.psgd) return fail(c, ACP_E_UNSUPPORTED, "this context runs Power-SGD (acp_powersgd_*)");
   if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
   if (b < 0 || b >= static_cast<int32_t>(c->plan.buckets.size()))
     return fail(c, ACP_E_INVALID, "bucket index out of range");
@@ -420,6 +500,7 @@ acp_status acp_decompress(acp_ctx* c, int64_t step, int32_t b, const float* agg_
 acp_status acp_compress_all(acp_ctx* c, int64_t step, const float* const* grads,
                             float* const* factor_bufs, void* stream) {
   if (!c) return ACP_E_INVALID;
+  if (c->plan.psgd) return fail(c, ACP_E_UNSUPPORTED, "this context runs Power-SGD (acp_powersgd_*)");
   if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
   if (!grads || !factor_bufs) return fail(c, ACP_E_INVALID, "null pointer array");
   const int32_t nb = static_cast<int32_t>(c->plan.buckets.size());
@@ -443,10 +524,15 @@ acp_status acp_compress_all(acp_ctx* c, int64_t step, const float* const* grads,
     acp::KArgs a = base_args(c);
     a.base = static_cast<int32_t>(g) * acp::kMaxGroup;
     a.parity = static_cast<int32_t>(step & 1);
+    a.step = step;
     for (int32_t i = 0; i < acp::kMaxGroup && a.base + i < nb; ++i) {
       a.src[i] = grads[a.base + i];
       a.dst[i] = factor_bufs[a.base + i];
       set_form(a, i, c->deferred[a.base + i]);
+    }
+    if (!c->plan.reuse) {
+      const acp_status sd = run(c, c->plan.group_draw[g][step & 1], a, static_cast<hipStream_t>(stream));
+      if (sd != ACP_OK) return sd;
     }
     const acp_status st = run(c, c->plan.group_compress[g][step & 1], a, static_cast<hipStream_t>(stream));
     if (st != ACP_OK) return st;
@@ -461,6 +547,7 @@ acp_status acp_compress_all(acp_ctx* c, int64_t step, const float* const* grads,
 acp_status acp_decompress_all(acp_ctx* c, int64_t step, const float* const* agg_factors,
                               float* const* outs, void* stream) {
   if (!c) return ACP_E_INVALID;
+  if (c->plan.psgd) return fail(c, ACP_E_UNSUPPORTED, "this context runs Power-SGD (acp_powersgd_*)");
   if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
   if (!agg_factors || !outs) return fail(c, ACP_E_INVALID, "null pointer array");
   const int32_t nb = static_cast<int32_t>(c->plan.buckets.size());
@@ -499,6 +586,176 @@ acp_status acp_decompress_all(acp_ctx* c, int64_t step, const float* const* agg_
   return ACP_OK;
 }
 
+acp_status acp_powersgd_p(acp_ctx* c, int64_t step, int32_t b, const float* grad, float* p_buf,
+                          void* stream) {
+  if (!c) return ACP_E_INVALID;
+  acp_status st = psgd_ready(c, step, b, 0);
+  if (st != ACP_OK) return st;
+  if (!grad || !p_buf) return fail(c, ACP_E_INVALID, "null buffer");
+  if (!aligned16(grad) || !aligned16(p_buf)) return fail(c, ACP_E_INVALID, "buffers must be 16-byte aligned");
+  const acp::BucketPlan& bk = c->plan.buckets[b];
+  if (overlaps(grad, bk.grad_elems, p_buf, bk.fac_elems_p)) return fail(c, ACP_E_INVALID, "p_buf overlaps grad");
+  if ((st = check_device(c)) != ACP_OK) return st;
+  if ((st = psgd_p_bucket(c, step, b, grad, p_buf, static_cast<hipStream_t>(stream))) != ACP_OK) return st;
+  c->pending[b] = step;
+  c->phase[b] = 1;
+  return ACP_OK;
+}
+
+acp_status acp_powersgd_q(acp_ctx* c, int64_t step, int32_t b, const float* grad, const float* p_agg,
+                          float* q_buf, void* stream) {
+  if (!c) return ACP_E_INVALID;
+  acp_status st = psgd_ready(c, step, b, 1);
+  if (st != ACP_OK) return st;
+  if (!grad || !p_agg || !q_buf) return fail(c, ACP_E_INVALID, "null buffer");
+  if (!aligned16(grad) || !aligned16(p_agg) || !aligned16(q_buf))
+    return fail(c, ACP_E_INVALID, "buffers must be 16-byte aligned");
+  const acp::BucketPlan& bk = c->plan.buckets[b];
+  if (overlaps(q_buf, bk.fac_elems_q, grad, bk.grad_elems) || overlaps(q_buf, bk.fac_elems_q, p_agg, bk.fac_elems_p))
+    return fail(c, ACP_E_INVALID, "q_buf overlaps grad or p_agg");
+  if ((st = check_device(c)) != ACP_OK) return st;
+  if ((st = psgd_q_bucket(c, b, grad, p_agg, q_buf, static_cast<hipStream_t>(stream))) != ACP_OK) return st;
+  c->phase[b] = 2;
+  c->deferred[b] = c->plan.ef ? kHoldsF : kExplicit;
+  return ACP_OK;
+}
+
+acp_status acp_powersgd_decompress(acp_ctx* c, int64_t step, int32_t b, const float* q_agg, float* out,
+                                   void* stream) {
+  if (!c) return ACP_E_INVALID;
+  acp_status st = psgd_ready(c, step, b, 2);
+  if (st != ACP_OK) return st;
+  if (!q_agg || !out) return fail(c, ACP_E_INVALID, "null buffer");
+  if (!aligned16(q_agg) || !aligned16(out)) return fail(c, ACP_E_INVALID, "buffers must be 16-byte aligned");
+  const acp::BucketPlan& bk = c->plan.buckets[b];
+  if (overlaps(out, bk.grad_elems, q_agg, bk.fac_elems_q)) return fail(c, ACP_E_INVALID, "out overlaps q_agg");
+  if ((st = check_device(c)) != ACP_OK) return st;
+  acp::KArgs a = base_args(c);
+  a.copy_only = 1;
+  a.base = b;
+  a.src[0] = q_agg;
+  a.dst[0] = out;
+  a.parity = 0;
+  set_form(a, 0, c->deferred[b]);
+  if ((st = run(c, bk.decompress[0], a, static_cast<hipStream_t>(stream), true)) != ACP_OK) return st;
+  c->pending[b] = 0;
+  c->phase[b] = 0;
+  c->last_step[b] = step;
+  return ACP_OK;
+}
+
+acp_status acp_powersgd_p_all(acp_ctx* c, int64_t step, const float* const* grads, float* const* p_bufs,
+                              void* stream) {
+  if (!c) return ACP_E_INVALID;
+  if (!grads || !p_bufs) return fail(c, ACP_E_INVALID, "null pointer array");
+  const int32_t nb = static_cast<int32_t>(c->plan.buckets.size());
+  for (int32_t b = 0; b < nb; ++b) {
+    const acp_status st = psgd_ready(c, step, b, 0);
+    if (st != ACP_OK) return st;
+    const acp::BucketPlan& bk = c->plan.buckets[b];
+    if (!grads[b] || !p_bufs[b]) return fail(c, ACP_E_INVALID, "null buffer");
+    if (!aligned16(grads[b]) || !aligned16(p_bufs[b])) return fail(c, ACP_E_INVALID, "buffers must be 16-byte aligned");
+    if (overlaps(grads[b], bk.grad_elems, p_bufs[b], bk.fac_elems_p)) return fail(c, ACP_E_INVALID, "p_buf overlaps grad");
+  }
+  acp_status st = check_device(c);
+  if (st != ACP_OK) return st;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  for (size_t g = 0; g < c->plan.group_compress.size(); ++g) {
+    acp::KArgs a = base_args(c), m = base_args(c);
+    a.base = m.base = static_cast<int32_t>(g) * acp::kMaxGroup;
+    a.parity = m.parity = 1;
+    m.ef = 0;
+    for (int32_t i = 0; i < acp::kMaxGroup && a.base + i < nb; ++i) {
+      a.src[i] = grads[a.base + i];
+      set_form(a, i, c->deferred[a.base + i]);
+      m.src[i] = psgd_source(c, a.base + i, grads[a.base + i]);
+      m.dst[i] = p_bufs[a.base + i];
+    }
+    if ((st = run(c, c->plan.group_psgd_image[g], a, s)) != ACP_OK) return st;
+    if ((st = run(c, c->plan.group_compress[g][1], m, s)) != ACP_OK) return st;
+  }
+  for (int32_t b = 0; b < nb; ++b) {
+    c->pending[b] = step;
+    c->phase[b] = 1;
+  }
+  return ACP_OK;
+}
+
+acp_status acp_powersgd_q_all(acp_ctx* c, int64_t step, const float* const* grads, const float* const* p_aggs,
+                              float* const* q_bufs, void* stream) {
+  if (!c) return ACP_E_INVALID;
+  if (!grads || !p_aggs || !q_bufs) return fail(c, ACP_E_INVALID, "null pointer array");
+  const int32_t nb = static_cast<int32_t>(c->plan.buckets.size());
+  for (int32_t b = 0; b < nb; ++b) {
+    const acp_status st = psgd_ready(c, step, b, 1);
+    if (st != ACP_OK) return st;
+    const acp::BucketPlan& bk = c->plan.buckets[b];
+    if (!grads[b] || !p_aggs[b] || !q_bufs[b]) return fail(c, ACP_E_INVALID, "null buffer");
+    if (!aligned16(grads[b]) || !aligned16(p_aggs[b]) || !aligned16(q_bufs[b]))
+      return fail(c, ACP_E_INVALID, "buffers must be 16-byte aligned");
+    if (overlaps(q_bufs[b], bk.fac_elems_q, grads[b], bk.grad_elems) ||
+        overlaps(q_bufs[b], bk.fac_elems_q, p_aggs[b], bk.fac_elems_p))
+      return fail(c, ACP_E_INVALID, "q_buf overlaps grad or p_agg");
+  }
+  acp_status st = check_device(c);
+  if (st != ACP_OK) return st;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  for (size_t g = 0; g < c->plan.group_compress.size(); ++g) {
+    acp::KArgs a = base_args(c), m = base_args(c);
+    a.base = m.base = static_cast<int32_t>(g) * acp::kMaxGroup;
+    a.parity = m.parity = 0;
+    m.ef = 0;
+    for (int32_t i = 0; i < acp::kMaxGroup && a.base + i < nb; ++i) {
+      a.src[i] = p_aggs[a.base + i];
+      m.src[i] = psgd_source(c, a.base + i, grads[a.base + i]);
+      m.dst[i] = q_bufs[a.base + i];
+    }
+    if ((st = run(c, c->plan.group_psgd_fact[g], a, s)) != ACP_OK) return st;
+    if ((st = run(c, c->plan.group_compress[g][0], m, s)) != ACP_OK) return st;
+  }
+  for (int32_t b = 0; b < nb; ++b) {
+    c->phase[b] = 2;
+    c->deferred[b] = c->plan.ef ? kHoldsF : kExplicit;
+  }
+  return ACP_OK;
+}
+
+acp_status acp_powersgd_decompress_all(acp_ctx* c, int64_t step, const float* const* q_aggs, float* const* outs,
+                                       void* stream) {
+  if (!c) return ACP_E_INVALID;
+  if (!q_aggs || !outs) return fail(c, ACP_E_INVALID, "null pointer array");
+  const int32_t nb = static_cast<int32_t>(c->plan.buckets.size());
+  for (int32_t b = 0; b < nb; ++b) {
+    const acp_status st = psgd_ready(c, step, b, 2);
+    if (st != ACP_OK) return st;
+    const acp::BucketPlan& bk = c->plan.buckets[b];
+    if (!q_aggs[b] || !outs[b]) return fail(c, ACP_E_INVALID, "null buffer");
+    if (!aligned16(q_aggs[b]) || !aligned16(outs[b])) return fail(c, ACP_E_INVALID, "buffers must be 16-byte aligned");
+    if (overlaps(outs[b], bk.grad_elems, q_aggs[b], bk.fac_elems_q)) return fail(c, ACP_E_INVALID, "out overlaps q_agg");
+  }
+  acp_status st = check_device(c);
+  if (st != ACP_OK) return st;
+  for (size_t g = 0; g < c->plan.group_decompress.size(); ++g) {
+    acp::KArgs a = base_args(c);
+    a.copy_only = 1;
+    a.base = static_cast<int32_t>(g) * acp::kMaxGroup;
+    a.parity = 0;
+    for (int32_t i = 0; i < acp::kMaxGroup && a.base + i < nb; ++i) {
+      a.src[i] = q_aggs[a.base + i];
+      a.dst[i] = outs[a.base + i];
+      set_form(a, i, c->deferred[a.base + i]);
+    }
+    if ((st = run(c, c->plan.group_decompress[g][0], a, static_cast<hipStream_t>(stream), true)) != ACP_OK)
+      return st;
+  }
+  for (int32_t b = 0; b < nb; ++b) {
+    c->pending[b] = 0;
+    c->phase[b] = 0;
+    c->last_step[b] = step;
+  }
+  return ACP_OK;
+}
+
 acp_status acp_error(const acp_ctx* c, int32_t b, float* e_out, void* stream) {
   if (!c) return ACP_E_INVALID;
   if (!c->dev) return fail(c, ACP_E_STATE, "state not bound");
@@ -506,6 +763,8 @@ acp_status acp_error(const acp_ctx* c, int32_t b, float* e_out, void* stream) {
   if (b < 0 || b >= static_cast<int32_t>(c->plan.buckets.size()))
     return fail(c, ACP_E_INVALID, "bucket index out of range");
   if (!e_out || !aligned16(e_out)) return fail(c, ACP_E_INVALID, "e_out must be a 16-byte aligned pointer");
+  if (c->plan.psgd && c->phase[b] == 1)
+    return fail(c, ACP_E_STEP, "between the halves of a Power-SGD step the E arena holds M + E");
   const acp_status ds = check_device(c);
   if (ds != ACP_OK) return ds;
   acp::KArgs a = base_args(c);
@@ -526,7 +785,7 @@ acp_status acp_factor(const acp_ctx* c, int32_t tensor_id, int32_t which, float*
   const int64_t step = c->last_step[t.bucket];
   if (step < 1) return fail(c, ACP_E_STEP, "no completed step");
   const acp::MatDesc& d = c->plan.mats[t.mat];
-  const bool odd = (step & 1) != 0;
+  const bool odd = (step & 1) != 0 && !c->plan.psgd;  // a Power-SGD step ends like a Q-step
   int64_t slot, rows;
   if (which == ACP_FACTOR_P) {
     slot = odd ? d.p_slot : d.ph_slot;

@@ -503,6 +503,14 @@ __device__ void gram_blocked(const float* X, int64_t r0, int64_t r1, double* out
 template <int RK>
 __device__ void fact_tile(const KArgs& a, const Tile& t, const float* src, float* dst, int64_t rows) {
   const MatDesc d = a.mats[t.idx];
+  if (a.copy_only) {  // Power-SGD keeps the aggregated Q as it is: copied, no W
+    const int sl = RK >= kBlockedRank ? (t.a & 0xffff) : t.a;
+    if (!dst || (RK >= kBlockedRank && (t.a >> 16) != 0)) return;
+    const int64_t r0 = static_cast<int64_t>(sl) * d.fact_rows;
+    const int64_t r1 = r0 + d.fact_rows < rows ? r0 + d.fact_rows : rows;
+    for (int64_t e = r0 * RK + tid(); e < r1 * RK; e += static_cast<int64_t>(blockDim.x)) dst[e] = src[e];
+    return;
+  }
   if constexpr (RK >= kBlockedRank) {  // always a partial: K_CHOL forms W
     const int sl = t.a & 0xffff, part = t.a >> 16;
     const int64_t r0 = static_cast<int64_t>(sl) * d.fact_rows;

@@ -24,12 +24,107 @@ hipError_t launch_wide(const Launch& l, int32_t rank, const KArgs& args, hipStre
 
 namespace {
 
+// Factor tiles alone: W of the P (variant bit 0 clear) or Q factor of a matrix, read from its slot,
+// or with kFactFromBuffer from the aggregated factor buffer and copied into the slot.
 template <int RK>
 __global__ __launch_bounds__(kBlock) void k_fact(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
   const bool q = (a.variant & 1) != 0;
-  fact_tile<RK>(a, t, a.fac + (q ? d.q_slot : d.p_slot), nullptr, q ? d.m : d.n);
+  float* slot = a.fac + (q ? d.q_slot : d.p_slot);
+  if (a.variant & kFactFromBuffer)
+    fact_tile<RK>(a, t, src_of(a, d.bucket) + (q ? d.fac_off_q : d.fac_off_p), slot, q ? d.m : d.n);
+  else
+    fact_tile<RK>(a, t, slot, nullptr, q ? d.m : d.n);
+}
+
+// No reuse (the ablation of Section V-B): the factor a step would have reused is drawn anew, i.i.d.
+// standard normal, from the initial factors' counter-based generator with the step in the high
+// half of the key: element i (row-major) of factor f (0: P, 1: Q) of tensor k at step t takes the
+// SplitMix64 outputs x = mix(s + (2i + 1) g), y = mix(s + (2i + 2) g) of the stream
+// s = mix(seed ^ mix(t 2^32 + 2k + f)) and becomes sqrt(-2 ln u1) cos(2 pi u2) in fp64 with
+// u1 = ((x >> 11) + 1) 2^-53, u2 = (y >> 11) 2^-53, rounded to fp32.  Tile: factor rows
+// [t.a, t.a + t.b) of the P (variant 0) or Q (variant 1) slot.
+__device__ inline uint64_t splitmix_mix(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+template <int RK>
+__global__ __launch_bounds__(kBlock) void k_draw(KArgs a) {
+  constexpr uint64_t kGamma = 0x9E3779B97F4A7C15ull;
+  constexpr double kTwoPi = 2.0 * 3.14159265358979323846;
+  const Tile t = a.tiles[blockIdx.x];
+  const MatDesc d = a.mats[t.idx];
+  const uint64_t f = static_cast<uint64_t>(a.variant & 1);
+  float* slot = a.fac + (f ? d.q_slot : d.p_slot);
+  const uint64_t key = (static_cast<uint64_t>(a.step) << 32) + 2ull * static_cast<uint64_t>(d.tid) + f;
+  const uint64_t s = splitmix_mix(a.seed ^ splitmix_mix(key));
+  const int64_t e0 = static_cast<int64_t>(t.a) * RK, ne = static_cast<int64_t>(t.b) * RK;
+  for (int64_t k = tid(); k < ne; k += kBlock) {
+    const uint64_t i = static_cast<uint64_t>(e0 + k);
+    const uint64_t x = splitmix_mix(s + (2ull * i + 1ull) * kGamma);
+    const uint64_t y = splitmix_mix(s + (2ull * i + 2ull) * kGamma);
+    const double u1 = static_cast<double>((x >> 11) + 1ull) * 0x1.0p-53;
+    const double u2 = static_cast<double>(y >> 11) * 0x1.0p-53;
+    const double rad = sqrt(-2.0 * log(u1));
+    const double ang = cos(kTwoPi * u2);
+    slot[e0 + k] = static_cast<float>(rad * ang);
+  }
+}
+
+// Power-SGD's first half with error feedback: the E arena receives M' = M + E_{t-1}, the image of
+// the bucket that both of the step's products then read, E_{t-1} taken in the form the arena holds
+// it (E itself, or F - Ph Q_loc^T after a Q-step).  T_QTILE tiles: `rows` rows from t.a and
+// kImageCols columns of a matrix, one thread per column; the tile's rows of the term's row factor
+// sit in LDS and, up to rank 32, the thread's column-factor row in registers.  T_VEC tiles copy
+// raw vectors into their arena slots; T_FACT tiles set W = I, so that the P-step kernels multiply
+// by Q_{t-1} itself.
+template <int RK>
+__global__ __launch_bounds__(kBlock) void k_image(KArgs a) {
+  const Tile t = a.tiles[blockIdx.x];
+  if (t.kind == T_FACT) {
+    const MatDesc d = a.mats[t.idx];
+    for (int e = tid(); e < RK * RK; e += kBlock) a.w[d.w_slot + e] = (e / RK == e % RK) ? 1.0 : 0.0;
+    return;
+  }
+  if (t.kind == T_VEC) {
+    const VecDesc v = a.vecs[t.idx];
+    const float* src = src_of(a, v.bucket) + v.grad_off + t.a;
+    float* dst = a.e + v.e_off + t.a;
+    for (int i = tid(); i < t.b; i += kBlock) dst[i] = src[i];
+    return;
+  }
+  const MatDesc d = a.mats[t.idx];
+  const int cb = t.b & 0xffff, rows = t.b >> 16;
+  const int64_t m = d.m;
+  const int64_t c = static_cast<int64_t>(cb) * kImageCols + tid();
+  const bool fform = deferred_of(a, d.bucket), xform = deferred_p_of(a, d.bucket);
+  const bool term = fform || xform;
+  const float* L = a.fac + (xform ? d.qh_slot : d.ql_slot);  // column factor of the term (m x r)
+  const float* R = a.fac + (xform ? d.pl_slot : d.ph_slot);  // row factor of the term (n x r)
+  __shared__ float rs[4096];  // the tile's rows of R (rows * RK <= 4096)
+  if (term)
+    for (int e = tid(); e < rows * RK; e += kBlock) rs[e] = R[static_cast<int64_t>(t.a) * RK + e];
+  __syncthreads();
+  if (c >= m) return;
+  constexpr int KR = RK <= 32 ? RK : 32;  // ranks of the column-factor row held in registers
+  float l[KR];
+#pragma unroll
+  for (int k = 0; k < KR; ++k) l[k] = term ? L[c * RK + k] : 0.f;
+  const float* M = src_of(a, d.bucket) + d.grad_off;
+  float* X = a.e + d.e_off;
+  for (int i = 0; i < rows; ++i) {
+    const int64_t idx = (static_cast<int64_t>(t.a) + i) * m + c;
+    float v = M[idx] + X[idx];
+    if (term) {
+#pragma unroll
+      for (int k = 0; k < KR; ++k) v -= rs[i * RK + k] * l[k];
+      for (int k = KR; k < RK; ++k) v -= rs[i * RK + k] * L[c * RK + k];
+    }
+    X[idx] = v;
+  }
 }
 
 // Cholesky G = R^T R and W = R^-1 of a Gram matrix in shared memory (RK = 128, row-major; only
@@ -1552,6 +1647,8 @@ hipError_t launch_rank(const Launch& l, const KArgs& args, hipStream_t s) {
       case K_GSUM: hipLaunchKernelGGL(k_gsum<RK>, grid, block, 0, s, args); break;
       case K_QFIN: hipLaunchKernelGGL(k_qfin<RK>, grid, block, 0, s, args); break;
       case K_VEC: hipLaunchKernelGGL(k_vec, grid, block, 0, s, args); break;
+      case K_DRAW: hipLaunchKernelGGL(k_draw<RK>, grid, block, 0, s, args); break;
+      case K_IMAGE: hipLaunchKernelGGL(k_image<RK>, grid, block, 0, s, args); break;
       default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -1617,6 +1714,8 @@ hipError_t launch_rank(const Launch& l, const KArgs& args, hipStream_t s) {
           return hipErrorInvalidValue;
         }
       case K_VEC: hipLaunchKernelGGL(k_vec, grid, block, 0, s, args); break;
+      case K_DRAW: hipLaunchKernelGGL(k_draw<RK>, grid, block, 0, s, args); break;
+      case K_IMAGE: hipLaunchKernelGGL(k_image<RK>, grid, block, 0, s, args); break;
       default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

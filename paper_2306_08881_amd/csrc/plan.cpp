@@ -14,6 +14,7 @@
 
 #include <algorithm>
 #include <array>
+#include <climits>
 #include <cmath>
 #include <map>
 
@@ -58,15 +59,21 @@ struct TileSink {
 }  // namespace
 
 std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, const int64_t* dims,
-                       int32_t rank, int64_t cap_bytes, bool ef) {
+                       int32_t rank, int64_t cap_bytes, bool ef, bool reuse, bool psgd) {
   if (num_tensors <= 0) return "num_tensors must be positive";
   if (!ndims || !dims) return "ndims and dims must not be NULL";
   if (!rank_supported(rank)) return "rank must be one of 1, 2, 4, 8, 16, 32, 64, 128, 256";
   if (cap_bytes <= 0) return "bucket_cap_bytes must be positive";
+  if (psgd && !reuse) return "Power-SGD reuses Q";
   plan = Plan{};
   plan.rank = rank;
   plan.cap_bytes = cap_bytes;
   plan.ef = ef;
+  plan.reuse = reuse;
+  plan.psgd = psgd;
+  // Power-SGD runs ACP-SGD's product kernels without error feedback on the image M' = M + E that
+  // its first half writes into the E arena: their lists carry no E update of their own
+  const bool list_ef = ef && !psgd;
   const int64_t r = rank;
 
   // ---- tensors: reshape and eligibility
@@ -99,8 +106,12 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       }
     }
     if (!t.compressed) {
+      // a raw tensor's element offsets travel as 32-bit tile fields
+      if (numel > INT32_MAX) return "tensor " + std::to_string(i) + ": raw tensors may have at most 2^31 - 1 elements";
       t.n = numel;
       t.m = 1;
+    } else if (t.n > INT32_MAX) {
+      return "tensor " + std::to_string(i) + ": compressed matrices may have at most 2^31 - 1 rows";
     }
   }
 
@@ -198,6 +209,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         v.fac_off_p = bk.fac_off_p[k];
         v.fac_off_q = bk.fac_off_q[k];
         v.numel = t.numel;
+        v.e_off = bk.e_base + bk.grad_off[k];
         v.bucket = b;
         t.vec = static_cast<int32_t>(plan.vecs.size());
         bk.vecs.push_back(t.vec);
@@ -211,6 +223,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       d.e_off = bk.e_base + bk.grad_off[k];
       d.fac_off_p = bk.fac_off_p[k];
       d.fac_off_q = bk.fac_off_q[k];
+      d.tid = bk.tids[k];
       const int64_t np = align_up(t.n * r, kSlotAlign), mp = align_up(t.m * r, kSlotAlign);
       d.p_slot = fac_floats;
       d.ph_slot = fac_floats + np;
@@ -569,7 +582,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         for (int32_t mi : generic) row_tiles(mi, 1);
         if (!vec_done) vec_tiles(bk), vec_done = true;
         sink.end(l, L);
-        if (ef) {
+        if (list_ef) {
           l = sink.begin(K_EUPD, 1);
           for (int32_t mi : generic)
             row_tiles(mi, std::max<int64_t>(1, kSmallTileElems / plan.mats[mi].m));
@@ -664,6 +677,51 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     }
     emat_launch(bk);
   }
+  // ---- no reuse: before each compress the reused factor is drawn anew (K_DRAW) and its W formed
+  // (factor tiles from its slot, then the Gram finish); [1]: P-steps draw Q, [0]: Q-steps draw P
+  for (BucketPlan& bk : plan.buckets) {
+    if (reuse) break;
+    for (int32_t par = 0; par < 2; ++par) {
+      const bool q = par == 1;
+      std::vector<Launch>& L = bk.draw[par];
+      Launch l = sink.begin(K_DRAW, q ? 1 : 0);
+      for (int32_t mi : bk.mats) {
+        const int64_t rows = q ? plan.mats[mi].m : plan.mats[mi].n;
+        for (int64_t s0 = 0; s0 < rows; s0 += kDrawRows)
+          plan.tiles.push_back(Tile{T_ROWS, mi, static_cast<int32_t>(s0),
+                                    static_cast<int32_t>(std::min<int64_t>(kDrawRows, rows - s0))});
+      }
+      sink.end(l, L);
+      l = sink.begin(K_FACT, q ? 1 : 0);
+      for (int32_t mi : bk.mats) fact_tiles(mi, q);
+      sink.end(l, L);
+      chol_launches(bk.mats, q, L);
+    }
+  }
+  // ---- Power-SGD: the first half writes M' = M + E (raw vectors too) into the E arena and sets
+  // W = I, then runs the P-step lists on it; the second half copies the all-reduced P into its slot
+  // and forms its W, then runs the Q-step lists; decompress is the Q-step decompress
+  for (BucketPlan& bk : plan.buckets) {
+    if (!psgd) break;
+    Launch l = sink.begin(K_IMAGE, 0);
+    const int64_t ir = image_rows(rank);
+    for (int32_t mi : bk.mats) {
+      plan.tiles.push_back(Tile{T_FACT, mi, 0, 0});
+      if (!ef) continue;
+      const MatDesc& d = plan.mats[mi];
+      const int64_t ncb = cdiv(d.m, kImageCols);
+      for (int64_t r0 = 0; r0 < d.n; r0 += ir)
+        for (int64_t cb = 0; cb < ncb; ++cb)
+          plan.tiles.push_back(Tile{T_QTILE, mi, static_cast<int32_t>(r0),
+                                    static_cast<int32_t>(cb | (std::min<int64_t>(ir, d.n - r0) << 16))});
+    }
+    if (ef) vec_tiles(bk);
+    sink.end(l, bk.psgd_image);
+    l = sink.begin(K_FACT, kFactFromBuffer);
+    for (int32_t mi : bk.mats) fact_tiles(mi, false);
+    sink.end(l, bk.psgd_fact);
+    chol_launches(bk.mats, false, bk.psgd_fact);
+  }
   {
     Launch l = sink.begin(K_FACT, 1);
     for (int32_t mi = 0; mi < static_cast<int32_t>(plan.mats.size()); ++mi) fact_tiles(mi, true);
@@ -675,7 +733,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
 
   // ---- launch families and algorithmic bytes (host-side profiling)
   auto tile_bytes = [&](const Launch& l, const Tile& t, bool odd) -> double {
-    const double eb = ef ? 12.0 : 4.0;  // M read, E read, E written per compress element
+    const double eb = list_ef ? 12.0 : 4.0;  // M read, E read, E written per compress element
     if (t.kind == T_VEC) return 8.0 * t.b;
     const MatDesc& d = plan.mats[t.idx];
     const double n = d.n, m = d.m, rr = double(r);
@@ -690,7 +748,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         return rows * m * eb + rows * rr * 8.0 + (t.a == 0 ? m * rr * 12.0 : 0.0);
       }
       case K_PROW:
-        return m * (ef ? 8.0 : 4.0) + rr * 8.0 + (t.a == 0 ? m * rr * 12.0 : 0.0);
+        return m * (list_ef ? 8.0 : 4.0) + rr * 8.0 + (t.a == 0 ? m * rr * 12.0 : 0.0);
       case K_EUPD:
         return t.b * m * 4.0;
       case K_QSTEP: {
@@ -735,18 +793,26 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         return (t.b & 0xffff) * rr * 8.0 / (r >= kApplyMfmaRank ? rr / 64.0 : 1.0);
       case K_FACT:
         if (t.a >> 16) return 0.0;
-        return std::min<double>(d.fact_rows, (l.variant & 1 ? m : n) - double(t.a & 0xffff) * d.fact_rows) * rr * 4.0;
+        return std::min<double>(d.fact_rows, (l.variant & 1 ? m : n) - double(t.a & 0xffff) * d.fact_rows) * rr *
+               (l.variant & kFactFromBuffer ? 8.0 : 4.0);
       case K_EMAT:
         return t.b * m * 8.0;
       case K_GSUM:  // the slices' partials read, the sum written
         return (t.b + 1.0) * kGsumEntries * 8.0;
+      case K_DRAW:
+        return t.b * rr * 4.0;
+      case K_IMAGE: {  // M read, E read, M' written
+        if (t.kind != T_QTILE) return 0.0;
+        const double cols = std::min<double>(kImageCols, m - double(t.b & 0xffff) * kImageCols);
+        return double(t.b >> 16) * cols * 12.0;
+      }
       default:
         return 0.0;
     }
   };
   auto family_of = [](int32_t kernel, bool odd) -> int32_t {
     switch (kernel) {
-      case K_PFUSED: case K_PROW: case K_EUPD: case K_WPSTEP:
+      case K_PFUSED: case K_PROW: case K_EUPD: case K_WPSTEP: case K_IMAGE:
         return 1;  // ACP_KERNEL_P_STEP
       case K_QSTEP: case K_WQSTEP:
         return 2;  // ACP_KERNEL_Q_STEP
@@ -754,7 +820,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       case K_RECON: case K_RECON4: case K_WRECON:
         return 4;  // ACP_KERNEL_RECONSTRUCT
       case K_WFACT: return 5;                                              // ACP_KERNEL_ORTH
-      case K_APPLY: case K_FACT: case K_CHOL: case K_GSUM: return 5;  // ACP_KERNEL_ORTH
+      case K_APPLY: case K_FACT: case K_CHOL: case K_GSUM: case K_DRAW: return 5;  // ACP_KERNEL_ORTH
       default: return 0;  // K_VEC (raw-vector launches of their own) and K_EMAT: no family
     }
   };
@@ -771,6 +837,10 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
     annotate(bk.decompress[0], false);
     annotate(bk.decompress[1], true);
     annotate(bk.emat, false);
+    annotate(bk.draw[0], false);
+    annotate(bk.draw[1], true);
+    annotate(bk.psgd_image, true);
+    annotate(bk.psgd_fact, false);
   }
   annotate(plan.gram_init, false);
 
@@ -778,6 +848,8 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   // one, in the dependency order the per-bucket lists already follow
   auto order_of = [](const Launch& l) -> int32_t {
     switch (l.kernel) {
+      case K_DRAW: case K_IMAGE: return -3;
+      case K_FACT: return -2;
       case K_APPLY: return 0;
       case K_PFUSED: return (l.variant & kEightWaves) ? 8 : (l.variant & kThreeWaves) ? 7 : 1 + l.variant;  // 2..8
       case K_PROW: return 10;
@@ -845,6 +917,14 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       }
       plan.group_compress.push_back(gc);
       plan.group_decompress.push_back(gd);
+      std::array<std::vector<Launch>, 2> gw;
+      for (int32_t par = 0; par < 2; ++par)
+        gw[par] = merge(b0, b1, [par](const BucketPlan& bk) -> const std::vector<Launch>& { return bk.draw[par]; }, par == 1);
+      plan.group_draw.push_back(gw);
+      plan.group_psgd_image.push_back(
+          merge(b0, b1, [](const BucketPlan& bk) -> const std::vector<Launch>& { return bk.psgd_image; }, true));
+      plan.group_psgd_fact.push_back(
+          merge(b0, b1, [](const BucketPlan& bk) -> const std::vector<Launch>& { return bk.psgd_fact; }, false));
     }
   }
 

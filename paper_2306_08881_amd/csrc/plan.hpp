@@ -33,12 +33,17 @@ struct BucketPlan {
   std::vector<Launch> compress[2];    // [0] even step (Q-step), [1] odd step (P-step)
   std::vector<Launch> decompress[2];
   std::vector<Launch> emat;
+  std::vector<Launch> draw[2];        // no reuse: the fresh reused factor and its W, before compress
+  std::vector<Launch> psgd_image;     // Power-SGD, first half: M' into the E arena, W = I
+  std::vector<Launch> psgd_fact;      // Power-SGD, second half: the all-reduced P into its slot, W
 };
 
 struct Plan {
   int32_t rank = 0;
   int64_t cap_bytes = 0;
   bool ef = true;
+  bool reuse = true;   // reuse the previous factor (else draw it anew every step)
+  bool psgd = false;   // Power-SGD (Algorithm 1) instead of ACP-SGD
   std::vector<TensorPlan> tensors;
   std::vector<BucketPlan> buckets;
   std::vector<MatDesc> mats;
@@ -47,7 +52,8 @@ struct Plan {
   std::vector<Launch> gram_init;     // W of every matrix's Q slot (after bind / restore)
   // launches covering whole groups of kMaxGroup buckets (the *_all entry points):
   // [group][parity] -> launches
-  std::vector<std::array<std::vector<Launch>, 2>> group_compress, group_decompress;
+  std::vector<std::array<std::vector<Launch>, 2>> group_compress, group_decompress, group_draw;
+  std::vector<std::vector<Launch>> group_psgd_image, group_psgd_fact;
 
   // device state regions (byte offsets from the block base)
   int64_t off_e = 0, off_fac = 0, off_w = 0, off_gpart = 0, off_qpart = 0;
@@ -56,8 +62,9 @@ struct Plan {
 };
 
 // Builds the plan; returns "" on success or an error text.
+// reuse = false: ACP-SGD drawing the reused factor anew every step; psgd: Power-SGD (needs reuse).
 std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, const int64_t* dims,
-                       int32_t rank, int64_t cap_bytes, bool ef);
+                       int32_t rank, int64_t cap_bytes, bool ef, bool reuse = true, bool psgd = false);
 
 // Initial factor (f = 0: P_0, n x r; f = 1: Q_0, m x r) of tensor `tid`, row-major fp32.
 void draw_init_factor(uint64_t seed, int32_t tid, int32_t f, int64_t count, float* out);

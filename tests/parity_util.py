@@ -69,10 +69,11 @@ class Runner:
     """One library context plus the device buffers of every bucket."""
 
     def __init__(self, shapes, rank, seed=0, cap=25 << 20, world=1, ef=True, device="cuda:0",
-                 grouped=False):
+                 grouped=False, reuse=True):
         self.dev = torch.device(device)
         self.grouped = grouped  # step() through acp_compress_all / acp_decompress_all
-        self.acp = Acp(shapes, rank, seed=seed, cap_bytes=cap, world_size=world, ef=ef, device=self.dev)
+        self.acp = Acp(shapes, rank, seed=seed, cap_bytes=cap, world_size=world, ef=ef, device=self.dev,
+                       reuse=reuse)
         self.nb = self.acp.num_buckets()
         self.info = [self.acp.bucket_info(b) for b in range(self.nb)]
         self.lay = [self.acp.layout(b) for b in range(self.nb)]
@@ -177,7 +178,7 @@ def read_state_into(run: Runner, orc: AcpOracle, t_done: int, tids: Sequence[int
 
 def run_parity(wl: sg.Workload, mode: str, steps: int, check: Sequence[int], tids: Sequence[int],
                ef: bool = True, tol: float = TOL, free: Optional[int] = None,
-               device="cuda:0", grouped: bool = False) -> Report:
+               device="cuda:0", grouped: bool = False, reuse: bool = True) -> Report:
     """Parity over ``steps`` steps, comparing the sampled tensors at the ``check`` steps.
 
     Steps 1..``free`` run free: the oracle carries its own fp64 state from step 1.  At a
@@ -190,8 +191,9 @@ def run_parity(wl: sg.Workload, mode: str, steps: int, check: Sequence[int], tid
     free = steps if free is None else free
     shapes = [p.shape for p in wl.params]
     t0 = time.time()
-    run = Runner(shapes, wl.rank, wl.seed, wl.cap_bytes, ef=ef, device=device, grouped=grouped)
-    orc = AcpOracle(shapes, wl.rank, seed=wl.seed, cap_bytes=wl.cap_bytes, ef=ef, tensor_ids=tids)
+    run = Runner(shapes, wl.rank, wl.seed, wl.cap_bytes, ef=ef, device=device, grouped=grouped, reuse=reuse)
+    orc = AcpOracle(shapes, wl.rank, seed=wl.seed, cap_bytes=wl.cap_bytes, ef=ef, tensor_ids=tids,
+                    reuse=reuse)
     rep = Report()
     cache: Dict[int, List[torch.Tensor]] = {}
     host_cache: Dict[int, Dict[int, np.ndarray]] = {}

@@ -11,8 +11,12 @@ value = algorithmic bytes per step / measured step time, where the algorithmic b
 vectors) plus the factor traffic 10 r (n + m) B per matrix (average of a P-step and a Q-step).
 
 Also reported: the roofline entry of the dominant kernel (its own bytes per launch over its
-event-timed average launch duration) and the CPU oracle's throughput on a bounded sample of
-the same workload.
+event-timed average launch duration, and its HBM traffic from the workload's rocprofv3 counter
+file when that was taken on the current kernel sources); the streaming ceilings of the probe
+kernels (libacp_probe.so: the compress kernels' 2-read-1-write mix and the decompress kernels'
+write-only stream) and the step's fraction of their mix; the CPU oracle's throughput on a bounded
+sample of the same workload; with --compare-powersgd, Power-SGD's compress and step times beside
+ACP-SGD's on the same workload.
 """
 
 from __future__ import annotations
@@ -72,11 +76,29 @@ def cpu_baseline(wl, seconds: float = 12.0):
         elapsed += time.perf_counter() - tb
         steps += 1
         del grads
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    pools = threadpool_info()
+    threads = max([i.get("num_threads", 1) for i in pools] or [1])
+    blas = ", ".join(sorted({f"{i.get('internal_api')} {i.get('version')}" for i in pools if i.get("user_api") == "blas"}))
     return {"value": round(steps * step_bytes / elapsed / 1e9, 4), "unit": "GB/s", "cores": int(threads),
             "kind": "oracle",
             "sample": f"{wl.name}: all {len(lay.buckets)} buckets, steps 1-{steps}, fp64 NumPy "
-                      f"(OpenBLAS), {elapsed:.1f} s of oracle work"}
+                      f"({blas or 'BLAS'}, {threads} threads), {elapsed:.1f} s of oracle work"}
+
+
+def host_info():
+    """The host the CPU baseline ran on: CPU model, cores this process may use, BLAS pools."""
+    from threadpoolctl import threadpool_info
+    model = platform.processor() or platform.machine()
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    pools = [{"api": i.get("internal_api"), "version": i.get("version"), "threads": i.get("num_threads")}
+             for i in threadpool_info() if i.get("user_api") == "blas"]
+    return {"cpu": model, "affinity_cores": len(os.sched_getaffinity(0)), "blas": pools}
 
 
 def kernel_families(rank: int):
@@ -102,7 +124,19 @@ def kernel_families(rank: int):
 WORKLOAD_KIND = {"conv": "one 256x64x3x3 convolution gradient", "resnet50": "ResNet-50-shaped gradients",
                  "resnet152": "ResNet-152-shaped gradients", "bert_base": "BERT-base-shaped gradients",
                  "bert_large": "BERT-large-shaped gradients"}
-TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "traffic.txt")
+PROFILES = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles")
+METRIC_NAME = {"conv256x576": "one 256x576 matrix", "resnet50": "ResNet-50", "resnet152": "ResNet-152",
+               "bert_base": "BERT-base", "bert_large": "BERT-large"}
+
+
+def traffic_file(workload: str) -> str:
+    """Per-kernel HBM bytes of a workload's benchmark from rocprofv3 counters (pmc_summary)."""
+    return os.path.join(PROFILES, f"{workload}_traffic.txt")
+
+
+def metric_of(wl) -> str:
+    base, r = wl.name.rsplit("_r", 1)
+    return f"ACP-SGD compress+decompress gradient GB/s and % HBM peak, {METRIC_NAME[base]} r={r}"
 
 
 def kernel_source_hash() -> str:
@@ -110,15 +144,19 @@ def kernel_source_hash() -> str:
     import hashlib
     csrc = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2306_08881_amd", "csrc")
     h = hashlib.sha256()
-    for f in ("kernels.hip", "wide.hip", "device.hpp", "acp_internal.hpp", "plan.cpp"):
+    for f in ("kernels.hip", "wide.hip", "device.hpp", "acp_internal.hpp", "plan.cpp", "probe.hip"):
         h.update(open(os.path.join(csrc, f), "rb").read())
     return h.hexdigest()[:16]
 
 
+PROBE_FLOATS = 1 << 28  # 1 GiB per probe array
+
+
 def pmc_summary(fetch_csv: str, write_csv: str, workload: str):
     """Per-kernel HBM bytes per dispatch from FETCH_SIZE / WRITE_SIZE runs, each scaled by what
-    the counter reads for the copy probe (a device-to-device copy of 1 GiB), written to
-    profiles/traffic.txt with the kernel source hash they were taken on."""
+    the counter reads for the streaming probe of known bytes (k_probe_rrw over 1 GiB arrays:
+    2 GiB read, 1 GiB written), written to profiles/traffic.txt with the kernel source hash they
+    were taken on."""
     import csv
     from collections import defaultdict
 
@@ -129,17 +167,18 @@ def pmc_summary(fetch_csv: str, write_csv: str, workload: str):
         return d
 
     f, w = load(fetch_csv), load(write_csv)
-    gib_kib = float(1 << 20)
-    copy_f = [v for k, vs in f.items() if "copyBuffer" in k for v in vs if v > 0.25 * gib_kib]
-    copy_w = [v for k, vs in w.items() if "copyBuffer" in k for v in vs if v > 0.5 * gib_kib]
-    sf = gib_kib / (sum(copy_f) / len(copy_f))
-    sw = gib_kib / (sum(copy_w) / len(copy_w))
+    gib_kib = PROBE_FLOATS * 4 / 1024.0
+    probe_f = [v for k, vs in f.items() if "k_probe_rrw" in k for v in vs]
+    probe_w = [v for k, vs in w.items() if "k_probe_rrw" in k for v in vs]
+    # every footprint of the probe moves the same bytes per dispatch
+    sf = 2 * gib_kib / (sum(probe_f) / len(probe_f))
+    sw = gib_kib / (sum(probe_w) / len(probe_w))
     out = {"source_hash": kernel_source_hash(), "workload": workload, "fetch_scale": round(sf, 4),
            "write_scale": round(sw, 4), "kernels": {}}
     print(f"| kernel | dispatches | FETCH_SIZE KiB/dispatch | WRITE_SIZE KiB/dispatch | HBM bytes/dispatch (scaled) |")
     print("|---|---|---|---|---|")
     for name in sorted(f):
-        if "acp::" not in name and "copyBuffer" not in name:
+        if "acp::" not in name and "k_probe" not in name:
             continue
         fv, wv = f[name], w.get(name, [0.0])
         fa, wa = sum(fv) / len(fv), sum(wv) / len(wv)
@@ -148,28 +187,140 @@ def pmc_summary(fetch_csv: str, write_csv: str, workload: str):
         out["kernels"][short] = {"dispatches": len(fv), "fetch_kib": round(fa, 1), "write_kib": round(wa, 1),
                                  "hbm_bytes": round(hbm, 1)}
         print(f"| {short} | {len(fv)} | {fa:.0f} | {wa:.0f} | {hbm:.4g} |")
-    print(f"\ncopy probe scale factors: FETCH_SIZE x{sf:.4f}, WRITE_SIZE x{sw:.4f}")
-    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
-    json.dump(out, open(TRAFFIC_FILE, "w"), indent=1)
+    print(f"\nscale factors from the probe k_probe_rrw (2 GiB read, 1 GiB written per dispatch): "
+          f"FETCH_SIZE x{sf:.4f}, WRITE_SIZE x{sw:.4f}")
+    os.makedirs(PROFILES, exist_ok=True)
+    json.dump(out, open(traffic_file(workload), "w"), indent=1)
 
 
-def measured_traffic(workload: str, family: str, launches: int):
-    """HBM bytes per launch of the dominant kernel family from profiles/traffic.txt, or None
-    when the counters were taken on other kernel sources or for another workload."""
+def measured_traffic(workload: str, family: str):
+    """(HBM bytes per launch of the dominant kernel family, provenance text) from the workload's
+    counter file, or (None, reason) when the counters were taken on other kernel sources."""
+    path = traffic_file(workload)
+    rel = os.path.relpath(path, os.path.dirname(os.path.abspath(__file__)))
     try:
-        t = json.load(open(TRAFFIC_FILE))
+        t = json.load(open(path))
     except (OSError, ValueError):
-        return None
+        return None, f"no counters: {rel} is missing"
     if t.get("source_hash") != kernel_source_hash() or t.get("workload") not in (None, workload):
-        return None
+        return None, f"no counters: {rel} was taken on other kernel sources"
     sym = next((k[2] for k in kernel_families(4) + kernel_families(8) + kernel_families(64) + kernel_families(256) if k[0] == family), None)
     ks = [v for k, v in t["kernels"].items() if sym and k.startswith(sym)]
     if not ks:
-        return None
+        return None, f"no counters for {sym} in {rel}"
     # dispatch-weighted bytes per launch of the family (its launches of every class)
     tot = sum(v["hbm_bytes"] * v["dispatches"] for v in ks)
     n = sum(v["dispatches"] for v in ks)
-    return round(tot / n, 1) if n else None
+    src = (f"{rel}: rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, over this benchmark on kernel sources "
+           f"{t['source_hash']}, not measured in this run; each counter scaled by what it reads for the "
+           f"probe k_probe_rrw of known bytes (FETCH_SIZE x{t['fetch_scale']}, WRITE_SIZE x{t['write_scale']})")
+    return (round(tot / n, 1) if n else None), src
+
+
+def probe_ceilings(dev, stream):
+    """Streaming ceilings of this GPU from the probe kernels (libacp_probe.so) over 1 GiB arrays:
+    the compress kernels' mix (read M, read E, write E in place) and the decompress kernels'
+    (write only), both nontemporal, each the best of 4, 8, 16 and 32 KB per workgroup; and the
+    step's mix of the two (12 B : 4 B per element)."""
+    import ctypes as C
+    import torch
+    lib = C.CDLL(os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2306_08881_amd",
+                              "libacp_probe.so"))
+    lib.acp_probe_rrw.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_int, C.c_void_p]
+    lib.acp_probe_w.argtypes = [C.c_void_p, C.c_int64, C.c_float, C.c_int, C.c_void_p]
+    m = torch.empty(PROBE_FLOATS, dtype=torch.float32, device=dev).normal_()
+    e = torch.zeros_like(m)
+    sp = stream.cuda_stream
+
+    def rate(fn, nbytes, reps=10):
+        for _ in range(3):
+            if fn() != 0:
+                raise RuntimeError("probe launch failed")
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return reps * nbytes / (a.elapsed_time(b) * 1e-3) / 1e9
+
+    rrw = {kb: rate(lambda: lib.acp_probe_rrw(m.data_ptr(), e.data_ptr(), PROBE_FLOATS, kb, sp), 12 * PROBE_FLOATS)
+           for kb in (4, 8, 16, 32)}
+    w = {kb: rate(lambda: lib.acp_probe_w(e.data_ptr(), PROBE_FLOATS, 1.0, kb, sp), 4 * PROBE_FLOATS)
+         for kb in (4, 8, 16, 32)}
+    del m, e
+    best_rrw, best_w = max(rrw.values()), max(w.values())
+    mix = 16.0 / (12.0 / best_rrw + 4.0 / best_w)
+    return {"compress_mix_gbs": round(best_rrw, 1), "write_gbs": round(best_w, 1), "step_mix_gbs": round(mix, 1),
+            "by_kb_per_workgroup": {"compress_mix": {k: round(v, 1) for k, v in rrw.items()},
+                                    "write": {k: round(v, 1) for k, v in w.items()}},
+            "probe": "k_probe_rrw (e = m + e in place) and k_probe_w (fill), 1 GiB arrays, nontemporal, "
+                     "best of 4-32 KB per workgroup and stream"}
+
+
+def compare_powersgd(acp, wl, shapes, gsets, fbuf, out, dev, stream, steps, warmup, step_no):
+    """ACP-SGD and Power-SGD (Algorithm 1, left, with error feedback) on the same workload and
+    resident gradients, all buckets per call: per step, events around the compress calls (ACP-SGD:
+    acp_compress_all; Power-SGD: acp_powersgd_p_all and acp_powersgd_q_all, the all-reduces being
+    the identity of one worker) and around the decompress call."""
+    import numpy as np
+    import torch
+    from paper_2306_08881_amd.acp import Acp
+
+    def phases(step_fn, n):
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n)]
+        torch.cuda.synchronize()
+        for e in ev:
+            step_fn(e)
+        torch.cuda.synchronize()
+        c = np.array([e[0].elapsed_time(e[1]) for e in ev])
+        d = np.array([e[1].elapsed_time(e[2]) for e in ev])
+        return float(c.mean()), float(d.mean()), float((c + d).mean())
+
+    def acp_step(e):
+        step_no[0] += 1
+        t = step_no[0]
+        e[0].record(stream)
+        acp.compress_all(t, gsets[t % 2], fbuf, stream=stream)
+        e[1].record(stream)
+        acp.decompress_all(t, fbuf, out, stream=stream)
+        e[2].record(stream)
+
+    if step_no[0] % 2:
+        acp_step([torch.cuda.Event() for _ in range(3)])
+    a_c, a_d, a_s = phases(acp_step, steps)
+
+    ps = Acp(shapes, wl.rank, seed=wl.seed, cap_bytes=wl.cap_bytes, device=dev, powersgd=True)
+    nb = ps.num_buckets()
+    info = [ps.bucket_info(b) for b in range(nb)]
+    pbuf = [torch.zeros(max(i[2], 4), dtype=torch.float32, device=dev) for i in info]
+    qbuf = [torch.zeros(max(i[3], 4), dtype=torch.float32, device=dev) for i in info]
+    k = [0]
+
+    def psgd_step(e):
+        k[0] += 1
+        t = k[0]
+        g = gsets[t % 2]
+        e[0].record(stream)
+        ps.powersgd_p_all(t, g, pbuf, stream=stream)
+        ps.powersgd_q_all(t, g, pbuf, qbuf, stream=stream)
+        e[1].record(stream)
+        ps.powersgd_decompress_all(t, qbuf, out, stream=stream)
+        e[2].record(stream)
+
+    for _ in range(warmup):
+        psgd_step([torch.cuda.Event() for _ in range(3)])
+    p_c, p_d, p_s = phases(psgd_step, steps)
+    ps.close()
+    return {"acp_compress_ms": round(a_c, 4), "acp_decompress_ms": round(a_d, 4), "acp_step_ms": round(a_s, 4),
+            "powersgd_compress_ms": round(p_c, 4), "powersgd_decompress_ms": round(p_d, 4),
+            "powersgd_step_ms": round(p_s, 4),
+            "compress_time_ratio": round(p_c / a_c, 3), "step_time_ratio": round(p_s / a_s, 3),
+            "bytes_per_compressed_element": {"acp": 16, "powersgd": 24},
+            "note": "events around each call group of every step (a pass of its own); Power-SGD's "
+                    "compress is both halves (P product, orthogonalisation of the all-reduced P, Q "
+                    "product), ACP-SGD's one product with the orthogonalisation of the reused factor"}
 
 
 def main():
@@ -187,6 +338,9 @@ def main():
                          "kernel kind); bucket: acp_compress / acp_decompress per bucket")
     ap.add_argument("--compare", action="store_true",
                     help="also time the other mode and report it in config")
+    ap.add_argument("--compare-powersgd", action="store_true",
+                    help="also run Power-SGD (Algorithm 1, left, with error feedback) on the same "
+                         "workload and report its compress and step times beside ACP-SGD's")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="summarise two rocprofv3 --pmc runs of this benchmark (FETCH_SIZE, then "
                          "WRITE_SIZE counter_collection.csv) and exit")
@@ -321,10 +475,12 @@ def main():
     dom = fams[1][0] if fams[1][0] in kern else max(kern, key=lambda k: kern[k]["ms_per_step"])
     dk = kern[dom]
     step_bytes, bp, bq, bd, nc, n1 = algorithmic_bytes(wl, wl.rank)
+    traffic, traffic_src = measured_traffic(wl.name, dom)
     gbs = step_bytes / (ms * 1e-3) / 1e9
     roof = {"bound": "hbm", "achieved": round(dk["gbs"], 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(dk["gbs"] / HBM_PEAK_GBS, 4),
-            "traffic": measured_traffic(wl.name, dom, dk["launches"]),
+            "traffic": traffic,
+            "traffic_source": traffic_src,
             "kernel": dom, "avg_launch_us": round(dk["avg_launch_us"], 3),
             "bytes_per_launch": round(dk["bytes_per_launch"], 1)}
     if wl.rank >= 8 and dom == fams[1][0]:
@@ -340,7 +496,7 @@ def main():
                          "unit": "TFLOP/s", "frac": round(tflops / MFMA_F32_PEAK_TFLOPS, 4),
                          "hbm_gbs": round(dk["gbs"], 2)})
     res = {
-        "metric": "ACP-SGD compress+decompress gradient GB/s and % HBM peak, BERT-large r=4",
+        "metric": metric_of(wl),
         "value": round(gbs, 2),
         "unit": "GB/s",
         "n_gpus": 1,
@@ -372,27 +528,15 @@ def main():
     if ms_other is not None:
         res["config"][f"ms_per_step_{other}_mode"] = round(ms_other, 4)
         res["config"][f"gbs_{other}_mode"] = round(step_bytes / (ms_other * 1e-3) / 1e9, 2)
-    # copy probe: device-to-device copy of 1 GiB, the achievable streaming ceiling on this GPU
-    src = torch.empty(1 << 28, dtype=torch.float32, device=dev).normal_()
-    dst = torch.empty_like(src)
-    for _ in range(3):
-        dst.copy_(src)
-    torch.cuda.synchronize()
-    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    c0.record(main)
-    for _ in range(10):
-        dst.copy_(src)
-    c1.record(main)
-    torch.cuda.synchronize()
-    copy_gbs = 10 * 2 * src.numel() * 4 / (c0.elapsed_time(c1) * 1e-3) / 1e9
-    res["config"]["copy_probe_gbs"] = round(copy_gbs, 1)
-    res["config"]["pct_of_copy_probe"] = round(100 * gbs / copy_gbs, 2)
-    del src, dst
-
+    if args.compare_powersgd:
+        res["config"]["powersgd"] = compare_powersgd(acp, wl, shapes, gsets, fbuf, out, dev, main, steps,
+                                                     args.warmup, step_no)
+    ceil = probe_ceilings(dev, main)
+    ceil["pct_of_step_mix"] = round(100 * gbs / ceil["step_mix_gbs"], 2)
+    res["config"]["ceilings"] = ceil
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl)
-    res["cpu_baseline_host"] = {"cpu": platform.processor() or platform.machine(),
-                                "affinity_cores": len(os.sched_getaffinity(0))}
+    res["cpu_baseline_host"] = host_info()
     print(json.dumps(res), flush=True)
 
 

@@ -1,4 +1,5 @@
-"""Build libacp.so (host planner + C ABI + gfx950 kernels) in-tree with hipcc.
+"""Build libacp.so (host planner + C ABI + gfx950 kernels) and the benchmark's streaming-probe
+library libacp_probe.so in-tree with hipcc.
 
 The planner and the initial-factor generator are plain C++ built with g++ (they use no
 HIP); the C ABI and the kernels are built with hipcc for gfx950.  Packed-fp32 instructions
@@ -19,6 +20,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libacp.so")
+PROBE_LIB = os.path.join(PKG, "libacp_probe.so")  # the benchmark's streaming ceilings
 ARCH = "gfx950"
 
 HOST_CXX = ["g++", "-O2", "-fPIC", "-std=c++17", "-Wall", "-Wextra", "-fno-fast-math",
@@ -62,6 +64,9 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     _run([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}"] + objs + ["-o", tmp])
     os.replace(tmp, LIB)
+    tmp = PROBE_LIB + ".tmp"
+    _run([HIPCC] + HIP_FLAGS + ["-shared", "-x", "hip", os.path.join(CSRC, "probe.hip"), "-o", tmp])
+    os.replace(tmp, PROBE_LIB)
     return LIB
 
 

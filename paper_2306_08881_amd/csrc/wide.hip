@@ -20,6 +20,8 @@
 // column drow(v, h) at step v, which lets the output of one MFMA feed the next directly.
 #include "device.hpp"
 
+#include <type_traits>
+
 namespace acp {
 
 namespace {
@@ -267,15 +269,20 @@ __global__ __launch_bounds__(kWideBlock, 2) void k_wqstep(KArgs a) {
   }
 }
 
-// Decompress: M_hat = A B^T / p over a tile (32-row block t.a, 1024-column group t.b), one wave
-// per workgroup walking the group's 32-column blocks.  Odd step: A = P_agg (factor buffer),
-// B = Qh; even step: A = Ph, B = Q_agg.  Lane l stores column c0 + l % 32 of rows
-// drow(v, l / 32): two 128-byte row segments per nontemporal store (plain stores leave M_hat's
-// lines dirty in the caches, and the next step's kernels pay for writing them back).  The next
-// block's B rows are requested before the current block's MFMAs.
+// Decompress from rank 64 (the four-wave kernel below takes the lower ranks): M_hat = A B^T / p
+// over a tile (32-row block t.a, 1024-column group t.b), one wave per workgroup walking the
+// group's 32-column blocks in bursts.  Odd step: A = P_agg (factor buffer), B = Qh; even step:
+// A = Ph, B = Q_agg.  A burst of BURST blocks is computed into one accumulator block each, then
+// stored row pair by row pair: lane l stores column c0 + l % 32 of rows drow(v, l / 32) for each
+// block of the burst in turn.  Stores are nontemporal (plain stores leave M_hat's lines dirty in
+// the caches, and the next step's kernels pay for writing them back).  Each block's B rows are
+// requested one block ahead of its MFMAs.
 template <int RK>
 __global__ __launch_bounds__(kWideBlock) void k_wrecon(KArgs a) {
   constexpr int KH = RK / 2;
+  constexpr int NB = kWideRCols / 32;                          // column blocks per tile
+  constexpr int BURST = RK <= 64 ? 2 : 1;  // blocks per burst (accumulators)
+  static_assert(NB % (2 * BURST) == 0, "pairs of bursts tile the column group");
   const Tile t = a.tiles[blockIdx.x];
   const bool odd = a.parity != 0;
   const MatDesc d = a.mats[t.idx];
@@ -295,27 +302,119 @@ __global__ __launch_bounds__(kWideBlock) void k_wrecon(KArgs a) {
   for (int s = 0; s < KH; ++s) av[s] *= a.inv_p;
   float* O = dst_of(a, d.bucket) + d.grad_off + r0 * m;
   const uint32_t row_bytes = u32(m) * 4u;
-  constexpr int NB = kWideRCols / 32;  // column blocks per tile
+  // one resource over the tile's rows: rows past `rows` fall outside it; columns past m are masked
+  const Rsrc Or = tile_rsrc(O, u32(rows) * row_bytes);
+  const uint32_t lane_row = u32(4 * h) * row_bytes;  // drow(v, h) = 8 (v / 4) + v % 4 + 4 h
   auto bcol = [&](int j) { return static_cast<int64_t>(t.b) * kWideRCols + j * 32; };
-  float bv[2][KH];  // B operand: B[c0 + l % 32][KH h + s], this block and the next
-  load_run<KH>(Br, bcol(0) + li < m ? u32((bcol(0) + li) * RK + KH * h) * 4u : kOut, b4, bv[0]);
+  auto boff = [&](int j) { return bcol(j) + li < m ? u32((bcol(j) + li) * RK + KH * h) * 4u : kOut; };
+  float bv[2][KH];  // B operand: B[c0 + l % 32][KH h + s] of block j in bv[j % 2], and the next
+  load_run<KH>(Br, boff(0), b4, bv[0]);
+  // one burst from block j0, whose parity P is a compile-time constant (register indices are)
+  auto burst = [&](int j0, auto parity) {
+    constexpr int P = decltype(parity)::value;
+    // the products: block j0 + jb into o[jb], the next block's B rows requested first
+    v16f o[BURST];
 #pragma unroll
-  for (int j = 0; j < NB; ++j) {
-    const int64_t c0 = bcol(j);
-    if (j + 1 < NB) {
-      const int64_t c1 = bcol(j + 1);
-      load_run<KH>(Br, c1 + li < m ? u32((c1 + li) * RK + KH * h) * 4u : kOut, b4, bv[(j + 1) & 1]);
+    for (int jb = 0; jb < BURST; ++jb) {
+      if (j0 + jb + 1 < NB) load_run<KH>(Br, boff(j0 + jb + 1), b4, bv[(P + jb + 1) & 1]);
+      o[jb] = zero16();
+#pragma unroll
+      for (int s = 0; s < KH; ++s) o[jb] = mfma(av[s], bv[(P + jb) & 1][s], o[jb]);
     }
-    if (c0 >= m) break;
-    const int64_t w = (m - c0) < 32 ? (m - c0) : 32;
+    // the stores: the lane's offset per block (kOut past m), to which each row adds a
+    // wave-uniform part; the empty asm keeps the compiler from carrying a running offset per row
+    const int64_t cb = bcol(j0);
+    const int wb = static_cast<int>((m - cb) < BURST * 32 ? (m - cb) : BURST * 32);
+    uint32_t base = lane_row + u32(cb + li) * 4u;
+    asm volatile("" : "+v"(base));
+    uint32_t bo[BURST];
+#pragma unroll
+    for (int jb = 0; jb < BURST; ++jb) bo[jb] = jb * 32 + li < wb ? base + u32(jb * 128) : kOut;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const uint32_t roff = u32(8 * (v >> 2) + (v & 3)) * row_bytes;
+#pragma unroll
+      for (int jb = 0; jb < BURST; ++jb) bst1_nt(Or, bo[jb] + roff, o[jb][v]);
+    }
+  };
+  // two bursts per iteration: the first starts on an even block, the second on block j0 + BURST
+  for (int j0 = 0; j0 < NB; j0 += 2 * BURST) {
+    if (bcol(j0) >= m) break;
+    burst(j0, std::integral_constant<int, 0>{});
+    if (bcol(j0 + BURST) >= m) break;
+    burst(j0 + BURST, std::integral_constant<int, BURST & 1>{});
+  }
+}
+
+// Decompress up to rank 32 with four waves per tile (32-row block t.a, 1024-column group t.b):
+// at step k the waves compute the 32 x 32 blocks 4k ... 4k + 3 (wave w block 4k + w), as the
+// one-wave kernel does, and put them in an LDS tile of 32 rows x 128 columns; then all 256
+// threads store that tile with 16-byte nontemporal stores, thread t taking the four columns
+// 4 (t % 32) ... of rows t / 32 + 8 i, so one store instruction writes 512 contiguous bytes of
+// each of two rows (the one-wave kernel's stores write 128 bytes of a row at a time).  Two LDS
+// tiles alternate, one barrier per step.  Rows past the tile fall outside the output resource;
+// columns past m are masked per float (16-byte stores need m and the tile start 16-byte aligned,
+// otherwise the same layout is stored float by float).
+template <int RK>
+__global__ __launch_bounds__(kBlock) void k_wrecon4w(KArgs a) {
+  constexpr int KH = RK / 2;
+  constexpr int LP = 132;  // LDS row pitch (floats): rows stay 16-byte aligned for the reads
+  const Tile t = a.tiles[blockIdx.x];
+  const bool odd = a.parity != 0;
+  const MatDesc d = a.mats[t.idx];
+  const int wave = __builtin_amdgcn_readfirstlane(tid() >> 6);
+  const int lane = tid() & 63, h = lane >> 5, li = lane & 31;
+  const int64_t n = d.n, m = d.m;
+  const int64_t r0 = static_cast<int64_t>(t.a) * 32;
+  const int rows = static_cast<int>((r0 + 32 < n) ? 32 : n - r0);
+  const float* agg = src_of(a, d.bucket);
+  const float* A = odd ? agg + d.fac_off_p : a.fac + d.ph_slot;
+  const float* B = odd ? a.fac + d.qh_slot : agg + d.fac_off_q;
+  const Rsrc Ar = tile_rsrc(A + r0 * RK, u32(rows) * RK * 4u);
+  const Rsrc Br = tile_rsrc(B, u32(m) * RK * 4u);
+  const bool a4 = aligned16(A), b4 = aligned16(B);
+  float av[KH];  // A operand: A[r0 + l % 32][KH h + s] / p
+  load_run<KH>(Ar, u32(li * RK + KH * h) * 4u, a4, av);
+#pragma unroll
+  for (int s = 0; s < KH; ++s) av[s] *= a.inv_p;
+  float* O = dst_of(a, d.bucket) + d.grad_off + r0 * m;
+  const uint32_t row_bytes = u32(m) * 4u;
+  const Rsrc Or = tile_rsrc(O, u32(rows) * row_bytes);
+  const bool vec = (m & 3) == 0 && aligned16(O);
+  const int64_t c0 = static_cast<int64_t>(t.b) * kWideRCols;
+  constexpr int NS = kWideRCols / 128;  // steps of four blocks
+  auto bcol = [&](int k) { return c0 + k * 128 + wave * 32; };  // the wave's block at step k
+  auto boff = [&](int k) { return bcol(k) + li < m ? u32((bcol(k) + li) * RK + KH * h) * 4u : kOut; };
+  __shared__ __attribute__((aligned(16))) float tile[2][32 * LP];
+  float bv[2][KH];
+  load_run<KH>(Br, boff(0), b4, bv[0]);
+  const int sc = tid() & 31, sr = tid() >> 5;  // store side: float4 column sc of rows sr + 8 i
+  for (int k = 0; k < NS; ++k) {
+    const int64_t cs = c0 + k * 128;  // the step's first column
+    if (cs >= m) break;
+    if (k + 1 < NS) load_run<KH>(Br, boff(k + 1), b4, bv[(k + 1) & 1]);
     v16f o = zero16();
 #pragma unroll
-    for (int s = 0; s < KH; ++s) o = mfma(av[s], bv[j & 1][s], o);
-    const Rsrc Or = tile_rsrc(O + c0, u32(rows - 1) * row_bytes + u32(w) * 4u);
-    const uint32_t coff = li < w ? u32(li) * 4u : kOut;
+    for (int s = 0; s < KH; ++s) o = mfma(av[s], bv[k & 1][s], o);
+    float* tl = tile[k & 1];
 #pragma unroll
-    for (int v = 0; v < 16; ++v)
-      bst1_nt(Or, coff == kOut ? kOut : u32(drow(v, h)) * row_bytes + coff, o[v]);
+    for (int v = 0; v < 16; ++v) tl[drow(v, h) * LP + wave * 32 + li] = o[v];
+    __syncthreads();
+    const int64_t col = cs + 4 * sc;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = sr + 8 * i;
+      const float4 q = *reinterpret_cast<const float4*>(tl + r * LP + 4 * sc);
+      const uint32_t off = u32(r) * row_bytes + u32(col) * 4u;
+      if (vec) {
+        bst4_nt(Or, col < m ? off : kOut, q);
+      } else {
+        bst1_nt(Or, col < m ? off : kOut, q.x);
+        bst1_nt(Or, col + 1 < m ? off + 4u : kOut, q.y);
+        bst1_nt(Or, col + 2 < m ? off + 8u : kOut, q.z);
+        bst1_nt(Or, col + 3 < m ? off + 12u : kOut, q.w);
+      }
+    }
   }
 }
 
@@ -654,7 +753,7 @@ hipError_t launch_wide_rank(const Launch& l, const KArgs& args, hipStream_t s) {
       case K_WFACT: hipLaunchKernelGGL(k_wfact<RK>, grid, dim3(kBlock), 0, s, args); break;
       case K_WPSTEP: hipLaunchKernelGGL(k_wpstep<RK>, grid, block, 0, s, args); break;
       case K_WQSTEP: hipLaunchKernelGGL(k_wqstep<RK>, grid, block, 0, s, args); break;
-      case K_WRECON: hipLaunchKernelGGL(k_wrecon<RK>, grid, block, 0, s, args); break;
+      case K_WRECON: hipLaunchKernelGGL(k_wrecon4w<RK>, grid, dim3(kBlock), 0, s, args); break;
       default: return hipErrorInvalidValue;
     }
   }

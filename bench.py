@@ -333,9 +333,11 @@ def main():
     ap.add_argument("--streams", type=int, default=4,
                     help="per-bucket mode: HIP streams the buckets are spread over (bucket b on "
                          "stream b %% streams)")
-    ap.add_argument("--mode", choices=["all", "bucket"], default="all",
+    ap.add_argument("--mode", choices=["all", "bucket", "graph"], default="all",
                     help="all: acp_compress_all / acp_decompress_all (every bucket in one launch per "
-                         "kernel kind); bucket: acp_compress / acp_decompress per bucket")
+                         "kernel kind); bucket: acp_compress / acp_decompress per bucket; graph: the "
+                         "all-bucket calls of one odd and one even step captured into two HIP graphs "
+                         "and replayed in turn")
     ap.add_argument("--compare", action="store_true",
                     help="also time the other mode and report it in config")
     ap.add_argument("--compare-powersgd", action="store_true",
@@ -392,14 +394,21 @@ def main():
           f"{nstreams} stream(s)", file=sys.stderr, flush=True)
 
     step_no = [0]
+    graphs = []     # [odd step, even step] after capture()
+    replayed = [0]  # replays so far: the context's step record does not count them
 
-    def one_step(mode):
+    def one_step(mode, stream=None):
+        if mode == "graph":
+            replayed[0] += 1
+            graphs[(replayed[0] - 1) % 2].replay()
+            return
         step_no[0] += 1
         t = step_no[0]
         g = gsets[t % 2]
         if mode == "all":
-            acp.compress_all(t, g, fbuf, stream=main)
-            acp.decompress_all(t, fbuf, out, stream=main)
+            st = main if stream is None else stream
+            acp.compress_all(t, g, fbuf, stream=st)
+            acp.decompress_all(t, fbuf, out, stream=st)
             return
         if nstreams > 1:
             fork = torch.cuda.Event()
@@ -441,11 +450,28 @@ def main():
         torch.cuda.synchronize()
         return np.array([e0.elapsed_time(e1) for e0, e1 in ev])
 
-    other = "bucket" if args.mode == "all" else "all"
-    for _ in range(args.warmup):
-        one_step(args.mode)
+    def capture():
+        """One odd and one even step of the all-bucket calls captured into HIP graphs (at steady
+        state: the step's kernel arguments then depend only on its parity).  Capture enqueues
+        nothing; replays of the pair, in turn, run the steps."""
+        assert step_no[0] % 2 == 0 and step_no[0] >= 2
+        side = torch.cuda.Stream(device=dev)
+        side.wait_stream(main)
+        for _ in range(2):
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr, stream=side):
+                one_step("all", stream=torch.cuda.current_stream())
+            graphs.append(gr)
+        main.wait_stream(side)
+
+    other = "bucket" if args.mode != "bucket" else "all"
+    eager = "all" if args.mode == "graph" else args.mode
+    for _ in range(max(args.warmup, 2)):
+        one_step(eager)
     if step_no[0] % 2:  # start every timed region on a P-step
-        one_step(args.mode)
+        one_step(eager)
+    if args.mode == "graph":
+        capture()
     steps = args.steps + (args.steps % 2)
     ms = timed(steps, args.mode)
     ms_other = timed(steps, other) if args.compare else None
@@ -464,7 +490,7 @@ def main():
     kern = {}
     for name, fam, _ in fams:
         acp.profile_start(fam, 64 * nb * steps)
-        timed(steps, args.mode)
+        timed(steps, eager)
         n, sec, by = acp.profile_stop()
         if n:
             kern[name] = {"launches": n, "avg_launch_us": sec / n * 1e6, "bytes_per_launch": by / n,
@@ -525,6 +551,10 @@ def main():
                                 "q_step_mean": round(float(t_step[1::2].mean()), 4)}
     res["config"]["mall_flushed"] = {"mean_ms": round(float(t_flush.mean()), 4),
                                      "gbs": round(step_bytes / (float(t_flush.mean()) * 1e-3) / 1e9, 2)}
+    if args.mode == "graph":
+        ms_eager = timed(steps, "all")
+        res["config"]["ms_per_step_all_mode_uncaptured"] = round(ms_eager, 4)
+        res["config"]["gbs_all_mode_uncaptured"] = round(step_bytes / (ms_eager * 1e-3) / 1e9, 2)
     if ms_other is not None:
         res["config"][f"ms_per_step_{other}_mode"] = round(ms_other, 4)
         res["config"][f"gbs_{other}_mode"] = round(step_bytes / (ms_other * 1e-3) / 1e9, 2)

@@ -217,6 +217,16 @@ acp_status acp_decompress(acp_ctx *ctx, int64_t step, int32_t b, const float *ag
  */
 acp_status acp_compress_all(acp_ctx *ctx, int64_t step, const float *const *grads,
                             float *const *factor_bufs, void *stream);
+/*
+ * HIP graphs: the compress and decompress calls enqueue kernels only (no memset, no allocation,
+ * no host synchronisation), with arguments that depend on the step only through its parity once
+ * every bucket has run two steps (with reuse; without it the draw is keyed by the step number).
+ * So one odd and one even step's calls may be captured (hipStreamBeginCapture on `stream`) and
+ * the two graphs replayed in turn for later steps, with the same buffers.  Capture enqueues
+ * nothing and advances the context's host-side step record by the captured steps; replays do not
+ * advance it, so calls made after replays see the parity of the last captured step: replay an
+ * even number of steps before calling the library again.
+ */
 acp_status acp_decompress_all(acp_ctx *ctx, int64_t step, const float *const *agg_factors,
                               float *const *outs, void *stream);
 

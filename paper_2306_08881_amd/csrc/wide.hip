@@ -60,23 +60,27 @@ __device__ inline void load_run(Rsrc r, uint32_t off, bool vec, float* out) {
 }
 __device__ inline bool aligned16(const float* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-// P-step over a tile of at most 32 rows and all m columns, one wave per workgroup, walking the
-// 32-column blocks in order.  Per block, lane l loads M and E for column c0 + l % 32 and rows
-// drow(v, l / 32) (coalesced 128-byte row segments), forms X = M + E, applies the correction
-// (F form) as an MFMA with D indexed (row, column) and stores X in that layout.  The product
-// P += X Qh reduces over columns, so it needs the row on the lane: X goes through a padded
-// 32 x 33 LDS tile (two of them, alternating) and comes back with lane l holding row l % 32 and
-// columns drow(v, l / 32), the A operand; the accumulator lane l holds P[r0 + drow(v, l / 32)]
-// [l % 32].  The next block's M, E and factor rows are requested before the current block's
-// MFMAs.
+// P-step over a tile of at most 32 rows and all m columns on four waves: wave w walks the
+// 32-column blocks w, w + 4, ... in step with the others (one barrier per block), so that the
+// workgroup reads 512 contiguous bytes of each of its rows at a time.  Per block, lane l loads M
+// and E for column c0 + l % 32 and rows drow(v, l / 32) (128-byte row segments), forms X = M + E,
+// applies the correction (F form) as an MFMA with D indexed (row, column) and stores X in that
+// layout.  The product P += X Qh reduces over columns, so it needs the row on the lane: X goes
+// through the wave's padded 32 x 33 LDS tile (two of them, alternating) and comes back with lane
+// l holding row l % 32 and columns drow(v, l / 32), the A operand; the accumulator lane l holds
+// the wave's share of P[r0 + drow(v, l / 32)][l % 32].  The four shares are added in wave order
+// through LDS at the end.  The next block's M and E are requested before the current block's
+// MFMAs, its factor rows after them.
 template <int RK>
-__global__ __launch_bounds__(kWideBlock, 2) void k_wpstep(KArgs a) {
+__global__ __launch_bounds__(kWideBlock * kWidePWaves, 2) void k_wpstep(KArgs a) {
   constexpr int KH = RK / 2;
   constexpr int NR = RK > 32 ? RK / 32 : 1;  // 32-rank blocks of P (one MFMA block each)
   constexpr int LD = 33;  // padded LDS row: the transposed reads hit 32 different banks
+  constexpr int CS = 32 * kWidePWaves;  // columns per step of the workgroup
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
-  const int lane = tid(), h = lane >> 5, li = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid() >> 6);
+  const int lane = tid() & 63, h = lane >> 5, li = lane & 31;
   const int64_t m = d.m, r0 = t.a;
   const int rows = t.b;
   const bool fform = deferred_of(a, d.bucket);
@@ -116,61 +120,62 @@ __global__ __launch_bounds__(kWideBlock, 2) void k_wpstep(KArgs a) {
         qb[kb][v] = bld1(Qhr, (col < m && rank < RK) ? u32(col * RK + rank) * 4u : kOut);
       }
   };
-  __shared__ float xt[2][32 * LD];
+  __shared__ float xt[kWidePWaves][2][32 * LD];
   float g[16], e[16], qa[KH], qb[NR][16];
-  load_block(0, g, e);
-  load_ops(0, qa, qb);
+  load_block(32 * wave, g, e);
+  load_ops(32 * wave, qa, qb);
 
   v16f p[NR];
 #pragma unroll
   for (int kb = 0; kb < NR; ++kb) p[kb] = zero16();
   int buf = 0;
-  for (int64_t c0 = 0; c0 < m; c0 += 32, buf ^= 1) {
+  // every wave takes the same number of steps (blocks past m: zero loads, dropped stores)
+  for (int64_t cs = 0; cs < m; cs += CS, buf ^= 1) {
+    const int64_t c0 = cs + 32 * wave;
     v16f x;
 #pragma unroll
     for (int v = 0; v < 16; ++v) x[v] = g[v] + e[v];
-    float ca[KH], cb[NR][16];
-#pragma unroll
-    for (int s = 0; s < KH; ++s) ca[s] = qa[s];
-#pragma unroll
-    for (int kb = 0; kb < NR; ++kb)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) cb[kb][v] = qb[kb][v];
     const uint32_t coff = c0 + li < m ? u32(c0 + li) * 4u : kOut;
-    load_block(c0 + 32, g, e);  // next block (past m: zeros, no traffic)
-    load_ops(c0 + 32, qa, qb);
+    load_block(c0 + CS, g, e);  // next block (past m: zeros, no traffic)
     if (fform) {  // X -= Ph Ql^T: A = -Ph (row, rank), B = Ql^T (rank, column)
 #pragma unroll
-      for (int s = 0; s < KH; ++s) x = mfma(pa[s], ca[s], x);
+      for (int s = 0; s < KH; ++s) x = mfma(pa[s], qa[s], x);
     }
+    float* tl = xt[wave][buf];
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       bst1_nt(E, coff == kOut ? kOut : u32(drow(v, h)) * row_bytes + coff, x[v]);
-      xt[buf][drow(v, h) * LD + li] = x[v];
+      tl[drow(v, h) * LD + li] = x[v];
     }
     __syncthreads();
 #pragma unroll
     for (int v = 0; v < 16; ++v) {  // P += X Qh: A = X (row, column), B = Qh (column, rank)
-      const float xa = xt[buf][li * LD + drow(v, h)];
+      const float xa = tl[li * LD + drow(v, h)];
 #pragma unroll
-      for (int kb = 0; kb < NR; ++kb) p[kb] = mfma(xa, cb[kb][v], p[kb]);
+      for (int kb = 0; kb < NR; ++kb) p[kb] = mfma(xa, qb[kb][v], p[kb]);
     }
+    load_ops(c0 + CS, qa, qb);
   }
 
+  // the waves' shares of P, added in wave order: entry (v, lane) of rank block kb
+  float* red = &xt[0][0][0];  // 4 x 1024 floats per rank block (the transposing tiles are free)
   float* P = dst_of(a, d.bucket) + d.fac_off_p;
   float* Pl = a.fac + d.pl_slot;
 #pragma unroll
   for (int kb = 0; kb < NR; ++kb) {
-    const int rank = kb * 32 + li;
-    if (rank < RK)
+    __syncthreads();  // the last products have read the tiles (and the previous block's sums)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = drow(v, h);
-        if (row < rows) {
-          P[(r0 + row) * RK + rank] = p[kb][v];
-          Pl[(r0 + row) * RK + rank] = p[kb][v];
-        }
+    for (int v = 0; v < 16; ++v) red[wave * 1024 + v * 64 + lane] = p[kb][v];
+    __syncthreads();
+    for (int en = tid(); en < 1024; en += kWideBlock * kWidePWaves) {
+      const float sum = ((red[en] + red[1024 + en]) + red[2048 + en]) + red[3072 + en];
+      const int v = en >> 6, ln = en & 63;
+      const int row = drow(v, ln >> 5), rank = kb * 32 + (ln & 31);
+      if (rank < RK && row < rows) {
+        P[(r0 + row) * RK + rank] = sum;
+        Pl[(r0 + row) * RK + rank] = sum;
       }
+    }
   }
 }
 
@@ -236,15 +241,9 @@ __global__ __launch_bounds__(kWideBlock, 2) void k_wqstep(KArgs a) {
     v16f x;
 #pragma unroll
     for (int v = 0; v < 16; ++v) x[v] = g[v] + e[v];
-    float ca[KH], cb[NR][16];
-#pragma unroll
-    for (int s = 0; s < KH; ++s) ca[s] = pa[s];
-#pragma unroll
-    for (int kb = 0; kb < NR; ++kb)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) cb[kb][v] = pb[kb][v];
+    float* ca = pa;
+    float (*cb)[16] = pb;
     load_block(rb + 32, g, e);  // next block (past the chunk: zeros, no traffic)
-    load_ops(rb + 32, pa, pb);
     if (xform) {  // F -= Pl Qh^T: A = -Pl (row, rank), B = Qh^T (rank, column)
 #pragma unroll
       for (int s = 0; s < KH; ++s) x = mfma(-ca[s], qv[s], x);
@@ -256,6 +255,7 @@ __global__ __launch_bounds__(kWideBlock, 2) void k_wqstep(KArgs a) {
     for (int v = 0; v < 16; ++v)  // Q += F^T Ph: A = F^T, B = Ph
 #pragma unroll
       for (int kb = 0; kb < NR; ++kb) q[kb] = mfma(x[v], cb[kb][v], q[kb]);
+    load_ops(rb + 32, pa, pb);
   }
   const int64_t ncb = (m + d.q_cb - 1) / d.q_cb;
   const int64_t stride = ncb * d.q_cb * RK;  // one row chunk of partials
@@ -751,7 +751,7 @@ hipError_t launch_wide_rank(const Launch& l, const KArgs& args, hipStream_t s) {
     const dim3 block(kWideBlock);
     switch (l.kernel) {
       case K_WFACT: hipLaunchKernelGGL(k_wfact<RK>, grid, dim3(kBlock), 0, s, args); break;
-      case K_WPSTEP: hipLaunchKernelGGL(k_wpstep<RK>, grid, block, 0, s, args); break;
+      case K_WPSTEP: hipLaunchKernelGGL(k_wpstep<RK>, grid, dim3(kWideBlock * kWidePWaves), 0, s, args); break;
       case K_WQSTEP: hipLaunchKernelGGL(k_wqstep<RK>, grid, block, 0, s, args); break;
       case K_WRECON: hipLaunchKernelGGL(k_wrecon4w<RK>, grid, dim3(kBlock), 0, s, args); break;
       default: return hipErrorInvalidValue;

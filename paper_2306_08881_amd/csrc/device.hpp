@@ -178,14 +178,15 @@ __device__ void vec_tile(const KArgs& a, const Tile& t, bool compress) {
 // residual norm is at most tau times the column norm.
 
 typedef double v4d __attribute__((ext_vector_type(4)));
-template <int RK, bool DIAG>
+template <int RK, bool DIAG, int NB = 4>
 __device__ void gram_band(const float* X, int64_t r0, int64_t r1, float* copy, int I, int J, int nw, int w,
-                          v4d (&acc)[4][4]);
+                          v4d (&acc)[NB][NB]);
 
 // Gram of rows [r0, r1) of X (row-major, RK columns) into shared G (RK x RK), by the whole
 // workgroup, in a fixed order; the rows are also copied to `copy` when it is set.
 template <int RK>
 __device__ void gram_rows(const float* X, int64_t r0, int64_t r1, double* G, float* copy) {
+  static_assert(RK <= 8 || RK == 16 || RK == 32 || RK == 64, "from kBlockedRank on gram_blocked forms the Gram");
   if constexpr (RK <= 8) {
     constexpr int NT = RK * (RK + 1) / 2;
     constexpr int PER = 8;  // rows per thread per pass, loaded together
@@ -236,19 +237,20 @@ __device__ void gram_rows(const float* X, int64_t r0, int64_t r1, double* G, flo
       G[j * RK + i] = s;
     }
     __syncthreads();
-  } else if constexpr (RK == 64) {
-    // on the fp64 matrix cores (gram_band): the four waves take interleaved steps of 16 rows,
-    // each forming the products a <= b of the one band block; their sums are added into G in
-    // wave order, then the blocks a > b mirrored
+  } else if constexpr (RK == 16 || RK == 32 || RK == 64) {
+    // on the fp64 matrix cores (gram_band, one band of all RK columns): the four waves take
+    // interleaved steps of 16 rows, each forming the products a <= b of the band's 16-column
+    // blocks; their sums are added into G in wave order, then the blocks a > b mirrored
+    constexpr int NB = RK / 16;
     const int w = tid() / kWave, lane = tid() % kWave, i = lane % 16, k = lane / 16;
-    v4d acc[4][4];
-    gram_band<RK, true>(X, r0, r1, copy, 0, 0, kBlock / kWave, w, acc);
+    v4d acc[NB][NB];
+    gram_band<RK, true, NB>(X, r0, r1, copy, 0, 0, kBlock / kWave, w, acc);
     for (int q = 0; q < kBlock / kWave; ++q) {
       if (w == q)
 #pragma unroll
-        for (int a = 0; a < 4; ++a)
+        for (int a = 0; a < NB; ++a)
 #pragma unroll
-          for (int b = a; b < 4; ++b)
+          for (int b = a; b < NB; ++b)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
               double& g = G[(16 * a + 4 * v + k) * RK + 16 * b + i];
@@ -259,69 +261,6 @@ __device__ void gram_rows(const float* X, int64_t r0, int64_t r1, double* G, flo
     for (int e = tid(); e < RK * RK; e += kBlock) {
       const int r = e / RK, c = e % RK;
       if (r / 16 > c / 16) G[e] = G[c * RK + r];
-    }
-    __syncthreads();
-  } else {
-    // G in 4 x 4 blocks: thread t owns block t % NB of the NB = (RK / 4)^2 blocks for the rows
-    // of phase t / NB (rows congruent to the phase modulo NP = 256 / NB within a chunk); the
-    // chunk's rows sit in LDS as doubles.  The phases' sums are added in phase order.
-    constexpr int CH = 64;
-    constexpr int NB4 = RK / 4, NB = NB4 * NB4, NP = kBlock / NB;
-    static_assert(NB * NP == kBlock, "blocks times phases must fill the workgroup");
-    constexpr int PT = CH * RK / kBlock;  // chunk elements per thread
-    constexpr int SH = (CH * RK > NP * RK * RK) ? CH * RK : NP * RK * RK;
-    __shared__ __align__(16) double sh[SH];  // chunk rows, then the phases' partial sums
-    const int b = tid() % NB, ph = tid() / NB;
-    const int bi = 4 * (b / NB4), bj = 4 * (b % NB4);
-    double acc[4][4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) acc[u][v] = 0.0;
-    // the next chunk is requested before the current one's products (rows past r1 read zero)
-    const int64_t end = r1 * RK;
-    float nx[PT];
-    auto fetch = [&](int64_t c0) {
-#pragma unroll
-      for (int k = 0; k < PT; ++k) {
-        const int64_t e = c0 * RK + tid() + k * kBlock;
-        nx[k] = e < end ? X[e] : 0.f;
-      }
-    };
-    fetch(r0);
-    for (int64_t c0 = r0; c0 < r1; c0 += CH) {
-      const int cn = static_cast<int>((r1 - c0) < CH ? (r1 - c0) : CH);
-#pragma unroll
-      for (int k = 0; k < PT; ++k) {
-        const int e = tid() + k * kBlock;
-        sh[e] = static_cast<double>(nx[k]);
-        if (copy && c0 * RK + e < end) copy[c0 * RK + e] = nx[k];
-      }
-      __syncthreads();
-      fetch(c0 + CH);
-      for (int rr = ph; rr < cn; rr += NP) {
-        double xi[4], xj[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          xi[u] = sh[rr * RK + bi + u];
-          xj[u] = sh[rr * RK + bj + u];
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-          for (int v = 0; v < 4; ++v) acc[u][v] = fma(xi[u], xj[v], acc[u][v]);
-      }
-      __syncthreads();
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) sh[ph * RK * RK + (bi + u) * RK + bj + v] = acc[u][v];
-    __syncthreads();
-    for (int e = tid(); e < RK * RK; e += kBlock) {
-      double g = sh[e];
-      for (int q = 1; q < NP; ++q) g += sh[q * RK * RK + e];
-      G[e] = g;
     }
     __syncthreads();
   }
@@ -393,17 +332,18 @@ __device__ void cholesky_w(const double* G, double* w_out) {
 // steps of 16, of which the wave takes steps w, w + nw, ...; each product adds them in increasing
 // groups of four, and the wave's next step is requested before the current one's products.  A
 // diagonal block also copies its steps' rows of the band to `copy` when set.
-template <int RK, bool DIAG>
+template <int RK, bool DIAG, int NB>
 __device__ void gram_band(const float* X, int64_t r0, int64_t r1, float* copy, int I, int J, int nw, int w,
-                          v4d (&acc)[4][4]) {
+                          v4d (&acc)[NB][NB]) {
   constexpr int G = 4;  // groups of four rows per step
+  constexpr int BW = 16 * NB;  // band width (columns)
   const int lane = tid() % kWave, i = lane % 16, k = lane / 16;
-  const float* xa = X + 64 * I + i;
-  const float* xb = X + 64 * J + i;
+  const float* xa = X + BW * I + i;
+  const float* xb = X + BW * J + i;
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < NB; ++a)
 #pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = v4d{0.0, 0.0, 0.0, 0.0};
+    for (int b = 0; b < NB; ++b) acc[a][b] = v4d{0.0, 0.0, 0.0, 0.0};
   // rows past the slice read its last row (no branch around the loads, so the wait for a step's
   // rows leaves the next step's requests in flight); the A operand of those rows is zeroed
   auto row_of = [&](int64_t g0, int s) {
@@ -411,14 +351,14 @@ __device__ void gram_band(const float* X, int64_t r0, int64_t r1, float* copy, i
     return row < r1 ? row : r1 - 1;
   };
   // two register buffers of G groups, filled and consumed in turn
-  typedef float Buf[G][4];
+  typedef float Buf[G][NB];
   auto fetch = [&](int64_t g0, Buf& ba, Buf& bb) {
 #pragma unroll
     for (int s = 0; s < G; ++s) {
       const float* pa = xa + row_of(g0, s) * RK;
       const float* pb = xb + row_of(g0, s) * RK;
 #pragma unroll
-      for (int a = 0; a < 4; ++a) {
+      for (int a = 0; a < NB; ++a) {
         ba[s][a] = pa[16 * a];
         if (!DIAG) bb[s][a] = pb[16 * a];
       }
@@ -429,7 +369,7 @@ __device__ void gram_band(const float* X, int64_t r0, int64_t r1, float* copy, i
 #pragma unroll
     for (int s = 0; s < G; ++s)
 #pragma unroll
-      for (int a = 0; a < 4; ++a) {
+      for (int a = 0; a < NB; ++a) {
         asm volatile("" : "+v"(ba[s][a]));
         if (!DIAG) asm volatile("" : "+v"(bb[s][a]));
       }
@@ -438,20 +378,20 @@ __device__ void gram_band(const float* X, int64_t r0, int64_t r1, float* copy, i
 #pragma unroll
       for (int s = 0; s < G; ++s)
 #pragma unroll
-        for (int a = 0; a < 4; ++a) copy[row_of(g0, s) * RK + 64 * I + 16 * a + i] = ba[s][a];
+        for (int a = 0; a < NB; ++a) copy[row_of(g0, s) * RK + BW * I + 16 * a + i] = ba[s][a];
 #pragma unroll
     for (int s = 0; s < G; ++s) {
       const bool in = g0 + 4 * s + k < r1;
-      double xa4[4], xb4[4];
+      double xa4[NB], xb4[NB];
 #pragma unroll
-      for (int a = 0; a < 4; ++a) {
+      for (int a = 0; a < NB; ++a) {
         xa4[a] = in ? static_cast<double>(ba[s][a]) : 0.0;
         xb4[a] = static_cast<double>(DIAG ? ba[s][a] : bb[s][a]);
       }
 #pragma unroll
-      for (int a = 0; a < 4; ++a)
+      for (int a = 0; a < NB; ++a)
 #pragma unroll
-        for (int b = 0; b < 4; ++b)
+        for (int b = 0; b < NB; ++b)
           if (!DIAG || a <= b) acc[a][b] = __builtin_amdgcn_mfma_f64_16x16x4f64(xa4[a], xb4[b], acc[a][b], 0, 0, 0);
     }
   };

@@ -573,9 +573,9 @@ __global__ __launch_bounds__(kBlock, RK >= kApplyMfmaRank ? 2 : 1) void k_apply(
   if constexpr (RK >= kApplyMfmaRank) {
     apply_mfma<RK>(a, t, d);
   } else {
-    __shared__ double W[RK * RK];
-    for (int e = tid(); e < RK * RK; e += kBlock) W[e] = a.w[d.w_slot + e];
-    __syncthreads();
+    // W (upper triangular) is read at wave-uniform addresses, through the scalar cache into
+    // SGPRs: every product takes its W entry from there rather than from an LDS broadcast
+    const double* __restrict__ W = a.w + d.w_slot;
     {
       const int64_t row = static_cast<int64_t>(t.a) + tid();
       if (tid() >= t.b) return;
@@ -597,13 +597,17 @@ __global__ __launch_bounds__(kBlock, RK >= kApplyMfmaRank ? 2 : 1) void k_apply(
 #pragma unroll
         for (int l = 0; l < RK; ++l) x[l] = static_cast<double>(X[l]);
       }
+      // y[k] = sum over l <= k of x[l] W[l][k], added in increasing l; by rows of W, each
+      // row's entries loaded together
+      double acc[RK];
 #pragma unroll
-      for (int k = 0; k < RK; ++k) {
-        double s = 0.0;
+      for (int k = 0; k < RK; ++k) acc[k] = 0.0;
 #pragma unroll
-        for (int l = 0; l <= k; ++l) s = fma(x[l], W[l * RK + k], s);
-        y[k] = static_cast<float>(s);
-      }
+      for (int l = 0; l < RK; ++l)
+#pragma unroll
+        for (int k = l; k < RK; ++k) acc[k] = fma(x[l], W[l * RK + k], acc[k]);
+#pragma unroll
+      for (int k = 0; k < RK; ++k) y[k] = static_cast<float>(acc[k]);
       if constexpr (RK % 4 == 0) {
 #pragma unroll
         for (int k = 0; k < RK; k += 4)

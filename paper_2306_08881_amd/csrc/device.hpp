@@ -304,23 +304,29 @@ __device__ void cholesky_w(const double* G, double* w_out) {
       for (int i = k + 1; i < RK; ++i) g[i] -= readlane_d(rkj, i) * rkj;
   }
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  // W = R^-1 by rows (lane = row a), right-looking: once W[a][i] is final it is subtracted
+  // from every later column at once, so the loads of R and the products of a step are
+  // independent and only the divisions form a chain.  W[a][c] = (delta_ac - sum over i < c of
+  // R[i][c] W[a][i]) / R[c][c], the sum in increasing i (the terms i < a are zero); zero for a
+  // dropped pivot c or c < a.
   const int arow = j;
   if (arow < RK) {
-    double wr[RK];
+    double acc[RK];
 #pragma unroll
-    for (int c = 0; c < RK; ++c) {
-      double v = 0.0;
-      if (drop[c] == 0 && arow <= c) {
-        v = (arow == c) ? 1.0 : 0.0;
+    for (int c = 0; c < RK; ++c) acc[c] = (arow == c) ? 1.0 : 0.0;
 #pragma unroll
-        for (int i = 0; i < c; ++i)
-          if (i >= arow) v -= R[i * RK + c] * wr[i];
-        v /= R[c * RK + c];
-      }
-      wr[c] = v;
+    for (int i = 0; i < RK; ++i) {
+      asm volatile("" ::: "memory");  // this step's loads of R only (the registers stay few)
+      // no branch: a dropped pivot divides by one and is then discarded
+      const bool use = drop[i] == 0 && arow <= i;
+      const double q = acc[i] / (use ? R[i * RK + i] : 1.0);
+      const double wi = use ? q : 0.0;
+      acc[i] = wi;
+#pragma unroll
+      for (int c = i + 1; c < RK; ++c) acc[c] -= R[i * RK + c] * wi;
     }
 #pragma unroll
-    for (int c = 0; c < RK; ++c) w_out[arow * RK + c] = wr[c];
+    for (int c = 0; c < RK; ++c) w_out[arow * RK + c] = acc[c];
   }
 }
 

@@ -153,9 +153,10 @@ constexpr int32_t kBlockedRank = 128;  // ranks whose W K_CHOL forms from Gram p
 constexpr int32_t kSplitRank = 64;
 constexpr int32_t kSplitReconRank = 256;
 constexpr int32_t kCholBlockRank = 256;
-// ranks whose orthogonal factor X W is formed on the fp64 matrix cores (one 64-column block per
-// tile; below kBlockedRank a factor has one such block)
-constexpr int32_t kApplyMfmaRank = 64;
+// ranks whose orthogonal factor X W is formed on the fp64 matrix cores (one block of
+// min(r, 64) columns per tile; below kBlockedRank a factor has one such block)
+constexpr int32_t kApplyMfmaRank = 32;
+constexpr int32_t apply_blocks(int32_t r) { return r >= 64 ? r / 64 : 1; }  // column blocks of X W
 // tiles that share one slice's Gram from kBlockedRank on: the (r / 64)(r / 64 + 1) / 2 blocks of
 // 64 x 64 on and above the diagonal, one per wave of a four-wave tile
 constexpr int32_t gram_parts(int32_t r) {

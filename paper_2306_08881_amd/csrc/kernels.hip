@@ -455,37 +455,49 @@ __global__ __launch_bounds__(kBlock) void k_chol(KArgs a) {
       cholesky_w_blocked<RK>(Gs, a.w + d.w_slot);
     }
   } else {
-    // eight slices' partials requested together, each entry added in slice order
-    for (int e = tid(); e < RK * RK; e += kBlock) {
-      double s = 0.0;
-      int sl = 0;
-      for (; sl + 8 <= t.b; sl += 8) {
-        double v[8];
+    // each entry added in slice order; per round, eight slices of all the thread's entries are
+    // requested together (one round trip per eight slices)
+    constexpr int EPT = (RK * RK + kBlock - 1) / kBlock;  // entries per thread
+    double acc[EPT];
 #pragma unroll
-        for (int w = 0; w < 8; ++w) v[w] = gp[static_cast<int64_t>(sl + w) * RK * RK + e];
+    for (int q = 0; q < EPT; ++q) acc[q] = 0.0;
+    for (int sl = 0; sl < t.b; sl += 8) {
+      double v[EPT][8];
 #pragma unroll
-        for (int w = 0; w < 8; ++w) s += v[w];
+      for (int q = 0; q < EPT; ++q) {
+        const int e = tid() + q * kBlock;
+#pragma unroll
+        for (int w = 0; w < 8; ++w)
+          v[q][w] = (e < RK * RK && sl + w < t.b) ? gp[static_cast<int64_t>(sl + w) * RK * RK + e] : 0.0;
       }
-      for (; sl < t.b; ++sl) s += gp[static_cast<int64_t>(sl) * RK * RK + e];
-      Gs[e] = s;
+#pragma unroll
+      for (int q = 0; q < EPT; ++q)
+#pragma unroll
+        for (int w = 0; w < 8; ++w)
+          if (sl + w < t.b) acc[q] += v[q][w];
     }
+#pragma unroll
+    for (int q = 0; q < EPT; ++q)
+      if (tid() + q * kBlock < RK * RK) Gs[tid() + q * kBlock] = acc[q];
     __syncthreads();
     cholesky_w<RK>(Gs, a.w + d.w_slot);
   }
 }
 
-// Xh = X W from kApplyMfmaRank on, for rows [t.a, t.a + rows) and the 64 columns c0 = 64 cb ... of
-// Xh (t.b = rows | cb << 16), on the fp64 matrix cores: wave w forms rows 64 w ... + 63 as 4 x 4
-// products of 16 x 16 (v_mfma_f64_16x16x4f64; operand entry [i][k] on lane i + 16 k, result
-// entry [4 v + l / 16][l % 16] in item v of lane l), over the ranks 0 ... c0 + 63 in steps of
-// 16.  W is upper triangular: later ranks add zero, and so do the ranks from c0 + 16 (b + 1) on
+// Xh = X W from kApplyMfmaRank on, for rows [t.a, t.a + rows) and the BW = min(r, 64) columns
+// c0 = BW cb ... of Xh (t.b = rows | cb << 16), on the fp64 matrix cores: wave w forms rows
+// 64 w ... + 63 as 4 x BW / 16 products of 16 x 16 (v_mfma_f64_16x16x4f64; operand entry
+// [i][k] on lane i + 16 k, result entry [4 v + l / 16][l % 16] in item v of lane l), over the
+// ranks 0 ... c0 + BW - 1 in steps of 16.  W is upper triangular: later ranks add zero, and so do the ranks from c0 + 16 (b + 1) on
 // for the columns c0 + 16 b ... + 15, whose products are skipped.  Within a step, lane i + 16 k
 // holds the four ranks 4 k ... + 3 of its row as one 16-byte word, and product s of the step
 // takes rank 4 k + s from lane i + 16 k in both operands, so every rank enters once.  The next
 // step's rows of X are requested before the current step's products.
 template <int RK>
 __device__ void apply_mfma(const KArgs& a, const Tile& t, const MatDesc& d) {
-  const int rows = t.b & 0xffff, c0 = 64 * (t.b >> 16);
+  constexpr int CB = RK >= 64 ? 4 : RK / 16;  // 16-column groups of the block
+  static_assert(CB % 2 == 0, "the 16-rank steps are taken in pairs");
+  const int rows = t.b & 0xffff, c0 = 16 * CB * (t.b >> 16);
   const int lane = tid() % kWave, i = lane % 16, k = lane / 16;
   const int rb = 64 * (tid() / kWave);
   if (rb >= rows) return;
@@ -501,11 +513,11 @@ __device__ void apply_mfma(const KArgs& a, const Tile& t, const MatDesc& d) {
     xr[ra] = X + (static_cast<int64_t>(t.a) + (r < rows ? r : rows - 1)) * RK + 4 * k;
   }
   const double* wr = W + static_cast<int64_t>(4 * k) * RK + c0 + i;
-  v4d acc[4][4];
+  v4d acc[4][CB];
 #pragma unroll
   for (int ra = 0; ra < 4; ++ra)
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb) acc[ra][cb] = v4d{0.0, 0.0, 0.0, 0.0};
+    for (int cb = 0; cb < CB; ++cb) acc[ra][cb] = v4d{0.0, 0.0, 0.0, 0.0};
   // per step the W rows (from L2, where every tile of the matrix reads them) are requested
   // first, then the next step's X rows (from HBM), so that the wait for the former leaves the
   // latter in flight
@@ -517,11 +529,11 @@ __device__ void apply_mfma(const KArgs& a, const Tile& t, const MatDesc& d) {
   auto step = [&](int k0, XBuf& b, int k1, XBuf& nb) {
     // column group cb of the block takes ranks up to c0 + 16 cb + 15 only (W is upper triangular)
     const int kz = k0 - c0;
-    double w[4][4];  // [s][cb]
+    double w[4][CB];  // [s][cb]
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb) w[s][cb] = wr[static_cast<int64_t>(k0 + s) * RK + 16 * cb];
+      for (int cb = 0; cb < CB; ++cb) w[s][cb] = wr[static_cast<int64_t>(k0 + s) * RK + 16 * cb];
     __builtin_amdgcn_sched_barrier(0);  // in this order
     fetch_x(k1, nb);
     __builtin_amdgcn_sched_barrier(0);
@@ -538,16 +550,16 @@ __device__ void apply_mfma(const KArgs& a, const Tile& t, const MatDesc& d) {
         xa[ra] = static_cast<double>(s == 0 ? v.x : s == 1 ? v.y : s == 2 ? v.z : v.w);
       }
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb)
+      for (int cb = 0; cb < CB; ++cb)
         if (kz <= 16 * cb)
 #pragma unroll
           for (int ra = 0; ra < 4; ++ra)
             acc[ra][cb] = __builtin_amdgcn_mfma_f64_16x16x4f64(xa[ra], w[s][cb], acc[ra][cb], 0, 0, 0);
     }
   };
-  // c0 + 64 ranks: an even number of 16-rank steps, taken in pairs; past the last pair the X
+  // c0 + BW ranks: an even number of 16-rank steps, taken in pairs; past the last pair the X
   // request repeats the last step's ranks, unused (no branch around it)
-  const int kend = c0 + 64;
+  const int kend = c0 + 16 * CB;
   XBuf x0, x1;
   fetch_x(0, x0);
   for (int k0 = 0; k0 < kend; k0 += 32) {
@@ -561,7 +573,7 @@ __device__ void apply_mfma(const KArgs& a, const Tile& t, const MatDesc& d) {
       const int r = rb + 16 * ra + 4 * v + k;
       if (r < rows)
 #pragma unroll
-        for (int cb = 0; cb < 4; ++cb)
+        for (int cb = 0; cb < CB; ++cb)
           Y[(static_cast<int64_t>(t.a) + r) * RK + c0 + 16 * cb + i] = static_cast<float>(acc[ra][cb][v]);
     }
 }
@@ -1460,18 +1472,19 @@ __global__ __launch_bounds__(kBlock) void k_qfin(KArgs a) {
       e[k] = static_cast<int64_t>(t.a) * ne + tid() + k * kBlock;
       s[k] = 0.f;
     }
-    for (int ch = 0; ch < d.q_chunks; ch += 2) {
-      float v[EPT][2];
+    {
+      // all (at most 8) chunks of the thread's entries requested together, added in chunk order
+      float v[EPT][8];
 #pragma unroll
       for (int k = 0; k < EPT; ++k)
 #pragma unroll
-        for (int u = 0; u < 2; ++u)
-          v[k][u] = (e[k] < m * RK && ch + u < d.q_chunks) ? part[(ch + u) * stride + e[k]] : 0.f;
+        for (int u = 0; u < 8; ++u)
+          v[k][u] = (e[k] < m * RK && u < d.q_chunks) ? part[u * stride + e[k]] : 0.f;
 #pragma unroll
-      for (int k = 0; k < EPT; ++k) {
-        s[k] += v[k][0];
-        if (ch + 1 < d.q_chunks) s[k] += v[k][1];
-      }
+      for (int k = 0; k < EPT; ++k)
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (u < d.q_chunks) s[k] += v[k][u];
     }
 #pragma unroll
     for (int k = 0; k < EPT; ++k)

@@ -295,10 +295,10 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
                                   static_cast<int32_t>(std::min(kVecChunk, n - s))});
     }
   };
-  // orthogonalisation tiles of kApplyRows factor rows; from kApplyMfmaRank on one per 64-column
+  // orthogonalisation tiles of kApplyRows factor rows; from kApplyMfmaRank on one per column
   // block of Xh as well (b = rows | block << 16)
   auto apply_tiles = [&](const std::vector<int32_t>& mats, bool q) {
-    const int32_t ncb = r >= kApplyMfmaRank ? static_cast<int32_t>(r / 64) : 1;
+    const int32_t ncb = r >= kApplyMfmaRank ? apply_blocks(static_cast<int32_t>(r)) : 1;
     for (int32_t mi : mats) {
       const int64_t rows = q ? plan.mats[mi].m : plan.mats[mi].n;
       for (int64_t s = 0; s < rows; s += kApplyRows)
@@ -789,8 +789,8 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         const double cols = std::min<double>(kWideRCols, m - double(kWideRCols) * t.b);
         return rows * cols * 4.0 + (t.b == 0 ? rows * rr * 4.0 : 0.0) + (t.a == 0 ? cols * rr * 4.0 : 0.0);
       }
-      case K_APPLY:  // from kApplyMfmaRank on a tile covers one of r / 64 column blocks
-        return (t.b & 0xffff) * rr * 8.0 / (r >= kApplyMfmaRank ? rr / 64.0 : 1.0);
+      case K_APPLY:  // from kApplyMfmaRank on a tile covers one of apply_blocks(r) column blocks
+        return (t.b & 0xffff) * rr * 8.0 / apply_blocks(static_cast<int32_t>(r));
       case K_FACT:
         if (t.a >> 16) return 0.0;
         return std::min<double>(d.fact_rows, (l.variant & 1 ? m : n) - double(t.a & 0xffff) * d.fact_rows) * rr *

@@ -1454,6 +1454,10 @@ __global__ __launch_bounds__(kBlock) void k_qstep(KArgs a) {
 template <int RK>
 __global__ __launch_bounds__(kBlock) void k_qfin(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
+  if (t.kind == T_VEC) {  // from kWideRank on the finish launch packs the raw vectors too
+    vec_tile(a, t, true);
+    return;
+  }
   const MatDesc d = a.mats[t.idx];
   const int64_t m = d.m;
   const int64_t ncb = (m + d.q_cb - 1) / d.q_cb;

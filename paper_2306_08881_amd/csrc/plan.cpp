@@ -400,7 +400,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   };
 
   // Q-step finish tiles: entry blocks of each matrix's column blocks
-  auto qfin_launch = [&](const BucketPlan& bk, std::vector<Launch>& L) {
+  auto qfin_launch = [&](const BucketPlan& bk, std::vector<Launch>& L, bool with_vecs) {
     Launch l = sink.begin(K_QFIN, 0);
     for (int32_t mi : bk.mats) {
       const MatDesc& d = plan.mats[mi];
@@ -409,6 +409,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       for (int64_t eb = 0; eb < nblk; ++eb)
         plan.tiles.push_back(Tile{T_QTILE, mi, static_cast<int32_t>(eb), 0});
     }
+    if (with_vecs) vec_tiles(bk);
     sink.end(l, L);
   };
   auto emat_launch = [&](BucketPlan& bk) {
@@ -418,8 +419,8 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
   };
   // ranks 8..32: every matrix of the bucket takes the MFMA kernels
   auto wide_lists = [&](BucketPlan& bk) {
-    // The MFMA kernels run one wave per workgroup over matrix tiles only; raw vectors and
-    // factor tiles (which need whole workgroups) go to launches of their own.
+    // The compress kernels take matrix tiles, and the raw vectors ride along in the P-step and
+    // Q-finish launches; factor tiles go to launches of their own.
     // -- P-step (odd t): Qh = Q W, then 32-row tiles
     {
       std::vector<Launch>& L = bk.compress[1];
@@ -428,9 +429,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       sink.end(l, L);
       l = sink.begin(K_WPSTEP, 0);
       for (int32_t mi : bk.mats) row_tiles(mi, 32);
-      sink.end(l, L);
-      l = sink.begin(K_VEC, 1);
-      vec_tiles(bk);
+      vec_tiles(bk);  // packed by the P-step launch's workgroups
       sink.end(l, L);
     }
     // -- Q-step (even t): Ph = P W, (row chunk, 32-column block) tiles, vectors, finish
@@ -447,10 +446,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
           for (int32_t cb = 0; cb < ncb; ++cb) plan.tiles.push_back(Tile{T_QTILE, mi, c, cb});
       }
       sink.end(l, L);
-      l = sink.begin(K_VEC, 0);
-      vec_tiles(bk);
-      sink.end(l, L);
-      qfin_launch(bk, L);
+      qfin_launch(bk, L, true);  // the vectors packed by the finish launch's workgroups
     }
     // -- decompress: (32-row block, 512-column group) tiles, then factor tiles and vectors
     for (int32_t par = 0; par < 2; ++par) {
@@ -629,7 +625,7 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
         if (any && !vec_done) vec_tiles(bk), vec_done = true;
         sink.end(l, L);
       }
-      qfin_launch(bk, L);
+      qfin_launch(bk, L, false);
       if (!vec_done) {
         l = sink.begin(K_VEC, 0);
         vec_tiles(bk);

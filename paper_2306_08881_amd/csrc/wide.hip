@@ -78,6 +78,10 @@ __global__ __launch_bounds__(kWideBlock * kWidePWaves, 2) void k_wpstep(KArgs a)
   constexpr int LD = 33;  // padded LDS row: the transposed reads hit 32 different banks
   constexpr int CS = 32 * kWidePWaves;  // columns per step of the workgroup
   const Tile t = a.tiles[blockIdx.x];
+  if (t.kind == T_VEC) {  // a raw vector packed into the factor buffer
+    vec_tile(a, t, true);
+    return;
+  }
   const MatDesc d = a.mats[t.idx];
   const int wave = __builtin_amdgcn_readfirstlane(tid() >> 6);
   const int lane = tid() & 63, h = lane >> 5, li = lane & 31;
@@ -440,6 +444,10 @@ __global__ __launch_bounds__(kWave * split_waves(RK), 2) void k_spstep(KArgs a) 
   static_assert(RS % 32 == 0 && EPW * SW == 16, "whole 32-rank blocks and entries per wave");
   constexpr int LD = 33;
   const Tile t = a.tiles[blockIdx.x];
+  if (t.kind == T_VEC) {  // a raw vector packed into the factor buffer
+    vec_tile(a, t, true);
+    return;
+  }
   const MatDesc d = a.mats[t.idx];
   const int wave = tid() >> 6, lane = tid() & 63, h = lane >> 5, li = lane & 31;
   const int rk0 = wave * RS;

@@ -166,6 +166,7 @@ constexpr int32_t kGsumEntries = 4096;  // Gram entries per K_GSUM tile
 constexpr int kWideBlock = 64;     // threads per workgroup of K_WPSTEP, K_WQSTEP, K_WRECON: one wave
 constexpr int kWideQCols = 32;     // K_WQSTEP column block (one MFMA block)
 constexpr int kWidePWaves = 4;     // ranks 8..32: waves of a K_WPSTEP workgroup (adjacent column blocks)
+constexpr int kWideQWaves = 4;     // ranks 8..32: waves of a K_WQSTEP workgroup (adjacent column blocks)
 constexpr int kWideQRows = 512;    // K_WQSTEP rows per chunk (at most)
 constexpr int kWideRCols = 1024;   // K_WRECON columns per tile: 32 blocks of 32
 constexpr int kImageCols = 256;    // K_IMAGE columns per tile: one per thread

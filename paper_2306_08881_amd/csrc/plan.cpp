@@ -441,7 +441,9 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       l = sink.begin(K_WQSTEP, 0);
       for (int32_t mi : bk.mats) {
         const MatDesc& d = plan.mats[mi];
-        const int32_t ncb = static_cast<int32_t>(cdiv(d.m, d.q_cb));
+        // below kSplitRank a tile takes kWideQWaves adjacent column blocks, one per wave
+        const int32_t per = r < kSplitRank ? kWideQWaves : 1;
+        const int32_t ncb = static_cast<int32_t>(cdiv(cdiv(d.m, d.q_cb), per));
         for (int32_t c = 0; c < d.q_chunks; ++c)
           for (int32_t cb = 0; cb < ncb; ++cb) plan.tiles.push_back(Tile{T_QTILE, mi, c, cb});
       }
@@ -772,7 +774,8 @@ std::string build_plan(Plan& plan, int32_t num_tensors, const int32_t* ndims, co
       case K_WQSTEP: {
         const double r0 = double(t.a) * d.q_rows;
         const double rows = std::min<double>(d.q_rows, n - r0);
-        const double cols = std::min<double>(d.q_cb, m - double(t.b) * d.q_cb);
+        const double cw = double(d.q_cb) * (r < kSplitRank ? kWideQWaves : 1);  // a tile's columns
+        const double cols = std::min<double>(cw, m - double(t.b) * cw);
         return rows * cols * eb + (t.b == 0 ? rows * rr * 8.0 : 0.0);
       }
       case K_WFACT: {  // from kBlockedRank on a slice's rows are read and copied once, counted on its first part

@@ -183,27 +183,32 @@ __global__ __launch_bounds__(kWideBlock * kWidePWaves, 2) void k_wpstep(KArgs a)
   }
 }
 
-// Q-step over a tile (row chunk t.a of q_rows rows, column block t.b of 32 columns c0 ...
-// c0 + 31), one wave per workgroup.  Per 32-row block, lane l holds
+// Q-step over a tile (row chunk t.a of q_rows rows, column blocks 4 t.b ... 4 t.b + 3 of 32
+// columns), four waves per workgroup: wave w takes column block 4 t.b + w (columns c0 ...
+// c0 + 31) and the waves walk the chunk's 32-row blocks in step (one barrier per block), so
+// that the workgroup reads 512 contiguous bytes of each row at a time.  Per 32-row block, lane l holds
 // F for column c0 + l % 32 and rows drow(v, l / 32): coalesced 128-byte row segments.  The
 // correction (X form) is an MFMA with D indexed (row, column); F then is the A operand of
 // Q += F^T Ph with the rows as K.  Lane l's partial Q of column c0 + drow(v, l / 32), rank
 // l % 32, goes to the chunk's partial block for K_QFIN.
 template <int RK>
-__global__ __launch_bounds__(kWideBlock, 2) void k_wqstep(KArgs a) {
+__global__ __launch_bounds__(kWideBlock * kWideQWaves, 2) void k_wqstep(KArgs a) {
   constexpr int KH = RK / 2;
   constexpr int NR = RK > 32 ? RK / 32 : 1;  // 32-rank blocks of Q (one MFMA block each)
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
-  const int lane = tid(), h = lane >> 5, li = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid() >> 6);
+  const int lane = tid() & 63, h = lane >> 5, li = lane & 31;
   const int64_t n = d.n, m = d.m;
   const int64_t r0 = static_cast<int64_t>(t.a) * d.q_rows;
   const int rows = static_cast<int>((r0 + d.q_rows < n) ? d.q_rows : n - r0);
-  const int64_t c0 = static_cast<int64_t>(t.b) * d.q_cb;
-  const int64_t w = (m - c0) < 32 ? (m - c0) : 32;  // valid columns of the block
+  const int64_t c0 = (static_cast<int64_t>(t.b) * kWideQWaves + wave) * d.q_cb;
+  // valid columns of the wave's block: none for a block past m (its wave loads zeros, stores
+  // nothing and keeps the others' barriers)
+  const int64_t w = (m - c0) < 32 ? ((m - c0) > 0 ? (m - c0) : 0) : 32;
   const bool xform = deferred_p_of(a, d.bucket);
   const uint32_t row_bytes = u32(m) * 4u;
-  const uint32_t ext = u32(rows - 1) * row_bytes + u32(w) * 4u;
+  const uint32_t ext = w > 0 ? u32(rows - 1) * row_bytes + u32(w) * 4u : 0u;
   const Rsrc G = tile_rsrc(src_of(a, d.bucket) + d.grad_off + r0 * m + c0, ext);
   const Rsrc E = tile_rsrc(a.e + d.e_off + r0 * m + c0, a.ef ? ext : 0u);
   const Rsrc Qhr = tile_rsrc(a.fac + d.qh_slot + c0 * RK, xform ? u32(w) * RK * 4u : 0u);
@@ -260,7 +265,9 @@ __global__ __launch_bounds__(kWideBlock, 2) void k_wqstep(KArgs a) {
 #pragma unroll
       for (int kb = 0; kb < NR; ++kb) q[kb] = mfma(x[v], cb[kb][v], q[kb]);
     load_ops(rb + 32, pa, pb);
+    __syncthreads();  // the waves stay on the same rows
   }
+  if (w == 0) return;  // a block past m has no partials
   const int64_t ncb = (m + d.q_cb - 1) / d.q_cb;
   const int64_t stride = ncb * d.q_cb * RK;  // one row chunk of partials
   float* part = a.qpart + d.qpart + static_cast<int64_t>(t.a) * stride + c0 * RK;
@@ -760,7 +767,7 @@ hipError_t launch_wide_rank(const Launch& l, const KArgs& args, hipStream_t s) {
     switch (l.kernel) {
       case K_WFACT: hipLaunchKernelGGL(k_wfact<RK>, grid, dim3(kBlock), 0, s, args); break;
       case K_WPSTEP: hipLaunchKernelGGL(k_wpstep<RK>, grid, dim3(kWideBlock * kWidePWaves), 0, s, args); break;
-      case K_WQSTEP: hipLaunchKernelGGL(k_wqstep<RK>, grid, block, 0, s, args); break;
+      case K_WQSTEP: hipLaunchKernelGGL(k_wqstep<RK>, grid, dim3(kWideBlock * kWideQWaves), 0, s, args); break;
       case K_WRECON: hipLaunchKernelGGL(k_wrecon4w<RK>, grid, dim3(kBlock), 0, s, args); break;
       default: return hipErrorInvalidValue;
     }

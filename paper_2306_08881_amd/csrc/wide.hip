@@ -162,7 +162,7 @@ __global__ __launch_bounds__(kWideBlock * kWidePWaves, 2) void k_wpstep(KArgs a)
   }
 
   // the waves' shares of P, added in wave order: entry (v, lane) of rank block kb
-  float* red = &xt[0][0][0];  // 4 x 1024 floats per rank block (the transposing tiles are free)
+  float* red = &xt[0][0][0];  // kWidePWaves x 1024 floats per rank block (the transposing tiles are free)
   float* P = dst_of(a, d.bucket) + d.fac_off_p;
   float* Pl = a.fac + d.pl_slot;
 #pragma unroll
@@ -172,7 +172,9 @@ __global__ __launch_bounds__(kWideBlock * kWidePWaves, 2) void k_wpstep(KArgs a)
     for (int v = 0; v < 16; ++v) red[wave * 1024 + v * 64 + lane] = p[kb][v];
     __syncthreads();
     for (int en = tid(); en < 1024; en += kWideBlock * kWidePWaves) {
-      const float sum = ((red[en] + red[1024 + en]) + red[2048 + en]) + red[3072 + en];
+      float sum = red[en];
+#pragma unroll
+      for (int q = 1; q < kWidePWaves; ++q) sum += red[q * 1024 + en];
       const int v = en >> 6, ln = en & 63;
       const int row = drow(v, ln >> 5), rank = kb * 32 + (ln & 31);
       if (rank < RK && row < rows) {

@@ -213,7 +213,7 @@ def test_zero_gradient_then_nonzero():
         assert PU.rel_err(run.error_slice(0), orc.error(0)) <= PU.TOL
 
 
-@pytest.mark.parametrize("rank,k", [(8, 3), (32, 10), (64, 20), (128, 40), (256, 100)])
+@pytest.mark.parametrize("rank,k", [(8, 3), (16, 5), (32, 10), (64, 20), (128, 40), (256, 100)])
 def test_rank_deficient_high_rank(rank, k):
     """Gradients of exact rank k < r: from step 2 on the orthogonalisation drops r - k columns of
     the reused factor (r <= 64: the one-wave Cholesky; r = 128 and 256: kept and dropped pivots

@@ -765,7 +765,6 @@ hipError_t launch_wide_rank(const Launch& l, const KArgs& args, hipStream_t s) {
       default: return hipErrorInvalidValue;
     }
   } else {
-    const dim3 block(kWideBlock);
     switch (l.kernel) {
       case K_WFACT: hipLaunchKernelGGL(k_wfact<RK>, grid, dim3(kBlock), 0, s, args); break;
       case K_WPSTEP: hipLaunchKernelGGL(k_wpstep<RK>, grid, dim3(kWideBlock * kWidePWaves), 0, s, args); break;

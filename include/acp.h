@@ -109,7 +109,7 @@ acp_status acp_init(acp_ctx **out, int32_t num_tensors, const int32_t *ndims, co
 /*
  * acp_state_bytes - size in bytes of the device state block the caller must allocate (256-byte
  * aligned): the error E of Algorithm 2 (one fp32 slot per bucket element, Section IV-A
- * "Error-feedback"), the factors P and Q kept from step to step (Section IV-A, "query reuse"),
+ * "Error-feedback"), the factors P and Q kept from step to step (Section IV-A, query reuse),
  * the orthogonalisation transforms, the Q-step and Gram partial sums and the launch tables.
  * ACP_E_INVALID for a NULL argument.
  */
@@ -201,7 +201,7 @@ acp_status acp_compress_noalloc(acp_ctx *ctx, int64_t step, int32_t b, const flo
  * all-reduce): from the aggregated (summed) factor buffer `agg_factor` (device), write
  * M_hat = P_t Q_t^T / p for every compressed tensor and raw/p for every vector into `out`
  * (device, grad_elems(b) floats; may alias the gradient bucket but not agg_factor), and keep the
- * aggregated factor as the next step's reused factor (Section IV-A, "query reuse").
+ * aggregated factor as the next step's reused factor (Section IV-A, query reuse).
  * ACP_E_STEP unless compress(step) of this bucket came last; ACP_E_INVALID for bad buffers.
  */
 acp_status acp_decompress(acp_ctx *ctx, int64_t step, int32_t b, const float *agg_factor, float *out,

@@ -16,7 +16,7 @@ Readings taken where the paper is silent (each listed in the design notes):
 * t starts at 1, so the first step is a P-step and P0 is drawn but unused.
 * E_t uses the local factor, computed before the all-reduce; the returned
   product and the factor kept for the next step use the aggregated one.
-* the all-reduce sums (Section II-A: gradients are "summed up"), and the
+* the all-reduce sums (Section II-A aggregates the workers' gradients by addition), and the
   returned gradient is divided by the number of workers p, as S-SGD's mean.
 * vector-shaped gradients pass through: sent raw, summed and divided by p.
 * E_0 = 0 and P0, Q0 come from ``oracle.rng``.

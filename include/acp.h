@@ -176,6 +176,10 @@ acp_status acp_init_factor(const acp_ctx *ctx, int32_t tensor_id, int32_t which,
  * bucket `grad` (device), updates E in the state and writes the local factors and raw vectors
  * into `factor_buf` (device, factor_elems_p/q(b) floats by parity), enqueued on `stream`.
  * `factor_buf` must not overlap `grad`.  The caller all-reduces (sums) factor_buf across workers.
+ * At rank 4 a P-step whose column-class launches are all small may run some of them on a stream
+ * the context owns (made at bind on the bound device, default priority), forked from `stream`
+ * by an event and joined back into it before the call returns: work enqueued on `stream` after
+ * the call, and a graph captured on it, see the whole step.
  */
 acp_status acp_compress(acp_ctx *ctx, int64_t step, int32_t b, const float *grad, float *factor_buf,
                         void *stream);
@@ -219,7 +223,8 @@ acp_status acp_compress_all(acp_ctx *ctx, int64_t step, const float *const *grad
                             float *const *factor_bufs, void *stream);
 /*
  * HIP graphs: the compress and decompress calls enqueue kernels only (no memset, no allocation,
- * no host synchronisation), with arguments that depend on the step only through its parity once
+ * no host synchronisation; the fork to the context's stream and the join back are event waits,
+ * which capture records), with arguments that depend on the step only through its parity once
  * every bucket has run two steps (with reuse; without it the draw is keyed by the step number).
  * So one odd and one even step's calls may be captured (hipStreamBeginCapture on `stream`) and
  * the two graphs replayed in turn for later steps, with the same buffers.  Capture enqueues

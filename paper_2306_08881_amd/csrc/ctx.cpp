@@ -28,6 +28,10 @@ struct acp_ctx {
   int device = -1;
   float* scratch = nullptr;     // the bound device's static Q-step scratch (acp_compress_noalloc)
   std::string scratch_err;      // why it is null after a bind
+  // a second stream (default priority) and fork / join events on the bound device: the rank-4
+  // P-step's class launches after the first run there, beside it
+  hipStream_t side = nullptr;
+  hipEvent_t fork_ev = nullptr, join_ev = nullptr;
   std::vector<int64_t> last_step;   // per bucket: last completed step
   std::vector<int64_t> pending;     // per bucket: compressed step awaiting decompress (0 = none)
   std::vector<uint8_t> deferred;    // per bucket: E form of the arena (kExplicit, kHoldsF, kHoldsX)
@@ -100,32 +104,80 @@ bool overlaps(const void* x, int64_t x_floats, const void* y, int64_t y_floats) 
   return a < b + y_floats * 4 && b < a + x_floats * 4;
 }
 
+// A run of two or more consecutive rank-4 P-step launches (K_PFUSED: one per column class, on
+// disjoint matrices, none reading what another writes) from launch i on, each moving less than
+// kOverlapBytes: their tails are a large part of their time, which running them side by side
+// fills (larger launches slowed each other down when run so: BERT-base and BERT-large).
+constexpr double kOverlapBytes = 512.0 * (1 << 20);
+bool small_pstep_run(const std::vector<acp::Launch>& launches, size_t i) {
+  size_t k = i;
+  while (k < launches.size() && launches[k].kernel == acp::K_PFUSED) {
+    if (launches[k].alg_bytes >= kOverlapBytes) return false;
+    ++k;
+  }
+  return k - i >= 2;
+}
+
 // Enqueues `launches` on s; skip_chol leaves out the Gram finish (K_GSUM, K_CHOL), which factor
-// tiles that only copy (KArgs::copy_only) do not need.
+// tiles that only copy (KArgs::copy_only) do not need.  A small P-step run (small_pstep_run) is
+// split over two streams: its first launch on s, the others on the context's side stream,
+// forked from s before the run and joined back into s after it (the joins keep graph capture on
+// s whole).
 acp_status run(const acp_ctx* c, const std::vector<acp::Launch>& launches, acp::KArgs a,
                hipStream_t s, bool skip_chol = false) {
   const acp::Tile* tiles = reinterpret_cast<const acp::Tile*>(c->dev + c->plan.off_tiles);
   acp_ctx* mc = const_cast<acp_ctx*>(c);
-  for (const acp::Launch& l : launches) {
+  const hipStream_t s0 = s;
+  bool forked = false;  // launches go to the side stream until the run ends
+  // s0 waits for the side stream's work (also before an error return)
+  auto join = [&]() -> bool {
+    forked = false;
+    s = s0;
+    return hipEventRecord(c->join_ev, c->side) == hipSuccess && hipStreamWaitEvent(s0, c->join_ev, 0) == hipSuccess;
+  };
+  auto error = [&](const std::string& msg) {
+    if (forked) (void)join();
+    return fail(c, ACP_E_DEVICE, msg);
+  };
+  for (size_t i = 0; i < launches.size(); ++i) {
+    const acp::Launch& l = launches[i];
     if (skip_chol && (l.kernel == acp::K_GSUM || l.kernel == acp::K_CHOL)) continue;
+    const bool pstep = l.kernel == acp::K_PFUSED;
+    if (forked && !pstep && !join()) return fail(c, ACP_E_DEVICE, "side stream join failed");
+    if (!forked && pstep && c->side && small_pstep_run(launches, i)) {
+      if (hipEventRecord(c->fork_ev, s0) != hipSuccess || hipStreamWaitEvent(c->side, c->fork_ev, 0) != hipSuccess)
+        return fail(c, ACP_E_DEVICE, "side stream fork failed");  // nothing is on the side yet
+      forked = true;
+      s = s0;  // this first launch of the run stays on s, the rest go to the side
+    } else if (forked) {
+      s = c->side;
+    }
     a.tiles = tiles + l.tile_off;
     a.ntiles = l.ntiles;
     a.variant = l.variant;
     const bool timed = mc->prof_family != 0 && l.family == mc->prof_family &&
                        2 * mc->prof_used < static_cast<int64_t>(mc->prof_events.size());
     if (timed && hipEventRecord(mc->prof_events[2 * mc->prof_used], s) != hipSuccess)
-      return fail(c, ACP_E_DEVICE, "hipEventRecord failed");
+      return error("hipEventRecord failed");
     const hipError_t e = acp::launch(l, c->plan.rank, a, s);
-    if (e != hipSuccess)
-      return fail(c, ACP_E_DEVICE, std::string("kernel launch failed: ") + hipGetErrorString(e));
+    if (e != hipSuccess) return error(std::string("kernel launch failed: ") + hipGetErrorString(e));
     if (timed) {
       if (hipEventRecord(mc->prof_events[2 * mc->prof_used + 1], s) != hipSuccess)
-        return fail(c, ACP_E_DEVICE, "hipEventRecord failed");
+        return error("hipEventRecord failed");
       mc->prof_used += 1;
       mc->prof_bytes += l.alg_bytes;
     }
   }
+  if (forked && !join()) return fail(c, ACP_E_DEVICE, "side stream join failed");
   return ACP_OK;
+}
+
+void release_side(acp_ctx* c) {
+  if (c->side) (void)hipStreamDestroy(c->side);
+  if (c->fork_ev) (void)hipEventDestroy(c->fork_ev);
+  if (c->join_ev) (void)hipEventDestroy(c->join_ev);
+  c->side = nullptr;
+  c->fork_ev = c->join_ev = nullptr;
 }
 
 int64_t checkpoint_payload(const acp::Plan& p) {
@@ -333,6 +385,15 @@ acp_status acp_bind_state(acp_ctx* c, void* device_ptr, int64_t bytes, void* str
   std::fill(c->pending.begin(), c->pending.end(), 0);
   std::fill(c->deferred.begin(), c->deferred.end(), 0);
   std::fill(c->phase.begin(), c->phase.end(), 0);
+  // the side stream, on the bound device
+  release_side(c);
+  if (hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess ||
+      hipEventCreateWithFlags(&c->fork_ev, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c->join_ev, hipEventDisableTiming) != hipSuccess) {
+    release_side(c);
+    c->dev = nullptr;
+    return fail(c, ACP_E_DEVICE, "side stream creation failed");
+  }
   // the static scratch of acp_compress_noalloc: looked up once per device, with it current
   c->scratch = nullptr;
   c->scratch_err.clear();
@@ -942,6 +1003,7 @@ void acp_destroy(acp_ctx* c) {
   if (!c) return;
   for (hipEvent_t& ev : c->prof_events)
     if (ev) (void)hipEventDestroy(ev);
+  release_side(c);
   delete c;
 }
 

@@ -351,7 +351,7 @@ def main():
         pmc_summary(*args.pmc_summary, workload=args.workload)
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
               "(the compressor is data-parallel: each rank runs this same step on its own GPU).",
               file=sys.stderr)
         sys.exit(2)

@@ -61,7 +61,7 @@ typedef enum {
   ACP_E_STEP = -2,        /* call out of step order */
   ACP_E_STATE = -3,       /* state not bound / wrong size / corrupt checkpoint */
   ACP_E_DEVICE = -4,      /* a HIP call failed */
-  ACP_E_UNSUPPORTED = -5  /* valid request this build does not implement */
+  ACP_E_UNSUPPORTED = -5  /* valid request the library does not implement */
 } acp_status;
 
 /* flags of acp_init */

@@ -495,6 +495,10 @@ def main():
         if n:
             kern[name] = {"launches": n, "avg_launch_us": sec / n * 1e6, "bytes_per_launch": by / n,
                           "gbs": by / sec / 1e9, "ms_per_step": sec / steps * 1e3}
+            if fam == fams[4][1] and 8 <= wl.rank < 128:
+                kern[name]["note"] = ("the Gram finish (k_wfact, k_chol) runs on the context's second "
+                                      "stream beside the decompress: its events time that span, most of "
+                                      "which the decompress hides")
     # the dominant kernel: the Q-step kernel, the longest-running single kernel of the step (one
     # launch per Q-step); at rank 4 the P-step time is split over one k_pfused launch per column
     # class

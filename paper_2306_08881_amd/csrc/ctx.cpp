@@ -118,38 +118,55 @@ bool small_pstep_run(const std::vector<acp::Launch>& launches, size_t i) {
   return k - i >= 2;
 }
 
+// The Gram finish of the aggregated factor (K_WFACT, then K_GSUM and K_CHOL) after a rank 8-256
+// decompress launch (K_WRECON): it reads the aggregated factor only and writes the factor slot,
+// the Gram partials, W and the raw vectors' part of the output, none of which the decompress
+// reads or writes, so it runs on the side stream beside the decompress (its few workgroups and
+// dependent launches are latency-bound, the decompress is bound by HBM writes).  From
+// kBlockedRank on the Gram's matrix-core work slowed the decompress beside it by more than the
+// overlap saved (BERT-large r=128), so those ranks keep the one stream.
+bool orth_kernel(int32_t k) { return k == acp::K_WFACT || k == acp::K_GSUM || k == acp::K_CHOL; }
+bool orth_after_recon(const acp_ctx* c, const std::vector<acp::Launch>& launches, size_t i) {
+  return c->plan.rank < acp::kBlockedRank && launches[i].kernel == acp::K_WRECON &&
+         i + 1 < launches.size() && launches[i + 1].kernel == acp::K_WFACT;
+}
+
 // Enqueues `launches` on s; skip_chol leaves out the Gram finish (K_GSUM, K_CHOL), which factor
-// tiles that only copy (KArgs::copy_only) do not need.  A small P-step run (small_pstep_run) is
-// split over two streams: its first launch on s, the others on the context's side stream,
-// forked from s before the run and joined back into s after it (the joins keep graph capture on
-// s whole).
+// tiles that only copy (KArgs::copy_only) do not need.  Two kinds of run are split over two
+// streams, their first launch on s and the others on the context's side stream, forked from s
+// before the run and joined back into s after it (the joins keep graph capture on s whole): a
+// small P-step run (small_pstep_run) and a decompress with the Gram finish after it
+// (orth_after_recon).
 acp_status run(const acp_ctx* c, const std::vector<acp::Launch>& launches, acp::KArgs a,
                hipStream_t s, bool skip_chol = false) {
   const acp::Tile* tiles = reinterpret_cast<const acp::Tile*>(c->dev + c->plan.off_tiles);
   acp_ctx* mc = const_cast<acp_ctx*>(c);
   const hipStream_t s0 = s;
-  bool forked = false;  // launches go to the side stream until the run ends
+  enum { kNone, kPstep, kOrth } forked = kNone;  // the run whose later launches go to the side
   // s0 waits for the side stream's work (also before an error return)
   auto join = [&]() -> bool {
-    forked = false;
+    forked = kNone;
     s = s0;
     return hipEventRecord(c->join_ev, c->side) == hipSuccess && hipStreamWaitEvent(s0, c->join_ev, 0) == hipSuccess;
   };
   auto error = [&](const std::string& msg) {
-    if (forked) (void)join();
+    if (forked != kNone) (void)join();
     return fail(c, ACP_E_DEVICE, msg);
   };
   for (size_t i = 0; i < launches.size(); ++i) {
     const acp::Launch& l = launches[i];
     if (skip_chol && (l.kernel == acp::K_GSUM || l.kernel == acp::K_CHOL)) continue;
     const bool pstep = l.kernel == acp::K_PFUSED;
-    if (forked && !pstep && !join()) return fail(c, ACP_E_DEVICE, "side stream join failed");
-    if (!forked && pstep && c->side && small_pstep_run(launches, i)) {
+    const bool continues = (forked == kPstep && pstep) || (forked == kOrth && orth_kernel(l.kernel));
+    if (forked != kNone && !continues && !join()) return fail(c, ACP_E_DEVICE, "side stream join failed");
+    const bool fork_p = forked == kNone && pstep && c->side && small_pstep_run(launches, i);
+    const bool fork_o = forked == kNone && !fork_p && c->side && orth_after_recon(c, launches, i);
+    if (fork_p || fork_o) {
       if (hipEventRecord(c->fork_ev, s0) != hipSuccess || hipStreamWaitEvent(c->side, c->fork_ev, 0) != hipSuccess)
         return fail(c, ACP_E_DEVICE, "side stream fork failed");  // nothing is on the side yet
-      forked = true;
+      forked = fork_p ? kPstep : kOrth;
       s = s0;  // this first launch of the run stays on s, the rest go to the side
-    } else if (forked) {
+    } else if (forked != kNone) {
       s = c->side;
     }
     a.tiles = tiles + l.tile_off;
@@ -168,7 +185,7 @@ acp_status run(const acp_ctx* c, const std::vector<acp::Launch>& launches, acp::
       mc->prof_bytes += l.alg_bytes;
     }
   }
-  if (forked && !join()) return fail(c, ACP_E_DEVICE, "side stream join failed");
+  if (forked != kNone && !join()) return fail(c, ACP_E_DEVICE, "side stream join failed");
   return ACP_OK;
 }
 

@@ -276,11 +276,13 @@ __device__ inline double readlane_d(double v, int src) {
 // Cholesky G = R^T R and W = R^-1 (dropped columns and rows zero), written to w_out.  G in
 // shared; every thread of the workgroup calls this, the first wave does the work.  Right-looking,
 // one column per lane: lane j keeps column j of the updated G in registers; at pivot k lane k's
-// diagonal decides the drop, each lane forms its entry R[k][j], and the trailing update takes
-// R[k][i] from lane i.  The subtractions come in the same order as in the left-looking form
-// (pivot 0 first), so R is the same.  W = R^-1 on the kept columns, row by row (lane = row).
+// diagonal decides the drop, each lane forms its entry R[k][j] and stores it to row k of R in
+// LDS, and the trailing update reads R[k][i] back from there (one broadcast read per two entries;
+// the wave's LDS accesses take effect in order).  The subtractions come in the same order as in
+// the left-looking form (pivot 0 first), so R is the same.  W = R^-1 on the kept columns, row by
+// row (lane = row).
 template <int RK>
-__device__ void cholesky_w(const double* G, double* w_out) {
+__device__ __attribute__((always_inline)) void cholesky_w(const double* G, double* w_out) {
   __shared__ double R[RK * RK];
   __shared__ int drop[RK];
   if (tid() >= kWave) return;
@@ -299,9 +301,10 @@ __device__ void cholesky_w(const double* G, double* w_out) {
     if (keep) rkj = j > k ? g[k] / rkk : (j == k ? rkk : 0.0);
     if (col) R[k * RK + j] = rkj;
     if (j == 0) drop[k] = keep ? 0 : 1;
+    __builtin_amdgcn_wave_barrier();
     if (keep)
 #pragma unroll
-      for (int i = k + 1; i < RK; ++i) g[i] -= readlane_d(rkj, i) * rkj;
+      for (int i = k + 1; i < RK; ++i) g[i] -= R[k * RK + i] * rkj;
   }
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   // W = R^-1 by rows (lane = row a), right-looking: once W[a][i] is final it is subtracted

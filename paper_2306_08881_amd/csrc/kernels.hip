@@ -439,7 +439,7 @@ __global__ __launch_bounds__(kBlock) void k_gsum(KArgs a) {
 // W from the Gram partials of a matrix's t.b slices, added in slice order (from kBlockedRank on
 // K_GSUM has added them into the first).
 template <int RK>
-__global__ __launch_bounds__(kBlock) void k_chol(KArgs a) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RK <= 32 ? 4 : 1))) void k_chol(KArgs a) {
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc d = a.mats[t.idx];
   constexpr bool SPLIT = RK >= kCholBlockRank;

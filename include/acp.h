@@ -206,6 +206,11 @@ acp_status acp_compress_noalloc(acp_ctx *ctx, int64_t step, int32_t b, const flo
  * M_hat = P_t Q_t^T / p for every compressed tensor and raw/p for every vector into `out`
  * (device, grad_elems(b) floats; may alias the gradient bucket but not agg_factor), and keep the
  * aggregated factor as the next step's reused factor (Section IV-A, query reuse).
+ * At ranks 8 to 64 the orthogonalisation of that factor (Section IV-A: its Gram, Cholesky and
+ * W, and the orthogonal factor the next compress multiplies by) runs on the context's second
+ * stream beside the decompress kernel, forked from `stream` and joined back into it before the
+ * call returns; the bucket's next compress then skips forming the orthogonal factor itself (it
+ * forms it after a fresh bind, a state load, or with fresh draws).
  * ACP_E_STEP unless compress(step) of this bucket came last; ACP_E_INVALID for bad buffers.
  */
 acp_status acp_decompress(acp_ctx *ctx, int64_t step, int32_t b, const float *agg_factor, float *out,

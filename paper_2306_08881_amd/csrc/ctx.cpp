@@ -36,6 +36,9 @@ struct acp_ctx {
   std::vector<int64_t> pending;     // per bucket: compressed step awaiting decompress (0 = none)
   std::vector<uint8_t> deferred;    // per bucket: E form of the arena (kExplicit, kHoldsF, kHoldsX)
   std::vector<uint8_t> phase;       // per bucket, Power-SGD: 1 after the first half, 2 after the second
+  // per bucket: the step whose compress finds its orthogonal factor (K_APPLY's Qh or Ph) already
+  // formed, beside the previous decompress (0: none)
+  std::vector<int64_t> applied;
   mutable std::string err;
 
   // kernel timing (acp_profile_start / acp_profile_stop)
@@ -132,33 +135,70 @@ bool orth_after_recon(const acp_ctx* c, const std::vector<acp::Launch>& launches
 }
 
 // Enqueues `launches` on s; skip_chol leaves out the Gram finish (K_GSUM, K_CHOL), which factor
-// tiles that only copy (KArgs::copy_only) do not need.  Two kinds of run are split over two
+// tiles that only copy (KArgs::copy_only) do not need, and skip_apply the orthogonal factor's
+// product (K_APPLY), when the previous decompress formed it.  Two kinds of run are split over two
 // streams, their first launch on s and the others on the context's side stream, forked from s
 // before the run and joined back into s after it (the joins keep graph capture on s whole): a
 // small P-step run (small_pstep_run) and a decompress with the Gram finish after it
-// (orth_after_recon).
+// (orth_after_recon).  In the latter, `apply` (the next compress's K_APPLY, or null) follows the
+// Gram finish on the side stream, and *applied tells whether it was enqueued.
+struct RunOpts {
+  bool skip_chol = false;
+  bool skip_apply = false;
+  const acp::Launch* apply = nullptr;
+  bool* applied = nullptr;
+};
 acp_status run(const acp_ctx* c, const std::vector<acp::Launch>& launches, acp::KArgs a,
-               hipStream_t s, bool skip_chol = false) {
+               hipStream_t s, const RunOpts& o = RunOpts{}) {
   const acp::Tile* tiles = reinterpret_cast<const acp::Tile*>(c->dev + c->plan.off_tiles);
   acp_ctx* mc = const_cast<acp_ctx*>(c);
   const hipStream_t s0 = s;
   enum { kNone, kPstep, kOrth } forked = kNone;  // the run whose later launches go to the side
-  // s0 waits for the side stream's work (also before an error return)
-  auto join = [&]() -> bool {
+  if (o.applied) *o.applied = false;
+  // one launch of the list (or o.apply) on stream st
+  auto enqueue = [&](const acp::Launch& l, hipStream_t st) -> std::string {
+    a.tiles = tiles + l.tile_off;
+    a.ntiles = l.ntiles;
+    a.variant = l.variant;
+    const bool timed = mc->prof_family != 0 && l.family == mc->prof_family &&
+                       2 * mc->prof_used < static_cast<int64_t>(mc->prof_events.size());
+    if (timed && hipEventRecord(mc->prof_events[2 * mc->prof_used], st) != hipSuccess)
+      return "hipEventRecord failed";
+    const hipError_t e = acp::launch(l, c->plan.rank, a, st);
+    if (e != hipSuccess) return std::string("kernel launch failed: ") + hipGetErrorString(e);
+    if (timed) {
+      if (hipEventRecord(mc->prof_events[2 * mc->prof_used + 1], st) != hipSuccess)
+        return "hipEventRecord failed";
+      mc->prof_used += 1;
+      mc->prof_bytes += l.alg_bytes;
+    }
+    return "";
+  };
+  // the Gram finish's run ends with o.apply on the side stream; then s0 waits for the side
+  // stream's work (also before an error return)
+  std::string apply_err;
+  auto join = [&](bool with_apply = true) -> bool {
+    if (with_apply && forked == kOrth && o.apply && apply_err.empty()) {
+      apply_err = enqueue(*o.apply, c->side);
+      if (apply_err.empty() && o.applied) *o.applied = true;
+    }
     forked = kNone;
     s = s0;
-    return hipEventRecord(c->join_ev, c->side) == hipSuccess && hipStreamWaitEvent(s0, c->join_ev, 0) == hipSuccess;
+    const bool ok = hipEventRecord(c->join_ev, c->side) == hipSuccess && hipStreamWaitEvent(s0, c->join_ev, 0) == hipSuccess;
+    return ok && apply_err.empty();
   };
   auto error = [&](const std::string& msg) {
-    if (forked != kNone) (void)join();
+    if (forked != kNone) (void)join(false);
     return fail(c, ACP_E_DEVICE, msg);
   };
   for (size_t i = 0; i < launches.size(); ++i) {
     const acp::Launch& l = launches[i];
-    if (skip_chol && (l.kernel == acp::K_GSUM || l.kernel == acp::K_CHOL)) continue;
+    if (o.skip_chol && (l.kernel == acp::K_GSUM || l.kernel == acp::K_CHOL)) continue;
+    if (o.skip_apply && l.kernel == acp::K_APPLY) continue;
     const bool pstep = l.kernel == acp::K_PFUSED;
     const bool continues = (forked == kPstep && pstep) || (forked == kOrth && orth_kernel(l.kernel));
-    if (forked != kNone && !continues && !join()) return fail(c, ACP_E_DEVICE, "side stream join failed");
+    if (forked != kNone && !continues && !join())
+      return fail(c, ACP_E_DEVICE, apply_err.empty() ? "side stream join failed" : apply_err);
     const bool fork_p = forked == kNone && pstep && c->side && small_pstep_run(launches, i);
     const bool fork_o = forked == kNone && !fork_p && c->side && orth_after_recon(c, launches, i);
     if (fork_p || fork_o) {
@@ -169,23 +209,11 @@ acp_status run(const acp_ctx* c, const std::vector<acp::Launch>& launches, acp::
     } else if (forked != kNone) {
       s = c->side;
     }
-    a.tiles = tiles + l.tile_off;
-    a.ntiles = l.ntiles;
-    a.variant = l.variant;
-    const bool timed = mc->prof_family != 0 && l.family == mc->prof_family &&
-                       2 * mc->prof_used < static_cast<int64_t>(mc->prof_events.size());
-    if (timed && hipEventRecord(mc->prof_events[2 * mc->prof_used], s) != hipSuccess)
-      return error("hipEventRecord failed");
-    const hipError_t e = acp::launch(l, c->plan.rank, a, s);
-    if (e != hipSuccess) return error(std::string("kernel launch failed: ") + hipGetErrorString(e));
-    if (timed) {
-      if (hipEventRecord(mc->prof_events[2 * mc->prof_used + 1], s) != hipSuccess)
-        return error("hipEventRecord failed");
-      mc->prof_used += 1;
-      mc->prof_bytes += l.alg_bytes;
-    }
+    const std::string msg = enqueue(l, s);
+    if (!msg.empty()) return error(msg);
   }
-  if (forked != kNone && !join()) return fail(c, ACP_E_DEVICE, "side stream join failed");
+  if (forked != kNone && !join())
+    return fail(c, ACP_E_DEVICE, apply_err.empty() ? "side stream join failed" : apply_err);
   return ACP_OK;
 }
 
@@ -207,6 +235,14 @@ struct CkptHeader {
   int64_t num_tensors, rank, cap, world, flags, nbuckets, seed;
   int64_t e_floats, fac_floats, w_doubles;
 };
+
+// The K_APPLY launch that opens a compress list (the orthogonal factor Qh = Q W or Ph = P W of
+// the reused factor), when the previous decompress may form it beside its own launches instead:
+// reused factors only (with fresh draws the factor is drawn in the compress call).
+const acp::Launch* leading_apply(const acp_ctx* c, const std::vector<acp::Launch>& compress) {
+  if (!c->plan.reuse || c->plan.psgd || compress.empty() || compress[0].kernel != acp::K_APPLY) return nullptr;
+  return &compress[0];
+}
 
 // acp_compress and acp_compress_noalloc: checks, then the bucket's compress launches.  `qpart`,
 // when not null, replaces the state block's Q-step partial region as the kernels' base.
@@ -246,10 +282,13 @@ acp_status compress_bucket(acp_ctx* c, int64_t step, int32_t b, const float* gra
     const acp_status sd = run(c, bk.draw[step & 1], a, static_cast<hipStream_t>(stream));
     if (sd != ACP_OK) return sd;
   }
-  const acp_status st = run(c, bk.compress[step & 1], a, static_cast<hipStream_t>(stream));
+  RunOpts o;
+  o.skip_apply = c->applied[b] == step;
+  const acp_status st = run(c, bk.compress[step & 1], a, static_cast<hipStream_t>(stream), o);
   if (st != ACP_OK) return st;
   c->pending[b] = step;
   c->deferred[b] = form_after_compress(c, step);
+  c->applied[b] = 0;
   return ACP_OK;
 }
 
@@ -349,6 +388,7 @@ acp_status acp_init(acp_ctx** out, int32_t num_tensors, const int32_t* ndims, co
   c->pending.assign(nb, 0);
   c->deferred.assign(nb, 0);
   c->phase.assign(nb, 0);
+  c->applied.assign(nb, 0);
   *out = c;
   return ACP_OK;
 }
@@ -387,6 +427,7 @@ acp_status acp_bind_state(acp_ctx* c, void* device_ptr, int64_t bytes, void* str
   c->dev = d;
   c->dev_bytes = bytes;
   c->device = dev;
+  c->applied.assign(p.buckets.size(), 0);
   acp::KArgs a = base_args(c);
   const acp_status st = run(c, p.gram_init, a, s);
   if (st != ACP_OK) {
@@ -568,10 +609,15 @@ acp_status acp_decompress(acp_ctx* c, int64_t step, int32_t b, const float* agg_
   a.dst[0] = out;
   a.parity = static_cast<int32_t>(step & 1);
   set_form(a, 0, c->deferred[b]);
-  const acp_status st = run(c, bk.decompress[step & 1], a, static_cast<hipStream_t>(stream));
+  bool applied = false;
+  RunOpts o;
+  o.apply = leading_apply(c, bk.compress[(step + 1) & 1]);
+  o.applied = &applied;
+  const acp_status st = run(c, bk.decompress[step & 1], a, static_cast<hipStream_t>(stream), o);
   if (st != ACP_OK) return st;
   c->pending[b] = 0;
   c->last_step[b] = step;
+  c->applied[b] = applied ? step + 1 : 0;
   return ACP_OK;
 }
 
@@ -612,12 +658,18 @@ acp_status acp_compress_all(acp_ctx* c, int64_t step, const float* const* grads,
       const acp_status sd = run(c, c->plan.group_draw[g][step & 1], a, static_cast<hipStream_t>(stream));
       if (sd != ACP_OK) return sd;
     }
-    const acp_status st = run(c, c->plan.group_compress[g][step & 1], a, static_cast<hipStream_t>(stream));
+    // the group's K_APPLY is left out when the previous decompress formed every bucket's factor
+    RunOpts o;
+    o.skip_apply = true;
+    for (int32_t i = 0; i < acp::kMaxGroup && a.base + i < nb; ++i)
+      if (c->applied[a.base + i] != step) o.skip_apply = false;
+    const acp_status st = run(c, c->plan.group_compress[g][step & 1], a, static_cast<hipStream_t>(stream), o);
     if (st != ACP_OK) return st;
   }
   for (int32_t b = 0; b < nb; ++b) {
     c->pending[b] = step;
     c->deferred[b] = form_after_compress(c, step);
+    c->applied[b] = 0;
   }
   return ACP_OK;
 }
@@ -645,6 +697,7 @@ acp_status acp_decompress_all(acp_ctx* c, int64_t step, const float* const* agg_
   }
   const acp_status ds = check_device(c);
   if (ds != ACP_OK) return ds;
+  std::vector<bool> group_applied(c->plan.group_decompress.size(), false);
   for (size_t g = 0; g < c->plan.group_decompress.size(); ++g) {
     acp::KArgs a = base_args(c);
     a.base = static_cast<int32_t>(g) * acp::kMaxGroup;
@@ -654,12 +707,18 @@ acp_status acp_decompress_all(acp_ctx* c, int64_t step, const float* const* agg_
       a.dst[i] = outs[a.base + i];
       set_form(a, i, c->deferred[a.base + i]);
     }
-    const acp_status st = run(c, c->plan.group_decompress[g][step & 1], a, static_cast<hipStream_t>(stream));
+    bool applied = false;
+    RunOpts o;
+    o.apply = leading_apply(c, c->plan.group_compress[g][(step + 1) & 1]);
+    o.applied = &applied;
+    const acp_status st = run(c, c->plan.group_decompress[g][step & 1], a, static_cast<hipStream_t>(stream), o);
     if (st != ACP_OK) return st;
+    group_applied[g] = applied;
   }
   for (int32_t b = 0; b < nb; ++b) {
     c->pending[b] = 0;
     c->last_step[b] = step;
+    c->applied[b] = group_applied[b / acp::kMaxGroup] ? step + 1 : 0;
   }
   return ACP_OK;
 }
@@ -715,7 +774,7 @@ acp_status acp_powersgd_decompress(acp_ctx* c, int64_t step, int32_t b, const fl
   a.dst[0] = out;
   a.parity = 0;
   set_form(a, 0, c->deferred[b]);
-  if ((st = run(c, bk.decompress[0], a, static_cast<hipStream_t>(stream), true)) != ACP_OK) return st;
+  if ((st = run(c, bk.decompress[0], a, static_cast<hipStream_t>(stream), RunOpts{true})) != ACP_OK) return st;
   c->pending[b] = 0;
   c->phase[b] = 0;
   c->last_step[b] = step;
@@ -823,7 +882,7 @@ acp_status acp_powersgd_decompress_all(acp_ctx* c, int64_t step, const float* co
       a.dst[i] = outs[a.base + i];
       set_form(a, i, c->deferred[a.base + i]);
     }
-    if ((st = run(c, c->plan.group_decompress[g][0], a, static_cast<hipStream_t>(stream), true)) != ACP_OK)
+    if ((st = run(c, c->plan.group_decompress[g][0], a, static_cast<hipStream_t>(stream), RunOpts{true})) != ACP_OK)
       return st;
   }
   for (int32_t b = 0; b < nb; ++b) {
@@ -961,6 +1020,7 @@ acp_status acp_set_state(acp_ctx* c, const void* host_buf, int64_t bytes) {
   if (e != hipSuccess) return fail(c, ACP_E_DEVICE, std::string("state upload failed: ") + hipGetErrorString(e));
   c->last_step = steps;
   c->deferred = defr;
+  c->applied.assign(p.buckets.size(), 0);
   return ACP_OK;
 }
 

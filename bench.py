@@ -546,7 +546,8 @@ def main():
                    "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
                    "gradient_elements_per_s": round(wl.numel / (ms * 1e-3), 1),
                    "algorithmic_bytes_per_step": step_bytes,
-                   "kernels": {k: {kk: round(vv, 3) for kk, vv in v.items()} for k, v in kern.items()}},
+                   "kernels": {k: {kk: round(vv, 3) if isinstance(vv, float) else vv for kk, vv in v.items()}
+                       for k, v in kern.items()}},
         "roofline": roof,
     }
     res["config"]["step_ms"] = {"mean": round(float(t_step.mean()), 4), "std": round(float(t_step.std()), 4),

@@ -161,6 +161,42 @@ def test_grouped_calls_over_several_launch_groups():
     assert nb > 64
 
 
+@pytest.mark.parametrize("rank", [16, 32, 64])
+def test_mixed_calls_and_reload_in_place(rank):
+    """From rank 8 to 64 a decompress also forms the next compress's orthogonal factor and the
+    context records it: per-bucket and all-bucket calls in alternation, and a state load into the
+    same context (which must drop the record while the slots hold the early factor), continue
+    bitwise like plain per-bucket calls."""
+    shapes = WIDE_SHAPES if rank < 64 else SPLIT_SHAPES
+    cap = 1 << 15 if rank < 64 else 1 << 20
+    wl = sg.Workload(f"mixed_r{rank}", [sg.Param(f"t{i}", s) for i, s in enumerate(shapes)], rank, 8,
+                     lambda p: 0.05, seed=13)
+    a = PU.Runner(shapes, rank, cap=cap)
+    b = PU.Runner(shapes, rank, cap=cap)
+    assert a.nb >= 2
+    for t in range(1, 9):
+        gb = a.pack(sg.gradient_set(wl, t))
+        a.step(t, gb)
+        if t % 2:  # all-bucket compress, per-bucket decompress
+            b.acp.compress_all(t, gb, b.fbuf)
+            for k in range(b.nb):
+                b.acp.decompress(t, k, b.fbuf[k], b.out[k])
+        else:      # per-bucket compress, all-bucket decompress
+            for k in range(b.nb):
+                b.acp.compress(t, k, gb[k], b.fbuf[k])
+            b.acp.decompress_all(t, b.fbuf, b.out)
+        assert _same(_snap(a, t), _snap(b, t)), f"mixed calls differ at step {t}"
+        if t == 3:
+            ckpt = b.acp.get_state()
+        if t == 5:  # back to step 3 in the same context, then steps 4 and 5 again
+            b.acp.set_state(ckpt)
+            for u in (4, 5):
+                gu = b.pack(sg.gradient_set(wl, u))
+                b.step(u, gu)
+            assert _same(_snap(a, t), _snap(b, t)), "reload in place differs at step 5"
+    PU.log(f"  rank {rank}: mixed calls and an in-place reload bitwise equal to per-bucket calls")
+
+
 def test_grouped_call_sequencing():
     from paper_2306_08881_amd import _lib as L
     shapes = [(32, 24), (24,), (40, 16)]

@@ -30,8 +30,11 @@ constexpr int kWave = 64;
 constexpr double kTau = 1e-4;     // rank-deficiency threshold of orth()
 constexpr int kMaxTileRows = 256; // rows per tile of the rank-4 row kernels (factor rows in LDS)
 // K_QFIN entries (e = column * r + rank, over the whole matrix) per tile: one thread per entry
-// for up to 8 row chunks, 4 threads for up to 64, 16 threads beyond
-constexpr int qfin_entries(int32_t q_chunks) { return q_chunks <= 8 ? 1024 : (q_chunks <= 64 ? 64 : 16); }
+// for up to 8 row chunks, 4 threads for up to 32, 8 for up to 64 (so that no thread adds more
+// than 8 chunks, all requested at once), 16 threads beyond
+constexpr int qfin_entries(int32_t q_chunks) {
+  return q_chunks <= 8 ? 1024 : (q_chunks <= 32 ? 64 : (q_chunks <= 64 ? 32 : 16));
+}
 constexpr int64_t kMaxCols = int64_t(1) << 24;  // columns of a compressed matrix, at most
 constexpr int kSmallRows = 256;  // T_SMALL matrices: rows (their P rows sit in LDS)
 constexpr int kSmallCols = 512;  // T_SMALL matrices: columns (their Q rows sit in LDS)

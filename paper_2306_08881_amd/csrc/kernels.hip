@@ -1515,7 +1515,14 @@ __global__ __launch_bounds__(kBlock) void k_qfin(KArgs a) {
 #pragma unroll
       for (int u = 0; u < U; ++u) s += v[u];
     }
-    for (; ch < ch1; ++ch) s += base[ch * stride];
+    if (ch < ch1) {  // the rest (fewer than U chunks) requested together too, added in order
+      float v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) v[u] = ch + u < ch1 ? base[(ch + u) * stride] : 0.f;
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (ch + u < ch1) s += v[u];
+    }
   }
   __shared__ float red[kBlock];
   red[tid()] = s;

@@ -61,11 +61,13 @@ __device__ inline void load_run(Rsrc r, uint32_t off, bool vec, float* out) {
 __device__ inline bool aligned16(const float* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // P-step over a tile of at most 32 rows and all m columns on four waves: wave w walks the
-// 32-column blocks w, w + 4, ... in step with the others (one barrier per block), so that the
-// workgroup reads 512 contiguous bytes of each of its rows at a time.  Per block, lane l loads M
-// and E for column c0 + l % 32 and rows drow(v, l / 32) (128-byte row segments), forms X = M + E,
-// applies the correction (F form) as an MFMA with D indexed (row, column) and stores X in that
-// layout.  The product P += X Qh reduces over columns, so it needs the row on the lane: X goes
+// 32-column blocks w, w + 4, ... in step with the others, so that the workgroup reads 512
+// contiguous bytes of each of its rows at a time.  Per step of 128 columns, wave w loads M and E
+// for rows 8 w ... 8 w + 7 as 16-byte vectors (lane l: row 8 w + 2 i + l / 32, columns
+// 4 (l % 32) ... + 3; one instruction reads 512 contiguous bytes of two rows), puts M + E in a
+// 32 x 128 LDS tile, and after a barrier takes its own block back with lane l holding column
+// c0 + l % 32 of rows drow(v, l / 32).  It applies the correction (F form) as an MFMA with D
+// indexed (row, column) and stores X in that layout.  The product P += X Qh reduces over columns, so it needs the row on the lane: X goes
 // through the wave's padded 32 x 33 LDS tile (two of them, alternating) and comes back with lane
 // l holding row l % 32 and columns drow(v, l / 32), the A operand; the accumulator lane l holds
 // the wave's share of P[r0 + drow(v, l / 32)][l % 32].  The four shares are added in wave order
@@ -102,13 +104,26 @@ __global__ __launch_bounds__(kWideBlock * kWidePWaves, 2) void k_wpstep(KArgs a)
 #pragma unroll
   for (int s = 0; s < KH; ++s) pa[s] = -pa[s];
 
-  auto load_block = [&](int64_t c0, float* g, float* e) {
-    const uint32_t coff = c0 + li < m ? u32(c0 + li) * 4u : kOut;
+  // M and E of the step from column cs: the lane's four rows 8 w + 2 i + h, columns cs + 4 li ...
+  // (past m: zeros); as 16-byte vectors when rows and tile starts are 16-byte aligned, else
+  // float by float in the same layout
+  const bool vec = (m & 3) == 0 && aligned16(src_of(a, d.bucket) + d.grad_off + r0 * m) &&
+                   aligned16(a.e + d.e_off + r0 * m);
+  const int vr = 8 * wave + h, vc = 4 * li;
+  auto load_block = [&](int64_t cs, float4* g, float4* e) {
+    const int64_t col = cs + vc;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const uint32_t o = coff == kOut ? kOut : u32(drow(v, h)) * row_bytes + coff;
-      g[v] = bld1_nt(G, o);
-      e[v] = bld1_nt(E, o);
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t o = u32(vr + 2 * i) * row_bytes + u32(col) * 4u;
+      if (vec) {
+        g[i] = bld4_nt(G, col < m ? o : kOut);
+        e[i] = bld4_nt(E, col < m ? o : kOut);
+      } else {
+        g[i] = make_float4(bld1_nt(G, col < m ? o : kOut), bld1_nt(G, col + 1 < m ? o + 4u : kOut),
+                           bld1_nt(G, col + 2 < m ? o + 8u : kOut), bld1_nt(G, col + 3 < m ? o + 12u : kOut));
+        e[i] = make_float4(bld1_nt(E, col < m ? o : kOut), bld1_nt(E, col + 1 < m ? o + 4u : kOut),
+                           bld1_nt(E, col + 2 < m ? o + 8u : kOut), bld1_nt(E, col + 3 < m ? o + 12u : kOut));
+      }
     }
   };
   // the block's factor operands: Ql rows (correction B) and Qh rows (product B, rank block kb)
@@ -125,8 +140,11 @@ __global__ __launch_bounds__(kWideBlock * kWidePWaves, 2) void k_wpstep(KArgs a)
       }
   };
   __shared__ float xt[kWidePWaves][2][32 * LD];
-  float g[16], e[16], qa[KH], qb[NR][16];
-  load_block(32 * wave, g, e);
+  constexpr int SP = 32 * kWidePWaves + 4;  // staging tile row pitch (floats, 16-byte aligned rows)
+  __shared__ __attribute__((aligned(16))) float st[32 * SP];
+  float4 g[4], e[4];
+  float qa[KH], qb[NR][16];
+  load_block(0, g, e);
   load_ops(32 * wave, qa, qb);
 
   v16f p[NR];
@@ -136,11 +154,15 @@ __global__ __launch_bounds__(kWideBlock * kWidePWaves, 2) void k_wpstep(KArgs a)
   // every wave takes the same number of steps (blocks past m: zero loads, dropped stores)
   for (int64_t cs = 0; cs < m; cs += CS, buf ^= 1) {
     const int64_t c0 = cs + 32 * wave;
+    // M + E to the staging tile (the previous step's readers have passed its second barrier)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) *reinterpret_cast<float4*>(st + (vr + 2 * i) * SP + vc) = g[i] + e[i];
+    load_block(cs + CS, g, e);  // next step (past m: zeros, no traffic)
+    __syncthreads();
     v16f x;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) x[v] = g[v] + e[v];
+    for (int v = 0; v < 16; ++v) x[v] = st[drow(v, h) * SP + 32 * wave + li];
     const uint32_t coff = c0 + li < m ? u32(c0 + li) * 4u : kOut;
-    load_block(c0 + CS, g, e);  // next block (past m: zeros, no traffic)
     if (fform) {  // X -= Ph Ql^T: A = -Ph (row, rank), B = Ql^T (rank, column)
 #pragma unroll
       for (int s = 0; s < KH; ++s) x = mfma(pa[s], qa[s], x);
@@ -187,10 +209,12 @@ __global__ __launch_bounds__(kWideBlock * kWidePWaves, 2) void k_wpstep(KArgs a)
 
 // Q-step over a tile (row chunk t.a of q_rows rows, column blocks 4 t.b ... 4 t.b + 3 of 32
 // columns), four waves per workgroup: wave w takes column block 4 t.b + w (columns c0 ...
-// c0 + 31) and the waves walk the chunk's 32-row blocks in step (one barrier per block), so
-// that the workgroup reads 512 contiguous bytes of each row at a time.  Per 32-row block, lane l holds
-// F for column c0 + l % 32 and rows drow(v, l / 32): coalesced 128-byte row segments.  The
-// correction (X form) is an MFMA with D indexed (row, column); F then is the A operand of
+// c0 + 31) and the waves walk the chunk's 32-row blocks in step, so that the workgroup reads 512
+// contiguous bytes of each row at a time.  Per 32-row block, wave w loads M and E for rows
+// 8 w ... 8 w + 7 of the workgroup's 128 columns as 16-byte vectors (as the P-step does), puts
+// M + E in a 32 x 128 LDS tile and after a barrier takes its own block back with lane l holding
+// column c0 + l % 32 of rows drow(v, l / 32).  The correction (X form) is an MFMA with D indexed
+// (row, column); F then is the A operand of
 // Q += F^T Ph with the rows as K.  Lane l's partial Q of column c0 + drow(v, l / 32), rank
 // l % 32, goes to the chunk's partial block for K_QFIN.
 template <int RK>
@@ -211,8 +235,16 @@ __global__ __launch_bounds__(kWideBlock * kWideQWaves, 2) void k_wqstep(KArgs a)
   const bool xform = deferred_p_of(a, d.bucket);
   const uint32_t row_bytes = u32(m) * 4u;
   const uint32_t ext = w > 0 ? u32(rows - 1) * row_bytes + u32(w) * 4u : 0u;
-  const Rsrc G = tile_rsrc(src_of(a, d.bucket) + d.grad_off + r0 * m + c0, ext);
-  const Rsrc E = tile_rsrc(a.e + d.e_off + r0 * m + c0, a.ef ? ext : 0u);
+  const Rsrc E = tile_rsrc(a.e + d.e_off + r0 * m + c0, a.ef ? ext : 0u);  // the wave's block (stores)
+  // the workgroup's columns ct ... ct + wt - 1 (loads)
+  const int64_t ct = static_cast<int64_t>(t.b) * kWideQWaves * d.q_cb;
+  const int64_t wt = (m - ct) < 32 * kWideQWaves ? m - ct : 32 * kWideQWaves;
+  const uint32_t extw = u32(rows - 1) * row_bytes + u32(wt) * 4u;
+  const float* gbase = src_of(a, d.bucket) + d.grad_off + r0 * m + ct;
+  const float* ebase = a.e + d.e_off + r0 * m + ct;
+  const Rsrc Gw = tile_rsrc(gbase, extw);
+  const Rsrc Ew = tile_rsrc(ebase, a.ef ? extw : 0u);
+  const bool vec = (m & 3) == 0 && aligned16(gbase) && aligned16(ebase);
   const Rsrc Qhr = tile_rsrc(a.fac + d.qh_slot + c0 * RK, xform ? u32(w) * RK * 4u : 0u);
   const Rsrc Plr = tile_rsrc(a.fac + d.pl_slot + r0 * RK, xform ? u32(rows) * RK * 4u : 0u);
   const Rsrc Phr = tile_rsrc(a.fac + d.ph_slot + r0 * RK, u32(rows) * RK * 4u);
@@ -223,12 +255,23 @@ __global__ __launch_bounds__(kWideBlock * kWideQWaves, 2) void k_wqstep(KArgs a)
   const uint32_t coff = li < w ? u32(li) * 4u : kOut;
 
   const bool pl4 = aligned16(a.fac + d.pl_slot);
-  auto load_block = [&](int rb, float* g, float* e) {
+  // M and E of the 32-row block from row rb: the lane's rows rb + 8 w + 2 i + h, columns
+  // 4 li ... 4 li + 3 of the workgroup's (past wt or the chunk: zeros); 16-byte vectors when the
+  // rows and the first column are 16-byte aligned, else float by float in the same layout
+  const int vr = 8 * wave + h, vc = 4 * li;
+  auto load_block = [&](int rb, float4* g, float4* e) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const uint32_t o = coff == kOut ? kOut : u32(rb + drow(v, h)) * row_bytes + coff;
-      g[v] = bld1_nt(G, o);
-      e[v] = bld1_nt(E, o);
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t o = u32(rb + vr + 2 * i) * row_bytes + u32(vc) * 4u;
+      if (vec) {
+        g[i] = bld4_nt(Gw, vc < wt ? o : kOut);
+        e[i] = bld4_nt(Ew, vc < wt ? o : kOut);
+      } else {
+        g[i] = make_float4(bld1_nt(Gw, vc < wt ? o : kOut), bld1_nt(Gw, vc + 1 < wt ? o + 4u : kOut),
+                           bld1_nt(Gw, vc + 2 < wt ? o + 8u : kOut), bld1_nt(Gw, vc + 3 < wt ? o + 12u : kOut));
+        e[i] = make_float4(bld1_nt(Ew, vc < wt ? o : kOut), bld1_nt(Ew, vc + 1 < wt ? o + 4u : kOut),
+                           bld1_nt(Ew, vc + 2 < wt ? o + 8u : kOut), bld1_nt(Ew, vc + 3 < wt ? o + 12u : kOut));
+      }
     }
   };
   // the block's factor operands: Pl rows (correction A) and Ph rows (product B, rank block kb)
@@ -242,19 +285,26 @@ __global__ __launch_bounds__(kWideBlock * kWideQWaves, 2) void k_wqstep(KArgs a)
         pb[kb][v] = bld1(Phr, rank < RK ? u32((rb + drow(v, h)) * RK + rank) * 4u : kOut);
       }
   };
-  float g[16], e[16], pa[KH], pb[NR][16];
+  constexpr int SP = 32 * kWideQWaves + 4;  // staging tile row pitch (floats, 16-byte aligned rows)
+  __shared__ __attribute__((aligned(16))) float st[32 * SP];
+  float4 g[4], e[4];
+  float pa[KH], pb[NR][16];
   load_block(0, g, e);
   load_ops(0, pa, pb);
   v16f q[NR];
 #pragma unroll
   for (int kb = 0; kb < NR; ++kb) q[kb] = zero16();
   for (int rb = 0; rb < rows; rb += 32) {
+    // M + E to the staging tile (the previous block's readers have passed its last barrier)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) *reinterpret_cast<float4*>(st + (vr + 2 * i) * SP + vc) = g[i] + e[i];
+    load_block(rb + 32, g, e);  // next block (past the chunk: zeros, no traffic)
+    __syncthreads();
     v16f x;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) x[v] = g[v] + e[v];
+    for (int v = 0; v < 16; ++v) x[v] = st[drow(v, h) * SP + 32 * wave + li];
     float* ca = pa;
     float (*cb)[16] = pb;
-    load_block(rb + 32, g, e);  // next block (past the chunk: zeros, no traffic)
     if (xform) {  // F -= Pl Qh^T: A = -Pl (row, rank), B = Qh^T (rank, column)
 #pragma unroll
       for (int s = 0; s < KH; ++s) x = mfma(-ca[s], qv[s], x);
@@ -267,7 +317,7 @@ __global__ __launch_bounds__(kWideBlock * kWideQWaves, 2) void k_wqstep(KArgs a)
 #pragma unroll
       for (int kb = 0; kb < NR; ++kb) q[kb] = mfma(x[v], cb[kb][v], q[kb]);
     load_ops(rb + 32, pa, pb);
-    __syncthreads();  // the waves stay on the same rows
+    __syncthreads();  // the waves stay on the same rows; the staging tile's readers are done
   }
   if (w == 0) return;  // a block past m has no partials
   const int64_t ncb = (m + d.q_cb - 1) / d.q_cb;

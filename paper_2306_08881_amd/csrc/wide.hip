@@ -162,18 +162,34 @@ __global__ __launch_bounds__(kWideBlock * kWidePWaves, 2) void k_wpstep(KArgs a)
     v16f x;
 #pragma unroll
     for (int v = 0; v < 16; ++v) x[v] = st[drow(v, h) * SP + 32 * wave + li];
-    const uint32_t coff = c0 + li < m ? u32(c0 + li) * 4u : kOut;
     if (fform) {  // X -= Ph Ql^T: A = -Ph (row, rank), B = Ql^T (rank, column)
 #pragma unroll
       for (int s = 0; s < KH; ++s) x = mfma(pa[s], qa[s], x);
     }
     float* tl = xt[wave][buf];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      bst1_nt(E, coff == kOut ? kOut : u32(drow(v, h)) * row_bytes + coff, x[v]);
-      tl[drow(v, h) * LD + li] = x[v];
-    }
+    for (int v = 0; v < 16; ++v) tl[drow(v, h) * LD + li] = x[v];
     __syncthreads();
+    // X to the arena in the load layout: the lane's rows 8 w + 2 i + h, columns cs + 4 li ...,
+    // from the transposing tile of the wave that formed them (as 16-byte vectors when aligned)
+    {
+      const float* xs = &xt[li >> 3][buf][(vc & 31)];
+      const int64_t col = cs + vc;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = vr + 2 * i;
+        const float4 xv = make_float4(xs[row * LD], xs[row * LD + 1], xs[row * LD + 2], xs[row * LD + 3]);
+        const uint32_t o = u32(row) * row_bytes + u32(col) * 4u;
+        if (vec) {
+          bst4_nt(E, col < m ? o : kOut, xv);
+        } else {
+          bst1_nt(E, col < m ? o : kOut, xv.x);
+          bst1_nt(E, col + 1 < m ? o + 4u : kOut, xv.y);
+          bst1_nt(E, col + 2 < m ? o + 8u : kOut, xv.z);
+          bst1_nt(E, col + 3 < m ? o + 12u : kOut, xv.w);
+        }
+      }
+    }
 #pragma unroll
     for (int v = 0; v < 16; ++v) {  // P += X Qh: A = X (row, column), B = Qh (column, rank)
       const float xa = tl[li * LD + drow(v, h)];
@@ -234,9 +250,7 @@ __global__ __launch_bounds__(kWideBlock * kWideQWaves, 2) void k_wqstep(KArgs a)
   const int64_t w = (m - c0) < 32 ? ((m - c0) > 0 ? (m - c0) : 0) : 32;
   const bool xform = deferred_p_of(a, d.bucket);
   const uint32_t row_bytes = u32(m) * 4u;
-  const uint32_t ext = w > 0 ? u32(rows - 1) * row_bytes + u32(w) * 4u : 0u;
-  const Rsrc E = tile_rsrc(a.e + d.e_off + r0 * m + c0, a.ef ? ext : 0u);  // the wave's block (stores)
-  // the workgroup's columns ct ... ct + wt - 1 (loads)
+  // the workgroup's columns ct ... ct + wt - 1
   const int64_t ct = static_cast<int64_t>(t.b) * kWideQWaves * d.q_cb;
   const int64_t wt = (m - ct) < 32 * kWideQWaves ? m - ct : 32 * kWideQWaves;
   const uint32_t extw = u32(rows - 1) * row_bytes + u32(wt) * 4u;
@@ -252,7 +266,6 @@ __global__ __launch_bounds__(kWideBlock * kWideQWaves, 2) void k_wqstep(KArgs a)
   float qv[KH];  // correction B operand: Qh[c0 + l % 32][KH h + s]
 #pragma unroll
   for (int s = 0; s < KH; ++s) qv[s] = bld1(Qhr, u32(li * RK + KH * h + s) * 4u);
-  const uint32_t coff = li < w ? u32(li) * 4u : kOut;
 
   const bool pl4 = aligned16(a.fac + d.pl_slot);
   // M and E of the 32-row block from row rb: the lane's rows rb + 8 w + 2 i + h, columns
@@ -285,8 +298,10 @@ __global__ __launch_bounds__(kWideBlock * kWideQWaves, 2) void k_wqstep(KArgs a)
         pb[kb][v] = bld1(Phr, rank < RK ? u32((rb + drow(v, h)) * RK + rank) * 4u : kOut);
       }
   };
+  // two staging tiles in turn: block k's F goes back into tile k % 2 and is stored from there
+  // after the block's last barrier, while block k + 1 fills the other
   constexpr int SP = 32 * kWideQWaves + 4;  // staging tile row pitch (floats, 16-byte aligned rows)
-  __shared__ __attribute__((aligned(16))) float st[32 * SP];
+  __shared__ __attribute__((aligned(16))) float st[2][32 * SP];
   float4 g[4], e[4];
   float pa[KH], pb[NR][16];
   load_block(0, g, e);
@@ -294,30 +309,46 @@ __global__ __launch_bounds__(kWideBlock * kWideQWaves, 2) void k_wqstep(KArgs a)
   v16f q[NR];
 #pragma unroll
   for (int kb = 0; kb < NR; ++kb) q[kb] = zero16();
-  for (int rb = 0; rb < rows; rb += 32) {
-    // M + E to the staging tile (the previous block's readers have passed its last barrier)
+  int buf = 0;
+  for (int rb = 0; rb < rows; rb += 32, buf ^= 1) {
+    float* sb = st[buf];
+    // M + E to the staging tile (its readers of two blocks ago have passed the last barrier)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) *reinterpret_cast<float4*>(st + (vr + 2 * i) * SP + vc) = g[i] + e[i];
+    for (int i = 0; i < 4; ++i) *reinterpret_cast<float4*>(sb + (vr + 2 * i) * SP + vc) = g[i] + e[i];
     load_block(rb + 32, g, e);  // next block (past the chunk: zeros, no traffic)
     __syncthreads();
     v16f x;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) x[v] = st[drow(v, h) * SP + 32 * wave + li];
+    for (int v = 0; v < 16; ++v) x[v] = sb[drow(v, h) * SP + 32 * wave + li];
     float* ca = pa;
     float (*cb)[16] = pb;
     if (xform) {  // F -= Pl Qh^T: A = -Pl (row, rank), B = Qh^T (rank, column)
 #pragma unroll
       for (int s = 0; s < KH; ++s) x = mfma(-ca[s], qv[s], x);
     }
+    // F back into the wave's own block of the tile (only this wave has read it)
 #pragma unroll
-    for (int v = 0; v < 16; ++v)
-      bst1_nt(E, coff == kOut ? kOut : u32(rb + drow(v, h)) * row_bytes + coff, x[v]);
+    for (int v = 0; v < 16; ++v) sb[drow(v, h) * SP + 32 * wave + li] = x[v];
 #pragma unroll
     for (int v = 0; v < 16; ++v)  // Q += F^T Ph: A = F^T, B = Ph
 #pragma unroll
       for (int kb = 0; kb < NR; ++kb) q[kb] = mfma(x[v], cb[kb][v], q[kb]);
     load_ops(rb + 32, pa, pb);
-    __syncthreads();  // the waves stay on the same rows; the staging tile's readers are done
+    __syncthreads();  // the waves stay on the same rows; every block's F is in the tile
+    // F to the arena in the load layout, as 16-byte vectors when aligned
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float4 f = *reinterpret_cast<const float4*>(sb + (vr + 2 * i) * SP + vc);
+      const uint32_t o = u32(rb + vr + 2 * i) * row_bytes + u32(vc) * 4u;
+      if (vec) {
+        bst4_nt(Ew, vc < wt ? o : kOut, f);
+      } else {
+        bst1_nt(Ew, vc < wt ? o : kOut, f.x);
+        bst1_nt(Ew, vc + 1 < wt ? o + 4u : kOut, f.y);
+        bst1_nt(Ew, vc + 2 < wt ? o + 8u : kOut, f.z);
+        bst1_nt(Ew, vc + 3 < wt ? o + 12u : kOut, f.w);
+      }
+    }
   }
   if (w == 0) return;  // a block past m has no partials
   const int64_t ncb = (m + d.q_cb - 1) / d.q_cb;

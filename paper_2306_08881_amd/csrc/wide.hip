@@ -139,7 +139,11 @@ __global__ __launch_bounds__(kWideBlock * kWidePWaves, 2) void k_wpstep(KArgs a)
         qb[kb][v] = bld1(Qhr, (col < m && rank < RK) ? u32(col * RK + rank) * 4u : kOut);
       }
   };
-  __shared__ float xt[kWidePWaves][2][32 * LD];
+  // the waves' transposing tiles, two each; a wave's pair starts one float past the previous
+  // wave's, so that the row reads of the X stores (four waves' tiles at once) spread over the banks
+  constexpr int XW = 2 * 32 * LD + 1;
+  __shared__ float xt[kWidePWaves * XW];
+  auto xtile = [&](int w, int b) { return xt + w * XW + b * 32 * LD; };
   constexpr int SP = 32 * kWidePWaves + 4;  // staging tile row pitch (floats, 16-byte aligned rows)
   __shared__ __attribute__((aligned(16))) float st[32 * SP];
   float4 g[4], e[4];
@@ -166,14 +170,14 @@ __global__ __launch_bounds__(kWideBlock * kWidePWaves, 2) void k_wpstep(KArgs a)
 #pragma unroll
       for (int s = 0; s < KH; ++s) x = mfma(pa[s], qa[s], x);
     }
-    float* tl = xt[wave][buf];
+    float* tl = xtile(wave, buf);
 #pragma unroll
     for (int v = 0; v < 16; ++v) tl[drow(v, h) * LD + li] = x[v];
     __syncthreads();
     // X to the arena in the load layout: the lane's rows 8 w + 2 i + h, columns cs + 4 li ...,
     // from the transposing tile of the wave that formed them (as 16-byte vectors when aligned)
     {
-      const float* xs = &xt[li >> 3][buf][(vc & 31)];
+      const float* xs = xtile(li >> 3, buf) + (vc & 31);
       const int64_t col = cs + vc;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -200,7 +204,7 @@ __global__ __launch_bounds__(kWideBlock * kWidePWaves, 2) void k_wpstep(KArgs a)
   }
 
   // the waves' shares of P, added in wave order: entry (v, lane) of rank block kb
-  float* red = &xt[0][0][0];  // kWidePWaves x 1024 floats per rank block (the transposing tiles are free)
+  float* red = xt;  // kWidePWaves x 1024 floats per rank block (the transposing tiles are free)
   float* P = dst_of(a, d.bucket) + d.fac_off_p;
   float* Pl = a.fac + d.pl_slot;
 #pragma unroll

@@ -271,7 +271,6 @@ __global__ __launch_bounds__(kWideBlock * kWideQWaves, 2) void k_wqstep(KArgs a)
 #pragma unroll
   for (int s = 0; s < KH; ++s) qv[s] = bld1(Qhr, u32(li * RK + KH * h + s) * 4u);
 
-  const bool pl4 = aligned16(a.fac + d.pl_slot);
   // M and E of the 32-row block from row rb: the lane's rows rb + 8 w + 2 i + h, columns
   // 4 li ... 4 li + 3 of the workgroup's (past wt or the chunk: zeros); 16-byte vectors when the
   // rows and the first column are 16-byte aligned, else float by float in the same layout
@@ -291,53 +290,67 @@ __global__ __launch_bounds__(kWideBlock * kWideQWaves, 2) void k_wqstep(KArgs a)
       }
     }
   };
-  // the block's factor operands: Pl rows (correction A) and Ph rows (product B, rank block kb)
-  auto load_ops = [&](int rb, float* pa, float (*pb)[16]) {
-    if (xform) load_run<KH>(Plr, u32((rb + li) * RK + KH * h) * 4u, pl4, pa);
-#pragma unroll
-    for (int kb = 0; kb < NR; ++kb)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int rank = kb * 32 + li;
-        pb[kb][v] = bld1(Phr, rank < RK ? u32((rb + drow(v, h)) * RK + rank) * 4u : kOut);
-      }
+  // the block's factor rows, Pl (correction A) and Ph (product B): 32 x RK contiguous floats each
+  // (factor slots are 256-byte aligned), loaded once for the workgroup, one 16-byte word per
+  // thread, into a factor tile beside the staging tile, from which every wave takes its operands
+  static_assert(NR == 1, "one 32-rank block below kSplitRank");
+  constexpr int FP = RK + 4;        // factor tile row pitch (floats, 16-byte aligned rows)
+  constexpr int FV = 32 * RK / 4;   // 16-byte words per block and factor
+  const bool fw = tid() < FV;       // the thread has a word of the block
+  const int frow = tid() * 4 / RK, fcol = tid() * 4 % RK;
+  auto load_fac = [&](int rb, float4& l, float4& p) {
+    const uint32_t o = u32(rb * RK + tid() * 4) * 4u;
+    l = bld4(Plr, fw ? o : kOut);  // zeros past the chunk, and without the X form
+    p = bld4(Phr, fw ? o : kOut);
   };
   // two staging tiles in turn: block k's F goes back into tile k % 2 and is stored from there
   // after the block's last barrier, while block k + 1 fills the other
   constexpr int SP = 32 * kWideQWaves + 4;  // staging tile row pitch (floats, 16-byte aligned rows)
   __shared__ __attribute__((aligned(16))) float st[2][32 * SP];
-  float4 g[4], e[4];
-  float pa[KH], pb[NR][16];
+  __shared__ __attribute__((aligned(16))) float ft[2][2][32 * FP];  // [tile][Pl, Ph]
+  float4 g[4], e[4], fl, fh;
   load_block(0, g, e);
-  load_ops(0, pa, pb);
+  load_fac(0, fl, fh);
   v16f q[NR];
 #pragma unroll
   for (int kb = 0; kb < NR; ++kb) q[kb] = zero16();
   int buf = 0;
   for (int rb = 0; rb < rows; rb += 32, buf ^= 1) {
     float* sb = st[buf];
-    // M + E to the staging tile (its readers of two blocks ago have passed the last barrier)
+    float* fpl = ft[buf][0];
+    float* fph = ft[buf][1];
+    // M + E and the factor rows to the tiles (their readers of two blocks ago have passed the
+    // last barrier)
 #pragma unroll
     for (int i = 0; i < 4; ++i) *reinterpret_cast<float4*>(sb + (vr + 2 * i) * SP + vc) = g[i] + e[i];
+    if (fw) {
+      *reinterpret_cast<float4*>(fpl + frow * FP + fcol) = fl;
+      *reinterpret_cast<float4*>(fph + frow * FP + fcol) = fh;
+    }
     load_block(rb + 32, g, e);  // next block (past the chunk: zeros, no traffic)
+    load_fac(rb + 32, fl, fh);
     __syncthreads();
     v16f x;
 #pragma unroll
     for (int v = 0; v < 16; ++v) x[v] = sb[drow(v, h) * SP + 32 * wave + li];
-    float* ca = pa;
-    float (*cb)[16] = pb;
     if (xform) {  // F -= Pl Qh^T: A = -Pl (row, rank), B = Qh^T (rank, column)
+      float pa[KH];  // Pl[rb + l % 32][KH h + s]
 #pragma unroll
-      for (int s = 0; s < KH; ++s) x = mfma(-ca[s], qv[s], x);
+      for (int s = 0; s < KH; ++s) pa[s] = fpl[li * FP + KH * h + s];
+#pragma unroll
+      for (int s = 0; s < KH; ++s) x = mfma(-pa[s], qv[s], x);
     }
     // F back into the wave's own block of the tile (only this wave has read it)
 #pragma unroll
     for (int v = 0; v < 16; ++v) sb[drow(v, h) * SP + 32 * wave + li] = x[v];
+    {  // Q += F^T Ph: A = F^T, B = Ph (lane l: rank l % 32 of rows drow(v, l / 32); zero past r)
+      const int rk = li < RK ? li : RK - 1;
 #pragma unroll
-    for (int v = 0; v < 16; ++v)  // Q += F^T Ph: A = F^T, B = Ph
-#pragma unroll
-      for (int kb = 0; kb < NR; ++kb) q[kb] = mfma(x[v], cb[kb][v], q[kb]);
-    load_ops(rb + 32, pa, pb);
+      for (int v = 0; v < 16; ++v) {
+        const float pb = fph[drow(v, h) * FP + rk];
+        q[0] = mfma(x[v], li < RK ? pb : 0.f, q[0]);
+      }
+    }
     __syncthreads();  // the waves stay on the same rows; every block's F is in the tile
     // F to the arena in the load layout, as 16-byte vectors when aligned
 #pragma unroll

@@ -67,12 +67,14 @@ __device__ inline bool aligned16(const float* p) { return (reinterpret_cast<uint
 // 4 (l % 32) ... + 3; one instruction reads 512 contiguous bytes of two rows), puts M + E in a
 // 32 x 128 LDS tile, and after a barrier takes its own block back with lane l holding column
 // c0 + l % 32 of rows drow(v, l / 32).  It applies the correction (F form) as an MFMA with D
-// indexed (row, column) and stores X in that layout.  The product P += X Qh reduces over columns, so it needs the row on the lane: X goes
-// through the wave's padded 32 x 33 LDS tile (two of them, alternating) and comes back with lane
-// l holding row l % 32 and columns drow(v, l / 32), the A operand; the accumulator lane l holds
-// the wave's share of P[r0 + drow(v, l / 32)][l % 32].  The four shares are added in wave order
-// through LDS at the end.  The next block's M and E are requested before the current block's
-// MFMAs, its factor rows after them.
+// indexed (row, column).  The product P += X Qh reduces over columns, so it needs the row on the
+// lane: X goes through the wave's padded 32 x 33 LDS tile (two of them, alternating) and comes
+// back with lane l holding row l % 32 and columns drow(v, l / 32), the A operand; the
+// accumulator lane l holds the wave's share of P[r0 + drow(v, l / 32)][l % 32].  After the
+// barrier that publishes those tiles, every wave also reads its rows of X in the load layout
+// from the four waves' tiles and stores them as 16-byte vectors.  The four shares of P are added
+// in wave order through LDS at the end.  The next step's M and E are requested before the
+// current block's MFMAs, its factor rows after them.
 template <int RK>
 __global__ __launch_bounds__(kWideBlock * kWidePWaves, 2) void k_wpstep(KArgs a) {
   constexpr int KH = RK / 2;
@@ -233,9 +235,11 @@ __global__ __launch_bounds__(kWideBlock * kWidePWaves, 2) void k_wpstep(KArgs a)
 // contiguous bytes of each row at a time.  Per 32-row block, wave w loads M and E for rows
 // 8 w ... 8 w + 7 of the workgroup's 128 columns as 16-byte vectors (as the P-step does), puts
 // M + E in a 32 x 128 LDS tile and after a barrier takes its own block back with lane l holding
-// column c0 + l % 32 of rows drow(v, l / 32).  The correction (X form) is an MFMA with D indexed
-// (row, column); F then is the A operand of
-// Q += F^T Ph with the rows as K.  Lane l's partial Q of column c0 + drow(v, l / 32), rank
+// column c0 + l % 32 of rows drow(v, l / 32).  The block's Pl and Ph rows are loaded once for
+// the workgroup into a factor tile beside it.  The correction (X form) is an MFMA with D indexed
+// (row, column); F then is the A operand of Q += F^T Ph with the rows as K, and goes back into
+// the wave's block of the tile, from which every wave stores its rows of F as 16-byte vectors
+// after the block's last barrier.  Lane l's partial Q of column c0 + drow(v, l / 32), rank
 // l % 32, goes to the chunk's partial block for K_QFIN.
 template <int RK>
 __global__ __launch_bounds__(kWideBlock * kWideQWaves, 2) void k_wqstep(KArgs a) {
